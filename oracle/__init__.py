@@ -1,0 +1,166 @@
+"""CPU oracle of SwitchSD's per-step speculation-control path.
+
+TEST INFRASTRUCTURE ONLY.  This package is the checker of the HIP library:
+only the test-suite, the smoke check and the benchmark's CPU-baseline leg
+import it.  The product path never does, and it shares no code with it.
+
+The arithmetic lives in ``switchsd_oracle.c`` (plain scalar C); this module
+only marshals numpy arrays through ctypes.  Each function cites the passage
+of the paper it follows (see the C source for the readings R1-R8).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build_oracle
+
+_lib = None
+
+MAX_NGRAM = 8
+
+
+class OracleCfg(ctypes.Structure):
+    _fields_ = [("n_ngram", ctypes.c_int32),
+                ("ngram_lens", ctypes.c_int32 * MAX_NGRAM),
+                ("kappa", ctypes.c_int32),
+                ("k", ctypes.c_int32),
+                ("theta", ctypes.c_float)]
+
+
+def make_cfg(ngram_lens, kappa, k, theta):
+    c = OracleCfg()
+    c.n_ngram = len(ngram_lens)
+    for i, n in enumerate(ngram_lens):
+        c.ngram_lens[i] = int(n)
+    c.kappa = int(kappa)
+    c.k = int(k)
+    c.theta = float(theta)
+    return c
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(build_oracle.LIB):
+            build_oracle.build()
+        _lib = ctypes.CDLL(build_oracle.LIB)
+        P = ctypes.c_void_p
+        i32 = ctypes.c_int32
+        _lib.oracle_match.argtypes = [P, i32, P, P, P, P, P]
+        _lib.oracle_probe.argtypes = [P, P, i32, ctypes.c_float]
+        _lib.oracle_probe.restype = ctypes.c_float
+        _lib.oracle_select.argtypes = [i32, i32, P, ctypes.c_float, P, P, i32, i32, P, P, P, P]
+        _lib.oracle_select.restype = i32
+        _lib.oracle_argmax_row.argtypes = [P, i32]
+        _lib.oracle_argmax_row.restype = i32
+        _lib.oracle_accept.argtypes = [P, P, i32, P, i32, P, P, P, P]
+        _lib.oracle_step.argtypes = [i32, i32, i32, i32, i32] + [P] * 4 + [ctypes.c_float] + \
+            [P] * 5 + [P] * 14 + [i32]
+        _lib.oracle_step.restype = i32
+    return _lib
+
+
+def _p(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+def match(x, L, cfg):
+    """Step 1 (Sec. 3.3): longest-first, most-recent suffix n-gram match."""
+    lib = _load()
+    x = _c(x, np.int32)
+    mn, me, cl = (np.zeros(1, np.int32) for _ in range(3))
+    ct = np.full(max(cfg.k, 1), -1, np.int32)
+    lib.oracle_match(_p(x), int(L), ctypes.byref(cfg), _p(mn), _p(me), _p(cl), _p(ct))
+    return int(mn[0]), int(me[0]), int(cl[0]), ct[:cfg.k].copy()
+
+
+def probe(h_bf16, w, bias):
+    """Step 2 (Sec. 3.2, Eq. 3): z = w . h + bias, rounded once to float."""
+    lib = _load()
+    h = _c(h_bf16, np.uint16)
+    w = _c(w, np.float32)
+    return np.float32(lib.oracle_probe(_p(h), _p(w), int(h.size), float(bias)))
+
+
+def select(match_n, copy_len, copy_tokens, z, ntok, npar, nn, R, cfg):
+    """Step 3 (Sec. 3.3, Eq. 4 + kappa gate): chosen draft in node layout."""
+    lib = _load()
+    ct = _c(copy_tokens, np.int32) if cfg.k > 0 else np.zeros(1, np.int32)
+    ntok = _c(ntok, np.int32)
+    npar_a = _c(npar, np.int32) if npar is not None else None
+    dtok = np.zeros(R, np.int32)
+    dpar = np.zeros(R, np.int32)
+    dn = np.zeros(1, np.int32)
+    uc = lib.oracle_select(int(match_n), int(copy_len), _p(ct), float(z), _p(ntok), _p(npar_a),
+                           int(nn), int(R), ctypes.byref(cfg), _p(dtok), _p(dpar), _p(dn))
+    return int(uc), dtok, dpar, int(dn[0])
+
+
+def argmax_row(row_bf16):
+    """Step 4a (Sec. 2; App. A, T = 0): lowest index of the largest value."""
+    lib = _load()
+    r = _c(row_bf16, np.uint16)
+    return int(lib.oracle_argmax_row(_p(r), int(r.size)))
+
+
+def accept(dtok, dpar, dn, amax, R):
+    """Step 4b (Sec. 3.3): deepest accepted node, its path and the bonus."""
+    lib = _load()
+    dtok = _c(dtok, np.int32)
+    dpar = _c(dpar, np.int32)
+    amax = _c(amax, np.int32)
+    al, an, bo = (np.zeros(1, np.int32) for _ in range(3))
+    out = np.zeros(R, np.int32)
+    lib.oracle_accept(_p(dtok), _p(dpar), int(dn), _p(amax), int(R), _p(al), _p(an), _p(bo),
+                      _p(out))
+    return int(al[0]), int(an[0]), int(bo[0]), out
+
+
+STEP_OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_copy",
+                "dtok", "dpar", "dn", "amax", "accept_len", "accept_node", "bonus",
+                "out_tokens")
+
+
+def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=1):
+    """The whole step for B sequences (steps 1-4 in the paper's order).
+
+    tokens [B,Lmax] int32, lengths [B] int32, hidden [B,d] bf16 bits (uint16),
+    w [d] float32, ntok/npar [B,R] int32 (npar None = chains), nn [B] int32,
+    logits [B,R,V] bf16 bits (uint16).  Returns a dict of numpy outputs.
+    """
+    lib = _load()
+    tokens = _c(tokens, np.int32)
+    B, Lmax = tokens.shape
+    lengths = _c(lengths, np.int32)
+    hidden = _c(hidden, np.uint16).reshape(B, -1)
+    d = hidden.shape[1]
+    w = _c(w, np.float32)
+    ntok = _c(ntok, np.int32)
+    R = ntok.shape[1]
+    npar_a = _c(npar, np.int32) if npar is not None else None
+    nn = _c(nn, np.int32)
+    logits = _c(logits, np.uint16)
+    V = logits.shape[-1]
+    assert logits.size == B * R * V
+    K = cfg.k
+    o = {
+        "match_n": np.zeros(B, np.int32), "match_end": np.zeros(B, np.int32),
+        "copy_len": np.zeros(B, np.int32), "copy_tokens": np.zeros((B, max(K, 1)), np.int32),
+        "z": np.zeros(B, np.float32), "use_copy": np.zeros(B, np.int32),
+        "dtok": np.zeros((B, R), np.int32), "dpar": np.zeros((B, R), np.int32),
+        "dn": np.zeros(B, np.int32), "amax": np.zeros((B, R), np.int32),
+        "accept_len": np.zeros(B, np.int32), "accept_node": np.zeros(B, np.int32),
+        "bonus": np.zeros(B, np.int32), "out_tokens": np.zeros((B, R), np.int32),
+    }
+    rc = lib.oracle_step(B, Lmax, d, R, V, _p(tokens), _p(lengths), _p(hidden), _p(w),
+                         float(bias), _p(ntok), _p(npar_a), _p(nn), _p(logits),
+                         ctypes.byref(cfg), *[_p(o[k]) for k in STEP_OUTPUTS], int(threads))
+    if rc != 0:
+        raise ValueError("oracle_step rejected its arguments")
+    o["copy_tokens"] = o["copy_tokens"][:, :K]
+    return o

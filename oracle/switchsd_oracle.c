@@ -1,0 +1,291 @@
+/*
+ * switchsd_oracle.c -- plain, slow CPU oracle of SwitchSD's per-step
+ * speculation-control path.  TEST INFRASTRUCTURE ONLY (see the header).
+ *
+ * Every function is the definition written out with scalar loops, in the
+ * order the paper states the method.  No blocking, no packing, no early
+ * exits beyond what the definition itself implies.
+ *
+ * Readings taken where the paper is silent (each also listed in the design
+ * notes of the repository):
+ *   R1  a prior occurrence may overlap the current suffix; its end e must be
+ *       <= L-2 so that at least one continuation token exists;
+ *   R2  the n-gram lengths are tried longest first, and among the occurrences
+ *       of one length the most recent (largest end) wins -- "ranked by
+ *       recency", Sec. 3.3;
+ *   R3  the kappa gate is separate from the lengths searched: copy needs
+ *       match_n >= kappa;
+ *   R4  the threshold test PR(H) >= tau of Eq. 4 is taken in logit space as
+ *       z >= theta with theta = logit(tau), in float;
+ *   R5  the probe keeps an optional bias (Eq. 3 has none: bias = 0);
+ *   R6  argmax ties go to the lowest vocabulary index, -0 equals +0 and NaN
+ *       is below every number (a row of NaN gives index 0);
+ *   R7  node 0 of a draft is the anchor; a node whose parent index is not in
+ *       [0, i) is never accepted; among accepted nodes the deepest wins, ties
+ *       to the lowest node index;
+ *   R8  lengths are clamped to [0, Lmax] and neural node counts to [1, R].
+ */
+#include "switchsd_oracle.h"
+
+#include <math.h>
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* bf16 is the upper half of an IEEE binary32: widening is exact. */
+static float bf16_to_float(uint16_t h)
+{
+    uint32_t u = ((uint32_t)h) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* Step 1 -- Sec. 3.3 (Copy-Intent Decision Rule; Copy-Based Speculative
+ * Generation).  For each n in the configured order: the set of ends e with
+ * n-1 <= e <= L-2 and x[e-t] == x[L-1-t] for every t < n.  The first n whose
+ * set is non-empty gives match_n = n and match_end = the largest e.  The copy
+ * candidate is the continuation after the occurrence, cut to k tokens and to
+ * the end of the context. */
+int oracle_match(const int32_t *x, int32_t L, const oracle_cfg *cfg,
+                 int32_t *match_n, int32_t *match_end, int32_t *copy_len,
+                 int32_t *copy_tokens)
+{
+    *match_n = 0;
+    *match_end = -1;
+    for (int32_t j = 0; j < cfg->n_ngram; ++j) {
+        int32_t n = cfg->ngram_lens[j];
+        if (L < n + 1)
+            continue;
+        int32_t best = -1;
+        for (int32_t e = n - 1; e <= L - 2; ++e) {
+            int same = 1;
+            for (int32_t t = 0; t < n; ++t) {
+                if (x[e - t] != x[L - 1 - t]) {
+                    same = 0;
+                    break;
+                }
+            }
+            if (same && e > best)
+                best = e;
+        }
+        if (best >= 0) {
+            *match_n = n;
+            *match_end = best;
+            break;
+        }
+    }
+    for (int32_t j = 0; j < cfg->k; ++j)
+        copy_tokens[j] = -1;
+    if (*match_n == 0) {
+        *copy_len = 0;
+        return 0;
+    }
+    int32_t c = *match_end + 1;
+    int32_t len = L - c;
+    if (len > cfg->k)
+        len = cfg->k;
+    *copy_len = len;
+    for (int32_t j = 0; j < len; ++j)
+        copy_tokens[j] = x[c + j];
+    return 0;
+}
+
+/* Step 2 -- Sec. 3.2, Eq. 3: the probe is the linear score w^T H (the
+ * sigmoid is monotone, so the decision uses the logit).  Each product of a
+ * bf16 and a float is exact in long double (8 + 24 <= 64 significand bits);
+ * the running sum carries a 64-bit significand, and the result is rounded
+ * once to float. */
+float oracle_probe(const uint16_t *h_bf16, const float *w, int32_t d, float bias)
+{
+    long double s = 0.0L;
+    for (int32_t i = 0; i < d; ++i)
+        s += (long double)bf16_to_float(h_bf16[i]) * (long double)w[i];
+    s += (long double)bias;
+    return (float)s;
+}
+
+/* Step 3 -- Sec. 3.3, Eq. 4 with the kappa-gram gate: copy iff the probe
+ * clears the threshold AND a match of length >= kappa exists; otherwise the
+ * neural draft is used as given. */
+int32_t oracle_select(int32_t match_n, int32_t copy_len, const int32_t *copy_tokens,
+                      float z, const int32_t *ntok, const int32_t *npar,
+                      int32_t nn, int32_t R, const oracle_cfg *cfg,
+                      int32_t *dtok, int32_t *dpar, int32_t *dn)
+{
+    int32_t use_copy = (match_n >= cfg->kappa) && (z >= cfg->theta);
+    for (int32_t r = 0; r < R; ++r) {
+        dtok[r] = -1;
+        dpar[r] = -1;
+    }
+    if (use_copy) {
+        *dn = copy_len + 1;
+        for (int32_t i = 1; i <= copy_len; ++i) {
+            dtok[i] = copy_tokens[i - 1];
+            dpar[i] = i - 1;
+        }
+    } else {
+        if (nn < 1)
+            nn = 1;
+        if (nn > R)
+            nn = R;
+        *dn = nn;
+        for (int32_t i = 1; i < nn; ++i) {
+            dtok[i] = ntok[i];
+            dpar[i] = npar ? npar[i] : i - 1;
+        }
+    }
+    return use_copy;
+}
+
+/* Step 4a -- greedy verification at T = 0 (Sec. 2, App. A): the target's
+ * choice at a position is the lowest index holding the largest value. */
+int32_t oracle_argmax_row(const uint16_t *row_bf16, int32_t V)
+{
+    int32_t best = -1;
+    float best_val = 0.0f;
+    for (int32_t v = 0; v < V; ++v) {
+        float f = bf16_to_float(row_bf16[v]);
+        if (isnan(f))
+            continue;
+        if (best < 0 || f > best_val) {
+            best = v;
+            best_val = f;
+        }
+    }
+    return best < 0 ? 0 : best;
+}
+
+/* Step 4b -- Sec. 3.3 (select the longest validated continuation): a node is
+ * accepted when its parent is accepted and its token equals the target's
+ * choice at the parent.  The result is the deepest accepted node, the tokens
+ * on its path and the target's own token after it (the bonus). */
+void oracle_accept(const int32_t *dtok, const int32_t *dpar, int32_t dn,
+                   const int32_t *amax, int32_t R,
+                   int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                   int32_t *out_tokens)
+{
+    int32_t *accepted = (int32_t *)calloc((size_t)R, sizeof(int32_t));
+    int32_t *depth = (int32_t *)calloc((size_t)R, sizeof(int32_t));
+    accepted[0] = 1;
+    depth[0] = 0;
+    for (int32_t i = 1; i < dn; ++i) {
+        int32_t p = dpar[i];
+        if (p < 0 || p >= i)
+            continue;
+        if (accepted[p] && dtok[i] == amax[p]) {
+            accepted[i] = 1;
+            depth[i] = depth[p] + 1;
+        }
+    }
+    int32_t best = 0;
+    for (int32_t i = 1; i < dn; ++i)
+        if (accepted[i] && depth[i] > depth[best])
+            best = i;
+    *accept_node = best;
+    *accept_len = depth[best];
+    *bonus = amax[best];
+    for (int32_t r = 0; r < R; ++r)
+        out_tokens[r] = -1;
+    /* path tokens root -> best, root excluded, written back to front */
+    int32_t node = best;
+    for (int32_t pos = depth[best] - 1; pos >= 0; --pos) {
+        out_tokens[pos] = dtok[node];
+        node = dpar[node];
+    }
+    out_tokens[depth[best]] = *bonus;
+    free(accepted);
+    free(depth);
+}
+
+typedef struct {
+    int32_t b0, b1;
+    int32_t Lmax, d, R, V;
+    const int32_t *tokens, *lengths;
+    const uint16_t *hidden;
+    const float *w;
+    float bias;
+    const int32_t *ntok, *npar, *nn;
+    const uint16_t *logits;
+    const oracle_cfg *cfg;
+    int32_t *match_n, *match_end, *copy_len, *copy_tokens;
+    float *z;
+    int32_t *use_copy, *dtok, *dpar, *dn, *amax;
+    int32_t *accept_len, *accept_node, *bonus, *out_tokens;
+} step_job;
+
+static void step_range(const step_job *j)
+{
+    const int64_t R = j->R, V = j->V, K = j->cfg->k;
+    for (int32_t b = j->b0; b < j->b1; ++b) {
+        int32_t L = j->lengths[b];
+        if (L < 0)
+            L = 0;
+        if (L > j->Lmax)
+            L = j->Lmax;
+        const int32_t *x = j->tokens + (int64_t)b * j->Lmax;
+        oracle_match(x, L, j->cfg, &j->match_n[b], &j->match_end[b], &j->copy_len[b],
+                     j->copy_tokens + b * K);
+        j->z[b] = oracle_probe(j->hidden + (int64_t)b * j->d, j->w, j->d, j->bias);
+        j->use_copy[b] = oracle_select(j->match_n[b], j->copy_len[b], j->copy_tokens + b * K,
+                                       j->z[b], j->ntok + b * R,
+                                       j->npar ? j->npar + b * R : NULL, j->nn[b], j->R,
+                                       j->cfg, j->dtok + b * R, j->dpar + b * R, &j->dn[b]);
+        int32_t *am = j->amax + b * R;
+        for (int32_t r = 0; r < j->R; ++r)
+            am[r] = r < j->dn[b] ? oracle_argmax_row(j->logits + ((int64_t)b * R + r) * V, j->V)
+                                 : -1;
+        oracle_accept(j->dtok + b * R, j->dpar + b * R, j->dn[b], am, j->R,
+                      &j->accept_len[b], &j->accept_node[b], &j->bonus[b],
+                      j->out_tokens + b * R);
+    }
+}
+
+static void *step_thread(void *arg)
+{
+    step_range((const step_job *)arg);
+    return NULL;
+}
+
+int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
+                const int32_t *tokens, const int32_t *lengths,
+                const uint16_t *hidden, const float *w, float bias,
+                const int32_t *ntok, const int32_t *npar, const int32_t *nn,
+                const uint16_t *logits, const oracle_cfg *cfg,
+                int32_t *match_n, int32_t *match_end, int32_t *copy_len,
+                int32_t *copy_tokens, float *z, int32_t *use_copy,
+                int32_t *dtok, int32_t *dpar, int32_t *dn, int32_t *amax,
+                int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                int32_t *out_tokens, int32_t threads)
+{
+    if (B < 0 || Lmax < 1 || d < 0 || R < 1 || V < 1 || !cfg || cfg->k < 0 || cfg->k + 1 > R)
+        return -1;
+    if (cfg->n_ngram < 1 || cfg->n_ngram > ORACLE_MAX_NGRAM)
+        return -1;
+    if (threads < 1)
+        threads = 1;
+    if (threads > B)
+        threads = B > 0 ? B : 1;
+    step_job base = {0, 0, Lmax, d, R, V, tokens, lengths, hidden, w, bias, ntok, npar, nn,
+                     logits, cfg, match_n, match_end, copy_len, copy_tokens, z, use_copy,
+                     dtok, dpar, dn, amax, accept_len, accept_node, bonus, out_tokens};
+    if (threads == 1) {
+        base.b0 = 0;
+        base.b1 = B;
+        step_range(&base);
+        return 0;
+    }
+    step_job *jobs = (step_job *)malloc(sizeof(step_job) * (size_t)threads);
+    pthread_t *tid = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)threads);
+    for (int32_t t = 0; t < threads; ++t) {
+        jobs[t] = base;
+        jobs[t].b0 = (int32_t)((int64_t)B * t / threads);
+        jobs[t].b1 = (int32_t)((int64_t)B * (t + 1) / threads);
+        pthread_create(&tid[t], NULL, step_thread, &jobs[t]);
+    }
+    for (int32_t t = 0; t < threads; ++t)
+        pthread_join(tid[t], NULL);
+    free(jobs);
+    free(tid);
+    return 0;
+}

@@ -1,0 +1,88 @@
+/*
+ * switchsd_oracle.h -- plain, slow CPU oracle of SwitchSD's per-step
+ * speculation-control path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library includes,
+ * links or calls this code; only the test-suite, the smoke check and the
+ * CPU-baseline leg of the benchmark do.  It shares no source with the HIP
+ * path: every step below is written out from the paper's definitions.
+ *
+ * Paper: "To Copy or Not to Copy: Controlling Speculative Decoding via
+ * Intrinsic Model Signals" (SwitchSD).
+ *   step 1  suffix n-gram match      -- Sec. 3.3 (Copy-Intent Decision Rule:
+ *                                       kappa-gram with a prior occurrence;
+ *                                       Copy-Based Speculative Generation:
+ *                                       candidates ranked by recency)
+ *   step 2  copy-intent probe        -- Sec. 3.2, Eq. 3 (linear, sigmoid)
+ *   step 3  copy / neural switch     -- Sec. 3.3, Eq. 4 plus the kappa gate
+ *   step 4  greedy verification      -- Sec. 2 (Speculative Decoding), Sec. 3.3
+ *                                       (select the longest validated
+ *                                       continuation), App. A (T = 0)
+ *
+ * All pointers are host pointers.  Arrays are contiguous, row-major.
+ */
+#ifndef SWITCHSD_ORACLE_H
+#define SWITCHSD_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ORACLE_MAX_NGRAM 8
+
+typedef struct {
+    int32_t n_ngram;                      /* number of n-gram lengths tried     */
+    int32_t ngram_lens[ORACLE_MAX_NGRAM]; /* tried in this order (longest first) */
+    int32_t kappa;                        /* copy only if match_n >= kappa       */
+    int32_t k;                            /* maximum copy-draft length           */
+    float theta;                          /* probe threshold as a logit          */
+} oracle_cfg;
+
+/* Step 1 for one sequence x[0..L-1].  Writes match_n, match_end, copy_len
+ * and copy_tokens[0..k-1] (-1 padded).  Returns 0. */
+int oracle_match(const int32_t *x, int32_t L, const oracle_cfg *cfg,
+                 int32_t *match_n, int32_t *match_end, int32_t *copy_len,
+                 int32_t *copy_tokens);
+
+/* Step 2 for one hidden vector: z = w . h + bias, rounded once to float. */
+float oracle_probe(const uint16_t *h_bf16, const float *w, int32_t d, float bias);
+
+/* Step 3 for one sequence.  Writes the chosen draft in node layout
+ * (R rows; node 0 is the anchor).  Returns use_copy. */
+int32_t oracle_select(int32_t match_n, int32_t copy_len, const int32_t *copy_tokens,
+                      float z, const int32_t *ntok, const int32_t *npar,
+                      int32_t nn, int32_t R, const oracle_cfg *cfg,
+                      int32_t *dtok, int32_t *dpar, int32_t *dn);
+
+/* Step 4a: lowest index of the largest bf16 value of one row. */
+int32_t oracle_argmax_row(const uint16_t *row_bf16, int32_t V);
+
+/* Step 4b: accept walk over a chosen draft given the argmax of every
+ * draft row.  Writes accept_len, accept_node, bonus and out_tokens[R]. */
+void oracle_accept(const int32_t *dtok, const int32_t *dpar, int32_t dn,
+                   const int32_t *amax, int32_t R,
+                   int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                   int32_t *out_tokens);
+
+/* The whole step for B sequences; threads > 1 splits the batch across
+ * POSIX threads (sequences are independent).  npar may be NULL (chains).
+ * amax [B,R] receives the argmax of rows r < dn[b] and -1 elsewhere.
+ * Returns 0, or -1 on a bad argument. */
+int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
+                const int32_t *tokens, const int32_t *lengths,
+                const uint16_t *hidden, const float *w, float bias,
+                const int32_t *ntok, const int32_t *npar, const int32_t *nn,
+                const uint16_t *logits, const oracle_cfg *cfg,
+                int32_t *match_n, int32_t *match_end, int32_t *copy_len,
+                int32_t *copy_tokens, float *z, int32_t *use_copy,
+                int32_t *dtok, int32_t *dpar, int32_t *dn, int32_t *amax,
+                int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                int32_t *out_tokens, int32_t threads);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

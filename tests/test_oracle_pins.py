@@ -1,0 +1,257 @@
+"""Pins of the CPU oracle that do not come from the oracle itself.
+
+* hand-worked golden fixtures (tests/golden, derivations in each line);
+* invariants of the definitions (I1-I10) on planted and random inputs;
+* special cases that reduce to a known rule: CopySpec (theta = -inf: copy iff
+  a match exists), probe switched off (theta = +inf), the paper's own
+  setting (kappa = 5, D = 20), closed-form probe scores.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_20186_amd import workloads as wlmod
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _lines(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [json.loads(s) for s in f if s.strip()]
+
+
+def _bits(hexes):
+    return np.array([int(h, 16) for h in hexes], np.uint16)
+
+
+@pytest.mark.parametrize("case", _lines("match_cases.jsonl"), ids=lambda c: c["why"][:40])
+def test_golden_match(case):
+    cfg = oracle.make_cfg(case["lens"], 1, case["k"], 0.0)
+    mn, me, cl, ct = oracle.match(np.array(case["tokens"], np.int32), case["L"], cfg)
+    assert (mn, me, cl) == (case["match_n"], case["match_end"], case["copy_len"])
+    assert ct.tolist() == case["copy_tokens"]
+
+
+@pytest.mark.parametrize("case", _lines("argmax_cases.jsonl"), ids=lambda c: c["why"][:40])
+def test_golden_argmax(case):
+    assert oracle.argmax_row(_bits(case["row"])) == case["amax"]
+
+
+@pytest.mark.parametrize("case", _lines("accept_cases.jsonl"), ids=lambda c: c["why"][:40])
+def test_golden_accept(case):
+    al, an, bo, out = oracle.accept(case["dtok"], case["dpar"], case["dn"], case["amax"],
+                                    case["R"])
+    assert (al, an, bo) == (case["accept_len"], case["accept_node"], case["bonus"])
+    assert out.tolist() == case["out_tokens"]
+
+
+@pytest.mark.parametrize("case", _lines("probe_cases.jsonl"), ids=lambda c: c["why"][:40])
+def test_golden_probe(case):
+    z = oracle.probe(_bits(case["h"]), np.array(case["w"], np.float32), case["bias"])
+    assert z == np.float32(case["z"])
+
+
+# ---------------------------------------------------------------- invariants
+
+def test_I1_planted_span_found_c1():
+    """C1 repeats the head of a source window at the end of the context, so the
+    suffix 3-gram occurs inside the source window (unless brute force finds a
+    more recent coincidence, which uniform tokens over 32000 make unlikely)."""
+    wl = wlmod.WORKLOADS["C1"]
+    d = wlmod.generate(wl, logits=False)
+    cfg = oracle.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    x = d["tokens"][0]
+    mn, me, cl, ct = oracle.match(x, wl.L, cfg)
+    assert mn == 3 and cl == wl.k
+    # the continuation is the token stream right after the occurrence
+    assert ct.tolist() == x[me + 1:me + 1 + wl.k].tolist()
+    # the occurrence is inside the planted source window: its next 5 tokens
+    # were not copied to the end, so they differ from what follows nowhere
+    assert me < wl.L - 64
+
+
+def test_I2_longest_first():
+    x = np.array([7, 1, 2, 3, 4, 4, 2, 3, 5, 5, 2, 3, 1, 2, 3], np.int32)
+    cfg = oracle.make_cfg((3, 2, 1), 1, 3, 0.0)
+    mn, me, _, _ = oracle.match(x, x.size, cfg)
+    assert (mn, me) == (3, 3)           # older (1,2,3) beats newer (2,3) at e=11
+
+
+def test_I3_most_recent():
+    x = np.array([1, 2, 3, 8, 1, 2, 3, 9, 1, 2, 3], np.int32)
+    cfg = oracle.make_cfg((3,), 1, 2, 0.0)
+    mn, me, cl, ct = oracle.match(x, x.size, cfg)
+    assert (mn, me, cl, ct.tolist()) == (3, 6, 2, [9, 1])
+
+
+def test_I4_copy_len_iff_match():
+    rng = np.random.default_rng(3)
+    for _ in range(300):
+        L = int(rng.integers(0, 60))
+        x = rng.integers(0, 4, max(L, 1)).astype(np.int32)
+        k = int(rng.integers(0, 9))
+        cfg = oracle.make_cfg((4, 2), 1, k, 0.0)
+        mn, me, cl, ct = oracle.match(x, L, cfg)
+        if mn > 0:
+            assert min(1, k) <= cl <= k and 0 <= me <= L - 2
+            assert ct[:cl].tolist() == x[me + 1:me + 1 + cl].tolist()
+            assert (ct[cl:] == -1).all()
+        else:
+            assert cl == 0 and me == -1 and (ct == -1).all()
+
+
+def test_I5_probe_closed_forms():
+    rng = np.random.default_rng(9)
+    d = 4096
+    w = rng.standard_normal(d).astype(np.float32)
+    assert oracle.probe(np.zeros(d, np.uint16), w, -2.0) == np.float32(-2.0)
+    for i in (0, 17, d - 1):
+        h = np.zeros(d, np.uint16)
+        h[i] = 0x3F80
+        assert oracle.probe(h, w, 0.5) == np.float32(np.float64(w[i]) + 0.5)
+    assert oracle.probe(np.full(d, 0x3F80, np.uint16), np.full(d, 1.0 / d, np.float32),
+                        0.25) == np.float32(1.25)
+    # sign flip of h negates the score (bias 0)
+    h = wlmod.f32_to_bf16_bits(rng.standard_normal(d).astype(np.float32))
+    assert oracle.probe(h ^ np.uint16(0x8000), w, 0.0) == -oracle.probe(h, w, 0.0)
+
+
+def test_I6_switch_truth_table():
+    R, k = 6, 3
+    ntok = np.array([-1, 11, 12, 13, 14, 15], np.int32)
+    ct = np.array([21, 22, 23], np.int32)
+    for (mn, z, kappa, theta, want) in [
+        (0, 5.0, 1, 0.0, 0),        # no match: neural whatever the probe says
+        (3, -0.1, 1, 0.0, 0),       # match, probe below threshold: neural
+        (3, 0.0, 1, 0.0, 1),        # match, probe at threshold (>=): copy
+        (3, 2.0, 1, 0.0, 1),        # match and probe: copy
+        (2, 2.0, 3, 0.0, 0),        # match shorter than kappa: neural
+        (3, -1e30, 1, -np.inf, 1),  # CopySpec: theta=-inf, copy iff match
+        (0, -1e30, 1, -np.inf, 0),
+        (3, 1e30, 1, np.inf, 0),    # probe switched off
+    ]:
+        cfg = oracle.make_cfg((3, 2, 1), kappa, k, theta)
+        uc, dtok, dpar, dn = oracle.select(mn, 3 if mn else 0, ct, z, ntok, None, 6, R, cfg)
+        assert uc == want
+        if want:
+            assert dn == 4 and dtok.tolist() == [-1, 21, 22, 23, -1, -1]
+            assert dpar.tolist() == [-1, 0, 1, 2, -1, -1]
+        else:
+            assert dn == 6 and dtok.tolist() == [-1, 11, 12, 13, 14, 15]
+            assert dpar.tolist() == [-1, 0, 1, 2, 3, 4]
+
+
+def test_I7_argmax_ties_and_specials():
+    row = np.full(1000, 0x3F80, np.uint16)
+    row[[700, 300]] = 0x4000
+    assert oracle.argmax_row(row) == 300
+    row[100] = 0x7FC0                   # NaN ignored
+    assert oracle.argmax_row(row) == 300
+
+
+def _random_drafts(rng, B, R, V):
+    ntok = rng.integers(0, V, (B, R)).astype(np.int32)
+    npar = np.zeros((B, R), np.int32)
+    for b in range(B):
+        npar[b, 0] = -1
+        for i in range(1, R):
+            npar[b, i] = int(rng.integers(0, i))
+    return ntok, npar
+
+
+def test_I8_I9_accept_bounds_and_path():
+    rng = np.random.default_rng(21)
+    for _ in range(300):
+        R = int(rng.integers(1, 12))
+        V = int(rng.integers(1, 4))
+        ntok, npar = _random_drafts(rng, 1, R, V)
+        dn = int(rng.integers(1, R + 1))
+        amax = rng.integers(0, V, R).astype(np.int32)
+        al, an, bo, out = oracle.accept(ntok[0], npar[0], dn, amax, R)
+        assert 0 <= al <= dn - 1 <= R - 1 and 0 <= an < dn
+        assert bo == amax[an]
+        # the accepted tokens are the path root -> an, each matching amax at its parent
+        path = []
+        n = an
+        while n:
+            path.append(n)
+            n = int(npar[0][n])
+        path.reverse()
+        assert len(path) == al
+        assert out[:al].tolist() == [int(ntok[0][p]) for p in path]
+        prev = 0
+        for p in path:
+            assert ntok[0][p] == amax[prev]
+            prev = p
+        assert out[al] == bo and (out[al + 1:] == -1).all()
+
+
+def test_chain_as_tree_equals_chain():
+    rng = np.random.default_rng(4)
+    for _ in range(200):
+        R = int(rng.integers(2, 10))
+        dtok = rng.integers(0, 3, R).astype(np.int32)
+        amax = rng.integers(0, 3, R).astype(np.int32)
+        dn = int(rng.integers(1, R + 1))
+        chain_par = np.arange(-1, R - 1, dtype=np.int32)
+        r1 = oracle.accept(dtok, chain_par, dn, amax, R)
+        # chain rule: longest prefix with dtok[i] == amax[i-1]
+        a = 0
+        while a + 1 < dn and dtok[a + 1] == amax[a]:
+            a += 1
+        assert r1[0] == a and r1[1] == a and r1[2] == amax[a]
+
+
+@pytest.mark.parametrize("name,batch", [("C1", [0]), ("C2", [0, 5, 17]), ("C3", [1, 40]),
+                                        ("C4", [2]), ("C5", [0, 3, 100])])
+def test_I10_planted_acceptance_reproduced(name, batch):
+    wl = wlmod.WORKLOADS[name]
+    d = wlmod.generate(wl, batch=batch)
+    cfg = oracle.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    args = (d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"], d["npar"],
+            d["nn"])
+    first = oracle.step(*args, d["logits"], cfg)
+    target = wlmod.plant_batch(wl, d, first)
+    res = oracle.step(*args, d["logits"], cfg)
+    for key in ("use_copy", "dtok", "dpar", "dn", "match_n", "z"):
+        np.testing.assert_array_equal(res[key], first[key])    # planting touches logits only
+    np.testing.assert_array_equal(res["accept_node"], target)
+    for j in range(len(batch)):
+        assert res["accept_len"][j] == wlmod.depth_of(res["dpar"][j], int(target[j]))
+
+
+def test_paper_setting_single_candidate():
+    """kappa = 5 with a single length 5 and D = k = 20 (Sec. 3.3, App. D)."""
+    rng = np.random.default_rng(8)
+    src = rng.integers(0, 50, 60).astype(np.int32)
+    x = np.concatenate([src, rng.integers(50, 100, 30).astype(np.int32), src[:12]])
+    cfg = oracle.make_cfg((5,), 5, 20, 0.0)
+    mn, me, cl, ct = oracle.match(x, x.size, cfg)
+    assert (mn, me, cl) == (5, 11, 20)
+    assert ct.tolist() == src[12:32].tolist()
+    # a 4-token overlap is not enough for kappa = 5
+    cfg4 = oracle.make_cfg((5, 4), 5, 20, 0.0)
+    y = np.concatenate([src[:20], rng.integers(50, 100, 10).astype(np.int32), src[:4]])
+    mn, _, _, _ = oracle.match(y, y.size, cfg4)
+    assert mn == 4
+    uc, _, _, _ = oracle.select(mn, 20, np.arange(20, dtype=np.int32), 3.0,
+                                np.zeros(21, np.int32), None, 21, 21, cfg4)
+    assert uc == 0
+
+
+def test_workload_statistics():
+    """The generator's structure matches its recipe (span fraction, Zipf head)."""
+    wl = wlmod.WORKLOADS["C2"]
+    q = wlmod.span_start_prob(wl)
+    assert abs(q - 0.00297) < 2e-5
+    d = wlmod.generate(wl, batch=range(4), logits=False)
+    top = np.mean(d["tokens"] == 0)
+    assert 0.08 < top < 0.2                          # Zipf(1.1) head ~13%
+    again = wlmod.generate(wl, batch=[2], logits=False)
+    np.testing.assert_array_equal(again["tokens"][0], d["tokens"][2])   # per-sequence streams
+    p = wlmod.tree_parents(wlmod.WORKLOADS["C5"])
+    depth = [wlmod.depth_of(p, i) for i in range(len(p))]
+    assert max(depth) <= 7 and all(p[i] < i for i in range(1, len(p)))
