@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Benchmark of SwitchSD's speculation-control step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C2]
+
+One step = one call of ``switchsd_step`` over the whole batch: suffix n-gram
+match, probe, copy/neural switch, verify-argmax and accept for all B
+sequences, inputs resident in HBM.  The default workload is the Llama-3-8B
+shaped copy-heavy batch (B=32, L=4096, V=128256, d=4096, k=7).  Input sets
+are rotated so that more than 512 MB is touched between two uses of one set:
+the 256 MB Infinity Cache cannot serve a step from the previous one.
+
+Prints ONE JSON line (steps/s, ms/step, the fused kernel against the HBM
+roofline, the verify-argmax rate, and the CPU oracle timed on a bounded sample
+of the same workload on this host).
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2609_20186_amd import workloads as W  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "speculation-control steps/s + verify-argmax HBM GB/s (% peak), B=32 V=128256"
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_20186_amd", "csrc", "switchsd_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fused_step_C2.json")
+ROTATE_BYTES = 512 << 20
+
+
+def kernel_sha():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(wl, rows_read, d_sel=None):
+    """Bytes one step must move at least: each context token once, the hidden
+    states and probe weight, every logits row it reads, the neural draft and
+    the outputs."""
+    B, R, k = wl.B, wl.R, wl.k
+    ins = B * wl.L * 4 + B * 4 + B * wl.d * 2 + wl.d * 4 + B * R * 4 + B * 4
+    if not wl.chain:
+        ins += B * R * 4
+    logits = int(np.sum(rows_read)) * wl.V * 2
+    outs = B * 4 * 3 + B * k * 4 + B * 4 * 2 + B * R * 4 * 2 + B * 4 + B * R * 4 + B * 4 * 3 + \
+        B * R * 4
+    return ins + logits + outs, logits
+
+
+def upload(d):
+    import torch
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    return {"tokens": t(d["tokens"]), "lengths": t(d["lengths"]),
+            "hidden": t(d["hidden"].view(np.int16)), "w": t(d["w"]), "ntok": t(d["ntok"]),
+            "npar": None if d["npar"] is None else t(d["npar"]), "nn": t(d["nn"]),
+            "logits": t(d["logits"].view(np.int16)), "bias": float(d["bias"])}
+
+
+def plant_with_library(wl, d, sd):
+    """Plant the logits for the drafts the library itself selects (its split
+    step's front half writes the draft before any row is read)."""
+    import torch
+    dev = upload(d)
+    out = sd.alloc_outputs(wl.B, wl.R, wl.k)
+    ws = sd.alloc_workspace(wl.B, wl.R)
+    cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    sd.switchsd_step(sd.build_step_args(dev, out, cfg, sd.MODE_SPLIT), ws)
+    torch.cuda.synchronize()
+    sel = {k: out[k].cpu().numpy() for k in ("dtok", "dpar", "dn", "use_copy")}
+    W.plant_batch(wl, d, sel)
+    return sel
+
+
+def cpu_baseline(wl_name, budget_s):
+    """The oracle as it stands, on this host's cores, over whole steps of the
+    same workload (inputs generated and planted on the CPU), repeated until
+    about `budget_s` seconds of work."""
+    import oracle
+    wl = W.WORKLOADS[wl_name]
+    d = W.generate(wl)
+    cfg = oracle.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    sel = oracle.front(d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"],
+                       d["npar"], d["nn"], cfg)
+    W.plant_batch(wl, d, sel)
+    threads = max(1, min(16, os.cpu_count() or 1))
+    args = (d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"], d["npar"],
+            d["nn"], d["logits"], cfg)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.step(*args, threads=threads)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 100000:
+            break
+    return {"value": n / el, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} whole {wl_name} steps (B={wl.B}, all sequences) in {el:.1f} s, "
+                      f"{threads} threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--workload", default="C2", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--mode", type=int, default=0, help="0 auto, 1 fused, 2 split")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the speculation-control step shards by sequence with "
+              "no exchange, and this build runs on a single MI355X. Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_20186_amd import binding as sd
+
+    wl = W.WORKLOADS[args.workload]
+    print(f"[bench] generating {wl.name} inputs", file=sys.stderr, flush=True)
+    d = W.generate(wl)
+    sel = plant_with_library(wl, d, sd)
+
+    base = upload(d)
+    step_bytes = d["logits"].nbytes + d["tokens"].nbytes + d["hidden"].nbytes
+    nrot = max(1, math.ceil(ROTATE_BYTES / step_bytes))
+    sets = [base] + [{k: (v.clone() if hasattr(v, "clone") else v) for k, v in base.items()}
+                     for _ in range(nrot - 1)]
+    cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    outs = [sd.alloc_outputs(wl.B, wl.R, wl.k) for _ in range(nrot)]
+    ws = sd.alloc_workspace(wl.B, wl.R)
+    step_args = [sd.build_step_args(s, o, cfg, args.mode) for s, o in zip(sets, outs)]
+    import ctypes
+    lib = sd.lib
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+    wsp, wsn = ws.data_ptr(), ws.numel()
+    refs = [ctypes.byref(a) for a in step_args]
+
+    def run(n):
+        for i in range(n):
+            rc = lib.switchsd_step(refs[i % nrot], wsp, wsn, sptr)
+            if rc:
+                raise sd.SwitchsdError("switchsd_step", rc)
+
+    run(args.warmup)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    run(args.steps)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # every rotation set must agree with the first (same inputs, same outputs)
+    o0 = {k: v.cpu() for k, v in outs[0].items()}
+    for o in outs[1:]:
+        for k, v in o.items():
+            assert torch.equal(v.cpu(), o0[k]), f"rotation set disagrees on {k}"
+
+    mode = args.mode or (sd.MODE_FUSED if wl.k + 1 >= wl.R else sd.MODE_SPLIT)
+    if mode == sd.MODE_FUSED:
+        rows_read = np.maximum(np.clip(d["nn"], 1, wl.R), wl.k + 1) if wl.k + 1 < wl.R \
+            else np.full(wl.B, wl.R)
+    else:
+        rows_read = sel["dn"]
+    alg, alg_logits = algorithmic_bytes(wl, rows_read)
+    step_gbps = alg / (ms * 1e-3) / 1e9
+
+    # verify-argmax alone (stage entry point), rows of the chosen draft
+    vouts = outs
+    def run_verify(n):
+        for i in range(n):
+            s, o = sets[i % nrot], vouts[i % nrot]
+            sd.switchsd_verify_accept(s["logits"], o["dtok"], o["dpar"], o["dn"], o["accept_len"],
+                                      o["accept_node"], o["bonus"], o["out_tokens"], o["amax"],
+                                      ws)
+    nv = max(200, args.steps // 4)
+    run_verify(20)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    run_verify(nv)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    vms = e0.elapsed_time(e1) / nv
+    vbytes = int(np.sum(sel["dn"])) * wl.V * 2
+    v_gbps = vbytes / (vms * 1e-3) / 1e9
+
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("kernel_sha") == kernel_sha() and tr.get("workload") == wl.name:
+            traffic = tr.get("hbm_bytes_per_launch")
+
+    res = {
+        "metric": METRIC, "value": round(1e3 / ms, 1), "unit": "steps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: B={wl.B} L={wl.L} V={wl.V} d={wl.d} k={wl.k} R={wl.R}"
+                               f" ngram={list(wl.ngram_lens)} kappa={wl.kappa}",
+                   "global_batch": wl.B, "seq_len": wl.L, "parallelism": "none (1 GPU)",
+                   "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode],
+                   "rotation_sets": nrot},
+        "roofline": {"bound": "hbm", "achieved": round(step_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "kernel": "k_switchsd (fused step)",
+                     "algorithmic_bytes_per_launch": alg},
+        "verify_argmax": {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),
+                          "us_per_call": round(vms * 1e3, 2), "bytes_per_call": vbytes},
+        "copy_fraction": round(float(np.mean(sel["use_copy"])), 3),
+        "mean_accept_len": round(float(o0["accept_len"].float().mean()), 3),
+        "kernel_sha": kernel_sha(),
+    }
+    if not args.no_cpu:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(wl.name, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,187 @@
+/*
+ * switchsd.h -- C ABI of the SwitchSD speculation-control library (gfx950).
+ *
+ * Paper: "To Copy or Not to Copy: Controlling Speculative Decoding via
+ * Intrinsic Model Signals".  One decoding step of SwitchSD, for B sequences:
+ *
+ *   1. suffix n-gram match over the token history (the copy candidate) --
+ *      Sec. 3.3, Copy-Intent Decision Rule (a kappa-gram ending at the current
+ *      token must have a prior occurrence) and Copy-Based Speculative
+ *      Generation (continuations taken from the context, ranked by recency);
+ *   2. linear copy-intent probe on the target's hidden state -- Sec. 3.2,
+ *      Eq. 3 (p = sigmoid(w^T H), no bias in the paper; an optional bias is
+ *      carried here);
+ *   3. copy-versus-neural switch -- Sec. 3.3, Eq. 4 plus the kappa gate;
+ *   4. greedy verification -- Sec. 2 (Speculative Decoding) and App. A
+ *      (T = 0): the target's token at each drafted position is the argmax of
+ *      its logits, and the longest validated continuation is kept (Sec. 3.3,
+ *      Parallel Verification) together with the target's next token (bonus).
+ *
+ * Conventions for every entry point:
+ *   - All array pointers are DEVICE pointers owned by the caller; arrays are
+ *     contiguous and row-major.  The library never allocates or frees.
+ *   - Every call is asynchronous on `stream` and never synchronizes; outputs
+ *     are valid once the caller has synchronized with the stream.
+ *   - bf16 values are passed as their 16-bit patterns (uint16_t).
+ *   - Token ids are int32 and only compared for equality; -1 pads outputs.
+ *   - Drafts use a node layout of R rows per sequence: node 0 is the anchor
+ *     (the last context token; its token field is -1, its parent -1), node i
+ *     has parent dpar[i] < i.  Row r of the logits is the target's output at
+ *     node r, so node i is accepted iff its parent p is accepted and
+ *     dtok[i] == argmax(logits[p]).  A chain of m tokens is nodes 1..m with
+ *     dpar[i] = i - 1 and dn = m + 1.
+ *   - Device data is not validated, but it cannot make the library read or
+ *     write out of bounds: lengths are clamped to [0, Lmax], node counts to
+ *     [1, R], and a node whose parent is not in [0, i) is never accepted.
+ *   - Host-side validation runs before any HIP call; on failure a negative
+ *     status is returned and nothing is launched.  B = 0 is a valid no-op.
+ *   - Calls that take a workspace need `switchsd_workspace_bytes(B, R)`
+ *     bytes, 256-byte aligned, zeroed once by the caller at allocation.
+ *     Every kernel leaves the workspace zeroed again when it completes, so no
+ *     per-call clearing is needed.  After a call fails inside HIP, or if the
+ *     stream is torn down mid-call, zero it again.  Calls that share one
+ *     workspace must be ordered (same stream, or synchronized).
+ */
+#ifndef SWITCHSD_H
+#define SWITCHSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hipStream_t;
+
+typedef enum {
+    SWITCHSD_OK = 0,
+    SWITCHSD_EINVAL = -1,    /* null pointer, bad configuration value        */
+    SWITCHSD_ESHAPE = -2,    /* sizes out of range or inconsistent           */
+    SWITCHSD_EHIP = -3,      /* a HIP runtime call or kernel launch failed   */
+    SWITCHSD_EWORKSPACE = -4 /* workspace null, misaligned or too small      */
+} switchsd_status;
+
+#define SWITCHSD_MAX_NGRAM 8       /* most n-gram lengths in one configuration  */
+#define SWITCHSD_MAX_NGRAM_LEN 64  /* longest n-gram length                     */
+#define SWITCHSD_MAX_R 1024        /* most draft nodes (logits rows) per sequence */
+
+/* Step configuration.
+ *   ngram_lens  lengths searched, strictly descending, each in [1, 64]; the
+ *               first length with an occurrence wins, and among its
+ *               occurrences the most recent one (Sec. 3.3, recency).
+ *               The paper's setting is {5}; the synthetic workloads use {3,2,1}.
+ *   kappa       copy is allowed only if the matched length is >= kappa
+ *               (the paper's kappa = 5).  kappa >= 1.
+ *   k           maximum copy-draft length (the paper's D = 20); k + 1 <= R.
+ *   theta       probe threshold as a logit: copy needs z >= theta, which is
+ *               sigmoid(z) >= tau for theta = log(tau / (1 - tau)).
+ *               -inf gives the CopySpec rule (copy iff a match exists),
+ *               +inf or NaN switches copying off. */
+typedef struct {
+    int32_t n_ngram;
+    int32_t ngram_lens[SWITCHSD_MAX_NGRAM];
+    int32_t kappa;
+    int32_t k;
+    float theta;
+} switchsd_cfg;
+
+/* Step 1 -- Sec. 3.3.  For each sequence b with L = clamp(lengths[b], 0, Lmax)
+ * and context x = tokens[b, 0..L-1]: for each n in cfg->ngram_lens (in
+ * order), the occurrences of the suffix x[L-n..L-1] that end at e <= L-2
+ * (overlap with the suffix allowed).  The first n with an occurrence gives
+ * match_n[b] = n and match_end[b] = the largest such e; the copy candidate is
+ * copy_tokens[b, j] = x[e+1+j] for j < copy_len[b] = min(k, L-1-e), -1 after.
+ * Without an occurrence: match_n = 0, match_end = -1, copy_len = 0.
+ *   tokens [B, Lmax] int32, lengths [B] int32;
+ *   outputs match_n, match_end, copy_len [B] int32, copy_tokens [B, k] int32
+ *   (may be NULL when k == 0). */
+int switchsd_ngram_match(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
+                         const switchsd_cfg *cfg, int32_t *match_n, int32_t *match_end,
+                         int32_t *copy_len, int32_t *copy_tokens, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+
+/* Step 2 -- Sec. 3.2, Eq. 3.  z[b] = sum_i h[b,i] * w[i] + bias, with every
+ * product exact and the sum carried in double-double, rounded once to float.
+ * The probability of copy-mode is sigmoid(z[b]).
+ *   hidden [B, d] bf16 bits, w [d] float, z [B] float.  d may be 0 (z = bias). */
+int switchsd_probe_score(const uint16_t *hidden, const float *w, float bias, int32_t B,
+                         int32_t d, float *z, hipStream_t stream);
+
+/* Step 3 -- Sec. 3.3, Eq. 4 and the kappa gate.
+ * use_copy[b] = (match_n[b] >= kappa) && (z[b] >= theta).  The chosen draft is
+ * written in node layout: copy -> the chain of copy_tokens[b, 0..copy_len-1]
+ * (dn = copy_len + 1); neural -> the neural draft as given (ntok/npar, with
+ * nn[b] nodes including the anchor; npar == NULL means a chain).  Rows at and
+ * beyond dn[b] hold -1.
+ *   match_n, copy_len [B] int32, copy_tokens [B, k] int32, z [B] float,
+ *   ntok [B, R] int32, npar [B, R] int32 or NULL, nn [B] int32;
+ *   outputs use_copy, dn [B] int32, dtok, dpar [B, R] int32. */
+int switchsd_select_draft(const int32_t *match_n, const int32_t *copy_len,
+                          const int32_t *copy_tokens, const float *z, const int32_t *ntok,
+                          const int32_t *npar, const int32_t *nn, int32_t B, int32_t R,
+                          const switchsd_cfg *cfg, int32_t *use_copy, int32_t *dtok,
+                          int32_t *dpar, int32_t *dn, hipStream_t stream);
+
+/* Step 4 -- Sec. 2, Sec. 3.3 (Parallel Verification), App. A (T = 0).
+ * For each row r < dn[b]: amax[b,r] = the lowest index holding the largest
+ * value of logits[b,r,:] (-0 equals +0, NaN is below every number, a row of
+ * NaN gives 0); rows r >= dn[b] are not read and give amax = -1.  Accepted
+ * nodes: node 0, and node i when its parent is accepted and
+ * dtok[b,i] == amax[b,dpar[b,i]].  accept_node[b] = the deepest accepted node
+ * (ties to the lowest index), accept_len[b] = its depth,
+ * bonus[b] = amax[b, accept_node[b]], out_tokens[b, :] = the accepted path
+ * tokens (anchor excluded), then the bonus, then -1.
+ *   logits [B, R, V] bf16 bits (2-byte aligned), dtok/dpar [B, R], dn [B];
+ *   dpar == NULL means chains; amax [B, R] may be NULL. */
+int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
+                           const int32_t *dtok, const int32_t *dpar, const int32_t *dn,
+                           int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                           int32_t *out_tokens, int32_t *amax, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+/* How switchsd_step schedules its work. */
+typedef enum {
+    SWITCHSD_MODE_AUTO = 0,  /* FUSED when every row may be needed (k + 1 >= R), else SPLIT */
+    SWITCHSD_MODE_FUSED = 1, /* one launch; reads rows r < max(nn[b], k + 1)                */
+    SWITCHSD_MODE_SPLIT = 2  /* two launches; reads only rows r < dn[b] of the chosen draft  */
+} switchsd_mode;
+
+/* All arguments of one step (steps 1-4 in order).  Inputs as in the stage
+ * calls above; every output pointer is required except amax. */
+typedef struct {
+    const int32_t *tokens;   /* [B, Lmax] */
+    const int32_t *lengths;  /* [B]       */
+    const uint16_t *hidden;  /* [B, d] bf16 bits */
+    const float *w;          /* [d]       */
+    const int32_t *ntok;     /* [B, R] neural draft tokens */
+    const int32_t *npar;     /* [B, R] neural draft parents, NULL = chains */
+    const int32_t *nn;       /* [B] neural draft node count (anchor included) */
+    const uint16_t *logits;  /* [B, R, V] bf16 bits */
+    int32_t B, Lmax, d, R, V;
+    float bias;
+    switchsd_cfg cfg;
+    int32_t mode;            /* switchsd_mode */
+    int32_t *match_n, *match_end, *copy_len, *copy_tokens; /* [B],[B],[B],[B,k] */
+    float *z;                                              /* [B] */
+    int32_t *use_copy, *dtok, *dpar, *dn;                  /* [B],[B,R],[B,R],[B] */
+    int32_t *amax;                                         /* [B, R] or NULL */
+    int32_t *accept_len, *accept_node, *bonus, *out_tokens; /* [B],[B],[B],[B,R] */
+} switchsd_step_args;
+
+/* One whole step.  Results are identical to calling the four stage entry
+ * points in order; MODE_FUSED does it in one kernel launch. */
+int switchsd_step(const switchsd_step_args *args, void *workspace, size_t workspace_bytes,
+                  hipStream_t stream);
+
+/* Workspace bytes needed by calls with B sequences of R rows. */
+size_t switchsd_workspace_bytes(int32_t B, int32_t R);
+
+/* Static, thread-safe text of a status code. */
+const char *switchsd_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

@@ -164,3 +164,26 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=
         raise ValueError("oracle_step rejected its arguments")
     o["copy_tokens"] = o["copy_tokens"][:, :K]
     return o
+
+
+def front(tokens, lengths, hidden, w, bias, ntok, npar, nn, cfg):
+    """Steps 1-3 for every sequence (match, probe, switch), no logits needed."""
+    tokens = _c(tokens, np.int32)
+    B, Lmax = tokens.shape
+    R = ntok.shape[1]
+    o = {k: np.zeros(B, np.int32) for k in ("match_n", "match_end", "copy_len", "use_copy", "dn")}
+    o["z"] = np.zeros(B, np.float32)
+    o["copy_tokens"] = np.zeros((B, cfg.k), np.int32)
+    o["dtok"] = np.zeros((B, R), np.int32)
+    o["dpar"] = np.zeros((B, R), np.int32)
+    for b in range(B):
+        L = max(0, min(int(lengths[b]), Lmax))
+        mn, me, cl, ct = match(tokens[b], L, cfg)
+        z = probe(hidden[b], w, bias)
+        uc, dtok, dpar, dn = select(mn, cl, ct, z, ntok[b], None if npar is None else npar[b],
+                                    nn[b], R, cfg)
+        o["match_n"][b], o["match_end"][b], o["copy_len"][b] = mn, me, cl
+        o["copy_tokens"][b] = ct
+        o["z"][b], o["use_copy"][b], o["dn"][b] = z, uc, dn
+        o["dtok"][b], o["dpar"][b] = dtok, dpar
+    return o

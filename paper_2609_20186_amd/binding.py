@@ -1,0 +1,220 @@
+"""ctypes binding of libswitchsd.so (the C ABI in include/switchsd.h).
+
+Argument marshalling only: every step runs in the HIP kernels of the library.
+Tensors must be contiguous device tensors of the documented dtypes; bf16
+arrays may be passed as torch.bfloat16 or as their 16-bit patterns
+(int16/uint16).  Calls are asynchronous on the given (default: current) stream.
+If the library is not built, importing raises instead of falling back to
+anything else.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libswitchsd.so")
+
+MAX_NGRAM = 8
+MODE_AUTO, MODE_FUSED, MODE_SPLIT = 0, 1, 2
+
+STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE"}
+
+EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
+           "switchsd_verify_accept", "switchsd_step", "switchsd_workspace_bytes",
+           "switchsd_status_string")
+
+
+class SwitchsdError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} returned {status} ({STATUS.get(status, '?')}): "
+                         f"{status_string(status)}")
+
+
+class Cfg(ctypes.Structure):
+    _fields_ = [("n_ngram", ctypes.c_int32),
+                ("ngram_lens", ctypes.c_int32 * MAX_NGRAM),
+                ("kappa", ctypes.c_int32),
+                ("k", ctypes.c_int32),
+                ("theta", ctypes.c_float)]
+
+
+def make_cfg(ngram_lens=(3, 2, 1), kappa=1, k=7, theta=0.0):
+    c = Cfg()
+    c.n_ngram = len(ngram_lens)
+    for i, n in enumerate(ngram_lens):
+        c.ngram_lens[i] = int(n)
+    c.kappa = int(kappa)
+    c.k = int(k)
+    c.theta = float(theta)
+    return c
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+
+
+class StepArgs(ctypes.Structure):
+    _fields_ = [("tokens", _P), ("lengths", _P), ("hidden", _P), ("w", _P), ("ntok", _P),
+                ("npar", _P), ("nn", _P), ("logits", _P),
+                ("B", _I), ("Lmax", _I), ("d", _I), ("R", _I), ("V", _I),
+                ("bias", ctypes.c_float), ("cfg", Cfg), ("mode", _I),
+                ("match_n", _P), ("match_end", _P), ("copy_len", _P), ("copy_tokens", _P),
+                ("z", _P), ("use_copy", _P), ("dtok", _P), ("dpar", _P), ("dn", _P),
+                ("amax", _P), ("accept_len", _P), ("accept_node", _P), ("bonus", _P),
+                ("out_tokens", _P)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_20186_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    S = ctypes.c_size_t
+    lib.switchsd_ngram_match.argtypes = [_P, _P, _I, _I, ctypes.POINTER(Cfg), _P, _P, _P, _P,
+                                         _P, S, _P]
+    lib.switchsd_probe_score.argtypes = [_P, _P, ctypes.c_float, _I, _I, _P, _P]
+    lib.switchsd_select_draft.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I,
+                                          ctypes.POINTER(Cfg), _P, _P, _P, _P, _P]
+    lib.switchsd_verify_accept.argtypes = [_P, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                           S, _P]
+    lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
+    lib.switchsd_workspace_bytes.argtypes = [_I, _I]
+    lib.switchsd_workspace_bytes.restype = S
+    lib.switchsd_status_string.argtypes = [ctypes.c_int]
+    lib.switchsd_status_string.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
+    return lib
+
+
+lib = _load()
+
+
+def status_string(status):
+    return lib.switchsd_status_string(int(status)).decode()
+
+
+def workspace_bytes(B, R):
+    return int(lib.switchsd_workspace_bytes(int(B), int(R)))
+
+
+_DT = {"i32": (torch.int32,), "f32": (torch.float32,),
+       "bf16": (torch.bfloat16, torch.int16, torch.uint16), "u8": (torch.uint8,)}
+
+
+def _ptr(t, kind, name, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in _DT[kind]:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {_DT[kind]}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check(fn, rc):
+    if rc != 0:
+        raise SwitchsdError(fn, rc)
+
+
+def switchsd_ngram_match(tokens, lengths, cfg, match_n, match_end, copy_len, copy_tokens,
+                         workspace, stream=None):
+    B, Lmax = tokens.shape
+    _check("switchsd_ngram_match", lib.switchsd_ngram_match(
+        _ptr(tokens, "i32", "tokens"), _ptr(lengths, "i32", "lengths"), B, Lmax,
+        ctypes.byref(cfg), _ptr(match_n, "i32", "match_n"), _ptr(match_end, "i32", "match_end"),
+        _ptr(copy_len, "i32", "copy_len"), _ptr(copy_tokens, "i32", "copy_tokens", True),
+        _ptr(workspace, "u8", "workspace"), workspace.numel(), _stream(stream)))
+
+
+def switchsd_probe_score(hidden, w, bias, z, stream=None):
+    B, d = hidden.shape
+    _check("switchsd_probe_score", lib.switchsd_probe_score(
+        _ptr(hidden, "bf16", "hidden"), _ptr(w, "f32", "w"), float(bias), B, d,
+        _ptr(z, "f32", "z"), _stream(stream)))
+
+
+def switchsd_select_draft(match_n, copy_len, copy_tokens, z, ntok, npar, nn, cfg, use_copy,
+                          dtok, dpar, dn, stream=None):
+    B, R = ntok.shape
+    _check("switchsd_select_draft", lib.switchsd_select_draft(
+        _ptr(match_n, "i32", "match_n"), _ptr(copy_len, "i32", "copy_len"),
+        _ptr(copy_tokens, "i32", "copy_tokens", True), _ptr(z, "f32", "z"),
+        _ptr(ntok, "i32", "ntok"), _ptr(npar, "i32", "npar", True), _ptr(nn, "i32", "nn"),
+        B, R, ctypes.byref(cfg), _ptr(use_copy, "i32", "use_copy"), _ptr(dtok, "i32", "dtok"),
+        _ptr(dpar, "i32", "dpar"), _ptr(dn, "i32", "dn"), _stream(stream)))
+
+
+def switchsd_verify_accept(logits, dtok, dpar, dn, accept_len, accept_node, bonus, out_tokens,
+                           amax, workspace, stream=None):
+    B, R, V = logits.shape
+    _check("switchsd_verify_accept", lib.switchsd_verify_accept(
+        _ptr(logits, "bf16", "logits"), B, R, V, _ptr(dtok, "i32", "dtok"),
+        _ptr(dpar, "i32", "dpar", True), _ptr(dn, "i32", "dn"),
+        _ptr(accept_len, "i32", "accept_len"), _ptr(accept_node, "i32", "accept_node"),
+        _ptr(bonus, "i32", "bonus"), _ptr(out_tokens, "i32", "out_tokens"),
+        _ptr(amax, "i32", "amax", True), _ptr(workspace, "u8", "workspace"),
+        workspace.numel(), _stream(stream)))
+
+
+OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_copy", "dtok", "dpar",
+           "dn", "amax", "accept_len", "accept_node", "bonus", "out_tokens")
+
+
+def alloc_outputs(B, R, k, device="cuda"):
+    i32 = dict(dtype=torch.int32, device=device)
+    return {"match_n": torch.empty(B, **i32), "match_end": torch.empty(B, **i32),
+            "copy_len": torch.empty(B, **i32), "copy_tokens": torch.empty((B, k), **i32),
+            "z": torch.empty(B, dtype=torch.float32, device=device),
+            "use_copy": torch.empty(B, **i32), "dtok": torch.empty((B, R), **i32),
+            "dpar": torch.empty((B, R), **i32), "dn": torch.empty(B, **i32),
+            "amax": torch.empty((B, R), **i32), "accept_len": torch.empty(B, **i32),
+            "accept_node": torch.empty(B, **i32), "bonus": torch.empty(B, **i32),
+            "out_tokens": torch.empty((B, R), **i32)}
+
+
+def alloc_workspace(B, R, device="cuda"):
+    """Zeroed once here; the kernels leave it zeroed after every call."""
+    return torch.zeros(max(workspace_bytes(B, R), 256), dtype=torch.uint8, device=device)
+
+
+def build_step_args(inp, out, cfg, mode=MODE_AUTO):
+    """StepArgs for switchsd_step.  ``inp`` holds device tensors tokens [B,Lmax],
+    lengths [B], hidden [B,d], w [d], ntok [B,R], npar [B,R] or None, nn [B],
+    logits [B,R,V] and the float ``bias``; ``out`` is from alloc_outputs."""
+    tokens, logits, hidden = inp["tokens"], inp["logits"], inp["hidden"]
+    B, Lmax = tokens.shape
+    R, V = logits.shape[1], logits.shape[2]
+    a = StepArgs()
+    a.tokens = _ptr(tokens, "i32", "tokens")
+    a.lengths = _ptr(inp["lengths"], "i32", "lengths")
+    a.hidden = _ptr(hidden, "bf16", "hidden")
+    a.w = _ptr(inp["w"], "f32", "w")
+    a.ntok = _ptr(inp["ntok"], "i32", "ntok")
+    a.npar = _ptr(inp.get("npar"), "i32", "npar", True)
+    a.nn = _ptr(inp["nn"], "i32", "nn")
+    a.logits = _ptr(logits, "bf16", "logits")
+    a.B, a.Lmax, a.d, a.R, a.V = B, Lmax, hidden.shape[1], R, V
+    a.bias = float(inp["bias"])
+    a.cfg = cfg
+    a.mode = int(mode)
+    for name in OUTPUTS:
+        setattr(a, name, _ptr(out[name], "f32" if name == "z" else "i32", name,
+                              optional=(name == "amax" or name == "copy_tokens")))
+    return a
+
+
+def switchsd_step(args, workspace, stream=None):
+    _check("switchsd_step", lib.switchsd_step(ctypes.byref(args), _ptr(workspace, "u8",
+                                              "workspace"), workspace.numel(),
+                                              _stream(stream)))

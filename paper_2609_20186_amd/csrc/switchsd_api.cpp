@@ -1,0 +1,336 @@
+// switchsd_api.cpp -- C entry points: argument validation, grid layout and
+// dispatch of the gfx950 kernels.  Every check runs on the host before any
+// HIP call; a rejected call launches nothing.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "switchsd.h"
+#include "switchsd_internal.h"
+
+using namespace switchsd;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
+
+bool shape_ok_B(int32_t B) { return B >= 0 && B <= (1 << 24); }
+
+int check_cfg(const switchsd_cfg *cfg) {
+    if (!cfg)
+        return SWITCHSD_EINVAL;
+    if (cfg->n_ngram < 1 || cfg->n_ngram > SWITCHSD_MAX_NGRAM)
+        return SWITCHSD_EINVAL;
+    for (int j = 0; j < cfg->n_ngram; ++j) {
+        const int n = cfg->ngram_lens[j];
+        if (n < 1 || n > SWITCHSD_MAX_NGRAM_LEN)
+            return SWITCHSD_EINVAL;
+        if (j > 0 && n >= cfg->ngram_lens[j - 1])
+            return SWITCHSD_EINVAL;
+    }
+    if (cfg->kappa < 1 || cfg->k < 0)
+        return SWITCHSD_EINVAL;
+    return SWITCHSD_OK;
+}
+
+void fill_cfg(StepParams &p, const switchsd_cfg *cfg) {
+    p.n_ngram = cfg->n_ngram;
+    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+        p.lens[j] = j < cfg->n_ngram ? cfg->ngram_lens[j] : 0;
+    p.nmax = cfg->ngram_lens[0];
+    p.kappa = cfg->kappa;
+    p.k = cfg->k;
+    p.theta = cfg->theta;
+}
+
+int check_workspace(const void *ws, size_t bytes, int32_t B, int32_t R) {
+    if (!ws || ((uintptr_t)ws & (kAlign - 1)))
+        return SWITCHSD_EWORKSPACE;
+    if (bytes < switchsd_workspace_bytes(B, R))
+        return SWITCHSD_EWORKSPACE;
+    return SWITCHSD_OK;
+}
+
+Workspace carve(void *ws, int32_t B) {
+    Workspace w;
+    char *base = (char *)ws;
+    size_t off = 0;
+    w.tk_front = (uint32_t *)(base + off);
+    off += align_up((size_t)B * 4);
+    w.tk_all = (uint32_t *)(base + off);
+    off += align_up((size_t)B * 4);
+    w.mslot = (int32_t *)(base + off);
+    off += align_up((size_t)B * SWITCHSD_MAX_NGRAM * 4);
+    w.keys = (unsigned long long *)(base + off);
+    return w;
+}
+
+int scan_tiles_for(int32_t Lmax) { return (int)((Lmax + kScanTile - 1) / kScanTile); }
+
+int chunks_for(int32_t V) { return (int)((V + (int64_t)kChunkElems - 1) / kChunkElems); }
+
+// the grid must fit a 32-bit block index
+bool grid_ok(int64_t g) { return g >= 1 && g <= 0x7FFFFFFFll; }
+
+int set_scan(StepParams &p, int32_t B, int32_t Lmax) {
+    p.scan_tiles = scan_tiles_for(Lmax);
+    const int64_t n = (int64_t)B * p.scan_tiles;
+    if (n > 0x3FFFFFFFll)
+        return SWITCHSD_ESHAPE;
+    p.n_scan_wg = (int32_t)n;
+    return SWITCHSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t switchsd_workspace_bytes(int32_t B, int32_t R) {
+    if (B < 0 || R < 0)
+        return 0;
+    return align_up((size_t)B * 4) * 2 + align_up((size_t)B * SWITCHSD_MAX_NGRAM * 4) +
+           align_up((size_t)B * (size_t)R * 8);
+}
+
+const char *switchsd_status_string(int status) {
+    switch (status) {
+    case SWITCHSD_OK:
+        return "ok";
+    case SWITCHSD_EINVAL:
+        return "invalid argument (null pointer or bad configuration value)";
+    case SWITCHSD_ESHAPE:
+        return "sizes out of range or inconsistent";
+    case SWITCHSD_EHIP:
+        return "HIP runtime call or kernel launch failed";
+    case SWITCHSD_EWORKSPACE:
+        return "workspace null, not 256-byte aligned or too small";
+    default:
+        return "unknown status";
+    }
+}
+
+int switchsd_ngram_match(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
+                         const switchsd_cfg *cfg, int32_t *match_n, int32_t *match_end,
+                         int32_t *copy_len, int32_t *copy_tokens, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    int rc = check_cfg(cfg);
+    if (rc)
+        return rc;
+    if (!shape_ok_B(B) || Lmax < 1)
+        return SWITCHSD_ESHAPE;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!tokens || !lengths || !match_n || !match_end || !copy_len ||
+        (cfg->k > 0 && !copy_tokens))
+        return SWITCHSD_EINVAL;
+    if ((rc = check_workspace(workspace, workspace_bytes, B, 0)))
+        return rc;
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    fill_cfg(p, cfg);
+    p.tokens = tokens;
+    p.lengths = lengths;
+    p.B = B;
+    p.Lmax = Lmax;
+    p.R = 1;
+    p.match_n = match_n;
+    p.match_end = match_end;
+    p.copy_len = copy_len;
+    p.copy_tokens = copy_tokens;
+    p.ws = carve(workspace, B);
+    if ((rc = set_scan(p, B, Lmax)))
+        return rc;
+    p.n_front_wg = p.n_scan_wg;
+    p.epi_front = EPI_MATCH;
+    p.exp_front = (uint32_t)p.scan_tiles;
+    return launch_step_kernel(p, p.n_front_wg, stream);
+}
+
+int switchsd_probe_score(const uint16_t *hidden, const float *w, float bias, int32_t B,
+                         int32_t d, float *z, hipStream_t stream) {
+    if (!shape_ok_B(B) || d < 0)
+        return SWITCHSD_ESHAPE;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!z || (d > 0 && (!hidden || !w)))
+        return SWITCHSD_EINVAL;
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    p.hidden = hidden;
+    p.w = w;
+    p.bias = bias;
+    p.B = B;
+    p.d = d;
+    p.z = z;
+    p.probe_on = 1;
+    p.n_front_wg = B;
+    return launch_step_kernel(p, B, stream);
+}
+
+int switchsd_select_draft(const int32_t *match_n, const int32_t *copy_len,
+                          const int32_t *copy_tokens, const float *z, const int32_t *ntok,
+                          const int32_t *npar, const int32_t *nn, int32_t B, int32_t R,
+                          const switchsd_cfg *cfg, int32_t *use_copy, int32_t *dtok,
+                          int32_t *dpar, int32_t *dn, hipStream_t stream) {
+    int rc = check_cfg(cfg);
+    if (rc)
+        return rc;
+    if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || cfg->k + 1 > R)
+        return SWITCHSD_ESHAPE;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!match_n || !copy_len || (cfg->k > 0 && !copy_tokens) || !z || !ntok || !nn ||
+        !use_copy || !dtok || !dpar || !dn)
+        return SWITCHSD_EINVAL;
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    fill_cfg(p, cfg);
+    p.match_n_in = match_n;
+    p.copy_len_in = copy_len;
+    p.copy_tokens_in = copy_tokens;
+    p.z_in = z;
+    p.ntok = ntok;
+    p.npar = npar;
+    p.nn = nn;
+    p.B = B;
+    p.R = R;
+    p.use_copy = use_copy;
+    p.dtok = dtok;
+    p.dpar = dpar;
+    p.dn = dn;
+    return launch_select_kernel(p, stream);
+}
+
+int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
+                           const int32_t *dtok, const int32_t *dpar, const int32_t *dn,
+                           int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                           int32_t *out_tokens, int32_t *amax, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+    if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || V < 1)
+        return SWITCHSD_ESHAPE;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!logits || ((uintptr_t)logits & 1) || !dtok || !dn || !accept_len || !accept_node ||
+        !bonus || !out_tokens)
+        return SWITCHSD_EINVAL;
+    int rc = check_workspace(workspace, workspace_bytes, B, R);
+    if (rc)
+        return rc;
+    const int chunks = chunks_for(V);
+    const int64_t grid = (int64_t)B * R * chunks;
+    if (!grid_ok(grid))
+        return SWITCHSD_ESHAPE;
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    p.logits = logits;
+    p.B = B;
+    p.R = R;
+    p.V = V;
+    p.dtok = const_cast<int32_t *>(dtok);
+    p.dpar = const_cast<int32_t *>(dpar);
+    p.dn = const_cast<int32_t *>(dn);
+    p.accept_len = accept_len;
+    p.accept_node = accept_node;
+    p.bonus = bonus;
+    p.out_tokens = out_tokens;
+    p.amax = amax;
+    p.ws = carve(workspace, B);
+    p.chunks = chunks;
+    p.rows_mode = ROWS_DRAFT;
+    p.epi_accept = 1;
+    p.exp_all = (uint32_t)(R * chunks);
+    return launch_step_kernel(p, grid, stream);
+}
+
+int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace_bytes,
+                  hipStream_t stream) {
+    if (!a)
+        return SWITCHSD_EINVAL;
+    int rc = check_cfg(&a->cfg);
+    if (rc)
+        return rc;
+    const int32_t B = a->B, R = a->R, V = a->V;
+    if (!shape_ok_B(B) || a->Lmax < 1 || a->d < 0 || R < 1 || R > SWITCHSD_MAX_R || V < 1 ||
+        a->cfg.k + 1 > R)
+        return SWITCHSD_ESHAPE;
+    if (a->mode < SWITCHSD_MODE_AUTO || a->mode > SWITCHSD_MODE_SPLIT)
+        return SWITCHSD_EINVAL;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!a->tokens || !a->lengths || (a->d > 0 && (!a->hidden || !a->w)) || !a->ntok ||
+        !a->nn || !a->logits || ((uintptr_t)a->logits & 1) || !a->match_n || !a->match_end ||
+        !a->copy_len || (a->cfg.k > 0 && !a->copy_tokens) || !a->z || !a->use_copy ||
+        !a->dtok || !a->dpar || !a->dn || !a->accept_len || !a->accept_node || !a->bonus ||
+        !a->out_tokens)
+        return SWITCHSD_EINVAL;
+    if ((rc = check_workspace(workspace, workspace_bytes, B, R)))
+        return rc;
+    const int chunks = chunks_for(V);
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    fill_cfg(p, &a->cfg);
+    p.tokens = a->tokens;
+    p.lengths = a->lengths;
+    p.hidden = a->hidden;
+    p.w = a->w;
+    p.ntok = a->ntok;
+    p.npar = a->npar;
+    p.nn = a->nn;
+    p.logits = a->logits;
+    p.B = B;
+    p.Lmax = a->Lmax;
+    p.d = a->d;
+    p.R = R;
+    p.V = V;
+    p.bias = a->bias;
+    p.match_n = a->match_n;
+    p.match_end = a->match_end;
+    p.copy_len = a->copy_len;
+    p.copy_tokens = a->copy_tokens;
+    p.z = a->z;
+    p.use_copy = a->use_copy;
+    p.dtok = a->dtok;
+    p.dpar = a->dpar;
+    p.dn = a->dn;
+    p.amax = a->amax;
+    p.accept_len = a->accept_len;
+    p.accept_node = a->accept_node;
+    p.bonus = a->bonus;
+    p.out_tokens = a->out_tokens;
+    p.ws = carve(workspace, B);
+    if ((rc = set_scan(p, B, a->Lmax)))
+        return rc;
+    p.probe_on = 1;
+    p.n_front_wg = p.n_scan_wg + B;
+    p.epi_front = EPI_SELECT;
+    p.exp_front = (uint32_t)p.scan_tiles + 1u;
+
+    int mode = a->mode;
+    if (mode == SWITCHSD_MODE_AUTO)
+        mode = a->cfg.k + 1 >= R ? SWITCHSD_MODE_FUSED : SWITCHSD_MODE_SPLIT;
+    const int64_t argmax_wg = (int64_t)B * R * chunks;
+    if (mode == SWITCHSD_MODE_FUSED) {
+        const int64_t grid = p.n_front_wg + argmax_wg;
+        if (!grid_ok(grid))
+            return SWITCHSD_ESHAPE;
+        p.chunks = chunks;
+        p.rows_mode = a->cfg.k + 1 >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;
+        p.epi_accept = 1;
+        p.exp_all = p.exp_front + (uint32_t)(R * chunks);
+        return launch_step_kernel(p, grid, stream);
+    }
+    // SPLIT: front (scan + probe + select), then verify over the chosen rows
+    if (!grid_ok(argmax_wg))
+        return SWITCHSD_ESHAPE;
+    if ((rc = launch_step_kernel(p, p.n_front_wg, stream)))
+        return rc;
+    return switchsd_verify_accept(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
+                                  a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
+                                  workspace_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,76 @@
+// switchsd_internal.h -- parameters shared by the host API and the kernels.
+// Not part of the public interface (see include/switchsd.h).
+#pragma once
+
+#include <stdint.h>
+
+#include "switchsd.h"
+
+namespace switchsd {
+
+// Work-group shape of every kernel of the step: 256 lanes = 4 wave64s.
+constexpr int kThreads = 256;
+// 16-byte logits loads in flight per lane in one argmax work-group.
+constexpr int kUnroll = 16;
+// Logits elements covered by one argmax work-group (one pass, all loads in flight).
+constexpr int kChunkElems = kThreads * kUnroll * 8;
+// Context end positions covered by one scan work-group.
+constexpr int kScanTile = 4096;
+
+enum : int32_t { EPI_NONE = 0, EPI_MATCH = 1, EPI_SELECT = 2 };
+enum : int32_t { ROWS_ALL = 0, ROWS_NEURAL_OR_COPY = 1, ROWS_DRAFT = 2 };
+
+struct Workspace {
+    uint32_t *tk_front;           // [B] arrivals of the scan/probe work-groups
+    uint32_t *tk_all;             // [B] arrivals of every work-group of a sequence
+    int32_t *mslot;               // [B, 8] most recent end + 1 per n-gram length
+    unsigned long long *keys;     // [B, R] packed (value key, ~index) row maxima
+};
+
+struct StepParams {
+    // inputs
+    const int32_t *tokens;
+    const int32_t *lengths;
+    const uint16_t *hidden;
+    const float *w;
+    const int32_t *ntok;
+    const int32_t *npar;
+    const int32_t *nn;
+    const uint16_t *logits;
+    const int32_t *copy_tokens_in;  // select stage only
+    const int32_t *match_n_in;      // select stage only
+    const int32_t *copy_len_in;     // select stage only
+    const float *z_in;              // select stage only
+    int32_t B, Lmax, d, R, V;
+    float bias;
+    // configuration
+    int32_t n_ngram;
+    int32_t lens[SWITCHSD_MAX_NGRAM];
+    int32_t nmax;
+    int32_t kappa;
+    int32_t k;
+    float theta;
+    // outputs
+    int32_t *match_n, *match_end, *copy_len, *copy_tokens;
+    float *z;
+    int32_t *use_copy, *dtok, *dpar, *dn;
+    int32_t *amax;
+    int32_t *accept_len, *accept_node, *bonus, *out_tokens;
+    Workspace ws;
+    // grid layout: [scan tiles][probe][argmax chunks]
+    int32_t scan_tiles;  // per sequence (0: no scan role)
+    int32_t probe_on;    // 1: one probe work-group per sequence
+    int32_t chunks;      // argmax work-groups per row (0: no argmax role)
+    int32_t n_scan_wg;   // B * scan_tiles
+    int32_t n_front_wg;  // n_scan_wg + B * probe_on
+    int32_t rows_mode;
+    int32_t epi_front;
+    int32_t epi_accept;
+    uint32_t exp_front;  // arrivals per sequence at tk_front
+    uint32_t exp_all;    // arrivals per sequence at tk_all
+};
+
+int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
+int launch_select_kernel(const StepParams &p, hipStream_t stream);
+
+}  // namespace switchsd

@@ -1,0 +1,649 @@
+// switchsd_kernels.hip -- gfx950 kernels of SwitchSD's speculation-control step.
+//
+// One kernel body serves every entry point.  Its work-groups take one of
+// three roles by block index, laid out as [scan tiles | probe | argmax]:
+//
+//   scan    a 4096-position tile of one context, staged in LDS with an
+//           (n_max - 1)-token halo; every lane measures how far the suffix
+//           matches backwards from each of its end positions; the most recent
+//           end per n-gram length is max-reduced over the wave, the
+//           work-group and (atomicMax) the tiles of the sequence.
+//           (Sec. 3.3: kappa-gram with a prior occurrence, ranked by recency.)
+//   probe   w . h for one sequence: exact bf16 x float products, summed in
+//           double-double with a fixed reduction order.  (Sec. 3.2, Eq. 3.)
+//   argmax  32768 elements of one logits row, every 16-byte load in flight at
+//           once; lane maxima with the NaN-propagating v_maximum3_f32, then
+//           the lowest index of the work-group maximum, packed as
+//           (order key << 32 | ~index) and atomicMax-ed into the row's slot.
+//           (Sec. 2 / App. A: greedy verification at T = 0.)
+//
+// Two last-arriver epilogues close a sequence without a second launch:
+//   front   when its scan tiles and probe are done: pick the match, gather the
+//           copy candidate, apply the switch (Sec. 3.3, Eq. 4) and write the
+//           chosen draft;
+//   final   when every work-group of the sequence is done: decode the row
+//           argmaxes and run the accept walk (Sec. 3.3, Parallel Verification)
+//           by pointer jumping over the draft tree, one node per lane.
+// Arrivals use agent-scope acquire/release atomics, so the epilogue sees the
+// partial results of work-groups on other XCDs.  Each epilogue resets the
+// workspace slots it consumed, leaving the workspace zeroed for the next call.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "switchsd_internal.h"
+
+namespace switchsd {
+
+namespace {
+
+constexpr int kWaves = kThreads / 64;
+constexpr int kScanHaloMax = SWITCHSD_MAX_NGRAM_LEN;
+constexpr int kScanPerLane = (kScanTile + kScanHaloMax + kThreads - 1) / kThreads;
+
+struct ScanShared {
+    int32_t tile[kScanTile + kScanHaloMax];
+    int32_t pat[SWITCHSD_MAX_NGRAM_LEN];
+    int32_t red[kWaves][SWITCHSD_MAX_NGRAM];
+};
+struct ArgmaxShared {
+    float wmax[kWaves];
+    uint32_t widx[kWaves];
+};
+struct ProbeShared {
+    double s[kWaves];
+    double c[kWaves];
+};
+struct EpiShared {  // general accept walk, R > 64
+    int32_t a[SWITCHSD_MAX_R];
+    int32_t tok[SWITCHSD_MAX_R];
+    int32_t par[SWITCHSD_MAX_R];
+    int32_t dep[SWITCHSD_MAX_R];  // depth if accepted, -1 otherwise
+};
+union Shared {
+    ScanShared scan;
+    ArgmaxShared am;
+    ProbeShared probe;
+    EpiShared epi;
+};
+
+// ------------------------------------------------------------- atomics
+
+__device__ __forceinline__ int32_t ld_i32(const int32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_i32(int32_t *p, int32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_f32(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_f32(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long ld_u64(const unsigned long long *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u64(unsigned long long *p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u32(uint32_t *p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wave 0 arrives at a per-sequence ticket; true (wave-uniform) for the last
+// of `expected` arrivals.  Release orders this wave's earlier writes before
+// the arrival; acquire makes the others' writes visible to the last one.
+__device__ __forceinline__ bool arrive(uint32_t *ticket, uint32_t expected) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    uint32_t old = 0;
+    if (threadIdx.x == 0)
+        old = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    old = __shfl(old, 0);
+    const bool last = old + 1u == expected;
+    if (last)
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return last;
+}
+
+// ------------------------------------------------------------- wave reductions
+
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        v = __builtin_elementwise_maximum(v, __shfl_xor(v, o));
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        uint32_t t = __shfl_xor(v, o);
+        v = t < v ? t : v;
+    }
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        uint32_t t = __shfl_xor(v, o);
+        v = t > v ? t : v;
+    }
+    return v;
+}
+__device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        int32_t t = __shfl_xor(v, o);
+        v = t > v ? t : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int clampi(int v, int lo, int hi) {
+    return v < lo ? lo : (v > hi ? hi : v);
+}
+
+// ------------------------------------------------------------- scan role
+
+// Tile t of sequence b: end positions e in [t*4096, (t+1)*4096).
+__device__ void scan_role(const StepParams &p, int b, int t, Shared &sh) {
+    const int tid = threadIdx.x;
+    const int H = p.nmax - 1;
+    const int64_t row = (int64_t)b * p.Lmax;
+    const int t0 = t * kScanTile;
+    const int lo = t0 - H > 0 ? t0 - H : 0;
+    const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
+
+    // The tile loads do not depend on the sequence length: issue them first.
+    int32_t reg[kScanPerLane];
+#pragma unroll
+    for (int i = 0; i < kScanPerLane; ++i) {
+        const int x = lo + i * kThreads + tid;
+        reg[i] = x < hi ? p.tokens[row + x] : 0;
+    }
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+#pragma unroll
+    for (int i = 0; i < kScanPerLane; ++i) {
+        const int j = i * kThreads + tid;
+        if (lo + j < hi)
+            sh.scan.tile[j] = reg[i];
+    }
+    if (tid < p.nmax && tid < L)
+        sh.scan.pat[tid] = p.tokens[row + L - 1 - tid];
+    __syncthreads();
+
+    int32_t best[SWITCHSD_MAX_NGRAM];
+#pragma unroll
+    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+        best[j] = 0;
+    // occurrences end at e <= L-2
+    const int eend = t0 + kScanTile < L - 1 ? t0 + kScanTile : L - 1;
+    if (t0 < eend) {
+        for (int i = 0; i < kScanTile / kThreads; ++i) {
+            const int e = t0 + i * kThreads + tid;
+            if (e < eend) {
+                const int lim = p.nmax < e + 1 ? p.nmax : e + 1;
+                int m = 0;
+                while (m < lim && sh.scan.tile[e - m - lo] == sh.scan.pat[m])
+                    ++m;
+#pragma unroll
+                for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+                    if (j < p.n_ngram && m >= p.lens[j])
+                        best[j] = e + 1;
+            }
+        }
+    }
+    const int wave = tid >> 6, lane = tid & 63;
+#pragma unroll
+    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j) {
+        if (j < p.n_ngram) {
+            const int32_t v = wave_max_i32(best[j]);
+            if (lane == 0)
+                sh.scan.red[wave][j] = v;
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int j = 0; j < p.n_ngram; ++j) {
+            int32_t v = 0;
+            for (int q = 0; q < kWaves; ++q)
+                v = sh.scan.red[q][j] > v ? sh.scan.red[q][j] : v;
+            if (v > 0)
+                atomicMax(&p.ws.mslot[b * SWITCHSD_MAX_NGRAM + j], v);
+        }
+    }
+}
+
+// ------------------------------------------------------------- probe role
+
+__device__ __forceinline__ void two_sum(double a, double b, double &s, double &e) {
+    s = a + b;
+    const double bb = s - a;
+    e = (a - (s - bb)) + (b - bb);
+}
+__device__ __forceinline__ void dd_add_term(double &s, double &c, double x) {
+    double e;
+    two_sum(s, x, s, e);
+    c += e;
+}
+__device__ __forceinline__ void dd_add(double &s, double &c, double s2, double c2) {
+    double e;
+    two_sum(s, s2, s, e);
+    c += c2 + e;
+    double t;
+    two_sum(s, c, t, c);  // renormalize
+    s = t;
+}
+__device__ __forceinline__ double bf16_lo(uint32_t x) { return (double)__uint_as_float(x << 16); }
+__device__ __forceinline__ double bf16_hi(uint32_t x) {
+    return (double)__uint_as_float(x & 0xFFFF0000u);
+}
+
+__device__ void probe_role(const StepParams &p, int b, Shared &sh) {
+    const int tid = threadIdx.x;
+    const uint16_t *h = p.hidden + (int64_t)b * p.d;
+    double s = 0.0, c = 0.0;
+    const bool vec = (p.d & 7) == 0 && (((uintptr_t)h | (uintptr_t)p.w) & 15) == 0;
+    if (vec) {
+        const uint4 *hv = reinterpret_cast<const uint4 *>(h);
+        const float4 *wv = reinterpret_cast<const float4 *>(p.w);
+        for (int g = tid; g < (p.d >> 3); g += kThreads) {
+            const uint4 x = hv[g];
+            const float4 w0 = wv[2 * g], w1 = wv[2 * g + 1];
+            dd_add_term(s, c, bf16_lo(x.x) * (double)w0.x);
+            dd_add_term(s, c, bf16_hi(x.x) * (double)w0.y);
+            dd_add_term(s, c, bf16_lo(x.y) * (double)w0.z);
+            dd_add_term(s, c, bf16_hi(x.y) * (double)w0.w);
+            dd_add_term(s, c, bf16_lo(x.z) * (double)w1.x);
+            dd_add_term(s, c, bf16_hi(x.z) * (double)w1.y);
+            dd_add_term(s, c, bf16_lo(x.w) * (double)w1.z);
+            dd_add_term(s, c, bf16_hi(x.w) * (double)w1.w);
+        }
+    } else {
+        for (int i = tid; i < p.d; i += kThreads)
+            dd_add_term(s, c, bf16_lo((uint32_t)h[i]) * (double)p.w[i]);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const double s2 = __shfl_xor(s, o), c2 = __shfl_xor(c, o);
+        dd_add(s, c, s2, c2);
+    }
+    const int wave = tid >> 6, lane = tid & 63;
+    if (lane == 0) {
+        sh.probe.s[wave] = s;
+        sh.probe.c[wave] = c;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double S = sh.probe.s[0], C = sh.probe.c[0];
+        for (int q = 1; q < kWaves; ++q)
+            dd_add(S, C, sh.probe.s[q], sh.probe.c[q]);
+        dd_add(S, C, (double)p.bias, 0.0);
+        st_f32(&p.z[b], (float)(S + C));
+    }
+}
+
+// ------------------------------------------------------------- argmax role
+
+__device__ __forceinline__ float lo_f(uint32_t x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float hi_f(uint32_t x) { return __uint_as_float(x & 0xFFFF0000u); }
+__device__ __forceinline__ float max3n(float a, float b, float c) {
+    return __builtin_elementwise_maximum(a, __builtin_elementwise_maximum(b, c));
+}
+__device__ __forceinline__ float fmax_nonan(float m, float x) { return x > m ? x : m; }
+
+// Order-preserving key of a float; -0 is folded onto +0.
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    if (u == 0x80000000u)
+        u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
+    if (p.rows_mode == ROWS_ALL)
+        return (uint32_t)p.R;
+    if (p.rows_mode == ROWS_DRAFT)
+        return (uint32_t)clampi(ld_i32(&p.dn[b]), 1, p.R);
+    const int nnb = clampi(p.nn[b], 1, p.R);
+    return (uint32_t)(nnb > p.k + 1 ? nnb : p.k + 1);
+}
+
+__device__ void argmax_role(const StepParams &p, int b, int r, int c, Shared &sh) {
+    const int tid = threadIdx.x;
+    const int64_t rowoff = ((int64_t)b * p.R + r) * p.V;
+    const int64_t c0 = (int64_t)c * kChunkElems;
+    const int64_t c1 = c0 + kChunkElems < p.V ? c0 + kChunkElems : (int64_t)p.V;
+    // element g of the tensor sits at byte 2g from the base: the 16-byte
+    // aligned interior [a0, a1) is read with 16-byte loads, the head and the
+    // tail (at most 7 elements each) one element per lane.
+    const int64_t g0 = rowoff + c0, g1 = rowoff + c1;
+    const int64_t mis = (int64_t)((((uintptr_t)p.logits) >> 1) + (uint64_t)g0) & 7;
+    int64_t a0 = g0 + ((8 - mis) & 7);
+    if (a0 > g1)
+        a0 = g1;
+    const int64_t a1 = a0 + ((g1 - a0) & ~(int64_t)7);
+    const int nq = (int)((a1 - a0) >> 3);
+    const uint4 *vp = reinterpret_cast<const uint4 *>(p.logits + a0);
+    const uint4 neg_inf = make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
+
+    uint4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const int q = u * kThreads + tid;
+        v[u] = q < nq ? vp[q] : neg_inf;
+    }
+    const int nhead = (int)(a0 - g0), ntail = (int)(g1 - a1);
+    int64_t eg = -1;
+    if (tid < nhead)
+        eg = g0 + tid;
+    else if (tid < nhead + ntail)
+        eg = a1 + (tid - nhead);
+    const float ev = eg >= 0 ? lo_f((uint32_t)p.logits[eg]) : -__builtin_inff();
+
+    // phase 1: lane maximum (NaN propagates; handled below)
+    float m = ev;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        m = max3n(m, lo_f(v[u].x), hi_f(v[u].x));
+        m = max3n(m, lo_f(v[u].y), hi_f(v[u].y));
+        m = max3n(m, lo_f(v[u].z), hi_f(v[u].z));
+        m = max3n(m, lo_f(v[u].w), hi_f(v[u].w));
+    }
+    if (m != m) {  // a NaN in this lane: recompute ignoring NaN (never on finite data)
+        m = fmax_nonan(-__builtin_inff(), ev);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint32_t ws[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                m = fmax_nonan(m, lo_f(ws[q]));
+                m = fmax_nonan(m, hi_f(ws[q]));
+            }
+        }
+    }
+    const int wave = tid >> 6, lane = tid & 63;
+    const float wm = wave_max_f32(m);
+    if (lane == 0)
+        sh.am.wmax[wave] = wm;
+    __syncthreads();
+    float M = sh.am.wmax[0];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q)
+        M = __builtin_elementwise_maximum(M, sh.am.wmax[q]);
+
+    // phase 2 (only waves holding the maximum): lowest index equal to M
+    uint32_t idx = 0xFFFFFFFFu;
+    if (__any(m == M)) {
+        if (m == M) {
+            if (eg >= 0 && ev == M)
+                idx = (uint32_t)(eg - rowoff);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int q = u * kThreads + tid;
+                const uint32_t ws[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                for (int w4 = 0; w4 < 4; ++w4) {
+                    const uint32_t base = (uint32_t)(a0 - rowoff) + (uint32_t)q * 8u + w4 * 2u;
+                    if (q < nq && lo_f(ws[w4]) == M && base < idx)
+                        idx = base;
+                    if (q < nq && hi_f(ws[w4]) == M && base + 1u < idx)
+                        idx = base + 1u;
+                }
+            }
+        }
+        idx = wave_min_u32(idx);
+    }
+    if (lane == 0)
+        sh.am.widx[wave] = idx;
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t best = sh.am.widx[0];
+#pragma unroll
+        for (int q = 1; q < kWaves; ++q)
+            best = sh.am.widx[q] < best ? sh.am.widx[q] : best;
+        if (best != 0xFFFFFFFFu) {
+            const unsigned long long key =
+                ((unsigned long long)order_key(M) << 32) | (0xFFFFFFFFu - best);
+            atomicMax(&p.ws.keys[(int64_t)b * p.R + r], key);
+        }
+    }
+}
+
+// ------------------------------------------------------------- epilogues
+
+// Writes the chosen draft of sequence b (wave 0).  src[off + i] is the i-th
+// copied token (1-based); it is read only for 1 <= i <= copy_len.
+__device__ void select_write(const StepParams &p, int b, int mn, int cl, float zb,
+                             const int32_t *src, int64_t off) {
+    const int lane = threadIdx.x;
+    const int use = (mn >= p.kappa) && (zb >= p.theta);
+    const int nnb = clampi(p.nn[b], 1, p.R);
+    const int dnb = use ? cl + 1 : nnb;
+    const int64_t base = (int64_t)b * p.R;
+    for (int i = lane; i < p.R; i += 64) {
+        int tok = -1, par = -1;
+        if (i >= 1 && i < dnb) {
+            if (use) {
+                tok = src[off + i];
+                par = i - 1;
+            } else {
+                tok = p.ntok[base + i];
+                par = p.npar ? p.npar[base + i] : i - 1;
+            }
+        }
+        p.dtok[base + i] = tok;
+        p.dpar[base + i] = par;
+    }
+    if (lane == 0) {
+        p.use_copy[b] = use;
+        p.dn[b] = dnb;
+    }
+}
+
+__device__ void front_epilogue(const StepParams &p, int b) {
+    const int lane = threadIdx.x;
+    int32_t s = 0;
+    if (lane < p.n_ngram) {
+        s = ld_i32(&p.ws.mslot[b * SWITCHSD_MAX_NGRAM + lane]);
+        st_i32(&p.ws.mslot[b * SWITCHSD_MAX_NGRAM + lane], 0);
+    }
+    const unsigned long long hit = __ballot(s > 0);
+    int mn = 0, me = -1;
+    if (hit) {
+        const int j = __ffsll((long long)hit) - 1;
+#pragma unroll
+        for (int q = 0; q < SWITCHSD_MAX_NGRAM; ++q)
+            if (q == j)
+                mn = p.lens[q];
+        me = __shfl(s, j) - 1;
+    }
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+    const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
+    const int64_t row = (int64_t)b * p.Lmax;
+    if (lane == 0) {
+        p.match_n[b] = mn;
+        p.match_end[b] = me;
+        p.copy_len[b] = cl;
+    }
+    for (int i = lane; i < p.k; i += 64)
+        p.copy_tokens[(int64_t)b * p.k + i] = i < cl ? p.tokens[row + me + 1 + i] : -1;
+    if (p.epi_front == EPI_SELECT) {
+        const float zb = ld_f32(&p.z[b]);
+        // copied token i (1-based) is x[me + i]
+        select_write(p, b, mn, cl, zb, p.tokens, row + me);
+    }
+    if (lane == 0)
+        st_u32(&p.ws.tk_front[b], 0u);
+}
+
+__device__ __forceinline__ int32_t decode_key(unsigned long long key) {
+    return key ? (int32_t)(0xFFFFFFFFu - (uint32_t)key) : 0;
+}
+
+__device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
+    const int lane = threadIdx.x;
+    const int64_t base = (int64_t)b * p.R;
+    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    if (p.R <= 64) {
+        const int i = lane;
+        int a = -1, tok = -1, par = -1;
+        if (i < p.R) {
+            const unsigned long long key = ld_u64(&p.ws.keys[base + i]);
+            if (key)
+                st_u64(&p.ws.keys[base + i], 0ull);
+            if (i < dnb)
+                a = decode_key(key);
+            tok = ld_i32(&p.dtok[base + i]);
+            par = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
+            if (p.amax)
+                p.amax[base + i] = a;
+        }
+        const bool valid = i >= 1 && i < dnb && par >= 0 && par < i;
+        const int anc0 = valid ? par : 0;
+        const int apar = __shfl(a, anc0);
+        int ok = i == 0 ? 1 : (valid && tok == apar ? 1 : 0);
+        int dep = i == 0 ? 0 : 1;
+        int anc = anc0;
+#pragma unroll
+        for (int round = 0; round < 6; ++round) {  // 2^6 >= 64 levels
+            const int ok2 = __shfl(ok, anc), dep2 = __shfl(dep, anc), anc2 = __shfl(anc, anc);
+            ok &= ok2;
+            dep += dep2;
+            anc = anc2;
+        }
+        const uint32_t key2 = (ok && i < dnb) ? (((uint32_t)dep << 16) | (0xFFFFu - (uint32_t)i)) : 0u;
+        const uint32_t kbest = wave_max_u32(key2);
+        const int best = (int)(0xFFFFu - (kbest & 0xFFFFu));
+        const int depth = (int)(kbest >> 16);
+        const int bon = __shfl(a, best);
+        // nodes on the root -> best path
+        unsigned long long onpath = 0ull;
+        int cur = best;
+        for (int s2 = 0; s2 < depth; ++s2) {
+            onpath |= 1ull << cur;
+            cur = __shfl(anc0, cur);
+        }
+        if (i < p.R) {
+            if ((onpath >> i) & 1ull)
+                p.out_tokens[base + dep - 1] = tok;
+            if (i == depth)
+                p.out_tokens[base + i] = bon;
+            else if (i > depth)
+                p.out_tokens[base + i] = -1;
+        }
+        if (lane == 0) {
+            p.accept_len[b] = depth;
+            p.accept_node[b] = best;
+            p.bonus[b] = bon;
+        }
+    } else {
+        for (int i = lane; i < p.R; i += 64) {
+            const unsigned long long key = ld_u64(&p.ws.keys[base + i]);
+            if (key)
+                st_u64(&p.ws.keys[base + i], 0ull);
+            const int a = i < dnb ? decode_key(key) : -1;
+            sh.epi.a[i] = a;
+            sh.epi.tok[i] = ld_i32(&p.dtok[base + i]);
+            sh.epi.par[i] = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
+            if (p.amax)
+                p.amax[base + i] = a;
+        }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_s_waitcnt(0);
+        int best = 0, depth = 0;
+        if (lane == 0) {
+            sh.epi.dep[0] = 0;
+            for (int i = 1; i < dnb; ++i) {
+                const int q = sh.epi.par[i];
+                int d = -1;
+                if (q >= 0 && q < i && sh.epi.dep[q] >= 0 && sh.epi.tok[i] == sh.epi.a[q])
+                    d = sh.epi.dep[q] + 1;
+                sh.epi.dep[i] = d;
+                if (d > depth) {
+                    depth = d;
+                    best = i;
+                }
+            }
+        }
+        best = __shfl(best, 0);
+        depth = __shfl(depth, 0);
+        const int bon = sh.epi.a[best];
+        for (int i = lane; i < p.R; i += 64)
+            if (i > depth)
+                p.out_tokens[base + i] = -1;
+        if (lane == 0) {
+            int cur = best;
+            for (int pos = depth - 1; pos >= 0; --pos) {
+                p.out_tokens[base + pos] = sh.epi.tok[cur];
+                cur = sh.epi.par[cur];
+            }
+            p.out_tokens[base + depth] = bon;
+            p.accept_len[b] = depth;
+            p.accept_node[b] = best;
+            p.bonus[b] = bon;
+        }
+    }
+    if (lane == 0)
+        st_u32(&p.ws.tk_all[b], 0u);
+}
+
+// ------------------------------------------------------------- kernels
+
+__global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
+    __shared__ Shared sh;
+    const int blk = blockIdx.x;
+    int b;
+    bool front;
+    if (blk < p.n_scan_wg) {
+        b = blk / p.scan_tiles;
+        scan_role(p, b, blk - b * p.scan_tiles, sh);
+        front = true;
+    } else if (blk < p.n_front_wg) {
+        b = blk - p.n_scan_wg;
+        probe_role(p, b, sh);
+        front = true;
+    } else {
+        const int idx = blk - p.n_front_wg;
+        const int rowi = idx / p.chunks;
+        const int c = idx - rowi * p.chunks;
+        b = rowi / p.R;
+        const int r = rowi - b * p.R;
+        if ((uint32_t)r < rows_needed(p, b))
+            argmax_role(p, b, r, c, sh);
+        front = false;
+    }
+    if (threadIdx.x >= 64)
+        return;  // waves 1.. are done; wave 0 arrives and may run an epilogue
+    if (front && p.epi_front != EPI_NONE) {
+        if (arrive(&p.ws.tk_front[b], p.exp_front))
+            front_epilogue(p, b);
+    }
+    if (p.epi_accept) {
+        if (arrive(&p.ws.tk_all[b], p.exp_all))
+            final_epilogue(p, b, sh);
+    }
+}
+
+__global__ __launch_bounds__(64) void k_select(StepParams p) {
+    const int b = blockIdx.x;
+    const int mn = p.match_n_in[b];
+    const int cl = clampi(p.copy_len_in[b], 0, p.k);
+    const float zb = p.z_in[b];
+    // copied token i (1-based) is copy_tokens[b, i-1]
+    select_write(p, b, mn, cl, zb, p.copy_tokens_in, (int64_t)b * p.k - 1);
+}
+
+}  // namespace
+
+int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
+    hipLaunchKernelGGL(k_switchsd, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_select_kernel(const StepParams &p, hipStream_t stream) {
+    hipLaunchKernelGGL(k_select, dim3((unsigned)p.B), dim3(64), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+}  // namespace switchsd

@@ -22,9 +22,11 @@ Every array of sequence b is drawn from its own numpy PCG64 stream
 ``SeedSequence([20186, cfg_id, stream, b])``, so any subset of a batch can be
 regenerated on its own.
 """
-from dataclasses import dataclass, field
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass
 from functools import lru_cache
 import math
+import os
 
 import numpy as np
 
@@ -228,8 +230,16 @@ def generate(wl, batch=None, logits=True):
         if npar is not None:
             npar[j] = p
         nn[j] = c
-        if logits:
-            lg[j] = make_logits_rows(wl, b)
+    if logits:
+        def fill(j):
+            lg[j] = make_logits_rows(wl, idx[j])
+        workers = max(1, min(16, os.cpu_count() or 1, n))
+        if workers > 1 and n * wl.R * wl.V > (1 << 24):
+            with ThreadPoolExecutor(workers) as ex:
+                list(ex.map(fill, range(n)))
+        else:
+            for j in range(n):
+                fill(j)
     w = (rng_for(wl, S_W).standard_normal(wl.d) / math.sqrt(wl.d)).astype(np.float32)
     return {"tokens": tokens, "lengths": np.full(n, wl.L, np.int32), "hidden": hidden,
             "w": w, "bias": np.float32(wl.bias), "ntok": ntok, "npar": npar, "nn": nn,

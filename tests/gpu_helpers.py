@@ -1,0 +1,117 @@
+"""Shared plumbing of the GPU tests: seeded inputs, oracle expectations, device
+upload and the calls through the C ABI binding."""
+import os
+import sys
+
+import numpy as np
+
+import oracle
+from paper_2609_20186_amd import workloads as W
+
+ORACLE_THREADS = max(1, min(16, os.cpu_count() or 1))
+INT_KEYS = ("match_n", "match_end", "copy_len", "copy_tokens", "use_copy", "dtok", "dpar", "dn",
+            "amax", "accept_len", "accept_node", "bonus", "out_tokens")
+Z_TOL = 1e-3   # absolute tolerance on the probe logit
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def ocfg(lens, kappa, k, theta):
+    return oracle.make_cfg(lens, kappa, k, theta)
+
+
+def planted_workload(name, batch=None):
+    """Inputs of a named workload with logits planted for the draft the oracle
+    selects (steps 1-3), as the workload recipe prescribes."""
+    wl = W.WORKLOADS[name]
+    d = W.generate(wl, batch=batch)
+    cfg = ocfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    sel = oracle.front(d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"],
+                       d["npar"], d["nn"], cfg)
+    d["target"] = W.plant_batch(wl, d, sel)
+    d["cfg"] = dict(lens=wl.ngram_lens, kappa=wl.kappa, k=wl.k, theta=wl.theta)
+    return d
+
+
+def oracle_step(d, rows=None):
+    c = d["cfg"]
+    cfg = ocfg(c["lens"], c["kappa"], c["k"], c["theta"])
+    sl = slice(None) if rows is None else rows
+    npar = None if d["npar"] is None else d["npar"][sl]
+    return oracle.step(d["tokens"][sl], d["lengths"][sl], d["hidden"][sl], d["w"], d["bias"],
+                       d["ntok"][sl], npar, d["nn"][sl], d["logits"][sl], cfg,
+                       threads=ORACLE_THREADS)
+
+
+def to_device(d):
+    import torch
+    dev = {"tokens": torch.from_numpy(np.ascontiguousarray(d["tokens"])).cuda(),
+           "lengths": torch.from_numpy(np.ascontiguousarray(d["lengths"])).cuda(),
+           "hidden": torch.from_numpy(np.ascontiguousarray(d["hidden"]).view(np.int16)).cuda(),
+           "w": torch.from_numpy(np.ascontiguousarray(d["w"])).cuda(),
+           "ntok": torch.from_numpy(np.ascontiguousarray(d["ntok"])).cuda(),
+           "npar": None if d["npar"] is None else
+           torch.from_numpy(np.ascontiguousarray(d["npar"])).cuda(),
+           "nn": torch.from_numpy(np.ascontiguousarray(d["nn"])).cuda(),
+           "logits": torch.from_numpy(np.ascontiguousarray(d["logits"]).view(np.int16)).cuda(),
+           "bias": float(d["bias"])}
+    return dev
+
+
+def sd_cfg(d):
+    from paper_2609_20186_amd import binding as sd
+    c = d["cfg"]
+    return sd.make_cfg(c["lens"], c["kappa"], c["k"], c["theta"])
+
+
+def gpu_step(dev, d, mode=0, out=None, ws=None):
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    B, R = dev["ntok"].shape
+    k = d["cfg"]["k"]
+    out = out or sd.alloc_outputs(B, R, k)
+    ws = ws if ws is not None else sd.alloc_workspace(B, R)
+    args = sd.build_step_args(dev, out, sd_cfg(d), mode)
+    sd.switchsd_step(args, ws)
+    torch.cuda.synchronize()
+    res = {k2: v.cpu().numpy() for k2, v in out.items()}
+    return res, ws
+
+
+def gpu_stages(dev, d):
+    """The four stage entry points in order."""
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    B, R = dev["ntok"].shape
+    k = d["cfg"]["k"]
+    cfg = sd_cfg(d)
+    o = sd.alloc_outputs(B, R, k)
+    ws = sd.alloc_workspace(B, R)
+    sd.switchsd_ngram_match(dev["tokens"], dev["lengths"], cfg, o["match_n"], o["match_end"],
+                            o["copy_len"], o["copy_tokens"], ws)
+    sd.switchsd_probe_score(dev["hidden"], dev["w"], dev["bias"], o["z"])
+    sd.switchsd_select_draft(o["match_n"], o["copy_len"], o["copy_tokens"], o["z"], dev["ntok"],
+                             dev["npar"], dev["nn"], cfg, o["use_copy"], o["dtok"], o["dpar"],
+                             o["dn"])
+    sd.switchsd_verify_accept(dev["logits"], o["dtok"], o["dpar"], o["dn"], o["accept_len"],
+                              o["accept_node"], o["bonus"], o["out_tokens"], o["amax"], ws)
+    torch.cuda.synchronize()
+    return {k2: v.cpu().numpy() for k2, v in o.items()}, ws
+
+
+def assert_match(got, exp, rows=None, what=""):
+    sl = slice(None) if rows is None else rows
+    for key in INT_KEYS:
+        g = got[key][sl]
+        e = exp[key]
+        if key == "copy_tokens":
+            g = g.reshape(e.shape)
+        if not np.array_equal(g, e):
+            bad = np.argwhere(g != e)[:5]
+            raise AssertionError(f"{what}: {key} differs at {bad.tolist()}: "
+                                 f"gpu {g[tuple(bad[0])]} oracle {e[tuple(bad[0])]}")
+    dz = np.abs(got["z"][sl].astype(np.float64) - exp["z"].astype(np.float64))
+    assert dz.max(initial=0.0) <= Z_TOL, f"{what}: |dz| = {dz.max()}"

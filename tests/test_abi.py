@@ -1,0 +1,132 @@
+"""The C ABI library loads, exports every declared entry point, and rejects bad
+arguments on the host before any HIP call (no GPU needed: only invalid calls
+are made here, which return before touching the device)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_20186_amd import binding as sd
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "switchsd.h")
+
+OK, EINVAL, ESHAPE, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(switchsd_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert set(names) >= {"switchsd_ngram_match", "switchsd_probe_score",
+                          "switchsd_select_draft", "switchsd_verify_accept", "switchsd_step",
+                          "switchsd_workspace_bytes", "switchsd_status_string"}
+    lib = ctypes.CDLL(sd.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_workspace_size():
+    for s in (OK, EINVAL, ESHAPE, EHIP, EWORKSPACE):
+        assert sd.status_string(s) and sd.status_string(s) != "unknown status"
+    assert sd.status_string(17) == "unknown status"
+    assert sd.workspace_bytes(32, 8) >= 32 * 8 * 8 + 32 * 8 * 4 + 2 * 32 * 4
+    assert sd.workspace_bytes(64, 8) >= sd.workspace_bytes(32, 8)
+    assert sd.workspace_bytes(-1, 8) == 0
+
+
+# Host buffers stand in for device pointers: every call below fails validation
+# and never reaches HIP.
+_buf = np.zeros(1 << 16, np.uint8)
+P = _buf.ctypes.data
+WS = (P + 255) & ~255
+
+
+def step_args(**kw):
+    a = sd.StepArgs()
+    for f, _ in sd.StepArgs._fields_:
+        if f not in ("B", "Lmax", "d", "R", "V", "bias", "cfg", "mode"):
+            setattr(a, f, P)
+    a.B, a.Lmax, a.d, a.R, a.V = 2, 16, 8, 8, 100
+    a.cfg = sd.make_cfg((3, 2, 1), 1, 7, 0.0)
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def call_step(a, ws=WS, nbytes=4096):
+    return sd.lib.switchsd_step(ctypes.byref(a), ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), ESHAPE), (dict(Lmax=0), ESHAPE), (dict(d=-1), ESHAPE), (dict(R=0), ESHAPE),
+    (dict(R=2000), ESHAPE), (dict(V=0), ESHAPE), (dict(R=7), ESHAPE),   # k + 1 > R
+    (dict(mode=3), EINVAL), (dict(tokens=None), EINVAL), (dict(logits=None), EINVAL),
+    (dict(logits=P + 1), EINVAL), (dict(out_tokens=None), EINVAL), (dict(dn=None), EINVAL),
+    (dict(hidden=None), EINVAL), (dict(nn=None), EINVAL),
+])
+def test_step_rejects(kw, code):
+    assert call_step(step_args(**kw)) == code
+
+
+def test_step_optional_pointers_and_empty_batch():
+    # B = 0 is a no-op even with every pointer null
+    a = sd.StepArgs()
+    a.B, a.Lmax, a.d, a.R, a.V = 0, 1, 0, 1, 1
+    a.cfg = sd.make_cfg((1,), 1, 0, 0.0)
+    assert call_step(a, ws=None, nbytes=0) == OK
+    # d = 0 needs no hidden/w; k = 0 needs no copy_tokens (still rejected later
+    # for the deliberately tiny workspace, before any HIP call)
+    a = step_args(d=0, hidden=None, w=None)
+    assert call_step(a, nbytes=16) == EWORKSPACE
+
+
+@pytest.mark.parametrize("cfg", [
+    dict(ngram_lens=(), kappa=1), dict(ngram_lens=(2, 3), kappa=1), dict(ngram_lens=(3, 3)),
+    dict(ngram_lens=(65,)), dict(ngram_lens=(0,)), dict(ngram_lens=(3,), kappa=0),
+    dict(ngram_lens=(3,), k=-1),
+])
+def test_bad_cfg(cfg):
+    c = sd.make_cfg(**{"kappa": 1, "k": 7, **cfg})
+    if not cfg.get("ngram_lens"):
+        c.n_ngram = 0
+    assert call_step(step_args(cfg=c)) == EINVAL
+    rc = sd.lib.switchsd_ngram_match(P, P, 2, 16, ctypes.byref(c), P, P, P, P, WS, 4096, None)
+    assert rc == EINVAL
+
+
+def test_workspace_checks():
+    a = step_args()
+    need = sd.workspace_bytes(2, 8)
+    assert call_step(a, ws=None) == EWORKSPACE
+    assert call_step(a, ws=WS + 8, nbytes=need) == EWORKSPACE       # misaligned
+    assert call_step(a, ws=WS, nbytes=need - 1) == EWORKSPACE       # too small
+
+
+def test_stage_entry_points_reject():
+    cfg = sd.make_cfg((3, 2, 1), 1, 7, 0.0)
+    lib = sd.lib
+    assert lib.switchsd_ngram_match(P, P, -1, 16, ctypes.byref(cfg), P, P, P, P, WS, 4096,
+                                    None) == ESHAPE
+    assert lib.switchsd_ngram_match(None, P, 2, 16, ctypes.byref(cfg), P, P, P, P, WS, 4096,
+                                    None) == EINVAL
+    assert lib.switchsd_ngram_match(P, P, 0, 16, ctypes.byref(cfg), None, None, None, None,
+                                    None, 0, None) == OK
+    assert lib.switchsd_probe_score(P, P, 0.0, 2, -1, P, None) == ESHAPE
+    assert lib.switchsd_probe_score(None, P, 0.0, 2, 8, P, None) == EINVAL
+    assert lib.switchsd_probe_score(P, P, 0.0, 0, 8, None, None) == OK
+    assert lib.switchsd_select_draft(P, P, P, P, P, P, P, 2, 7, ctypes.byref(cfg), P, P, P, P,
+                                     None) == ESHAPE           # k + 1 > R
+    assert lib.switchsd_select_draft(P, P, P, P, None, P, P, 2, 8, ctypes.byref(cfg), P, P, P,
+                                     P, None) == EINVAL
+    assert lib.switchsd_verify_accept(P, 2, 8, 0, P, P, P, P, P, P, P, P, WS, 4096,
+                                      None) == ESHAPE
+    assert lib.switchsd_verify_accept(P + 1, 2, 8, 100, P, P, P, P, P, P, P, P, WS, 4096,
+                                      None) == EINVAL
+    assert lib.switchsd_verify_accept(P, 2, 8, 100, P, P, P, P, P, P, P, P, WS, 8,
+                                      None) == EWORKSPACE

@@ -1,0 +1,218 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integers (match positions, copied tokens, draft choice, argmaxes, accepted
+lengths, bonus and output tokens) must be bit-exact; the probe logit within
+1e-3 absolute, with the copy decision itself exact.
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import (assert_match, gpu_stages, gpu_step, oracle_step, planted_workload, say,
+                         to_device)
+from paper_2609_20186_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+SPLIT, FUSED, AUTO = 2, 1, 0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_20186_amd import binding  # noqa: F401  (fails loudly if not built)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4"])
+def test_parity_full_workload(name):
+    say(f"[parity] {name} full size, AUTO mode")
+    d = planted_workload(name)
+    exp = oracle_step(d)
+    np.testing.assert_array_equal(exp["accept_node"], d["target"])   # planted acceptance
+    dev = to_device(d)
+    got, ws = gpu_step(dev, d, AUTO)
+    assert_match(got, exp, what=name)
+    assert int(ws.count_nonzero()) == 0, "workspace not left zeroed"
+    say(f"[parity] {name}: copy on {int(exp['use_copy'].sum())}/{len(exp['use_copy'])}, "
+        f"mean accept {exp['accept_len'].mean():.2f}, min|z-theta| "
+        f"{np.abs(exp['z'] - W.WORKLOADS[name].theta).min():.3g}")
+
+
+def test_parity_c5_full_size_sampled():
+    """C5 at full size (256 x 60 x 128256 logits) in both launch modes; the
+    oracle checks a sample of sequences one by one."""
+    say("[parity] C5 full size, sampled oracle")
+    d = planted_workload("C5")
+    dev = to_device(d)
+    got, _ = gpu_step(dev, d, AUTO)          # SPLIT: rows of the chosen draft only
+    rows = np.array([0, 1, 2, 3, 63, 64, 127, 128, 200, 254, 255])
+    exp = oracle_step(d, rows)
+    assert_match(got, exp, rows, what="C5 split")
+    np.testing.assert_array_equal(got["accept_node"], d["target"])
+    fused, _ = gpu_step(dev, d, FUSED)       # one launch reading every row
+    for key in got:
+        np.testing.assert_array_equal(fused[key], got[key], err_msg=key)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2"])
+def test_stages_equal_fused_and_split(name):
+    say(f"[stages] {name}")
+    d = planted_workload(name)
+    dev = to_device(d)
+    fused, _ = gpu_step(dev, d, FUSED)
+    split, _ = gpu_step(dev, d, SPLIT)
+    stages, ws = gpu_stages(dev, d)
+    for key in fused:
+        np.testing.assert_array_equal(split[key], fused[key], err_msg="split " + key)
+        np.testing.assert_array_equal(stages[key], fused[key], err_msg="stages " + key)
+    assert int(ws.count_nonzero()) == 0
+
+
+def test_determinism_repeats():
+    say("[determinism] C2 x10")
+    d = planted_workload("C2")
+    dev = to_device(d)
+    first, ws = gpu_step(dev, d, AUTO)
+    from paper_2609_20186_amd import binding as sd
+    out = sd.alloc_outputs(32, 8, 7)
+    for i in range(10):
+        got, _ = gpu_step(dev, d, FUSED if i % 2 else SPLIT, out=out, ws=ws)
+        for key in first:
+            np.testing.assert_array_equal(got[key], first[key], err_msg=key)
+
+
+# ------------------------------------------------------------------ edge cases
+
+SPECIAL = np.array([0x7F80, 0xFF80, 0x7FC0, 0xFFC0, 0x8000, 0x0000, 0x0001], np.uint16)
+
+
+def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vocab=None,
+                ragged=True, specials=False, ties=False, repeat_tail=0, plant=False):
+    rng = np.random.default_rng(seed)
+    vocab = vocab or V
+    tokens = rng.integers(0, vocab, (B, Lmax)).astype(np.int32)
+    if repeat_tail:
+        # the last `repeat_tail` tokens also occur ending at position 4100, so a
+        # long match straddles the boundary between the first two scan tiles
+        tokens[:, 4101 - repeat_tail:4101] = tokens[:, Lmax - repeat_tail:]
+    lengths = np.full(B, Lmax, np.int32)
+    if ragged:
+        lengths = rng.integers(0, Lmax + 1, B).astype(np.int32)
+        lengths[0] = Lmax
+        if B > 2:
+            lengths[1], lengths[2] = 1, Lmax + 5       # single token; clamped to Lmax
+    hidden = W.f32_to_bf16_bits(rng.standard_normal((B, d)).astype(np.float32))
+    w = (rng.standard_normal(d) / np.sqrt(max(d, 1))).astype(np.float32)
+    ntok = rng.integers(0, vocab, (B, R)).astype(np.int32)
+    nn = rng.integers(1, R + 1, B).astype(np.int32)
+    npar = None
+    if tree:
+        npar = np.zeros((B, R), np.int32)
+        for b in range(B):
+            npar[b, 0] = -1
+            for i in range(1, R):
+                npar[b, i] = int(rng.integers(0, i))
+            if R > 3:
+                npar[b, R - 1] = R + 4                  # invalid: never accepted
+    if ties:
+        logits = rng.choice(np.array([0xBF80, 0x8000, 0x0000, 0x3F80, 0x4000], np.uint16),
+                            (B, R, V))
+    else:
+        logits = W.f32_to_bf16_bits(np.clip(rng.standard_normal((B, R, V)), -7.5, 7.5)
+                                    .astype(np.float32))
+    if specials:
+        m = rng.random((B, R, V)) < 0.05
+        logits[m] = rng.choice(SPECIAL, int(m.sum()))
+        logits[0, 0, :] = 0x7FC0                            # an all-NaN row
+    d_ = {"tokens": tokens, "lengths": lengths, "hidden": hidden, "w": w, "bias": np.float32(0.1),
+          "ntok": ntok, "npar": npar, "nn": nn, "logits": logits,
+          "cfg": dict(lens=tuple(lens), kappa=kappa, k=k, theta=theta)}
+    if plant:
+        # plant acceptance up to a random node of the draft the oracle selects
+        import oracle
+        sel = oracle.front(tokens, lengths, hidden, w, d_["bias"], ntok, npar, nn,
+                           oracle.make_cfg(lens, kappa, k, theta))
+        for b in range(B):
+            t = int(rng.integers(0, sel["dn"][b]))
+            W.plant(logits[b], sel["dtok"][b], sel["dpar"][b], int(sel["dn"][b]), t)
+    return d_
+
+
+CASES = {
+    # several scan tiles with a ragged tail, misaligned rows, several chunks
+    "tiles_ragged": dict(seed=1, B=5, Lmax=9000, V=70001, R=9, k=8, lens=(3, 2, 1), kappa=1,
+                         theta=0.0, vocab=50, plant=True),
+    "tiny_vocab_ties": dict(seed=2, B=7, Lmax=300, V=9, R=6, k=5, lens=(4, 2), kappa=2,
+                            theta=-0.3, vocab=3, ties=True),
+    "v1": dict(seed=3, B=3, Lmax=40, V=1, R=4, k=3, lens=(2, 1), kappa=1, theta=0.0, vocab=1),
+    "v7_specials": dict(seed=4, B=4, Lmax=64, V=7, R=5, k=4, lens=(3, 1), kappa=1, theta=0.0,
+                        vocab=4, specials=True),
+    "v32769_specials": dict(seed=5, B=3, Lmax=100, V=32769, R=4, k=3, lens=(2,), kappa=1,
+                            theta=-np.inf, vocab=5, specials=True),
+    "paper_setting": dict(seed=6, B=4, Lmax=5000, V=1000, R=21, k=20, lens=(5,), kappa=5,
+                          theta=-0.4, vocab=4, plant=True),
+    "copyspec": dict(seed=7, B=6, Lmax=700, V=500, R=8, k=7, lens=(3, 2, 1), kappa=1,
+                     theta=-np.inf, vocab=20, plant=True),
+    "probe_off": dict(seed=8, B=6, Lmax=700, V=500, R=8, k=7, lens=(3, 2, 1), kappa=1,
+                      theta=np.inf, vocab=20),
+    "tree_small": dict(seed=9, B=9, Lmax=2000, V=300, R=30, k=7, lens=(3, 2, 1), kappa=1,
+                       theta=0.0, vocab=3, tree=True, ties=True, plant=True),
+    "tree_r64": dict(seed=10, B=5, Lmax=500, V=40, R=64, k=10, lens=(2, 1), kappa=1, theta=0.0,
+                     vocab=2, tree=True, ties=True),
+    "tree_r100_general": dict(seed=11, B=4, Lmax=500, V=40, R=100, k=10, lens=(2, 1), kappa=1,
+                              theta=0.0, vocab=2, tree=True, ties=True),
+    "chain_r100_general": dict(seed=12, B=3, Lmax=300, V=3, R=100, k=99, lens=(1,), kappa=1,
+                               theta=-np.inf, vocab=2, ties=True, plant=True),
+    "long_halo_ngram64": dict(seed=13, B=3, Lmax=8300, V=100, R=3, k=2, lens=(64, 63, 1),
+                              kappa=1, theta=0.0, vocab=2, ragged=False, repeat_tail=80),
+    "k0_d0": dict(seed=14, B=4, Lmax=50, V=20, R=2, k=0, lens=(1,), kappa=1, theta=-np.inf,
+                  vocab=3, d=0),
+    "d_odd": dict(seed=15, B=3, Lmax=50, V=20, R=3, k=2, lens=(1,), kappa=1, theta=0.0,
+                  vocab=3, d=1027),
+}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_edge_case_parity(case):
+    say(f"[edge] {case}")
+    d = custom_case(**CASES[case])
+    exp = oracle_step(d)
+    dev = to_device(d)
+    for mode in (AUTO, FUSED, SPLIT):
+        got, ws = gpu_step(dev, d, mode)
+        assert_match(got, exp, what=f"{case} mode {mode}")
+        assert int(ws.count_nonzero()) == 0
+    stages, _ = gpu_stages(dev, d)
+    assert_match(stages, exp, what=f"{case} stages")
+
+
+def test_misaligned_logits_view():
+    """A logits view starting 2 bytes past an aligned address (every row
+    misaligned) gives the same argmaxes."""
+    say("[edge] misaligned logits view")
+    import torch
+    d = custom_case(seed=20, B=3, Lmax=100, V=40000, R=4, k=3, lens=(2, 1), kappa=1, theta=0.0,
+                    vocab=10)
+    exp = oracle_step(d)
+    dev = to_device(d)
+    flat = torch.empty(d["logits"].size + 1, dtype=torch.int16, device="cuda")
+    flat[1:] = dev["logits"].reshape(-1)
+    dev["logits"] = flat[1:].view(d["logits"].shape)
+    got, _ = gpu_step(dev, d, AUTO)
+    assert_match(got, exp, what="misaligned")
+
+
+def test_empty_batch():
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    e = torch.empty((0, 8), dtype=torch.int32, device="cuda")
+    out = sd.alloc_outputs(0, 8, 7)
+    dev = {"tokens": e, "lengths": torch.empty(0, dtype=torch.int32, device="cuda"),
+           "hidden": torch.empty((0, 16), dtype=torch.int16, device="cuda"),
+           "w": torch.zeros(16, device="cuda"), "ntok": e, "npar": None,
+           "nn": torch.empty(0, dtype=torch.int32, device="cuda"),
+           "logits": torch.empty((0, 8, 100), dtype=torch.int16, device="cuda"), "bias": 0.0}
+    args = sd.build_step_args(dev, out, sd.make_cfg((3, 2, 1), 1, 7, 0.0))
+    sd.switchsd_step(args, sd.alloc_workspace(1, 8))
+    torch.cuda.synchronize()
