@@ -55,25 +55,66 @@ int check_workspace(const void *ws, size_t bytes, int32_t B, int32_t R) {
     return SWITCHSD_OK;
 }
 
-Workspace carve(void *ws, int32_t B) {
+int32_t key_stride_for(int32_t R) {
+    return (int32_t)(((int64_t)R + kLineU64 - 1) / kLineU64 * kLineU64);
+}
+
+Workspace carve(void *ws, int32_t B, int32_t R) {
     Workspace w;
     char *base = (char *)ws;
-    size_t off = 0;
-    w.tk_front = (uint32_t *)(base + off);
-    off += align_up((size_t)B * 4);
-    w.tk_all = (uint32_t *)(base + off);
-    off += align_up((size_t)B * 4);
-    w.mslot = (int32_t *)(base + off);
-    off += align_up((size_t)B * SWITCHSD_MAX_NGRAM * 4);
-    w.keys = (unsigned long long *)(base + off);
+    const size_t line = (size_t)kLineU32 * 4;
+    w.tk_front = (uint32_t *)base;
+    w.tk_all = (uint32_t *)(base + (size_t)B * line);
+    w.mslot = (int32_t *)(base + 2 * (size_t)B * line);
+    w.keys = (unsigned long long *)(base + 3 * (size_t)B * line);
+    w.key_stride = key_stride_for(R);
     return w;
 }
 
 int scan_tiles_for(int32_t Lmax) { return (int)((Lmax + kScanTile - 1) / kScanTile); }
 
-int chunks_for(int32_t V) { return (int)((V + (int64_t)kChunkElems - 1) / kChunkElems); }
+// Compute units of the current device (cached per device).
+int cu_count(int *out) {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return SWITCHSD_EHIP;
+    if (dev >= 0 && dev < 64 && cache[dev] > 0) {
+        *out = cache[dev];
+        return SWITCHSD_OK;
+    }
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+        return SWITCHSD_EHIP;
+    if (dev >= 0 && dev < 64)
+        cache[dev] = n;
+    *out = n;
+    return SWITCHSD_OK;
+}
 
-// the grid must fit a 32-bit block index
+// Split each of `rows` logits rows into segments so that the argmax role has
+// about two work-groups per compute unit, each segment at least one 16 KB
+// chunk long.  Sets p.segs and p.seg_elems.
+int set_segments(StepParams &p, int64_t rows, int32_t V) {
+    int cus = 0;
+    const int rc = cu_count(&cus);
+    if (rc)
+        return rc;
+    const int64_t nvec = ((int64_t)V + 7) / 8;
+    int64_t segs = (2 * (int64_t)cus + rows - 1) / rows;
+    const int64_t max_segs = nvec / kChunkVecs > 1 ? nvec / kChunkVecs : 1;
+    if (segs > max_segs)
+        segs = max_segs;
+    if (segs < 1)
+        segs = 1;
+    int64_t seg_elems = ((V + segs - 1) / segs + 7) / 8 * 8;
+    segs = (V + seg_elems - 1) / seg_elems;
+    p.segs = (int32_t)segs;
+    p.seg_elems = (int32_t)seg_elems;
+    return SWITCHSD_OK;
+}
+
 bool grid_ok(int64_t g) { return g >= 1 && g <= 0x7FFFFFFFll; }
 
 int set_scan(StepParams &p, int32_t B, int32_t Lmax) {
@@ -92,8 +133,9 @@ extern "C" {
 size_t switchsd_workspace_bytes(int32_t B, int32_t R) {
     if (B < 0 || R < 0)
         return 0;
-    return align_up((size_t)B * 4) * 2 + align_up((size_t)B * SWITCHSD_MAX_NGRAM * 4) +
-           align_up((size_t)B * (size_t)R * 8);
+    // per sequence: three 256-byte lines (two tickets, the n-gram slots) and
+    // the row keys rounded up to whole lines
+    return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8);
 }
 
 const char *switchsd_status_string(int status) {
@@ -141,7 +183,7 @@ int switchsd_ngram_match(const int32_t *tokens, const int32_t *lengths, int32_t 
     p.match_end = match_end;
     p.copy_len = copy_len;
     p.copy_tokens = copy_tokens;
-    p.ws = carve(workspace, B);
+    p.ws = carve(workspace, B, 0);
     if ((rc = set_scan(p, B, Lmax)))
         return rc;
     p.n_front_wg = p.n_scan_wg;
@@ -220,12 +262,13 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
     int rc = check_workspace(workspace, workspace_bytes, B, R);
     if (rc)
         return rc;
-    const int chunks = chunks_for(V);
-    const int64_t grid = (int64_t)B * R * chunks;
-    if (!grid_ok(grid))
-        return SWITCHSD_ESHAPE;
     StepParams p;
     memset(&p, 0, sizeof p);
+    if ((rc = set_segments(p, (int64_t)B * R, V)))
+        return rc;
+    const int64_t grid = (int64_t)B * R * p.segs;
+    if (!grid_ok(grid))
+        return SWITCHSD_ESHAPE;
     p.logits = logits;
     p.B = B;
     p.R = R;
@@ -238,11 +281,10 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
     p.bonus = bonus;
     p.out_tokens = out_tokens;
     p.amax = amax;
-    p.ws = carve(workspace, B);
-    p.chunks = chunks;
+    p.ws = carve(workspace, B, R);
     p.rows_mode = ROWS_DRAFT;
     p.epi_accept = 1;
-    p.exp_all = (uint32_t)(R * chunks);
+    p.exp_all = (uint32_t)(R * p.segs);
     return launch_step_kernel(p, grid, stream);
 }
 
@@ -269,7 +311,6 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         return SWITCHSD_EINVAL;
     if ((rc = check_workspace(workspace, workspace_bytes, B, R)))
         return rc;
-    const int chunks = chunks_for(V);
     StepParams p;
     memset(&p, 0, sizeof p);
     fill_cfg(p, &a->cfg);
@@ -301,7 +342,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.accept_node = a->accept_node;
     p.bonus = a->bonus;
     p.out_tokens = a->out_tokens;
-    p.ws = carve(workspace, B);
+    p.ws = carve(workspace, B, R);
     if ((rc = set_scan(p, B, a->Lmax)))
         return rc;
     p.probe_on = 1;
@@ -312,20 +353,18 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     int mode = a->mode;
     if (mode == SWITCHSD_MODE_AUTO)
         mode = a->cfg.k + 1 >= R ? SWITCHSD_MODE_FUSED : SWITCHSD_MODE_SPLIT;
-    const int64_t argmax_wg = (int64_t)B * R * chunks;
     if (mode == SWITCHSD_MODE_FUSED) {
-        const int64_t grid = p.n_front_wg + argmax_wg;
+        if ((rc = set_segments(p, (int64_t)B * R, V)))
+            return rc;
+        const int64_t grid = p.n_front_wg + (int64_t)B * R * p.segs;
         if (!grid_ok(grid))
             return SWITCHSD_ESHAPE;
-        p.chunks = chunks;
         p.rows_mode = a->cfg.k + 1 >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;
         p.epi_accept = 1;
-        p.exp_all = p.exp_front + (uint32_t)(R * chunks);
+        p.exp_all = p.exp_front + (uint32_t)(R * p.segs);
         return launch_step_kernel(p, grid, stream);
     }
     // SPLIT: front (scan + probe + select), then verify over the chosen rows
-    if (!grid_ok(argmax_wg))
-        return SWITCHSD_ESHAPE;
     if ((rc = launch_step_kernel(p, p.n_front_wg, stream)))
         return rc;
     return switchsd_verify_accept(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,

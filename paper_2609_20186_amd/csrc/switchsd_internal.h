@@ -10,21 +10,26 @@ namespace switchsd {
 
 // Work-group shape of every kernel of the step: 256 lanes = 4 wave64s.
 constexpr int kThreads = 256;
-// 16-byte logits loads in flight per lane in one argmax work-group.
-constexpr int kUnroll = 16;
-// Logits elements covered by one argmax work-group (one pass, all loads in flight).
-constexpr int kChunkElems = kThreads * kUnroll * 8;
+// 16-byte logits vectors per lane in one chunk of the argmax stream.
+constexpr int kUnroll = 4;
+// 16-byte vectors in one chunk (16 KB); two chunks are in flight per work-group.
+constexpr int kChunkVecs = kThreads * kUnroll;
 // Context end positions covered by one scan work-group.
 constexpr int kScanTile = 4096;
+// Per-sequence workspace slots live on their own 256-byte lines: atomics to
+// one line serialize, and every work-group of a sequence arrives at its line.
+constexpr int kLineU32 = 64;
+constexpr int kLineU64 = 32;
 
 enum : int32_t { EPI_NONE = 0, EPI_MATCH = 1, EPI_SELECT = 2 };
 enum : int32_t { ROWS_ALL = 0, ROWS_NEURAL_OR_COPY = 1, ROWS_DRAFT = 2 };
 
 struct Workspace {
-    uint32_t *tk_front;           // [B] arrivals of the scan/probe work-groups
-    uint32_t *tk_all;             // [B] arrivals of every work-group of a sequence
-    int32_t *mslot;               // [B, 8] most recent end + 1 per n-gram length
-    unsigned long long *keys;     // [B, R] packed (value key, ~index) row maxima
+    uint32_t *tk_front;        // [B] x 256 B: arrivals of the scan/probe work-groups
+    uint32_t *tk_all;          // [B] x 256 B: arrivals of every work-group of a sequence
+    int32_t *mslot;            // [B] x 256 B: most recent end + 1 per n-gram length
+    unsigned long long *keys;  // [B] x key_stride: packed (value key, ~index) row maxima
+    int32_t key_stride;        // u64 per sequence (R rounded up to a 256-byte line)
 };
 
 struct StepParams {
@@ -57,10 +62,11 @@ struct StepParams {
     int32_t *amax;
     int32_t *accept_len, *accept_node, *bonus, *out_tokens;
     Workspace ws;
-    // grid layout: [scan tiles][probe][argmax chunks]
+    // grid layout: [scan tiles][probe][argmax row segments]
     int32_t scan_tiles;  // per sequence (0: no scan role)
     int32_t probe_on;    // 1: one probe work-group per sequence
-    int32_t chunks;      // argmax work-groups per row (0: no argmax role)
+    int32_t segs;        // argmax work-groups per row (0: no argmax role)
+    int32_t seg_elems;   // logits elements per row segment (multiple of 8)
     int32_t n_scan_wg;   // B * scan_tiles
     int32_t n_front_wg;  // n_scan_wg + B * probe_on
     int32_t rows_mode;

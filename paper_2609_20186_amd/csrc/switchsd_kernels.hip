@@ -6,27 +6,30 @@
 //   scan    a 4096-position tile of one context, staged in LDS with an
 //           (n_max - 1)-token halo; every lane measures how far the suffix
 //           matches backwards from each of its end positions; the most recent
-//           end per n-gram length is max-reduced over the wave, the
+//           end per n-gram length is max-reduced over the wave (DPP), the
 //           work-group and (atomicMax) the tiles of the sequence.
 //           (Sec. 3.3: kappa-gram with a prior occurrence, ranked by recency.)
 //   probe   w . h for one sequence: exact bf16 x float products, summed in
 //           double-double with a fixed reduction order.  (Sec. 3.2, Eq. 3.)
-//   argmax  32768 elements of one logits row, every 16-byte load in flight at
-//           once; lane maxima with the NaN-propagating v_maximum3_f32, then
-//           the lowest index of the work-group maximum, packed as
-//           (order key << 32 | ~index) and atomicMax-ed into the row's slot.
-//           (Sec. 2 / App. A: greedy verification at T = 0.)
+//   argmax  one segment of one logits row, streamed in 16 KB chunks with the
+//           next chunk's nontemporal 16-byte loads in flight while the current
+//           one is reduced.  Lane maxima use the NaN-propagating
+//           v_maximum3_f32 (1.5 VALU ops per element); a ballot asks whether
+//           any lane beat the wave's running maximum, and only then does the
+//           wave reduce and look up the lowest index holding it.  The segment
+//           result is packed as (order key << 32 | ~index) and atomicMax-ed
+//           into the row's slot.  (Sec. 2 / App. A: greedy verification, T = 0.)
 //
 // Two last-arriver epilogues close a sequence without a second launch:
 //   front   when its scan tiles and probe are done: pick the match, gather the
 //           copy candidate, apply the switch (Sec. 3.3, Eq. 4) and write the
 //           chosen draft;
 //   final   when every work-group of the sequence is done: decode the row
-//           argmaxes and run the accept walk (Sec. 3.3, Parallel Verification)
-//           by pointer jumping over the draft tree, one node per lane.
-// Arrivals use agent-scope acquire/release atomics, so the epilogue sees the
-// partial results of work-groups on other XCDs.  Each epilogue resets the
-// workspace slots it consumed, leaving the workspace zeroed for the next call.
+//           argmaxes and run the accept walk (Sec. 3.3, Parallel Verification):
+//           a ballot for chains, pointer jumping over the tree, one node per
+//           lane, for trees of up to 64 nodes, a sequential walk beyond.
+// Each epilogue resets the workspace slots it consumed, leaving the workspace
+// zeroed for the next call.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -37,14 +40,17 @@ namespace switchsd {
 
 namespace {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kWaves = kThreads / 64;
 constexpr int kScanHaloMax = SWITCHSD_MAX_NGRAM_LEN;
 constexpr int kScanPerLane = (kScanTile + kScanHaloMax + kThreads - 1) / kThreads;
+constexpr uint32_t kNoIdx = 0xFFFFFFFFu;
 
 struct ScanShared {
     int32_t tile[kScanTile + kScanHaloMax];
     int32_t pat[SWITCHSD_MAX_NGRAM_LEN];
-    int32_t red[kWaves][SWITCHSD_MAX_NGRAM];
+    int32_t red[SWITCHSD_MAX_NGRAM];
 };
 struct ArgmaxShared {
     float wmax[kWaves];
@@ -92,51 +98,53 @@ __device__ __forceinline__ void st_u32(uint32_t *p, uint32_t v) {
 }
 
 // Wave 0 arrives at a per-sequence ticket; true (wave-uniform) for the last
-// of `expected` arrivals.  Release orders this wave's earlier writes before
-// the arrival; acquire makes the others' writes visible to the last one.
+// of `expected` arrivals.
+//
+// Every value one work-group hands to another travels through agent-scope
+// atomics (RMW slots, or relaxed atomic stores and loads), which are coherent
+// across the XCDs without any L2 write-back or invalidation.  Waiting for this
+// wave's outstanding memory operations (vmcnt = 0) before the arrival
+// therefore orders all of them ahead of it; the last arriver's reads are
+// issued only after its arrival has returned.  An agent-scope release/acquire
+// fence would give the same order but write back and invalidate the L2 of the
+// XCD at every arrival, which costs more than the whole step.
 __device__ __forceinline__ bool arrive(uint32_t *ticket, uint32_t expected) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0);
     uint32_t old = 0;
     if (threadIdx.x == 0)
-        old = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        old = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     old = __shfl(old, 0);
-    const bool last = old + 1u == expected;
-    if (last)
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    return last;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    return old + 1u == expected;
 }
 
-// ------------------------------------------------------------- wave reductions
+// ------------------------------------------------------------- wave reductions (DPP)
 
+// Row shifts 1, 2, 4, 8 give every lane the reduction of its 16-lane row up
+// to itself; two row broadcasts fold the rows into lane 63.  Lanes whose DPP
+// source is out of range keep the identity.
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, uint32_t id, Op op) {
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x111, 0xf, 0xf, false));
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x112, 0xf, 0xf, false));
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x114, 0xf, 0xf, false));
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x118, 0xf, 0xf, false));
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x142, 0xa, 0xf, false));
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x143, 0xc, 0xf, false));
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
 __device__ __forceinline__ float wave_max_f32(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1)
-        v = __builtin_elementwise_maximum(v, __shfl_xor(v, o));
-    return v;
+    auto op = [](uint32_t a, uint32_t b) {
+        return __float_as_uint(__builtin_elementwise_maximum(__uint_as_float(a), __uint_as_float(b)));
+    };
+    return __uint_as_float(wave_reduce_u32(__float_as_uint(v), 0xFF800000u, op));
 }
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        uint32_t t = __shfl_xor(v, o);
-        v = t < v ? t : v;
-    }
-    return v;
+    return wave_reduce_u32(v, 0xFFFFFFFFu, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
 }
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        uint32_t t = __shfl_xor(v, o);
-        v = t > v ? t : v;
-    }
-    return v;
-}
-__device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        int32_t t = __shfl_xor(v, o);
-        v = t > v ? t : v;
-    }
-    return v;
+    return wave_reduce_u32(v, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
 }
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) {
@@ -154,13 +162,17 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh) {
     const int lo = t0 - H > 0 ? t0 - H : 0;
     const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
 
-    // The tile loads do not depend on the sequence length: issue them first.
+    // The tile, the length and the suffix of a full-length context do not
+    // depend on each other: issue all of them at once (indices clamped into
+    // range, so that no load sits behind a branch).
     int32_t reg[kScanPerLane];
 #pragma unroll
     for (int i = 0; i < kScanPerLane; ++i) {
         const int x = lo + i * kThreads + tid;
-        reg[i] = x < hi ? p.tokens[row + x] : 0;
+        reg[i] = p.tokens[row + (x < hi ? x : hi - 1)];
     }
+    const int tp = tid < p.nmax ? tid : 0;
+    const int32_t pat_full = p.tokens[row + (p.Lmax - 1 - tp >= 0 ? p.Lmax - 1 - tp : 0)];
     const int L = clampi(p.lengths[b], 0, p.Lmax);
 #pragma unroll
     for (int i = 0; i < kScanPerLane; ++i) {
@@ -168,8 +180,10 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh) {
         if (lo + j < hi)
             sh.scan.tile[j] = reg[i];
     }
+    if (tid < SWITCHSD_MAX_NGRAM)
+        sh.scan.red[tid] = 0;
     if (tid < p.nmax && tid < L)
-        sh.scan.pat[tid] = p.tokens[row + L - 1 - tid];
+        sh.scan.pat[tid] = L == p.Lmax ? pat_full : p.tokens[row + L - 1 - tid];
     __syncthreads();
 
     int32_t best[SWITCHSD_MAX_NGRAM];
@@ -179,13 +193,29 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh) {
     // occurrences end at e <= L-2
     const int eend = t0 + kScanTile < L - 1 ? t0 + kScanTile : L - 1;
     if (t0 < eend) {
+        const int p0 = sh.scan.pat[0];
+        const int p1 = p.nmax > 1 ? sh.scan.pat[1] : 0;
+        const int p2 = p.nmax > 2 ? sh.scan.pat[2] : 0;
+        const int p3 = p.nmax > 3 ? sh.scan.pat[3] : 0;
+#pragma unroll 4
         for (int i = 0; i < kScanTile / kThreads; ++i) {
             const int e = t0 + i * kThreads + tid;
             if (e < eend) {
                 const int lim = p.nmax < e + 1 ? p.nmax : e + 1;
-                int m = 0;
-                while (m < lim && sh.scan.tile[e - m - lo] == sh.scan.pat[m])
-                    ++m;
+                const int x = e - lo;  // tile index of position e; e - t >= lo for t < lim
+                // first four suffix positions without branches (reads clamped)
+                const int x0 = sh.scan.tile[x];
+                const int x1 = sh.scan.tile[x >= 1 ? x - 1 : 0];
+                const int x2 = sh.scan.tile[x >= 2 ? x - 2 : 0];
+                const int x3 = sh.scan.tile[x >= 3 ? x - 3 : 0];
+                int m = (lim > 0 && x0 == p0) ? 1 : 0;
+                m = (m == 1 && lim > 1 && x1 == p1) ? 2 : m;
+                m = (m == 2 && lim > 2 && x2 == p2) ? 3 : m;
+                m = (m == 3 && lim > 3 && x3 == p3) ? 4 : m;
+                if (m == 4) {
+                    while (m < lim && sh.scan.tile[x - m] == sh.scan.pat[m])
+                        ++m;
+                }
 #pragma unroll
                 for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
                     if (j < p.n_ngram && m >= p.lens[j])
@@ -193,24 +223,20 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh) {
             }
         }
     }
-    const int wave = tid >> 6, lane = tid & 63;
+    const int lane = tid & 63;
 #pragma unroll
     for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j) {
         if (j < p.n_ngram) {
-            const int32_t v = wave_max_i32(best[j]);
-            if (lane == 0)
-                sh.scan.red[wave][j] = v;
+            const uint32_t v = wave_max_u32((uint32_t)best[j]);
+            if (lane == 0 && v > 0)
+                atomicMax(&sh.scan.red[j], (int32_t)v);
         }
     }
     __syncthreads();
-    if (tid == 0) {
-        for (int j = 0; j < p.n_ngram; ++j) {
-            int32_t v = 0;
-            for (int q = 0; q < kWaves; ++q)
-                v = sh.scan.red[q][j] > v ? sh.scan.red[q][j] : v;
-            if (v > 0)
-                atomicMax(&p.ws.mslot[b * SWITCHSD_MAX_NGRAM + j], v);
-        }
+    if (tid < p.n_ngram) {
+        const int32_t v = sh.scan.red[tid];
+        if (v > 0)
+            atomicMax(&p.ws.mslot[b * kLineU32 + tid], v);
     }
 }
 
@@ -245,19 +271,19 @@ __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
     double s = 0.0, c = 0.0;
     const bool vec = (p.d & 7) == 0 && (((uintptr_t)h | (uintptr_t)p.w) & 15) == 0;
     if (vec) {
-        const uint4 *hv = reinterpret_cast<const uint4 *>(h);
+        const u32x4 *hv = reinterpret_cast<const u32x4 *>(h);
         const float4 *wv = reinterpret_cast<const float4 *>(p.w);
         for (int g = tid; g < (p.d >> 3); g += kThreads) {
-            const uint4 x = hv[g];
+            const u32x4 x = hv[g];
             const float4 w0 = wv[2 * g], w1 = wv[2 * g + 1];
-            dd_add_term(s, c, bf16_lo(x.x) * (double)w0.x);
-            dd_add_term(s, c, bf16_hi(x.x) * (double)w0.y);
-            dd_add_term(s, c, bf16_lo(x.y) * (double)w0.z);
-            dd_add_term(s, c, bf16_hi(x.y) * (double)w0.w);
-            dd_add_term(s, c, bf16_lo(x.z) * (double)w1.x);
-            dd_add_term(s, c, bf16_hi(x.z) * (double)w1.y);
-            dd_add_term(s, c, bf16_lo(x.w) * (double)w1.z);
-            dd_add_term(s, c, bf16_hi(x.w) * (double)w1.w);
+            dd_add_term(s, c, bf16_lo(x[0]) * (double)w0.x);
+            dd_add_term(s, c, bf16_hi(x[0]) * (double)w0.y);
+            dd_add_term(s, c, bf16_lo(x[1]) * (double)w0.z);
+            dd_add_term(s, c, bf16_hi(x[1]) * (double)w0.w);
+            dd_add_term(s, c, bf16_lo(x[2]) * (double)w1.x);
+            dd_add_term(s, c, bf16_hi(x[2]) * (double)w1.y);
+            dd_add_term(s, c, bf16_lo(x[3]) * (double)w1.z);
+            dd_add_term(s, c, bf16_hi(x[3]) * (double)w1.w);
         }
     } else {
         for (int i = tid; i < p.d; i += kThreads)
@@ -309,103 +335,157 @@ __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
     return (uint32_t)(nnb > p.k + 1 ? nnb : p.k + 1);
 }
 
-__device__ void argmax_role(const StepParams &p, int b, int r, int c, Shared &sh) {
+// One chunk of a segment: vectors [qc0, qc0 + kChunkVecs) of the segment's
+// aligned interior (nq vectors; row-relative element index of vector q is
+// ebase + 8q), plus this lane's head or tail element when `x_on`.  Updates
+// the wave's running maximum runM and the lowest row-relative index runI
+// holding it (kNoIdx: no candidate yet).  Chunks arrive in increasing index
+// order, so an equal maximum in a later chunk never replaces runI.
+__device__ __forceinline__ void argmax_chunk(u32x4 (&v)[kUnroll], int qc0, int nq, uint32_t ebase,
+                                             bool x_on, float xv, uint32_t xi, float &runM,
+                                             uint32_t &runI) {
+    const int tid = threadIdx.x;
+    if (qc0 + kChunkVecs > nq) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (qc0 + u * kThreads + tid >= nq)
+                v[u] = u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
+    }
+    float m = x_on ? xv : -__builtin_inff();
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        m = max3n(m, lo_f(v[u][0]), hi_f(v[u][0]));
+        m = max3n(m, lo_f(v[u][1]), hi_f(v[u][1]));
+        m = max3n(m, lo_f(v[u][2]), hi_f(v[u][2]));
+        m = max3n(m, lo_f(v[u][3]), hi_f(v[u][3]));
+    }
+    if (__any(m != m)) {  // a NaN somewhere: recompute those lanes ignoring NaN
+        if (m != m) {
+            m = x_on ? fmax_nonan(-__builtin_inff(), xv) : -__builtin_inff();
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                for (int w4 = 0; w4 < 4; ++w4) {
+                    m = fmax_nonan(m, lo_f(v[u][w4]));
+                    m = fmax_nonan(m, hi_f(v[u][w4]));
+                }
+        }
+    }
+    if (runI == kNoIdx || __any(m > runM)) {
+        const float W = wave_max_f32(m);
+        if (runI == kNoIdx || W > runM) {
+            uint32_t idx = kNoIdx;
+            if (m == W) {
+                if (x_on && xv == W)
+                    idx = xi;
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const int q = qc0 + u * kThreads + tid;
+                    const uint32_t e = ebase + (uint32_t)q * 8u;
+#pragma unroll
+                    for (int w4 = 0; w4 < 4; ++w4) {
+                        if (q < nq && lo_f(v[u][w4]) == W && e + w4 * 2u < idx)
+                            idx = e + w4 * 2u;
+                        if (q < nq && hi_f(v[u][w4]) == W && e + w4 * 2u + 1u < idx)
+                            idx = e + w4 * 2u + 1u;
+                    }
+                }
+            }
+            idx = wave_min_u32(idx);
+            if (idx != kNoIdx) {  // W is a real element (not only -inf padding)
+                runM = W;
+                runI = idx;
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void load_chunk(u32x4 (&v)[kUnroll], const u32x4 *vp, int qc0, int nq) {
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const int q = qc0 + u * kThreads + (int)threadIdx.x;
+        v[u] = __builtin_nontemporal_load(vp + (q < nq ? q : nq - 1));
+    }
+}
+
+// Segment s of row r of sequence b.
+__device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh) {
     const int tid = threadIdx.x;
     const int64_t rowoff = ((int64_t)b * p.R + r) * p.V;
-    const int64_t c0 = (int64_t)c * kChunkElems;
-    const int64_t c1 = c0 + kChunkElems < p.V ? c0 + kChunkElems : (int64_t)p.V;
+    const int64_t e0 = (int64_t)s * p.seg_elems;
+    const int64_t e1 = e0 + p.seg_elems < p.V ? e0 + p.seg_elems : (int64_t)p.V;
     // element g of the tensor sits at byte 2g from the base: the 16-byte
-    // aligned interior [a0, a1) is read with 16-byte loads, the head and the
-    // tail (at most 7 elements each) one element per lane.
-    const int64_t g0 = rowoff + c0, g1 = rowoff + c1;
+    // aligned interior [a0, a1) is read with 16-byte loads, the head [g0, a0)
+    // and the tail [a1, g1) (at most 7 elements each) one element per lane.
+    const int64_t g0 = rowoff + e0, g1 = rowoff + e1;
     const int64_t mis = (int64_t)((((uintptr_t)p.logits) >> 1) + (uint64_t)g0) & 7;
     int64_t a0 = g0 + ((8 - mis) & 7);
     if (a0 > g1)
         a0 = g1;
     const int64_t a1 = a0 + ((g1 - a0) & ~(int64_t)7);
     const int nq = (int)((a1 - a0) >> 3);
-    const uint4 *vp = reinterpret_cast<const uint4 *>(p.logits + a0);
-    const uint4 neg_inf = make_uint4(0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u);
+    const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + a0);
+    const uint32_t ebase = (uint32_t)(a0 - rowoff);
 
-    uint4 v[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        const int q = u * kThreads + tid;
-        v[u] = q < nq ? vp[q] : neg_inf;
-    }
     const int nhead = (int)(a0 - g0), ntail = (int)(g1 - a1);
-    int64_t eg = -1;
+    int64_t xg = -1;
     if (tid < nhead)
-        eg = g0 + tid;
+        xg = g0 + tid;
     else if (tid < nhead + ntail)
-        eg = a1 + (tid - nhead);
-    const float ev = eg >= 0 ? lo_f((uint32_t)p.logits[eg]) : -__builtin_inff();
+        xg = a1 + (tid - nhead);
+    const float xv = xg >= 0 ? lo_f((uint32_t)p.logits[xg]) : -__builtin_inff();
+    const uint32_t xi = (uint32_t)(xg - rowoff);
+    const bool is_head = tid < nhead;
+    const bool has_x = xg >= 0;
 
-    // phase 1: lane maximum (NaN propagates; handled below)
-    float m = ev;
+    float runM = -__builtin_inff();
+    uint32_t runI = kNoIdx;
+    const int nch = (nq + kChunkVecs - 1) / kChunkVecs;
+    if (nch == 0) {
+        u32x4 v[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        m = max3n(m, lo_f(v[u].x), hi_f(v[u].x));
-        m = max3n(m, lo_f(v[u].y), hi_f(v[u].y));
-        m = max3n(m, lo_f(v[u].z), hi_f(v[u].z));
-        m = max3n(m, lo_f(v[u].w), hi_f(v[u].w));
-    }
-    if (m != m) {  // a NaN in this lane: recompute ignoring NaN (never on finite data)
-        m = fmax_nonan(-__builtin_inff(), ev);
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const uint32_t ws[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                m = fmax_nonan(m, lo_f(ws[q]));
-                m = fmax_nonan(m, hi_f(ws[q]));
-            }
+        for (int u = 0; u < kUnroll; ++u)
+            v[u] = u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
+        argmax_chunk(v, 0, 0, ebase, has_x, xv, xi, runM, runI);
+    } else {
+        // double buffer: chunk c + 1 is in flight while chunk c is reduced; the
+        // head element joins the first chunk, the tail element the last one
+        u32x4 A[kUnroll], Bv[kUnroll];
+        load_chunk(A, vp, 0, nq);
+        for (int c = 0; c < nch; c += 2) {
+            load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
+            argmax_chunk(A, c * kChunkVecs, nq, ebase,
+                         has_x && ((is_head && c == 0) || (!is_head && c == nch - 1)), xv, xi,
+                         runM, runI);
+            if (c + 1 >= nch)
+                break;
+            load_chunk(A, vp, (c + 2) * kChunkVecs, nq);
+            argmax_chunk(Bv, (c + 1) * kChunkVecs, nq, ebase, has_x && !is_head && c + 1 == nch - 1,
+                         xv, xi, runM, runI);
         }
     }
     const int wave = tid >> 6, lane = tid & 63;
-    const float wm = wave_max_f32(m);
-    if (lane == 0)
-        sh.am.wmax[wave] = wm;
-    __syncthreads();
-    float M = sh.am.wmax[0];
-#pragma unroll
-    for (int q = 1; q < kWaves; ++q)
-        M = __builtin_elementwise_maximum(M, sh.am.wmax[q]);
-
-    // phase 2 (only waves holding the maximum): lowest index equal to M
-    uint32_t idx = 0xFFFFFFFFu;
-    if (__any(m == M)) {
-        if (m == M) {
-            if (eg >= 0 && ev == M)
-                idx = (uint32_t)(eg - rowoff);
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int q = u * kThreads + tid;
-                const uint32_t ws[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-                for (int w4 = 0; w4 < 4; ++w4) {
-                    const uint32_t base = (uint32_t)(a0 - rowoff) + (uint32_t)q * 8u + w4 * 2u;
-                    if (q < nq && lo_f(ws[w4]) == M && base < idx)
-                        idx = base;
-                    if (q < nq && hi_f(ws[w4]) == M && base + 1u < idx)
-                        idx = base + 1u;
-                }
-            }
-        }
-        idx = wave_min_u32(idx);
+    if (lane == 0) {
+        sh.am.wmax[wave] = runM;
+        sh.am.widx[wave] = runI;
     }
-    if (lane == 0)
-        sh.am.widx[wave] = idx;
     __syncthreads();
     if (tid == 0) {
-        uint32_t best = sh.am.widx[0];
+        float M = -__builtin_inff();
+        uint32_t best = kNoIdx;
 #pragma unroll
-        for (int q = 1; q < kWaves; ++q)
-            best = sh.am.widx[q] < best ? sh.am.widx[q] : best;
-        if (best != 0xFFFFFFFFu) {
+        for (int q = 0; q < kWaves; ++q) {
+            const uint32_t iq = sh.am.widx[q];
+            const float mq = sh.am.wmax[q];
+            if (iq != kNoIdx && (best == kNoIdx || mq > M || (mq == M && iq < best))) {
+                M = mq;
+                best = iq;
+            }
+        }
+        if (best != kNoIdx) {
             const unsigned long long key =
                 ((unsigned long long)order_key(M) << 32) | (0xFFFFFFFFu - best);
-            atomicMax(&p.ws.keys[(int64_t)b * p.R + r], key);
+            atomicMax(&p.ws.keys[(int64_t)b * p.ws.key_stride + r], key);
         }
     }
 }
@@ -432,22 +512,38 @@ __device__ void select_write(const StepParams &p, int b, int mn, int cl, float z
                 par = p.npar ? p.npar[base + i] : i - 1;
             }
         }
-        p.dtok[base + i] = tok;
-        p.dpar[base + i] = par;
+        st_i32(&p.dtok[base + i], tok);  // read by the accept epilogue of the same launch
+        st_i32(&p.dpar[base + i], par);
     }
     if (lane == 0) {
         p.use_copy[b] = use;
-        p.dn[b] = dnb;
+        st_i32(&p.dn[b], dnb);
     }
 }
 
 __device__ void front_epilogue(const StepParams &p, int b) {
     const int lane = threadIdx.x;
+    const int64_t row = (int64_t)b * p.Lmax;
+    const int64_t base = (int64_t)b * p.R;
+    const bool select = p.epi_front == EPI_SELECT;
+    // every load that does not depend on the match result, issued together
     int32_t s = 0;
-    if (lane < p.n_ngram) {
-        s = ld_i32(&p.ws.mslot[b * SWITCHSD_MAX_NGRAM + lane]);
-        st_i32(&p.ws.mslot[b * SWITCHSD_MAX_NGRAM + lane], 0);
+    if (lane < p.n_ngram)
+        s = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+    float zb = 0.0f;
+    int nnb = 1, ntok_l = -1, npar_l = -1;
+    const bool small = p.R <= 64 && p.k < 64;
+    if (select) {
+        zb = ld_f32(&p.z[b]);
+        nnb = clampi(p.nn[b], 1, p.R);
+        if (small && lane < p.R) {
+            ntok_l = p.ntok[base + lane];
+            npar_l = p.npar ? p.npar[base + lane] : lane - 1;
+        }
     }
+    if (lane < p.n_ngram)
+        st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
     const unsigned long long hit = __ballot(s > 0);
     int mn = 0, me = -1;
     if (hit) {
@@ -458,23 +554,43 @@ __device__ void front_epilogue(const StepParams &p, int b) {
                 mn = p.lens[q];
         me = __shfl(s, j) - 1;
     }
-    const int L = clampi(p.lengths[b], 0, p.Lmax);
     const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
-    const int64_t row = (int64_t)b * p.Lmax;
     if (lane == 0) {
         p.match_n[b] = mn;
         p.match_end[b] = me;
         p.copy_len[b] = cl;
     }
-    for (int i = lane; i < p.k; i += 64)
-        p.copy_tokens[(int64_t)b * p.k + i] = i < cl ? p.tokens[row + me + 1 + i] : -1;
-    if (p.epi_front == EPI_SELECT) {
-        const float zb = ld_f32(&p.z[b]);
-        // copied token i (1-based) is x[me + i]
-        select_write(p, b, mn, cl, zb, p.tokens, row + me);
+    if (small) {
+        // lane j holds copied token j (the only dependent load)
+        const int ct = lane < cl ? p.tokens[row + me + 1 + lane] : -1;
+        if (lane < p.k)
+            p.copy_tokens[(int64_t)b * p.k + lane] = ct;
+        if (select) {
+            const int use = (mn >= p.kappa) && (zb >= p.theta);
+            const int dnb = use ? cl + 1 : nnb;
+            const int ctp = __shfl(ct, lane >= 1 ? lane - 1 : 0);
+            int tok = -1, par = -1;
+            if (lane >= 1 && lane < dnb) {
+                tok = use ? ctp : ntok_l;
+                par = use ? lane - 1 : npar_l;
+            }
+            if (lane < p.R) {
+                st_i32(&p.dtok[base + lane], tok);  // read by the accept epilogue of this launch
+                st_i32(&p.dpar[base + lane], par);
+            }
+            if (lane == 0) {
+                p.use_copy[b] = use;
+                st_i32(&p.dn[b], dnb);
+            }
+        }
+    } else {
+        for (int i = lane; i < p.k; i += 64)
+            p.copy_tokens[(int64_t)b * p.k + i] = i < cl ? p.tokens[row + me + 1 + i] : -1;
+        if (select)  // copied token i (1-based) is x[me + i]
+            select_write(p, b, mn, cl, zb, p.tokens, row + me);
     }
     if (lane == 0)
-        st_u32(&p.ws.tk_front[b], 0u);
+        st_u32(&p.ws.tk_front[b * kLineU32], 0u);
 }
 
 __device__ __forceinline__ int32_t decode_key(unsigned long long key) {
@@ -484,18 +600,25 @@ __device__ __forceinline__ int32_t decode_key(unsigned long long key) {
 __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
     const int lane = threadIdx.x;
     const int64_t base = (int64_t)b * p.R;
-    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    unsigned long long *keys = p.ws.keys + (int64_t)b * p.ws.key_stride;
     if (p.R <= 64) {
         const int i = lane;
-        int a = -1, tok = -1, par = -1;
+        // the draft and the row maxima, all requested at once
+        const int dn_raw = ld_i32(&p.dn[b]);
+        unsigned long long key = 0ull;
+        int tok = -1, par = -1;
         if (i < p.R) {
-            const unsigned long long key = ld_u64(&p.ws.keys[base + i]);
-            if (key)
-                st_u64(&p.ws.keys[base + i], 0ull);
-            if (i < dnb)
-                a = decode_key(key);
+            key = ld_u64(&keys[i]);
             tok = ld_i32(&p.dtok[base + i]);
             par = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
+        }
+        const int dnb = clampi(dn_raw, 1, p.R);
+        int a = -1;
+        if (i < p.R) {
+            if (key)
+                st_u64(&keys[i], 0ull);
+            if (i < dnb)
+                a = decode_key(key);
             if (p.amax)
                 p.amax[base + i] = a;
         }
@@ -503,27 +626,41 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         const int anc0 = valid ? par : 0;
         const int apar = __shfl(a, anc0);
         int ok = i == 0 ? 1 : (valid && tok == apar ? 1 : 0);
-        int dep = i == 0 ? 0 : 1;
-        int anc = anc0;
+        int best, depth, dep;
+        unsigned long long onpath;
+        // a chain (every node's parent is the node before it): the accepted
+        // nodes are the prefix before the first rejection
+        const bool chain = __ballot(i >= 1 && i < dnb && par != i - 1) == 0ull;
+        if (chain) {
+            const unsigned long long rej = __ballot(i >= 1 && i < dnb && !ok);
+            depth = rej ? __ffsll((long long)rej) - 2 : dnb - 1;
+            best = depth;
+            dep = i;
+            onpath = depth > 0 ? (((~0ull) >> (64 - depth)) << 1) : 0ull;
+        } else {
+            dep = i == 0 ? 0 : 1;
+            int anc = anc0;
 #pragma unroll
-        for (int round = 0; round < 6; ++round) {  // 2^6 >= 64 levels
-            const int ok2 = __shfl(ok, anc), dep2 = __shfl(dep, anc), anc2 = __shfl(anc, anc);
-            ok &= ok2;
-            dep += dep2;
-            anc = anc2;
+            for (int round = 0; round < 6; ++round) {  // 2^6 >= 64 levels
+                const int ok2 = __shfl(ok, anc), dep2 = __shfl(dep, anc),
+                          anc2 = __shfl(anc, anc);
+                ok &= ok2;
+                dep += dep2;
+                anc = anc2;
+            }
+            const uint32_t key2 =
+                (ok && i < dnb) ? (((uint32_t)dep << 16) | (0xFFFFu - (uint32_t)i)) : 0u;
+            const uint32_t kbest = wave_max_u32(key2);
+            best = (int)(0xFFFFu - (kbest & 0xFFFFu));
+            depth = (int)(kbest >> 16);
+            onpath = 0ull;
+            int cur = best;
+            for (int s2 = 0; s2 < depth; ++s2) {
+                onpath |= 1ull << cur;
+                cur = __shfl(anc0, cur);
+            }
         }
-        const uint32_t key2 = (ok && i < dnb) ? (((uint32_t)dep << 16) | (0xFFFFu - (uint32_t)i)) : 0u;
-        const uint32_t kbest = wave_max_u32(key2);
-        const int best = (int)(0xFFFFu - (kbest & 0xFFFFu));
-        const int depth = (int)(kbest >> 16);
         const int bon = __shfl(a, best);
-        // nodes on the root -> best path
-        unsigned long long onpath = 0ull;
-        int cur = best;
-        for (int s2 = 0; s2 < depth; ++s2) {
-            onpath |= 1ull << cur;
-            cur = __shfl(anc0, cur);
-        }
         if (i < p.R) {
             if ((onpath >> i) & 1ull)
                 p.out_tokens[base + dep - 1] = tok;
@@ -538,10 +675,11 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
             p.bonus[b] = bon;
         }
     } else {
+        const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
         for (int i = lane; i < p.R; i += 64) {
-            const unsigned long long key = ld_u64(&p.ws.keys[base + i]);
+            const unsigned long long key = ld_u64(&keys[i]);
             if (key)
-                st_u64(&p.ws.keys[base + i], 0ull);
+                st_u64(&keys[i], 0ull);
             const int a = i < dnb ? decode_key(key) : -1;
             sh.epi.a[i] = a;
             sh.epi.tok[i] = ld_i32(&p.dtok[base + i]);
@@ -585,7 +723,7 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         }
     }
     if (lane == 0)
-        st_u32(&p.ws.tk_all[b], 0u);
+        st_u32(&p.ws.tk_all[b * kLineU32], 0u);
 }
 
 // ------------------------------------------------------------- kernels
@@ -605,22 +743,22 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
         front = true;
     } else {
         const int idx = blk - p.n_front_wg;
-        const int rowi = idx / p.chunks;
-        const int c = idx - rowi * p.chunks;
+        const int rowi = idx / p.segs;
+        const int s = idx - rowi * p.segs;
         b = rowi / p.R;
         const int r = rowi - b * p.R;
         if ((uint32_t)r < rows_needed(p, b))
-            argmax_role(p, b, r, c, sh);
+            argmax_role(p, b, r, s, sh);
         front = false;
     }
     if (threadIdx.x >= 64)
         return;  // waves 1.. are done; wave 0 arrives and may run an epilogue
     if (front && p.epi_front != EPI_NONE) {
-        if (arrive(&p.ws.tk_front[b], p.exp_front))
+        if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front))
             front_epilogue(p, b);
     }
     if (p.epi_accept) {
-        if (arrive(&p.ws.tk_all[b], p.exp_all))
+        if (arrive(&p.ws.tk_all[b * kLineU32], p.exp_all))
             final_epilogue(p, b, sh);
     }
 }
