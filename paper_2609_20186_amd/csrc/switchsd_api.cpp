@@ -247,11 +247,17 @@ int switchsd_select_draft(const int32_t *match_n, const int32_t *copy_len,
     return launch_select_kernel(p, stream);
 }
 
-int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
-                           const int32_t *dtok, const int32_t *dpar, const int32_t *dn,
-                           int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
-                           int32_t *out_tokens, int32_t *amax, void *workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Verify launch shared by the entry point and the split step.  `speculate`:
+// most rows of the drafts are expected to be read (chains), so a row's first
+// chunk is requested before its need is known.
+int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const int32_t *dtok,
+                  const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
+                  int32_t *accept_node, int32_t *bonus, int32_t *out_tokens, int32_t *amax,
+                  void *workspace, size_t workspace_bytes, bool speculate, hipStream_t stream) {
     if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || V < 1)
         return SWITCHSD_ESHAPE;
     if (B == 0)
@@ -283,9 +289,25 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
     p.amax = amax;
     p.ws = carve(workspace, B, R);
     p.rows_mode = ROWS_DRAFT;
+    p.speculate = speculate ? 1 : 0;
     p.epi_accept = 1;
     p.exp_all = (uint32_t)(R * p.segs);
     return launch_step_kernel(p, grid, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
+                           const int32_t *dtok, const int32_t *dpar, const int32_t *dn,
+                           int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                           int32_t *out_tokens, int32_t *amax, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+    // chains and short drafts usually use every row
+    const bool speculate = dpar == nullptr || R <= 16;
+    return verify_launch(logits, B, R, V, dtok, dpar, dn, accept_len, accept_node, bonus,
+                         out_tokens, amax, workspace, workspace_bytes, speculate, stream);
 }
 
 int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace_bytes,
@@ -345,10 +367,10 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.ws = carve(workspace, B, R);
     if ((rc = set_scan(p, B, a->Lmax)))
         return rc;
-    p.probe_on = 1;
-    p.n_front_wg = p.n_scan_wg + B;
+    p.scan_probe = 1;
+    p.n_front_wg = p.n_scan_wg;
     p.epi_front = EPI_SELECT;
-    p.exp_front = (uint32_t)p.scan_tiles + 1u;
+    p.exp_front = (uint32_t)p.scan_tiles;
 
     int mode = a->mode;
     if (mode == SWITCHSD_MODE_AUTO)
@@ -367,9 +389,10 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     // SPLIT: front (scan + probe + select), then verify over the chosen rows
     if ((rc = launch_step_kernel(p, p.n_front_wg, stream)))
         return rc;
-    return switchsd_verify_accept(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
-                                  a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
-                                  workspace_bytes, stream);
+    // a copy draft uses at most k + 1 of the R rows
+    return verify_launch(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
+                         a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
+                         workspace_bytes, 2 * (a->cfg.k + 1) >= R, stream);
 }
 
 }  // extern "C"

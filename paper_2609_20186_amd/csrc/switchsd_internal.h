@@ -64,12 +64,14 @@ struct StepParams {
     Workspace ws;
     // grid layout: [scan tiles][probe][argmax row segments]
     int32_t scan_tiles;  // per sequence (0: no scan role)
-    int32_t probe_on;    // 1: one probe work-group per sequence
+    int32_t probe_on;    // 1: one stand-alone probe work-group per sequence
+    int32_t scan_probe;  // 1: scan tile 0 of each sequence also computes the probe
     int32_t segs;        // argmax work-groups per row (0: no argmax role)
     int32_t seg_elems;   // logits elements per row segment (multiple of 8)
     int32_t n_scan_wg;   // B * scan_tiles
     int32_t n_front_wg;  // n_scan_wg + B * probe_on
     int32_t rows_mode;
+    int32_t speculate;   // 1: issue a row's first chunk before reading whether it is needed
     int32_t epi_front;
     int32_t epi_accept;
     uint32_t exp_front;  // arrivals per sequence at tk_front

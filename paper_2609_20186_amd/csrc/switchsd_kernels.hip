@@ -43,14 +43,15 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kThreads / 64;
-constexpr int kScanHaloMax = SWITCHSD_MAX_NGRAM_LEN;
-constexpr int kScanPerLane = (kScanTile + kScanHaloMax + kThreads - 1) / kThreads;
 constexpr uint32_t kNoIdx = 0xFFFFFFFFu;
 
 struct ScanShared {
-    int32_t tile[kScanTile + kScanHaloMax];
+    int32_t tile[kScanTile + 64];
     int32_t pat[SWITCHSD_MAX_NGRAM_LEN];
     int32_t red[SWITCHSD_MAX_NGRAM];
+    double ps[kWaves];  // probe partial sums of the waves (scan tile 0)
+    double pc[kWaves];
+    int32_t L;
 };
 struct ArgmaxShared {
     float wmax[kWaves];
@@ -151,95 +152,6 @@ __device__ __forceinline__ int clampi(int v, int lo, int hi) {
     return v < lo ? lo : (v > hi ? hi : v);
 }
 
-// ------------------------------------------------------------- scan role
-
-// Tile t of sequence b: end positions e in [t*4096, (t+1)*4096).
-__device__ void scan_role(const StepParams &p, int b, int t, Shared &sh) {
-    const int tid = threadIdx.x;
-    const int H = p.nmax - 1;
-    const int64_t row = (int64_t)b * p.Lmax;
-    const int t0 = t * kScanTile;
-    const int lo = t0 - H > 0 ? t0 - H : 0;
-    const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
-
-    // The tile, the length and the suffix of a full-length context do not
-    // depend on each other: issue all of them at once (indices clamped into
-    // range, so that no load sits behind a branch).
-    int32_t reg[kScanPerLane];
-#pragma unroll
-    for (int i = 0; i < kScanPerLane; ++i) {
-        const int x = lo + i * kThreads + tid;
-        reg[i] = p.tokens[row + (x < hi ? x : hi - 1)];
-    }
-    const int tp = tid < p.nmax ? tid : 0;
-    const int32_t pat_full = p.tokens[row + (p.Lmax - 1 - tp >= 0 ? p.Lmax - 1 - tp : 0)];
-    const int L = clampi(p.lengths[b], 0, p.Lmax);
-#pragma unroll
-    for (int i = 0; i < kScanPerLane; ++i) {
-        const int j = i * kThreads + tid;
-        if (lo + j < hi)
-            sh.scan.tile[j] = reg[i];
-    }
-    if (tid < SWITCHSD_MAX_NGRAM)
-        sh.scan.red[tid] = 0;
-    if (tid < p.nmax && tid < L)
-        sh.scan.pat[tid] = L == p.Lmax ? pat_full : p.tokens[row + L - 1 - tid];
-    __syncthreads();
-
-    int32_t best[SWITCHSD_MAX_NGRAM];
-#pragma unroll
-    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
-        best[j] = 0;
-    // occurrences end at e <= L-2
-    const int eend = t0 + kScanTile < L - 1 ? t0 + kScanTile : L - 1;
-    if (t0 < eend) {
-        const int p0 = sh.scan.pat[0];
-        const int p1 = p.nmax > 1 ? sh.scan.pat[1] : 0;
-        const int p2 = p.nmax > 2 ? sh.scan.pat[2] : 0;
-        const int p3 = p.nmax > 3 ? sh.scan.pat[3] : 0;
-#pragma unroll 4
-        for (int i = 0; i < kScanTile / kThreads; ++i) {
-            const int e = t0 + i * kThreads + tid;
-            if (e < eend) {
-                const int lim = p.nmax < e + 1 ? p.nmax : e + 1;
-                const int x = e - lo;  // tile index of position e; e - t >= lo for t < lim
-                // first four suffix positions without branches (reads clamped)
-                const int x0 = sh.scan.tile[x];
-                const int x1 = sh.scan.tile[x >= 1 ? x - 1 : 0];
-                const int x2 = sh.scan.tile[x >= 2 ? x - 2 : 0];
-                const int x3 = sh.scan.tile[x >= 3 ? x - 3 : 0];
-                int m = (lim > 0 && x0 == p0) ? 1 : 0;
-                m = (m == 1 && lim > 1 && x1 == p1) ? 2 : m;
-                m = (m == 2 && lim > 2 && x2 == p2) ? 3 : m;
-                m = (m == 3 && lim > 3 && x3 == p3) ? 4 : m;
-                if (m == 4) {
-                    while (m < lim && sh.scan.tile[x - m] == sh.scan.pat[m])
-                        ++m;
-                }
-#pragma unroll
-                for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
-                    if (j < p.n_ngram && m >= p.lens[j])
-                        best[j] = e + 1;
-            }
-        }
-    }
-    const int lane = tid & 63;
-#pragma unroll
-    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j) {
-        if (j < p.n_ngram) {
-            const uint32_t v = wave_max_u32((uint32_t)best[j]);
-            if (lane == 0 && v > 0)
-                atomicMax(&sh.scan.red[j], (int32_t)v);
-        }
-    }
-    __syncthreads();
-    if (tid < p.n_ngram) {
-        const int32_t v = sh.scan.red[tid];
-        if (v > 0)
-            atomicMax(&p.ws.mslot[b * kLineU32 + tid], v);
-    }
-}
-
 // ------------------------------------------------------------- probe role
 
 __device__ __forceinline__ void two_sum(double a, double b, double &s, double &e) {
@@ -265,25 +177,43 @@ __device__ __forceinline__ double bf16_hi(uint32_t x) {
     return (double)__uint_as_float(x & 0xFFFF0000u);
 }
 
-__device__ void probe_role(const StepParams &p, int b, Shared &sh) {
+// This lane's share of w . h for sequence b, as a double-double (s, c),
+// reduced over the wave.  Two groups of 8 elements per lane (4096 elements per
+// work-group) are requested before either is used.
+__device__ __forceinline__ void probe_partial(const StepParams &p, int b, double &s, double &c) {
     const int tid = threadIdx.x;
     const uint16_t *h = p.hidden + (int64_t)b * p.d;
-    double s = 0.0, c = 0.0;
+    s = 0.0;
+    c = 0.0;
     const bool vec = (p.d & 7) == 0 && (((uintptr_t)h | (uintptr_t)p.w) & 15) == 0;
     if (vec) {
         const u32x4 *hv = reinterpret_cast<const u32x4 *>(h);
         const float4 *wv = reinterpret_cast<const float4 *>(p.w);
-        for (int g = tid; g < (p.d >> 3); g += kThreads) {
-            const u32x4 x = hv[g];
-            const float4 w0 = wv[2 * g], w1 = wv[2 * g + 1];
-            dd_add_term(s, c, bf16_lo(x[0]) * (double)w0.x);
-            dd_add_term(s, c, bf16_hi(x[0]) * (double)w0.y);
-            dd_add_term(s, c, bf16_lo(x[1]) * (double)w0.z);
-            dd_add_term(s, c, bf16_hi(x[1]) * (double)w0.w);
-            dd_add_term(s, c, bf16_lo(x[2]) * (double)w1.x);
-            dd_add_term(s, c, bf16_hi(x[2]) * (double)w1.y);
-            dd_add_term(s, c, bf16_lo(x[3]) * (double)w1.z);
-            dd_add_term(s, c, bf16_hi(x[3]) * (double)w1.w);
+        const int ng = p.d >> 3;
+        for (int g0 = 0; g0 < ng; g0 += 2 * kThreads) {
+            u32x4 x[2];
+            float4 w0[2], w1[2];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                int g = g0 + q * kThreads + tid;
+                g = g < ng ? g : ng - 1;
+                x[q] = hv[g];
+                w0[q] = wv[2 * g];
+                w1[q] = wv[2 * g + 1];
+            }
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                if (g0 + q * kThreads + tid < ng) {
+                    dd_add_term(s, c, bf16_lo(x[q][0]) * (double)w0[q].x);
+                    dd_add_term(s, c, bf16_hi(x[q][0]) * (double)w0[q].y);
+                    dd_add_term(s, c, bf16_lo(x[q][1]) * (double)w0[q].z);
+                    dd_add_term(s, c, bf16_hi(x[q][1]) * (double)w0[q].w);
+                    dd_add_term(s, c, bf16_lo(x[q][2]) * (double)w1[q].x);
+                    dd_add_term(s, c, bf16_hi(x[q][2]) * (double)w1[q].y);
+                    dd_add_term(s, c, bf16_lo(x[q][3]) * (double)w1[q].z);
+                    dd_add_term(s, c, bf16_hi(x[q][3]) * (double)w1[q].w);
+                }
+            }
         }
     } else {
         for (int i = tid; i < p.d; i += kThreads)
@@ -294,19 +224,149 @@ __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
         const double s2 = __shfl_xor(s, o), c2 = __shfl_xor(c, o);
         dd_add(s, c, s2, c2);
     }
-    const int wave = tid >> 6, lane = tid & 63;
-    if (lane == 0) {
-        sh.probe.s[wave] = s;
-        sh.probe.c[wave] = c;
+}
+
+// Combines the waves' partial sums (fixed order) and the bias into z.
+__device__ __forceinline__ float probe_combine(const double *ps, const double *pc, float bias) {
+    double S = ps[0], C = pc[0];
+    for (int q = 1; q < kWaves; ++q)
+        dd_add(S, C, ps[q], pc[q]);
+    dd_add(S, C, (double)bias, 0.0);
+    return (float)(S + C);
+}
+
+// The neural draft as handed over, read by wave 0 of a scan work-group before
+// it is needed, so that the switch costs no extra round trip.
+struct Prefetch {
+    int nnb;   // node count clamped to [1, R]
+    int ntok;  // ntok[b, lane] (lane < R <= 64)
+    int npar;  // parent of node `lane`
+};
+
+// ------------------------------------------------------------- scan role
+
+// Tile t of sequence b: end positions e in [t*4096, (t+1)*4096).  Leaves the
+// tile's most recent end + 1 per n-gram length in sh.scan.red, the tokens of
+// positions [t*4096 - 64, t*4096 + 4096) in sh.scan.tile (index = position -
+// t*4096 + 64) and, for tile 0 when the probe rides along, the waves' probe
+// partial sums in sh.scan.ps/pc.
+//
+// Wave w owns the 16 blocks of 64 consecutive positions [t0 + 1024w, +1024),
+// one position per lane, plus the block before them.  For suffix offset u the
+// ballot of (x[y] == x[L-1-u]) over a block, shifted up by u (carrying the
+// previous block's top bits in), marks the ends e with x[e-u] == x[L-1-u];
+// AND-ing offsets 0..n-1 marks the ends of occurrences of the n-gram suffix,
+// and the highest marked lane is the most recent one.  Scalar 64-bit masks
+// only: one compare per position and offset, no LDS reads.
+constexpr int kScanBlocks = kScanTile / kThreads;  // blocks of 64 positions per wave
+
+__device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetch &pre) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int64_t row = (int64_t)b * p.Lmax;
+    const int t0 = t * kScanTile;
+    const int w0 = t0 + 64 * kScanBlocks * wave;  // first position of this wave
+
+    // The tokens, the length, the suffix of a full-length context and the
+    // neural draft do not depend on each other: issue all of them at once
+    // (indices clamped into range, so that no load sits behind a branch).
+    int32_t tok[kScanBlocks + 1];  // tok[i + 1]: position w0 + 64 i + lane; tok[0]: the block before
+#pragma unroll
+    for (int i = 0; i <= kScanBlocks; ++i) {
+        int x = w0 + 64 * (i - 1) + lane;
+        x = x < 0 ? 0 : (x < p.Lmax ? x : p.Lmax - 1);
+        tok[i] = p.tokens[row + x];
+    }
+    const int tp = tid < p.nmax ? tid : 0;
+    const int32_t pat_full = p.tokens[row + (p.Lmax - 1 - tp >= 0 ? p.Lmax - 1 - tp : 0)];
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+    if (p.epi_front == EPI_SELECT && tid < 64) {
+        const int64_t base = (int64_t)b * p.R;
+        const int i = tid < p.R ? tid : 0;
+        pre.nnb = clampi(p.nn[b], 1, p.R);
+        pre.ntok = p.ntok[base + i];
+        pre.npar = p.npar ? p.npar[base + i] : tid - 1;
+    }
+    if (t == 0 && p.scan_probe) {
+        double ps, pc;
+        probe_partial(p, b, ps, pc);
+        if (lane == 0) {
+            sh.scan.ps[wave] = ps;
+            sh.scan.pc[wave] = pc;
+        }
+    }
+    // the tile in LDS (for the copy candidate): index = position - t0 + 64
+#pragma unroll
+    for (int i = 0; i <= kScanBlocks; ++i)
+        sh.scan.tile[64 * kScanBlocks * wave + 64 * i + lane] = tok[i];
+    if (tid < SWITCHSD_MAX_NGRAM)
+        sh.scan.red[tid] = 0;
+    if (tid == 0)
+        sh.scan.L = L;
+    if (tid < p.nmax)
+        sh.scan.pat[tid] = tid >= L ? 0 : (L == p.Lmax ? pat_full : p.tokens[row + L - 1 - tid]);
+    __syncthreads();
+
+    int32_t best[SWITCHSD_MAX_NGRAM];
+#pragma unroll
+    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+        best[j] = 0;
+    // ends e <= L-2 of this wave's blocks
+    const int elim = L - 1 - w0;  // e - w0 < elim
+    if (elim > 0) {
+        unsigned long long M[kScanBlocks];
+#pragma unroll
+        for (int i = 0; i < kScanBlocks; ++i) {
+            const int n = elim - 64 * i;
+            M[i] = n >= 64 ? ~0ull : (n <= 0 ? 0ull : ((1ull << n) - 1ull));
+        }
+        const bool halo = w0 > 0;  // the block before holds real positions
+        for (int u = 0; u < p.nmax; ++u) {
+            const int pu = sh.scan.pat[u];
+            unsigned long long prev = halo ? __ballot(tok[0] == pu) : 0ull;
+#pragma unroll
+            for (int i = 0; i < kScanBlocks; ++i) {
+                const unsigned long long cur = __ballot(tok[i + 1] == pu);
+                M[i] &= u == 0 ? cur : ((cur << u) | (prev >> (64 - u)));
+                prev = cur;
+            }
+            // record the length equal to u + 1, if it is one of the lengths
+            int jm = -1;
+#pragma unroll
+            for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+                if (j < p.n_ngram && p.lens[j] == u + 1)
+                    jm = j;
+            if (jm >= 0) {
+                int e1 = 0;
+#pragma unroll
+                for (int i = 0; i < kScanBlocks; ++i)
+                    if (M[i])
+                        e1 = w0 + 64 * i + 64 - __clzll((long long)M[i]);  // highest end + 1
+#pragma unroll
+                for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+                    if (j == jm)
+                        best[j] = e1;
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+        if (j < p.n_ngram && lane == 0 && best[j] > 0)
+            atomicMax(&sh.scan.red[j], best[j]);
+    __syncthreads();
+}
+
+// Stand-alone probe work-group (the probe entry point).
+__device__ void probe_role(const StepParams &p, int b, Shared &sh) {
+    double s, c;
+    probe_partial(p, b, s, c);
+    const int tid = threadIdx.x;
+    if ((tid & 63) == 0) {
+        sh.probe.s[tid >> 6] = s;
+        sh.probe.c[tid >> 6] = c;
     }
     __syncthreads();
-    if (tid == 0) {
-        double S = sh.probe.s[0], C = sh.probe.c[0];
-        for (int q = 1; q < kWaves; ++q)
-            dd_add(S, C, sh.probe.s[q], sh.probe.c[q]);
-        dd_add(S, C, (double)p.bias, 0.0);
-        st_f32(&p.z[b], (float)(S + C));
-    }
+    if (tid == 0)
+        st_f32(&p.z[b], probe_combine(sh.probe.s, sh.probe.c, p.bias));
 }
 
 // ------------------------------------------------------------- argmax role
@@ -441,6 +501,16 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
     float runM = -__builtin_inff();
     uint32_t runI = kNoIdx;
     const int nch = (nq + kChunkVecs - 1) / kChunkVecs;
+    // Whether the row is needed at all may depend on the draft (a global read);
+    // with `speculate` the first chunk is already in flight meanwhile.
+    u32x4 A[kUnroll], Bv[kUnroll];
+    const bool spec = p.speculate && nch > 0;
+    if (spec)
+        load_chunk(A, vp, 0, nq);
+    if ((uint32_t)r >= rows_needed(p, b)) {
+        __builtin_amdgcn_s_waitcnt(0);
+        return;
+    }
     if (nch == 0) {
         u32x4 v[kUnroll];
 #pragma unroll
@@ -450,8 +520,8 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
     } else {
         // double buffer: chunk c + 1 is in flight while chunk c is reduced; the
         // head element joins the first chunk, the tail element the last one
-        u32x4 A[kUnroll], Bv[kUnroll];
-        load_chunk(A, vp, 0, nq);
+        if (!spec)
+            load_chunk(A, vp, 0, nq);
         for (int c = 0; c < nch; c += 2) {
             load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
             argmax_chunk(A, c * kChunkVecs, nq, ebase,
@@ -521,58 +591,35 @@ __device__ void select_write(const StepParams &p, int b, int mn, int cl, float z
     }
 }
 
-__device__ void front_epilogue(const StepParams &p, int b) {
+// Steps 1 and 3 for sequence b in wave 0 once the match (mn, me) is known:
+// copy candidate, switch (Eq. 4 with the kappa gate), chosen draft.  When
+// `have_ct`, ct_in is this lane's copied token (read from LDS by the caller);
+// otherwise it is read from the context here.
+__device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, float zb,
+                             const Prefetch &pre, int ct_in, bool have_ct) {
     const int lane = threadIdx.x;
     const int64_t row = (int64_t)b * p.Lmax;
     const int64_t base = (int64_t)b * p.R;
     const bool select = p.epi_front == EPI_SELECT;
-    // every load that does not depend on the match result, issued together
-    int32_t s = 0;
-    if (lane < p.n_ngram)
-        s = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
-    const int L = clampi(p.lengths[b], 0, p.Lmax);
-    float zb = 0.0f;
-    int nnb = 1, ntok_l = -1, npar_l = -1;
-    const bool small = p.R <= 64 && p.k < 64;
-    if (select) {
-        zb = ld_f32(&p.z[b]);
-        nnb = clampi(p.nn[b], 1, p.R);
-        if (small && lane < p.R) {
-            ntok_l = p.ntok[base + lane];
-            npar_l = p.npar ? p.npar[base + lane] : lane - 1;
-        }
-    }
-    if (lane < p.n_ngram)
-        st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
-    const unsigned long long hit = __ballot(s > 0);
-    int mn = 0, me = -1;
-    if (hit) {
-        const int j = __ffsll((long long)hit) - 1;
-#pragma unroll
-        for (int q = 0; q < SWITCHSD_MAX_NGRAM; ++q)
-            if (q == j)
-                mn = p.lens[q];
-        me = __shfl(s, j) - 1;
-    }
     const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
     if (lane == 0) {
         p.match_n[b] = mn;
         p.match_end[b] = me;
         p.copy_len[b] = cl;
     }
-    if (small) {
-        // lane j holds copied token j (the only dependent load)
-        const int ct = lane < cl ? p.tokens[row + me + 1 + lane] : -1;
+    if (p.R <= 64 && p.k < 64) {
+        // lane j holds copied token j
+        const int ct = lane < cl ? (have_ct ? ct_in : p.tokens[row + me + 1 + lane]) : -1;
         if (lane < p.k)
             p.copy_tokens[(int64_t)b * p.k + lane] = ct;
         if (select) {
             const int use = (mn >= p.kappa) && (zb >= p.theta);
-            const int dnb = use ? cl + 1 : nnb;
+            const int dnb = use ? cl + 1 : pre.nnb;
             const int ctp = __shfl(ct, lane >= 1 ? lane - 1 : 0);
             int tok = -1, par = -1;
             if (lane >= 1 && lane < dnb) {
-                tok = use ? ctp : ntok_l;
-                par = use ? lane - 1 : npar_l;
+                tok = use ? ctp : pre.ntok;
+                par = use ? lane - 1 : pre.npar;
             }
             if (lane < p.R) {
                 st_i32(&p.dtok[base + lane], tok);  // read by the accept epilogue of this launch
@@ -589,6 +636,71 @@ __device__ void front_epilogue(const StepParams &p, int b) {
         if (select)  // copied token i (1-based) is x[me + i]
             select_write(p, b, mn, cl, zb, p.tokens, row + me);
     }
+}
+
+// First length (in the configured order) whose slot holds an occurrence:
+// (match_n, match_end), or (0, -1).  s is lane j's slot value (end + 1).
+__device__ __forceinline__ void pick_match(const StepParams &p, int32_t s, int &mn, int &me) {
+    const unsigned long long hit = __ballot(s > 0);
+    mn = 0;
+    me = -1;
+    if (hit) {
+        const int j = __ffsll((long long)hit) - 1;
+#pragma unroll
+        for (int q = 0; q < SWITCHSD_MAX_NGRAM; ++q)
+            if (q == j)
+                mn = p.lens[q];
+        me = __shfl(s, j) - 1;
+    }
+}
+
+// A context held by one scan tile: everything the switch needs is already in
+// this work-group (match in LDS, probe partial sums in LDS, the copy
+// candidate in the LDS tile, the neural draft prefetched).  No arrival.
+__device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefetch &pre) {
+    const int lane = threadIdx.x;
+    const int32_t s = lane < p.n_ngram ? sh.scan.red[lane] : 0;
+    int mn, me;
+    pick_match(p, s, mn, me);
+    const int L = sh.scan.L;
+    float zb = 0.0f;
+    if (p.scan_probe) {
+        float z0 = 0.0f;
+        if (lane == 0) {
+            z0 = probe_combine(sh.scan.ps, sh.scan.pc, p.bias);
+            p.z[b] = z0;
+        }
+        zb = __shfl(z0, 0);
+    }
+    const int pos = me + 1 + lane;  // tile index = position + 64 (tile 0)
+    const int ct = (mn > 0 && lane < p.k && pos < L) ? sh.scan.tile[pos + 64] : -1;
+    front_finish(p, b, mn, me, L, zb, pre, ct, true);
+}
+
+// Last arriving scan tile of a longer context: the other tiles' results come
+// from the workspace; the copy candidate from this tile's LDS when it lies
+// there, else from the context.
+__device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, const Prefetch &pre) {
+    const int lane = threadIdx.x;
+    int32_t s = 0;
+    if (lane < p.n_ngram) {
+        s = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
+        st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
+    }
+    const float zb = p.epi_front == EPI_SELECT ? ld_f32(&p.z[b]) : 0.0f;
+    int mn, me;
+    pick_match(p, s, mn, me);
+    const int L = sh.scan.L;
+    const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
+    // this tile's LDS holds positions [t0 - 64, t0 + 4096) (index = position - t0 + 64)
+    const int t0 = t * kScanTile;
+    const int lo = t0 - 64 > 0 ? t0 - 64 : 0;
+    const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
+    const bool in_tile = cl > 0 && me + 1 >= lo && me + cl < hi;
+    int ct = -1;
+    if (in_tile && lane < cl)
+        ct = sh.scan.tile[me + 1 + lane - t0 + 64];
+    front_finish(p, b, mn, me, L, zb, pre, ct, in_tile);
     if (lane == 0)
         st_u32(&p.ws.tk_front[b * kLineU32], 0u);
 }
@@ -731,33 +843,42 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     __shared__ Shared sh;
     const int blk = blockIdx.x;
-    int b;
-    bool front;
+    int b, t = 0;
+    int role;  // 0 scan, 1 stand-alone probe, 2 argmax
+    Prefetch pre = {1, -1, -1};
     if (blk < p.n_scan_wg) {
         b = blk / p.scan_tiles;
-        scan_role(p, b, blk - b * p.scan_tiles, sh);
-        front = true;
+        t = blk - b * p.scan_tiles;
+        scan_role(p, b, t, sh, pre);
+        role = 0;
     } else if (blk < p.n_front_wg) {
         b = blk - p.n_scan_wg;
         probe_role(p, b, sh);
-        front = true;
+        role = 1;
     } else {
         const int idx = blk - p.n_front_wg;
         const int rowi = idx / p.segs;
         const int s = idx - rowi * p.segs;
         b = rowi / p.R;
-        const int r = rowi - b * p.R;
-        if ((uint32_t)r < rows_needed(p, b))
-            argmax_role(p, b, r, s, sh);
-        front = false;
+        argmax_role(p, b, rowi - b * p.R, s, sh);
+        role = 2;
     }
     if (threadIdx.x >= 64)
         return;  // waves 1.. are done; wave 0 arrives and may run an epilogue
-    if (front && p.epi_front != EPI_NONE) {
-        if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front))
-            front_epilogue(p, b);
+    if (role == 0 && p.epi_front != EPI_NONE) {
+        if (p.scan_tiles == 1) {
+            front_local(p, b, sh, pre);
+        } else {
+            const int lane = threadIdx.x;
+            if (lane < p.n_ngram && sh.scan.red[lane] > 0)
+                atomicMax(&p.ws.mslot[b * kLineU32 + lane], sh.scan.red[lane]);
+            if (t == 0 && p.scan_probe && lane == 0)
+                st_f32(&p.z[b], probe_combine(sh.scan.ps, sh.scan.pc, p.bias));
+            if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front))
+                front_remote(p, b, t, sh, pre);
+        }
     }
-    if (p.epi_accept) {
+    if (p.epi_accept && role != 1) {
         if (arrive(&p.ws.tk_all[b * kLineU32], p.exp_all))
             final_epilogue(p, b, sh);
     }
