@@ -115,6 +115,9 @@ def main():
     ap.add_argument("--mode", type=int, default=0, help="0 auto, 1 fused, 2 split")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="after timing, run a plain device copy of this many MB five times "
+                         "(the reference kernel for scaling HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -179,13 +182,17 @@ def main():
     step_gbps = alg / (ms * 1e-3) / 1e9
 
     # verify-argmax alone (stage entry point), rows of the chosen draft
-    vouts = outs
+    vargs = [(st["logits"].data_ptr(), wl.B, wl.R, wl.V, o["dtok"].data_ptr(),
+              o["dpar"].data_ptr(), o["dn"].data_ptr(), o["accept_len"].data_ptr(),
+              o["accept_node"].data_ptr(), o["bonus"].data_ptr(), o["out_tokens"].data_ptr(),
+              o["amax"].data_ptr(), wsp, wsn, sptr) for st, o in zip(sets, outs)]
+
     def run_verify(n):
         for i in range(n):
-            s, o = sets[i % nrot], vouts[i % nrot]
-            sd.switchsd_verify_accept(s["logits"], o["dtok"], o["dpar"], o["dn"], o["accept_len"],
-                                      o["accept_node"], o["bonus"], o["out_tokens"], o["amax"],
-                                      ws)
+            rc = lib.switchsd_verify_accept(*vargs[i % nrot])
+            if rc:
+                raise sd.SwitchsdError("switchsd_verify_accept", rc)
+
     nv = max(200, args.steps // 4)
     run_verify(20)
     torch.cuda.synchronize()
@@ -196,6 +203,16 @@ def main():
     vms = e0.elapsed_time(e1) / nv
     vbytes = int(np.sum(sel["dn"])) * wl.V * 2
     v_gbps = vbytes / (vms * 1e-3) / 1e9
+
+    if args.copy_calibration_mb > 0:
+        n = args.copy_calibration_mb << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
