@@ -252,12 +252,12 @@ struct Prefetch {
 // partial sums in sh.scan.ps/pc.
 //
 // Wave w owns the 16 blocks of 64 consecutive positions [t0 + 1024w, +1024),
-// one position per lane, plus the block before them.  For suffix offset u the
-// ballot of (x[y] == x[L-1-u]) over a block, shifted up by u (carrying the
-// previous block's top bits in), marks the ends e with x[e-u] == x[L-1-u];
-// AND-ing offsets 0..n-1 marks the ends of occurrences of the n-gram suffix,
-// and the highest marked lane is the most recent one.  Scalar 64-bit masks
-// only: one compare per position and offset, no LDS reads.
+// one position per lane.  For suffix offset u, the ballot of
+// (x[e-u] == x[L-1-u]) over a block marks its ends e whose u-th token back
+// matches; AND-ing offsets 0..n-1 marks the ends of occurrences of the n-gram
+// suffix, and the highest marked lane is the most recent one.  x[e-u] comes
+// from the LDS tile (its 64-position halo covers u < 64), with the 16 blocks'
+// reads issued together: one compare and one 64-bit AND per block and offset.
 constexpr int kScanBlocks = kScanTile / kThreads;  // blocks of 64 positions per wave
 
 __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetch &pre) {
@@ -319,16 +319,19 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
             const int n = elim - 64 * i;
             M[i] = n >= 64 ? ~0ull : (n <= 0 ? 0ull : ((1ull << n) - 1ull));
         }
-        const bool halo = w0 > 0;  // the block before holds real positions
+        // LDS index of position w0 + 64 i + lane is lx0 + 64 i
+        const int lx0 = w0 - t0 + 64 + lane;
         for (int u = 0; u < p.nmax; ++u) {
             const int pu = sh.scan.pat[u];
-            unsigned long long prev = halo ? __ballot(tok[0] == pu) : 0ull;
+            // x[e - u] for the 16 blocks: independent LDS reads, issued together
+            int xu[kScanBlocks];
 #pragma unroll
-            for (int i = 0; i < kScanBlocks; ++i) {
-                const unsigned long long cur = __ballot(tok[i + 1] == pu);
-                M[i] &= u == 0 ? cur : ((cur << u) | (prev >> (64 - u)));
-                prev = cur;
-            }
+            for (int i = 0; i < kScanBlocks; ++i)
+                xu[i] = u == 0 ? tok[i + 1] : sh.scan.tile[lx0 + 64 * i - u];
+            // positions e < u have no u-th token back (only in the context's first block)
+#pragma unroll
+            for (int i = 0; i < kScanBlocks; ++i)
+                M[i] &= __ballot(xu[i] == pu && (i > 0 || w0 > 0 || lane >= u));
             // record the length equal to u + 1, if it is one of the lengths
             int jm = -1;
 #pragma unroll

@@ -216,3 +216,21 @@ def test_empty_batch():
     args = sd.build_step_args(dev, out, sd.make_cfg((3, 2, 1), 1, 7, 0.0))
     sd.switchsd_step(args, sd.alloc_workspace(1, 8))
     torch.cuda.synchronize()
+
+
+def test_scan_start_of_context_has_no_false_match():
+    """Context 7, 9, ..., 9, 7, 7 with lengths (2, 1): the only (7, 7) pair is the
+    suffix itself, so the answer is the 1-gram at e = L-2.  Reading anything
+    before position 0 as a 7 would report a 2-gram ending at e = 0."""
+    say("[edge] start-of-context halo")
+    B, Lmax = 4, 64
+    tokens = np.full((B, Lmax), 9, np.int32)
+    tokens[:, 0] = 7
+    tokens[:, -2:] = 7
+    d = custom_case(seed=30, B=B, Lmax=Lmax, V=50, R=4, k=3, lens=(2, 1), kappa=1,
+                    theta=-np.inf, ragged=False)
+    d["tokens"] = tokens
+    exp = oracle_step(d)
+    assert (exp["match_n"] == 1).all() and (exp["match_end"] == Lmax - 2).all()
+    got, _ = gpu_step(to_device(d), d, AUTO)
+    assert_match(got, exp, what="halo")
