@@ -25,10 +25,11 @@ class OracleCfg(ctypes.Structure):
                 ("ngram_lens", ctypes.c_int32 * MAX_NGRAM),
                 ("kappa", ctypes.c_int32),
                 ("k", ctypes.c_int32),
-                ("theta", ctypes.c_float)]
+                ("theta", ctypes.c_float),
+                ("n_cand", ctypes.c_int32)]
 
 
-def make_cfg(ngram_lens, kappa, k, theta):
+def make_cfg(ngram_lens, kappa, k, theta, n_cand=1):
     c = OracleCfg()
     c.n_ngram = len(ngram_lens)
     for i, n in enumerate(ngram_lens):
@@ -36,7 +37,13 @@ def make_cfg(ngram_lens, kappa, k, theta):
     c.kappa = int(kappa)
     c.k = int(k)
     c.theta = float(theta)
+    c.n_cand = int(n_cand)
     return c
+
+
+def n_cand_of(cfg):
+    """W: candidates per sequence (0 or 1 both mean one)."""
+    return max(1, int(cfg.n_cand))
 
 
 def _load():
@@ -50,11 +57,13 @@ def _load():
         _lib.oracle_match.argtypes = [P, i32, P, P, P, P, P]
         _lib.oracle_probe.argtypes = [P, P, i32, ctypes.c_float]
         _lib.oracle_probe.restype = ctypes.c_float
-        _lib.oracle_select.argtypes = [i32, i32, P, ctypes.c_float, P, P, i32, i32, P, P, P, P]
+        _lib.oracle_match.restype = ctypes.c_int
+        _lib.oracle_select.argtypes = [i32, P, P, ctypes.c_float, P, P, i32, i32, P, P, P, P]
         _lib.oracle_select.restype = i32
         _lib.oracle_argmax_row.argtypes = [P, i32]
         _lib.oracle_argmax_row.restype = i32
         _lib.oracle_accept.argtypes = [P, P, i32, P, i32, P, P, P, P]
+        _lib.oracle_tree_mask.argtypes = [P, i32, i32, i32, P]
         _lib.oracle_step.argtypes = [i32, i32, i32, i32, i32] + [P] * 4 + [ctypes.c_float] + \
             [P] * 5 + [P] * 14 + [i32]
         _lib.oracle_step.restype = i32
@@ -70,13 +79,25 @@ def _c(a, dt):
 
 
 def match(x, L, cfg):
-    """Step 1 (Sec. 3.3): longest-first, most-recent suffix n-gram match."""
+    """Step 1 (Sec. 3.3): longest-first suffix n-gram match, W most recent ends.
+
+    Returns (match_n, match_end[W], copy_len[W], copy_tokens[W, k]); with
+    W = 1 the last three are scalars and a [k] row, as before.
+    """
     lib = _load()
+    W = n_cand_of(cfg)
     x = _c(x, np.int32)
-    mn, me, cl = (np.zeros(1, np.int32) for _ in range(3))
-    ct = np.full(max(cfg.k, 1), -1, np.int32)
+    if x.size == 0:
+        x = np.zeros(1, np.int32)
+    mn = np.zeros(1, np.int32)
+    me = np.zeros(W, np.int32)
+    cl = np.zeros(W, np.int32)
+    ct = np.full(W * max(cfg.k, 1), -1, np.int32)
     lib.oracle_match(_p(x), int(L), ctypes.byref(cfg), _p(mn), _p(me), _p(cl), _p(ct))
-    return int(mn[0]), int(me[0]), int(cl[0]), ct[:cfg.k].copy()
+    ct = ct[:W * cfg.k].reshape(W, cfg.k).copy()
+    if cfg.n_cand <= 1:
+        return int(mn[0]), int(me[0]), int(cl[0]), ct[0]
+    return int(mn[0]), me, cl, ct
 
 
 def probe(h_bf16, w, bias):
@@ -90,13 +111,16 @@ def probe(h_bf16, w, bias):
 def select(match_n, copy_len, copy_tokens, z, ntok, npar, nn, R, cfg):
     """Step 3 (Sec. 3.3, Eq. 4 + kappa gate): chosen draft in node layout."""
     lib = _load()
-    ct = _c(copy_tokens, np.int32) if cfg.k > 0 else np.zeros(1, np.int32)
+    W = n_cand_of(cfg)
+    cl = _c(np.reshape(copy_len, (-1,)), np.int32)
+    assert cl.size == W
+    ct = _c(copy_tokens, np.int32).reshape(-1) if cfg.k > 0 else np.zeros(1, np.int32)
     ntok = _c(ntok, np.int32)
     npar_a = _c(npar, np.int32) if npar is not None else None
     dtok = np.zeros(R, np.int32)
     dpar = np.zeros(R, np.int32)
     dn = np.zeros(1, np.int32)
-    uc = lib.oracle_select(int(match_n), int(copy_len), _p(ct), float(z), _p(ntok), _p(npar_a),
+    uc = lib.oracle_select(int(match_n), _p(cl), _p(ct), float(z), _p(ntok), _p(npar_a),
                            int(nn), int(R), ctypes.byref(cfg), _p(dtok), _p(dpar), _p(dn))
     return int(uc), dtok, dpar, int(dn[0])
 
@@ -119,6 +143,21 @@ def accept(dtok, dpar, dn, amax, R):
     lib.oracle_accept(_p(dtok), _p(dpar), int(dn), _p(amax), int(R), _p(al), _p(an), _p(bo),
                       _p(out))
     return int(al[0]), int(an[0]), int(bo[0]), out
+
+
+def tree_mask(dpar, dn, R, words=None):
+    """Sec. 3.3 (block-triangular attention): ancestor-or-self bit rows.
+
+    Returns uint32 [R, words]; bit j of row i is set iff node j is on node i's
+    path to the anchor (itself included).
+    """
+    lib = _load()
+    if words is None:
+        words = (R + 31) // 32
+    dpar = _c(dpar, np.int32)
+    m = np.zeros((R, words), np.uint32)
+    lib.oracle_tree_mask(_p(dpar), int(dn), int(R), int(words), _p(m))
+    return m
 
 
 STEP_OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_copy",
@@ -148,9 +187,11 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=
     V = logits.shape[-1]
     assert logits.size == B * R * V
     K = cfg.k
+    W = n_cand_of(cfg)
     o = {
-        "match_n": np.zeros(B, np.int32), "match_end": np.zeros(B, np.int32),
-        "copy_len": np.zeros(B, np.int32), "copy_tokens": np.zeros((B, max(K, 1)), np.int32),
+        "match_n": np.zeros(B, np.int32), "match_end": np.zeros((B, W), np.int32),
+        "copy_len": np.zeros((B, W), np.int32),
+        "copy_tokens": np.zeros((B, W, max(K, 1)), np.int32),
         "z": np.zeros(B, np.float32), "use_copy": np.zeros(B, np.int32),
         "dtok": np.zeros((B, R), np.int32), "dpar": np.zeros((B, R), np.int32),
         "dn": np.zeros(B, np.int32), "amax": np.zeros((B, R), np.int32),
@@ -162,7 +203,11 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=
                          ctypes.byref(cfg), *[_p(o[k]) for k in STEP_OUTPUTS], int(threads))
     if rc != 0:
         raise ValueError("oracle_step rejected its arguments")
-    o["copy_tokens"] = o["copy_tokens"][:, :K]
+    o["copy_tokens"] = o["copy_tokens"][:, :, :K]
+    if cfg.n_cand <= 1:
+        o["match_end"] = o["match_end"][:, 0].copy()
+        o["copy_len"] = o["copy_len"][:, 0].copy()
+        o["copy_tokens"] = o["copy_tokens"][:, 0].copy()
     return o
 
 
@@ -171,9 +216,13 @@ def front(tokens, lengths, hidden, w, bias, ntok, npar, nn, cfg):
     tokens = _c(tokens, np.int32)
     B, Lmax = tokens.shape
     R = ntok.shape[1]
-    o = {k: np.zeros(B, np.int32) for k in ("match_n", "match_end", "copy_len", "use_copy", "dn")}
+    W = n_cand_of(cfg)
+    wsh = (B,) if cfg.n_cand <= 1 else (B, W)
+    o = {k: np.zeros(B, np.int32) for k in ("match_n", "use_copy", "dn")}
+    o["match_end"] = np.zeros(wsh, np.int32)
+    o["copy_len"] = np.zeros(wsh, np.int32)
     o["z"] = np.zeros(B, np.float32)
-    o["copy_tokens"] = np.zeros((B, cfg.k), np.int32)
+    o["copy_tokens"] = np.zeros(wsh + (cfg.k,), np.int32)
     o["dtok"] = np.zeros((B, R), np.int32)
     o["dpar"] = np.zeros((B, R), np.int32)
     for b in range(B):

@@ -41,24 +41,37 @@ static float bf16_to_float(uint16_t h)
     return f;
 }
 
+static int32_t n_cand_of(const oracle_cfg *cfg)
+{
+    return cfg->n_cand > 1 ? cfg->n_cand : 1;
+}
+
 /* Step 1 -- Sec. 3.3 (Copy-Intent Decision Rule; Copy-Based Speculative
  * Generation).  For each n in the configured order: the set of ends e with
  * n-1 <= e <= L-2 and x[e-t] == x[L-1-t] for every t < n.  The first n whose
- * set is non-empty gives match_n = n and match_end = the largest e.  The copy
- * candidate is the continuation after the occurrence, cut to k tokens and to
- * the end of the context. */
+ * set is non-empty gives match_n = n.  Its W largest ends, most recent first,
+ * are the candidates ("ranked by recency"); each candidate is the
+ * continuation after its occurrence, cut to k tokens and to the end of the
+ * context. */
 int oracle_match(const int32_t *x, int32_t L, const oracle_cfg *cfg,
                  int32_t *match_n, int32_t *match_end, int32_t *copy_len,
                  int32_t *copy_tokens)
 {
+    const int32_t W = n_cand_of(cfg);
+    int32_t found = 0;
     *match_n = 0;
-    *match_end = -1;
-    for (int32_t j = 0; j < cfg->n_ngram; ++j) {
+    for (int32_t c = 0; c < W; ++c) {
+        match_end[c] = -1;
+        copy_len[c] = 0;
+        for (int32_t j = 0; j < cfg->k; ++j)
+            copy_tokens[c * cfg->k + j] = -1;
+    }
+    for (int32_t j = 0; j < cfg->n_ngram && found == 0; ++j) {
         int32_t n = cfg->ngram_lens[j];
         if (L < n + 1)
             continue;
-        int32_t best = -1;
-        for (int32_t e = n - 1; e <= L - 2; ++e) {
+        /* ends from the most recent down */
+        for (int32_t e = L - 2; e >= n - 1 && found < W; --e) {
             int same = 1;
             for (int32_t t = 0; t < n; ++t) {
                 if (x[e - t] != x[L - 1 - t]) {
@@ -66,29 +79,24 @@ int oracle_match(const int32_t *x, int32_t L, const oracle_cfg *cfg,
                     break;
                 }
             }
-            if (same && e > best)
-                best = e;
+            if (same) {
+                match_end[found] = e;
+                ++found;
+            }
         }
-        if (best >= 0) {
+        if (found > 0)
             *match_n = n;
-            *match_end = best;
-            break;
-        }
     }
-    for (int32_t j = 0; j < cfg->k; ++j)
-        copy_tokens[j] = -1;
-    if (*match_n == 0) {
-        *copy_len = 0;
-        return 0;
+    for (int32_t c = 0; c < found; ++c) {
+        int32_t start = match_end[c] + 1;
+        int32_t len = L - start;
+        if (len > cfg->k)
+            len = cfg->k;
+        copy_len[c] = len;
+        for (int32_t j = 0; j < len; ++j)
+            copy_tokens[c * cfg->k + j] = x[start + j];
     }
-    int32_t c = *match_end + 1;
-    int32_t len = L - c;
-    if (len > cfg->k)
-        len = cfg->k;
-    *copy_len = len;
-    for (int32_t j = 0; j < len; ++j)
-        copy_tokens[j] = x[c + j];
-    return 0;
+    return found;
 }
 
 /* Step 2 -- Sec. 3.2, Eq. 3: the probe is the linear score w^T H (the
@@ -108,7 +116,7 @@ float oracle_probe(const uint16_t *h_bf16, const float *w, int32_t d, float bias
 /* Step 3 -- Sec. 3.3, Eq. 4 with the kappa-gram gate: copy iff the probe
  * clears the threshold AND a match of length >= kappa exists; otherwise the
  * neural draft is used as given. */
-int32_t oracle_select(int32_t match_n, int32_t copy_len, const int32_t *copy_tokens,
+int32_t oracle_select(int32_t match_n, const int32_t *copy_len, const int32_t *copy_tokens,
                       float z, const int32_t *ntok, const int32_t *npar,
                       int32_t nn, int32_t R, const oracle_cfg *cfg,
                       int32_t *dtok, int32_t *dpar, int32_t *dn)
@@ -119,11 +127,16 @@ int32_t oracle_select(int32_t match_n, int32_t copy_len, const int32_t *copy_tok
         dpar[r] = -1;
     }
     if (use_copy) {
-        *dn = copy_len + 1;
-        for (int32_t i = 1; i <= copy_len; ++i) {
-            dtok[i] = copy_tokens[i - 1];
-            dpar[i] = i - 1;
+        /* the candidates one after another, each a chain from the anchor */
+        int32_t node = 1;
+        for (int32_t c = 0; c < n_cand_of(cfg); ++c) {
+            for (int32_t i = 0; i < copy_len[c]; ++i) {
+                dtok[node] = copy_tokens[c * cfg->k + i];
+                dpar[node] = i == 0 ? 0 : node - 1;
+                ++node;
+            }
         }
+        *dn = node;
     } else {
         if (nn < 1)
             nn = 1;
@@ -198,6 +211,29 @@ void oracle_accept(const int32_t *dtok, const int32_t *dpar, int32_t dn,
     free(depth);
 }
 
+/* Sec. 3.3 (Parallel Verification with Block-Triangular Attention): a draft
+ * token sees itself and the tokens on its path back to the anchor (and the
+ * whole prefix, which is not part of this mask). */
+void oracle_tree_mask(const int32_t *dpar, int32_t dn, int32_t R, int32_t words,
+                      uint32_t *mask)
+{
+    for (int32_t i = 0; i < R; ++i)
+        for (int32_t w = 0; w < words; ++w)
+            mask[i * words + w] = 0;
+    for (int32_t i = 0; i < dn; ++i) {
+        int32_t node = i;
+        for (;;) {
+            mask[i * words + node / 32] |= 1u << (node % 32);
+            if (node == 0)
+                break;
+            int32_t p = dpar[node];
+            if (p < 0 || p >= node)
+                break;
+            node = p;
+        }
+    }
+}
+
 typedef struct {
     int32_t b0, b1;
     int32_t Lmax, d, R, V;
@@ -216,7 +252,7 @@ typedef struct {
 
 static void step_range(const step_job *j)
 {
-    const int64_t R = j->R, V = j->V, K = j->cfg->k;
+    const int64_t R = j->R, V = j->V, K = j->cfg->k, W = n_cand_of(j->cfg);
     for (int32_t b = j->b0; b < j->b1; ++b) {
         int32_t L = j->lengths[b];
         if (L < 0)
@@ -224,10 +260,11 @@ static void step_range(const step_job *j)
         if (L > j->Lmax)
             L = j->Lmax;
         const int32_t *x = j->tokens + (int64_t)b * j->Lmax;
-        oracle_match(x, L, j->cfg, &j->match_n[b], &j->match_end[b], &j->copy_len[b],
-                     j->copy_tokens + b * K);
+        oracle_match(x, L, j->cfg, &j->match_n[b], j->match_end + b * W, j->copy_len + b * W,
+                     j->copy_tokens + b * W * K);
         j->z[b] = oracle_probe(j->hidden + (int64_t)b * j->d, j->w, j->d, j->bias);
-        j->use_copy[b] = oracle_select(j->match_n[b], j->copy_len[b], j->copy_tokens + b * K,
+        j->use_copy[b] = oracle_select(j->match_n[b], j->copy_len + b * W,
+                                       j->copy_tokens + b * W * K,
                                        j->z[b], j->ntok + b * R,
                                        j->npar ? j->npar + b * R : NULL, j->nn[b], j->R,
                                        j->cfg, j->dtok + b * R, j->dpar + b * R, &j->dn[b]);
@@ -258,7 +295,8 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
                 int32_t *out_tokens, int32_t threads)
 {
-    if (B < 0 || Lmax < 1 || d < 0 || R < 1 || V < 1 || !cfg || cfg->k < 0 || cfg->k + 1 > R)
+    if (B < 0 || Lmax < 1 || d < 0 || R < 1 || V < 1 || !cfg || cfg->k < 0 ||
+        n_cand_of(cfg) * cfg->k + 1 > R)
         return -1;
     if (cfg->n_ngram < 1 || cfg->n_ngram > ORACLE_MAX_NGRAM)
         return -1;

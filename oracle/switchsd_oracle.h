@@ -36,12 +36,15 @@ typedef struct {
     int32_t n_ngram;                      /* number of n-gram lengths tried     */
     int32_t ngram_lens[ORACLE_MAX_NGRAM]; /* tried in this order (longest first) */
     int32_t kappa;                        /* copy only if match_n >= kappa       */
-    int32_t k;                            /* maximum copy-draft length           */
+    int32_t k;                            /* maximum copy-draft length (D)       */
     float theta;                          /* probe threshold as a logit          */
+    int32_t n_cand;                       /* copy candidates W (0 or 1: one)     */
 } oracle_cfg;
 
-/* Step 1 for one sequence x[0..L-1].  Writes match_n, match_end, copy_len
- * and copy_tokens[0..k-1] (-1 padded).  Returns 0. */
+/* Step 1 for one sequence x[0..L-1] with W = max(1, n_cand) candidates.
+ * Writes match_n, match_end[W] (-1 padded), copy_len[W] (0 padded) and
+ * copy_tokens[W*k] (-1 padded), candidates in order of recency.  Returns the
+ * number of candidates found. */
 int oracle_match(const int32_t *x, int32_t L, const oracle_cfg *cfg,
                  int32_t *match_n, int32_t *match_end, int32_t *copy_len,
                  int32_t *copy_tokens);
@@ -50,8 +53,10 @@ int oracle_match(const int32_t *x, int32_t L, const oracle_cfg *cfg,
 float oracle_probe(const uint16_t *h_bf16, const float *w, int32_t d, float bias);
 
 /* Step 3 for one sequence.  Writes the chosen draft in node layout
- * (R rows; node 0 is the anchor).  Returns use_copy. */
-int32_t oracle_select(int32_t match_n, int32_t copy_len, const int32_t *copy_tokens,
+ * (R rows; node 0 is the anchor); a copy draft is one chain per candidate,
+ * each hanging off the anchor, candidates in order.  copy_len[W] and
+ * copy_tokens[W*k] as written by oracle_match.  Returns use_copy. */
+int32_t oracle_select(int32_t match_n, const int32_t *copy_len, const int32_t *copy_tokens,
                       float z, const int32_t *ntok, const int32_t *npar,
                       int32_t nn, int32_t R, const oracle_cfg *cfg,
                       int32_t *dtok, int32_t *dpar, int32_t *dn);
@@ -66,9 +71,17 @@ void oracle_accept(const int32_t *dtok, const int32_t *dpar, int32_t dn,
                    int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
                    int32_t *out_tokens);
 
+/* Attention mask of a draft tree for the parallel verification pass:
+ * bit j of row i (words of 32 bits, `words` per row) is set iff node j is
+ * node i or one of its ancestors (the walk stops at an invalid parent).  Rows
+ * at and beyond dn are zero. */
+void oracle_tree_mask(const int32_t *dpar, int32_t dn, int32_t R, int32_t words,
+                      uint32_t *mask);
+
 /* The whole step for B sequences; threads > 1 splits the batch across
  * POSIX threads (sequences are independent).  npar may be NULL (chains).
  * amax [B,R] receives the argmax of rows r < dn[b] and -1 elsewhere.
+ * match_end and copy_len are [B,W], copy_tokens [B,W,k] (W = max(1, n_cand)).
  * Returns 0, or -1 on a bad argument. */
 int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 const int32_t *tokens, const int32_t *lengths,

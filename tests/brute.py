@@ -25,7 +25,11 @@ def bf16_to_f32(h):
     return (np.asarray(h, np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def match(x, L, lens, k):
+def match_all(x, L, lens, k, W):
+    """The W most recent occurrences of the longest matching suffix length.
+
+    Returns (n, ends[W], lens[W], tokens[W][k]) padded with -1 / 0 / -1.
+    """
     x = np.asarray(x[:L], dtype="<i4")
     for n in lens:
         if L < n + 1:
@@ -33,22 +37,31 @@ def match(x, L, lens, k):
         pat = x[L - n:].tobytes()
         hay = x[:L - 1].tobytes()          # occurrences must end at e <= L-2
         pos = len(hay)
-        found = -1
-        while True:
+        starts = []
+        while len(starts) < W:
             i = hay.rfind(pat, 0, pos)
             if i < 0:
                 break
             if i % 4 == 0:
-                found = i // 4
-                break
+                starts.append(i // 4)
             pos = i + len(pat) - 1      # retry strictly before this hit's end
-        if found >= 0:
-            e = found + n - 1
-            c = e + 1
-            cl = min(k, L - c)
-            ct = [int(t) for t in x[c:c + cl]] + [-1] * (k - cl)
-            return n, e, cl, ct
-    return 0, -1, 0, [-1] * k
+        if starts:
+            ends, cls, cts = [], [], []
+            for s0 in starts:
+                e = s0 + n - 1
+                c = e + 1
+                cl = min(k, L - c)
+                ends.append(e)
+                cls.append(cl)
+                cts.append([int(t) for t in x[c:c + cl]] + [-1] * (k - cl))
+            pad = W - len(starts)
+            return (n, ends + [-1] * pad, cls + [0] * pad, cts + [[-1] * k] * pad)
+    return 0, [-1] * W, [0] * W, [[-1] * k] * W
+
+
+def match(x, L, lens, k):
+    n, ends, cls, cts = match_all(x, L, lens, k, 1)
+    return n, ends[0], cls[0], cts[0]
 
 
 def probe(h_bf16, w, bias):
@@ -71,10 +84,15 @@ def select(match_n, copy_len, copy_tokens, z, ntok, npar, nn, R, kappa, theta):
     dtok = [-1] * R
     dpar = [-1] * R
     if match_n >= kappa and np.float32(z) >= np.float32(theta):
-        for i in range(copy_len):
-            dtok[i + 1] = int(copy_tokens[i])
-            dpar[i + 1] = i
-        return 1, dtok, dpar, copy_len + 1
+        if np.ndim(copy_len) == 0:                  # one candidate
+            copy_len, copy_tokens = [copy_len], [copy_tokens]
+        nodes = [(0, -1)]                           # (token, parent); anchor first
+        for cl, ct in zip(copy_len, copy_tokens):
+            for i in range(int(cl)):
+                nodes.append((int(ct[i]), 0 if i == 0 else len(nodes) - 1))
+        for i, (t, par) in enumerate(nodes[1:], start=1):
+            dtok[i], dpar[i] = t, par
+        return 1, dtok, dpar, len(nodes)
     nn = max(1, min(int(nn), R))
     for i in range(1, nn):
         dtok[i] = int(ntok[i])
@@ -102,7 +120,24 @@ def accept(dtok, dpar, dn, amax, R):
     return best_depth, best, bonus, out
 
 
-def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, lens, kappa, k, theta):
+def tree_mask(dpar, dn, R):
+    """Ancestor-or-self sets as Python sets (a node with a bad parent stops)."""
+    rows = []
+    for i in range(R):
+        s = set()
+        if i < dn:
+            c = i
+            s.add(c)
+            while c != 0 and 0 <= int(dpar[c]) < c:
+                c = int(dpar[c])
+                s.add(c)
+        rows.append(s)
+    return rows
+
+
+def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, lens, kappa, k, theta,
+         n_cand=1):
+    W = max(1, n_cand)
     B, Lmax = tokens.shape
     R = ntok.shape[1]
     res = {key: [] for key in ("match_n", "match_end", "copy_len", "copy_tokens", "z",
@@ -110,7 +145,10 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, lens, kappa, 
                                "accept_node", "bonus", "out_tokens")}
     for b in range(B):
         L = max(0, min(int(lengths[b]), Lmax))
-        mn, me, cl, ct = match(tokens[b], L, lens, k)
+        if n_cand <= 1:
+            mn, me, cl, ct = match(tokens[b], L, lens, k)
+        else:
+            mn, me, cl, ct = match_all(tokens[b], L, lens, k, W)
         z = probe(hidden[b], w, bias)
         uc, dtok, dpar, dn = select(mn, cl, ct, z, ntok[b], None if npar is None else npar[b],
                                     nn[b], R, kappa, theta)
@@ -121,5 +159,5 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, lens, kappa, 
     out = {}
     for key, v in res.items():
         out[key] = np.asarray(v, np.float32 if key == "z" else np.int32)
-    out["copy_tokens"] = out["copy_tokens"].reshape(B, k)
+    out["copy_tokens"] = out["copy_tokens"].reshape((B, k) if n_cand <= 1 else (B, W, k))
     return out

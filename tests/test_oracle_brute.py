@@ -68,6 +68,27 @@ def test_oracle_equals_brute_force(chain):
             np.testing.assert_array_equal(got[key], exp[key], err_msg=f"{key} {c}")
 
 
+@pytest.mark.parametrize("W", [2, 3, 10])
+def test_oracle_equals_brute_force_multi_candidate(W):
+    """W candidates (Sec. 3.3): the brute force collects every occurrence with
+    repeated byte-string searches and builds the W chains itself."""
+    rng = np.random.default_rng(4321 + W)
+    for _ in range(300):
+        c = random_case(rng, chain=True)
+        k = int(rng.integers(0, 5))
+        R = 1 + W * k + int(rng.integers(0, 3))
+        c["ntok"] = rng.integers(-1, 4, (c["ntok"].shape[0], R)).astype(np.int32)
+        c["logits"] = rng.choice(BF16_VALUES, (c["ntok"].shape[0], R, c["logits"].shape[2]))
+        cfg = oracle.make_cfg(c["lens"], c["kappa"], k, c["theta"], n_cand=W)
+        got = oracle.step(c["tokens"], c["lengths"], c["hidden"], c["w"], c["bias"], c["ntok"],
+                          None, c["nn"], c["logits"], cfg)
+        exp = brute.step(c["tokens"], c["lengths"], c["hidden"], c["w"], c["bias"], c["ntok"],
+                         None, c["nn"], c["logits"], c["lens"], c["kappa"], k, c["theta"],
+                         n_cand=W)
+        for key in exp:
+            np.testing.assert_array_equal(got[key], exp[key], err_msg=f"{key} W={W}")
+
+
 def test_oracle_threads_do_not_change_results():
     rng = np.random.default_rng(7)
     c = random_case(rng, False)

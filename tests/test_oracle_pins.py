@@ -54,6 +54,115 @@ def test_golden_probe(case):
     assert z == np.float32(case["z"])
 
 
+@pytest.mark.parametrize("case", _lines("multicand_cases.jsonl"), ids=lambda c: c["why"][:40])
+def test_golden_multi_candidate(case):
+    W, R = case["W"], case["R"]
+    cfg = oracle.make_cfg(case["lens"], 1, case["k"], -np.inf, n_cand=W)
+    mn, me, cl, ct = oracle.match(np.array(case["tokens"], np.int32), case["L"], cfg)
+    assert mn == case["match_n"]
+    assert me.tolist() == case["match_end"] and cl.tolist() == case["copy_len"]
+    assert ct.tolist() == case["copy_tokens"]
+    uc, dtok, dpar, dn = oracle.select(mn, cl, ct, 0.0, np.zeros(R, np.int32), None, 1, R, cfg)
+    assert uc == 1 and dn == case["dn"]
+    assert dtok.tolist() == case["dtok"] and dpar.tolist() == case["dpar"]
+    mask = oracle.tree_mask(dpar, dn, R, 1)
+    assert mask[:, 0].tolist() == case["mask"]
+    al, an, bo, out = oracle.accept(dtok, dpar, dn, case["amax"], R)
+    assert (al, an, bo) == (case["accept_len"], case["accept_node"], case["bonus"])
+    assert out.tolist() == case["out_tokens"]
+
+
+def _mask_sets(mask):
+    return [{32 * w + j for w in range(mask.shape[1]) for j in range(32)
+             if (int(mask[i, w]) >> j) & 1} for i in range(mask.shape[0])]
+
+
+def test_tree_mask_block_triangular_closed_form():
+    """W chains behind the anchor: the mask is block-diagonal below the anchor
+    column, each block lower-triangular (Sec. 3.3, block-triangular attention),
+    written here from the block sizes alone."""
+    rng = np.random.default_rng(21)
+    for _ in range(100):
+        W = int(rng.integers(1, 11))
+        k = int(rng.integers(0, 21))
+        lens = rng.integers(0, k + 1, W)
+        R = 1 + W * k + int(rng.integers(0, 3))
+        cfg = oracle.make_cfg((1,), 1, k, -np.inf, n_cand=W)
+        ct = rng.integers(0, 9, (W, max(k, 1)))[:, :k]
+        _, dtok, dpar, dn = oracle.select(1, lens, ct, 0.0, np.zeros(R, np.int32), None, 1, R,
+                                          cfg)
+        assert dn == 1 + int(lens.sum())
+        words = (R + 31) // 32
+        got = _mask_sets(oracle.tree_mask(dpar, dn, R, words))
+        exp = [{0}] + [set() for _ in range(R - 1)]
+        start = 1
+        for c in range(W):
+            for i in range(int(lens[c])):
+                exp[start + i] = {0} | set(range(start, start + i + 1))
+            start += int(lens[c])
+        assert got == exp
+
+
+def test_tree_mask_equals_ancestor_sets():
+    """Random trees (with broken parent links): the mask rows equal the
+    ancestor-or-self sets of an independent walk, rows past dn are empty,
+    and each valid row is its parent's row plus itself."""
+    import brute
+    rng = np.random.default_rng(22)
+    for _ in range(300):
+        R = int(rng.integers(1, 130))
+        dpar = np.array([-1] + [int(rng.integers(0, i)) for i in range(1, R)], np.int32)
+        if R > 1 and rng.random() < 0.3:
+            i = int(rng.integers(1, R))
+            dpar[i] = int(rng.choice([-1, i, R + 5]))
+        dn = int(rng.integers(1, R + 1))
+        words = (R + 31) // 32 + int(rng.integers(0, 2))
+        m = oracle.tree_mask(dpar, dn, R, words)
+        got = _mask_sets(m)
+        assert got == brute.tree_mask(dpar, dn, R)
+        for i in range(1, dn):
+            if 0 <= dpar[i] < i:
+                assert got[i] == got[dpar[i]] | {i}
+
+
+def test_multi_candidate_w1_equals_single():
+    """n_cand = 1 (and 0) is the single most-recent candidate of before."""
+    rng = np.random.default_rng(23)
+    for _ in range(200):
+        L = int(rng.integers(1, 40))
+        x = rng.integers(0, 3, L).astype(np.int32)
+        k = int(rng.integers(0, 6))
+        single = oracle.match(x, L, oracle.make_cfg((3, 2, 1), 1, k, 0.0))
+        for wv in (0, 1):
+            got = oracle.match(x, L, oracle.make_cfg((3, 2, 1), 1, k, 0.0, n_cand=wv))
+            assert got[:3] == single[:3] and got[3].tolist() == single[3].tolist()
+        many = oracle.match(x, L, oracle.make_cfg((3, 2, 1), 1, k, 0.0, n_cand=4))
+        assert many[0] == single[0] and many[1][0] == single[1]
+        assert many[2][0] == single[2] and many[3][0].tolist() == single[3].tolist()
+
+
+def test_multi_candidate_ends_are_all_occurrences():
+    """Candidates are exactly the W largest ends of the matched length, in
+    decreasing order, each a true occurrence of the suffix."""
+    rng = np.random.default_rng(24)
+    for _ in range(300):
+        L = int(rng.integers(1, 60))
+        x = rng.integers(0, 2, L).astype(np.int32)
+        W = int(rng.integers(2, 12))
+        cfg = oracle.make_cfg((4, 2), 1, 3, 0.0, n_cand=W)
+        mn, me, cl, ct = oracle.match(x, L, cfg)
+        if mn == 0:
+            assert (me == -1).all() and (cl == 0).all()
+            continue
+        occ = [e for e in range(mn - 1, L - 1)
+               if x[e - mn + 1:e + 1].tolist() == x[L - mn:L].tolist()]
+        occ = occ[::-1][:W]
+        assert me[:len(occ)].tolist() == occ and (me[len(occ):] == -1).all()
+        for c, e in enumerate(occ):
+            assert cl[c] == min(3, L - 1 - e)
+            assert ct[c, :cl[c]].tolist() == x[e + 1:e + 1 + cl[c]].tolist()
+
+
 # ---------------------------------------------------------------- invariants
 
 def test_I1_planted_span_found_c1():
