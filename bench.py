@@ -32,7 +32,7 @@ from paper_2609_20186_amd import workloads as W  # noqa: E402
 HBM_PEAK_GBPS = 8000.0
 METRIC = "speculation-control steps/s + verify-argmax HBM GB/s (% peak), B=32 V=128256"
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_20186_amd", "csrc", "switchsd_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fused_step_C2.json")
+PROFILES = os.path.join(ROOT, "profiles")
 ROTATE_BYTES = 512 << 20
 
 
@@ -45,14 +45,24 @@ def algorithmic_bytes(wl, rows_read, d_sel=None):
     """Bytes one step must move at least: each context token once, the hidden
     states and probe weight, every logits row it reads, the neural draft and
     the outputs."""
-    B, R, k = wl.B, wl.R, wl.k
+    B, R, k, Wc = wl.B, wl.R, wl.k, max(1, wl.n_cand)
     ins = B * wl.L * 4 + B * 4 + B * wl.d * 2 + wl.d * 4 + B * R * 4 + B * 4
     if not wl.chain:
         ins += B * R * 4
     logits = int(np.sum(rows_read)) * wl.V * 2
-    outs = B * 4 * 3 + B * k * 4 + B * 4 * 2 + B * R * 4 * 2 + B * 4 + B * R * 4 + B * 4 * 3 + \
-        B * R * 4
+    # match_n, match_end [W], copy_len [W], copy_tokens [W, k], z, use_copy, dtok,
+    # dpar, dn, amax, accept_len, accept_node, bonus, out_tokens
+    outs = B * 4 + 2 * B * Wc * 4 + B * Wc * k * 4 + B * 4 * 2 + B * R * 4 * 2 + B * 4 + \
+        B * R * 4 + B * 4 * 3 + B * R * 4
     return ins + logits + outs, logits
+
+
+def resolve_mode(wl, mode):
+    """The launch the library's AUTO mode picks (switchsd_step)."""
+    if mode:
+        return mode
+    cn = 1 + max(1, wl.n_cand) * wl.k
+    return 1 if cn >= wl.R and wl.R <= 64 else 2
 
 
 def upload(d):
@@ -69,9 +79,9 @@ def plant_with_library(wl, d, sd):
     step's front half writes the draft before any row is read)."""
     import torch
     dev = upload(d)
-    out = sd.alloc_outputs(wl.B, wl.R, wl.k)
-    ws = sd.alloc_workspace(wl.B, wl.R)
-    cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    out = sd.alloc_outputs(wl.B, wl.R, wl.k, wl.n_cand)
+    ws = sd.alloc_workspace(wl.B, wl.R, wl.L, wl.n_cand)
+    cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta, wl.n_cand)
     sd.switchsd_step(sd.build_step_args(dev, out, cfg, sd.MODE_SPLIT), ws)
     torch.cuda.synchronize()
     sel = {k: out[k].cpu().numpy() for k in ("dtok", "dpar", "dn", "use_copy")}
@@ -86,7 +96,7 @@ def cpu_baseline(wl_name, budget_s):
     import oracle
     wl = W.WORKLOADS[wl_name]
     d = W.generate(wl)
-    cfg = oracle.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    cfg = oracle.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta, wl.n_cand)
     sel = oracle.front(d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"],
                        d["npar"], d["nn"], cfg)
     W.plant_batch(wl, d, sel)
@@ -139,9 +149,9 @@ def main():
     nrot = max(1, math.ceil(ROTATE_BYTES / step_bytes))
     sets = [base] + [{k: (v.clone() if hasattr(v, "clone") else v) for k, v in base.items()}
                      for _ in range(nrot - 1)]
-    cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
-    outs = [sd.alloc_outputs(wl.B, wl.R, wl.k) for _ in range(nrot)]
-    ws = sd.alloc_workspace(wl.B, wl.R)
+    cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta, wl.n_cand)
+    outs = [sd.alloc_outputs(wl.B, wl.R, wl.k, wl.n_cand) for _ in range(nrot)]
+    ws = sd.alloc_workspace(wl.B, wl.R, wl.L, wl.n_cand)
     step_args = [sd.build_step_args(s, o, cfg, args.mode) for s, o in zip(sets, outs)]
     import ctypes
     lib = sd.lib
@@ -172,9 +182,10 @@ def main():
         for k, v in o.items():
             assert torch.equal(v.cpu(), o0[k]), f"rotation set disagrees on {k}"
 
-    mode = args.mode or (sd.MODE_FUSED if wl.k + 1 >= wl.R else sd.MODE_SPLIT)
+    mode = resolve_mode(wl, args.mode)
+    cn = 1 + max(1, wl.n_cand) * wl.k
     if mode == sd.MODE_FUSED:
-        rows_read = np.maximum(np.clip(d["nn"], 1, wl.R), wl.k + 1) if wl.k + 1 < wl.R \
+        rows_read = np.maximum(np.clip(d["nn"], 1, wl.R), cn) if cn < wl.R \
             else np.full(wl.B, wl.R)
     else:
         rows_read = sel["dn"]
@@ -214,9 +225,17 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    # the dominant kernel: the fused launch, or the verify launch of a split step
+    if mode == sd.MODE_FUSED:
+        dom = {"kernel": "k_switchsd (fused step)", "gbps": step_gbps, "bytes": alg,
+               "traffic_file": f"traffic_fused_step_{wl.name}.json"}
+    else:
+        dom = {"kernel": "k_switchsd (verify launch of the split step)", "gbps": v_gbps,
+               "bytes": vbytes, "traffic_file": f"traffic_verify_{wl.name}.json"}
     traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
+    tf = os.path.join(PROFILES, dom["traffic_file"])
+    if os.path.exists(tf):
+        with open(tf) as f:
             tr = json.load(f)
         if tr.get("kernel_sha") == kernel_sha() and tr.get("workload") == wl.name:
             traffic = tr.get("hbm_bytes_per_launch")
@@ -227,14 +246,16 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: B={wl.B} L={wl.L} V={wl.V} d={wl.d} k={wl.k} R={wl.R}"
-                               f" ngram={list(wl.ngram_lens)} kappa={wl.kappa}",
+                               f" W={max(1, wl.n_cand)} ngram={list(wl.ngram_lens)}"
+                               f" kappa={wl.kappa}",
                    "global_batch": wl.B, "seq_len": wl.L, "parallelism": "none (1 GPU)",
                    "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode],
                    "rotation_sets": nrot},
-        "roofline": {"bound": "hbm", "achieved": round(step_gbps, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic, "kernel": "k_switchsd (fused step)",
-                     "algorithmic_bytes_per_launch": alg},
+        "roofline": {"bound": "hbm", "achieved": round(dom["gbps"], 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dom["gbps"] / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "kernel": dom["kernel"],
+                     "algorithmic_bytes_per_launch": dom["bytes"]},
+        "step_GBps": round(step_gbps, 1),
         "verify_argmax": {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),
                           "us_per_call": round(vms * 1e3, 2), "bytes_per_call": vbytes},
         "copy_fraction": round(float(np.mean(sel["use_copy"])), 3),

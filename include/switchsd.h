@@ -4,10 +4,11 @@
  * Paper: "To Copy or Not to Copy: Controlling Speculative Decoding via
  * Intrinsic Model Signals".  One decoding step of SwitchSD, for B sequences:
  *
- *   1. suffix n-gram match over the token history (the copy candidate) --
+ *   1. suffix n-gram match over the token history (the copy candidates) --
  *      Sec. 3.3, Copy-Intent Decision Rule (a kappa-gram ending at the current
  *      token must have a prior occurrence) and Copy-Based Speculative
- *      Generation (continuations taken from the context, ranked by recency);
+ *      Generation (up to W continuations of up to D tokens taken from the
+ *      context, ranked by recency);
  *   2. linear copy-intent probe on the target's hidden state -- Sec. 3.2,
  *      Eq. 3 (p = sigmoid(w^T H), no bias in the paper; an optional bias is
  *      carried here);
@@ -35,10 +36,12 @@
  *     [1, R], and a node whose parent is not in [0, i) is never accepted.
  *   - Host-side validation runs before any HIP call; on failure a negative
  *     status is returned and nothing is launched.  B = 0 is a valid no-op.
- *   - Calls that take a workspace need `switchsd_workspace_bytes(B, R)`
- *     bytes, 256-byte aligned, zeroed once by the caller at allocation.
- *     Every kernel leaves the workspace zeroed again when it completes, so no
- *     per-call clearing is needed.  After a call fails inside HIP, or if the
+ *   - Calls that take a workspace need
+ *     `switchsd_workspace_bytes(B, R, Lmax, cfg.n_cand)` bytes, 256-byte
+ *     aligned, zeroed once by the caller at allocation.  Every kernel leaves
+ *     its tickets, slots and row keys zeroed again when it completes (the
+ *     candidate lists of long contexts are rewritten before every read), so
+ *     no per-call clearing is needed.  After a call fails inside HIP, or if the
  *     stream is torn down mid-call, zero it again.  Calls that share one
  *     workspace must be ordered (same stream, or synchronized).
  */
@@ -65,6 +68,7 @@ typedef enum {
 #define SWITCHSD_MAX_NGRAM 8       /* most n-gram lengths in one configuration  */
 #define SWITCHSD_MAX_NGRAM_LEN 64  /* longest n-gram length                     */
 #define SWITCHSD_MAX_R 1024        /* most draft nodes (logits rows) per sequence */
+#define SWITCHSD_MAX_CAND 16       /* most copy candidates W                     */
 
 /* Step configuration.
  *   ngram_lens  lengths searched, strictly descending, each in [1, 64]; the
@@ -73,7 +77,10 @@ typedef enum {
  *               The paper's setting is {5}; the synthetic workloads use {3,2,1}.
  *   kappa       copy is allowed only if the matched length is >= kappa
  *               (the paper's kappa = 5).  kappa >= 1.
- *   k           maximum copy-draft length (the paper's D = 20); k + 1 <= R.
+ *   k           maximum length of one copy candidate (the paper's D = 20).
+ *   n_cand      copy candidates W in [0, 16]; 0 and 1 both mean one (the
+ *               paper's W = 10, Sec. 3.3 and App. D).  A copy draft holds up to
+ *               W * k tokens: 1 + W * k <= R.
  *   theta       probe threshold as a logit: copy needs z >= theta, which is
  *               sigmoid(z) >= tau for theta = log(tau / (1 - tau)).
  *               -inf gives the CopySpec rule (copy iff a match exists),
@@ -84,18 +91,21 @@ typedef struct {
     int32_t kappa;
     int32_t k;
     float theta;
+    int32_t n_cand;
 } switchsd_cfg;
 
 /* Step 1 -- Sec. 3.3.  For each sequence b with L = clamp(lengths[b], 0, Lmax)
  * and context x = tokens[b, 0..L-1]: for each n in cfg->ngram_lens (in
  * order), the occurrences of the suffix x[L-n..L-1] that end at e <= L-2
  * (overlap with the suffix allowed).  The first n with an occurrence gives
- * match_n[b] = n and match_end[b] = the largest such e; the copy candidate is
- * copy_tokens[b, j] = x[e+1+j] for j < copy_len[b] = min(k, L-1-e), -1 after.
- * Without an occurrence: match_n = 0, match_end = -1, copy_len = 0.
+ * match_n[b] = n; its W = max(1, n_cand) largest ends e_0 > e_1 > ... are the
+ * candidates, most recent first: match_end[b, c] = e_c, and candidate c is
+ * copy_tokens[b, c, j] = x[e_c+1+j] for j < copy_len[b, c] = min(k, L-1-e_c),
+ * -1 after.  Candidate slots without an occurrence (all of them when there is
+ * no match, and then match_n = 0) hold match_end = -1, copy_len = 0.
  *   tokens [B, Lmax] int32, lengths [B] int32;
- *   outputs match_n, match_end, copy_len [B] int32, copy_tokens [B, k] int32
- *   (may be NULL when k == 0). */
+ *   outputs match_n [B], match_end, copy_len [B, W] int32, copy_tokens
+ *   [B, W, k] int32 (may be NULL when k == 0). */
 int switchsd_ngram_match(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
                          const switchsd_cfg *cfg, int32_t *match_n, int32_t *match_end,
                          int32_t *copy_len, int32_t *copy_tokens, void *workspace,
@@ -110,12 +120,15 @@ int switchsd_probe_score(const uint16_t *hidden, const float *w, float bias, int
 
 /* Step 3 -- Sec. 3.3, Eq. 4 and the kappa gate.
  * use_copy[b] = (match_n[b] >= kappa) && (z[b] >= theta).  The chosen draft is
- * written in node layout: copy -> the chain of copy_tokens[b, 0..copy_len-1]
- * (dn = copy_len + 1); neural -> the neural draft as given (ntok/npar, with
- * nn[b] nodes including the anchor; npar == NULL means a chain).  Rows at and
- * beyond dn[b] hold -1.
- *   match_n, copy_len [B] int32, copy_tokens [B, k] int32, z [B] float,
- *   ntok [B, R] int32, npar [B, R] int32 or NULL, nn [B] int32;
+ * written in node layout: copy -> the W candidates placed one after another
+ * behind the anchor (Sec. 3.3, Parallel Verification), candidate c a chain of
+ * its copy_len[b, c] tokens whose first node hangs off the anchor
+ * (dn = 1 + sum_c copy_len[b, c]; with W = 1 the chain of the one candidate);
+ * neural -> the neural draft as given (ntok/npar, with nn[b] nodes including
+ * the anchor; npar == NULL means a chain).  Rows at and beyond dn[b] hold -1.
+ *   match_n [B] int32, copy_len [B, W] int32 (clamped to [0, k]),
+ *   copy_tokens [B, W, k] int32, z [B] float, ntok [B, R] int32,
+ *   npar [B, R] int32 or NULL, nn [B] int32;
  *   outputs use_copy, dn [B] int32, dtok, dpar [B, R] int32. */
 int switchsd_select_draft(const int32_t *match_n, const int32_t *copy_len,
                           const int32_t *copy_tokens, const float *z, const int32_t *ntok,
@@ -140,10 +153,25 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
                            int32_t *out_tokens, int32_t *amax, void *workspace,
                            size_t workspace_bytes, hipStream_t stream);
 
+/* Attention mask of the chosen drafts for the target's verification pass --
+ * Sec. 3.3, Parallel Verification with Block-Triangular Attention: a drafted
+ * token attends to the whole prefix (not represented here) and to the draft
+ * nodes on its own path back to the anchor, itself included; for W copy
+ * candidates this is block-triangular (each candidate sees only its own
+ * earlier tokens).  mask[b, i, :] is a bitset of words = (R + 31) / 32 uint32
+ * words: bit j of word j / 32 is set iff node j is node i or one of its
+ * ancestors, the walk stopping at a parent outside [0, node).  Rows
+ * i >= clamp(dn[b], 0, R) are all zero.
+ *   dpar [B, R] int32 or NULL (chains), dn [B] int32;
+ *   output mask [B, R, (R + 31) / 32] uint32. */
+int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
+                       uint32_t *mask, hipStream_t stream);
+
 /* How switchsd_step schedules its work. */
 typedef enum {
-    SWITCHSD_MODE_AUTO = 0,  /* FUSED when every row may be needed (k + 1 >= R), else SPLIT */
-    SWITCHSD_MODE_FUSED = 1, /* one launch; reads rows r < max(nn[b], k + 1)                */
+    SWITCHSD_MODE_AUTO = 0,  /* FUSED when every row may be needed (1 + W k >= R) and
+                                R <= 64, else SPLIT                                       */
+    SWITCHSD_MODE_FUSED = 1, /* one launch; reads rows r < max(nn[b], 1 + W k)                */
     SWITCHSD_MODE_SPLIT = 2  /* two launches; reads only rows r < dn[b] of the chosen draft  */
 } switchsd_mode;
 
@@ -162,7 +190,7 @@ typedef struct {
     float bias;
     switchsd_cfg cfg;
     int32_t mode;            /* switchsd_mode */
-    int32_t *match_n, *match_end, *copy_len, *copy_tokens; /* [B],[B],[B],[B,k] */
+    int32_t *match_n, *match_end, *copy_len, *copy_tokens; /* [B],[B,W],[B,W],[B,W,k] */
     float *z;                                              /* [B] */
     int32_t *use_copy, *dtok, *dpar, *dn;                  /* [B],[B,R],[B,R],[B] */
     int32_t *amax;                                         /* [B, R] or NULL */
@@ -174,8 +202,11 @@ typedef struct {
 int switchsd_step(const switchsd_step_args *args, void *workspace, size_t workspace_bytes,
                   hipStream_t stream);
 
-/* Workspace bytes needed by calls with B sequences of R rows. */
-size_t switchsd_workspace_bytes(int32_t B, int32_t R);
+/* Workspace bytes needed by calls with B sequences of R rows, contexts of up
+ * to Lmax tokens and n_cand copy candidates (pass 0 for what a call does not
+ * take: R for the match stage, Lmax for verification).  0 for a negative
+ * argument. */
+size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_cand);
 
 /* Static, thread-safe text of a status code. */
 const char *switchsd_status_string(int status);

@@ -16,13 +16,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libswitchsd.so")
 
 MAX_NGRAM = 8
+MAX_CAND = 16
 MODE_AUTO, MODE_FUSED, MODE_SPLIT = 0, 1, 2
 
 STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE"}
 
 EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
-           "switchsd_verify_accept", "switchsd_step", "switchsd_workspace_bytes",
-           "switchsd_status_string")
+           "switchsd_verify_accept", "switchsd_tree_mask", "switchsd_step",
+           "switchsd_workspace_bytes", "switchsd_status_string")
 
 
 class SwitchsdError(RuntimeError):
@@ -37,10 +38,11 @@ class Cfg(ctypes.Structure):
                 ("ngram_lens", ctypes.c_int32 * MAX_NGRAM),
                 ("kappa", ctypes.c_int32),
                 ("k", ctypes.c_int32),
-                ("theta", ctypes.c_float)]
+                ("theta", ctypes.c_float),
+                ("n_cand", ctypes.c_int32)]
 
 
-def make_cfg(ngram_lens=(3, 2, 1), kappa=1, k=7, theta=0.0):
+def make_cfg(ngram_lens=(3, 2, 1), kappa=1, k=7, theta=0.0, n_cand=1):
     c = Cfg()
     c.n_ngram = len(ngram_lens)
     for i, n in enumerate(ngram_lens):
@@ -48,6 +50,7 @@ def make_cfg(ngram_lens=(3, 2, 1), kappa=1, k=7, theta=0.0):
     c.kappa = int(kappa)
     c.k = int(k)
     c.theta = float(theta)
+    c.n_cand = int(n_cand)
     return c
 
 
@@ -78,8 +81,9 @@ def _load():
                                           ctypes.POINTER(Cfg), _P, _P, _P, _P, _P]
     lib.switchsd_verify_accept.argtypes = [_P, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                            S, _P]
+    lib.switchsd_tree_mask.argtypes = [_P, _P, _I, _I, _P, _P]
     lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
-    lib.switchsd_workspace_bytes.argtypes = [_I, _I]
+    lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
     lib.switchsd_workspace_bytes.restype = S
     lib.switchsd_status_string.argtypes = [ctypes.c_int]
     lib.switchsd_status_string.restype = ctypes.c_char_p
@@ -95,12 +99,13 @@ def status_string(status):
     return lib.switchsd_status_string(int(status)).decode()
 
 
-def workspace_bytes(B, R):
-    return int(lib.switchsd_workspace_bytes(int(B), int(R)))
+def workspace_bytes(B, R, Lmax=0, n_cand=0):
+    return int(lib.switchsd_workspace_bytes(int(B), int(R), int(Lmax), int(n_cand)))
 
 
 _DT = {"i32": (torch.int32,), "f32": (torch.float32,),
-       "bf16": (torch.bfloat16, torch.int16, torch.uint16), "u8": (torch.uint8,)}
+       "bf16": (torch.bfloat16, torch.int16, torch.uint16), "u8": (torch.uint8,),
+       "u32": (torch.int32, torch.uint32)}
 
 
 def _ptr(t, kind, name, optional=False):
@@ -167,14 +172,27 @@ def switchsd_verify_accept(logits, dtok, dpar, dn, accept_len, accept_node, bonu
         workspace.numel(), _stream(stream)))
 
 
+def switchsd_tree_mask(dpar, dn, mask, stream=None):
+    """mask: uint32 (or int32 holding the same bits) [B, R, (R + 31) // 32]."""
+    B, R = mask.shape[0], mask.shape[1]
+    if mask.shape[2] != (R + 31) // 32:
+        raise ValueError("mask must be [B, R, (R + 31) // 32]")
+    _check("switchsd_tree_mask", lib.switchsd_tree_mask(
+        _ptr(dpar, "i32", "dpar", True), _ptr(dn, "i32", "dn"), B, R,
+        _ptr(mask, "u32", "mask"), _stream(stream)))
+
+
 OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_copy", "dtok", "dpar",
            "dn", "amax", "accept_len", "accept_node", "bonus", "out_tokens")
 
 
-def alloc_outputs(B, R, k, device="cuda"):
+def alloc_outputs(B, R, k, n_cand=1, device="cuda"):
+    """Output tensors of a step; with n_cand > 1 the candidate outputs carry a
+    W axis (match_end, copy_len [B, W], copy_tokens [B, W, k])."""
     i32 = dict(dtype=torch.int32, device=device)
-    return {"match_n": torch.empty(B, **i32), "match_end": torch.empty(B, **i32),
-            "copy_len": torch.empty(B, **i32), "copy_tokens": torch.empty((B, k), **i32),
+    wsh = (B,) if n_cand <= 1 else (B, n_cand)
+    return {"match_n": torch.empty(B, **i32), "match_end": torch.empty(wsh, **i32),
+            "copy_len": torch.empty(wsh, **i32), "copy_tokens": torch.empty(wsh + (k,), **i32),
             "z": torch.empty(B, dtype=torch.float32, device=device),
             "use_copy": torch.empty(B, **i32), "dtok": torch.empty((B, R), **i32),
             "dpar": torch.empty((B, R), **i32), "dn": torch.empty(B, **i32),
@@ -183,9 +201,10 @@ def alloc_outputs(B, R, k, device="cuda"):
             "out_tokens": torch.empty((B, R), **i32)}
 
 
-def alloc_workspace(B, R, device="cuda"):
-    """Zeroed once here; the kernels leave it zeroed after every call."""
-    return torch.zeros(max(workspace_bytes(B, R), 256), dtype=torch.uint8, device=device)
+def alloc_workspace(B, R, Lmax=0, n_cand=0, device="cuda"):
+    """Zeroed once here; the kernels keep it usable for every later call."""
+    return torch.zeros(max(workspace_bytes(B, R, Lmax, n_cand), 256), dtype=torch.uint8,
+                       device=device)
 
 
 def build_step_args(inp, out, cfg, mode=MODE_AUTO):

@@ -16,7 +16,6 @@ namespace {
 
 constexpr size_t kAlign = 256;
 
-size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 
 bool shape_ok_B(int32_t B) { return B >= 0 && B <= (1 << 24); }
 
@@ -32,9 +31,16 @@ int check_cfg(const switchsd_cfg *cfg) {
         if (j > 0 && n >= cfg->ngram_lens[j - 1])
             return SWITCHSD_EINVAL;
     }
-    if (cfg->kappa < 1 || cfg->k < 0)
+    if (cfg->kappa < 1 || cfg->k < 0 || cfg->n_cand < 0 || cfg->n_cand > SWITCHSD_MAX_CAND)
         return SWITCHSD_EINVAL;
     return SWITCHSD_OK;
+}
+
+int32_t n_cand_of(int32_t n_cand) { return n_cand > 1 ? n_cand : 1; }
+
+// Nodes of the longest copy draft: the anchor and W candidates of k tokens.
+int64_t copy_nodes(const switchsd_cfg *cfg) {
+    return 1 + (int64_t)n_cand_of(cfg->n_cand) * cfg->k;
 }
 
 void fill_cfg(StepParams &p, const switchsd_cfg *cfg) {
@@ -45,12 +51,14 @@ void fill_cfg(StepParams &p, const switchsd_cfg *cfg) {
     p.kappa = cfg->kappa;
     p.k = cfg->k;
     p.theta = cfg->theta;
+    p.W = n_cand_of(cfg->n_cand);
 }
 
-int check_workspace(const void *ws, size_t bytes, int32_t B, int32_t R) {
+int check_workspace(const void *ws, size_t bytes, int32_t B, int32_t R, int32_t Lmax,
+                    int32_t W) {
     if (!ws || ((uintptr_t)ws & (kAlign - 1)))
         return SWITCHSD_EWORKSPACE;
-    if (bytes < switchsd_workspace_bytes(B, R))
+    if (bytes < switchsd_workspace_bytes(B, R, Lmax, W))
         return SWITCHSD_EWORKSPACE;
     return SWITCHSD_OK;
 }
@@ -59,7 +67,18 @@ int32_t key_stride_for(int32_t R) {
     return (int32_t)(((int64_t)R + kLineU64 - 1) / kLineU64 * kLineU64);
 }
 
-Workspace carve(void *ws, int32_t B, int32_t R) {
+int scan_tiles_for(int32_t Lmax) { return (int)((Lmax + kScanTile - 1) / kScanTile); }
+
+// int32 per sequence of the candidate lists: every scan tile keeps W ends per
+// n-gram length; needed only with several candidates and several tiles.
+int64_t cand_stride_for(int32_t Lmax, int32_t W) {
+    const int64_t tiles = Lmax > 0 ? scan_tiles_for(Lmax) : 0;
+    if (W <= 1 || tiles <= 1)
+        return 0;
+    return (tiles * SWITCHSD_MAX_NGRAM * W + kLineU32 - 1) / kLineU32 * kLineU32;
+}
+
+Workspace carve(void *ws, int32_t B, int32_t R, int32_t Lmax, int32_t W) {
     Workspace w;
     char *base = (char *)ws;
     const size_t line = (size_t)kLineU32 * 4;
@@ -68,10 +87,10 @@ Workspace carve(void *ws, int32_t B, int32_t R) {
     w.mslot = (int32_t *)(base + 2 * (size_t)B * line);
     w.keys = (unsigned long long *)(base + 3 * (size_t)B * line);
     w.key_stride = key_stride_for(R);
+    w.cand = (int32_t *)(base + 3 * (size_t)B * line + (size_t)B * w.key_stride * 8);
+    w.cand_stride = (int32_t)cand_stride_for(Lmax, W);
     return w;
 }
-
-int scan_tiles_for(int32_t Lmax) { return (int)((Lmax + kScanTile - 1) / kScanTile); }
 
 // Compute units of the current device (cached per device).
 int cu_count(int *out) {
@@ -130,12 +149,14 @@ int set_scan(StepParams &p, int32_t B, int32_t Lmax) {
 
 extern "C" {
 
-size_t switchsd_workspace_bytes(int32_t B, int32_t R) {
-    if (B < 0 || R < 0)
+size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_cand) {
+    if (B < 0 || R < 0 || Lmax < 0 || n_cand < 0)
         return 0;
-    // per sequence: three 256-byte lines (two tickets, the n-gram slots) and
-    // the row keys rounded up to whole lines
-    return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8);
+    // per sequence: three 256-byte lines (two tickets, the n-gram slots), the
+    // row keys and the candidate lists, each rounded up to whole lines
+    const int64_t W = n_cand > SWITCHSD_MAX_CAND ? SWITCHSD_MAX_CAND : n_cand_of(n_cand);
+    return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8 +
+                        (size_t)cand_stride_for(Lmax, (int32_t)W) * 4);
 }
 
 const char *switchsd_status_string(int status) {
@@ -169,11 +190,11 @@ int switchsd_ngram_match(const int32_t *tokens, const int32_t *lengths, int32_t 
     if (!tokens || !lengths || !match_n || !match_end || !copy_len ||
         (cfg->k > 0 && !copy_tokens))
         return SWITCHSD_EINVAL;
-    if ((rc = check_workspace(workspace, workspace_bytes, B, 0)))
-        return rc;
     StepParams p;
     memset(&p, 0, sizeof p);
     fill_cfg(p, cfg);
+    if ((rc = check_workspace(workspace, workspace_bytes, B, 0, Lmax, p.W)))
+        return rc;
     p.tokens = tokens;
     p.lengths = lengths;
     p.B = B;
@@ -183,7 +204,7 @@ int switchsd_ngram_match(const int32_t *tokens, const int32_t *lengths, int32_t 
     p.match_end = match_end;
     p.copy_len = copy_len;
     p.copy_tokens = copy_tokens;
-    p.ws = carve(workspace, B, 0);
+    p.ws = carve(workspace, B, 0, Lmax, p.W);
     if ((rc = set_scan(p, B, Lmax)))
         return rc;
     p.n_front_wg = p.n_scan_wg;
@@ -221,7 +242,7 @@ int switchsd_select_draft(const int32_t *match_n, const int32_t *copy_len,
     int rc = check_cfg(cfg);
     if (rc)
         return rc;
-    if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || cfg->k + 1 > R)
+    if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || copy_nodes(cfg) > R)
         return SWITCHSD_ESHAPE;
     if (B == 0)
         return SWITCHSD_OK;
@@ -265,11 +286,12 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
     if (!logits || ((uintptr_t)logits & 1) || !dtok || !dn || !accept_len || !accept_node ||
         !bonus || !out_tokens)
         return SWITCHSD_EINVAL;
-    int rc = check_workspace(workspace, workspace_bytes, B, R);
+    int rc = check_workspace(workspace, workspace_bytes, B, R, 0, 0);
     if (rc)
         return rc;
     StepParams p;
     memset(&p, 0, sizeof p);
+    p.W = 1;
     if ((rc = set_segments(p, (int64_t)B * R, V)))
         return rc;
     const int64_t grid = (int64_t)B * R * p.segs;
@@ -287,7 +309,7 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
     p.bonus = bonus;
     p.out_tokens = out_tokens;
     p.amax = amax;
-    p.ws = carve(workspace, B, R);
+    p.ws = carve(workspace, B, R, 0, 0);
     p.rows_mode = ROWS_DRAFT;
     p.speculate = speculate ? 1 : 0;
     p.epi_accept = 1;
@@ -319,7 +341,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         return rc;
     const int32_t B = a->B, R = a->R, V = a->V;
     if (!shape_ok_B(B) || a->Lmax < 1 || a->d < 0 || R < 1 || R > SWITCHSD_MAX_R || V < 1 ||
-        a->cfg.k + 1 > R)
+        copy_nodes(&a->cfg) > R)
         return SWITCHSD_ESHAPE;
     if (a->mode < SWITCHSD_MODE_AUTO || a->mode > SWITCHSD_MODE_SPLIT)
         return SWITCHSD_EINVAL;
@@ -331,11 +353,11 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         !a->dtok || !a->dpar || !a->dn || !a->accept_len || !a->accept_node || !a->bonus ||
         !a->out_tokens)
         return SWITCHSD_EINVAL;
-    if ((rc = check_workspace(workspace, workspace_bytes, B, R)))
-        return rc;
     StepParams p;
     memset(&p, 0, sizeof p);
     fill_cfg(p, &a->cfg);
+    if ((rc = check_workspace(workspace, workspace_bytes, B, R, a->Lmax, p.W)))
+        return rc;
     p.tokens = a->tokens;
     p.lengths = a->lengths;
     p.hidden = a->hidden;
@@ -364,7 +386,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.accept_node = a->accept_node;
     p.bonus = a->bonus;
     p.out_tokens = a->out_tokens;
-    p.ws = carve(workspace, B, R);
+    p.ws = carve(workspace, B, R, a->Lmax, p.W);
     if ((rc = set_scan(p, B, a->Lmax)))
         return rc;
     p.scan_probe = 1;
@@ -372,16 +394,17 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.epi_front = EPI_SELECT;
     p.exp_front = (uint32_t)p.scan_tiles;
 
+    const int64_t cn = copy_nodes(&a->cfg);
     int mode = a->mode;
-    if (mode == SWITCHSD_MODE_AUTO)
-        mode = a->cfg.k + 1 >= R ? SWITCHSD_MODE_FUSED : SWITCHSD_MODE_SPLIT;
+    if (mode == SWITCHSD_MODE_AUTO)  // short drafts that may use every row: one launch
+        mode = cn >= R && R <= 64 ? SWITCHSD_MODE_FUSED : SWITCHSD_MODE_SPLIT;
     if (mode == SWITCHSD_MODE_FUSED) {
         if ((rc = set_segments(p, (int64_t)B * R, V)))
             return rc;
         const int64_t grid = p.n_front_wg + (int64_t)B * R * p.segs;
         if (!grid_ok(grid))
             return SWITCHSD_ESHAPE;
-        p.rows_mode = a->cfg.k + 1 >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;
+        p.rows_mode = cn >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;
         p.epi_accept = 1;
         p.exp_all = p.exp_front + (uint32_t)(R * p.segs);
         return launch_step_kernel(p, grid, stream);
@@ -389,10 +412,24 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     // SPLIT: front (scan + probe + select), then verify over the chosen rows
     if ((rc = launch_step_kernel(p, p.n_front_wg, stream)))
         return rc;
-    // a copy draft uses at most k + 1 of the R rows
+    // a copy draft uses at most 1 + W k of the R rows
     return verify_launch(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
                          a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
-                         workspace_bytes, 2 * (a->cfg.k + 1) >= R, stream);
+                         workspace_bytes, 2 * cn >= R, stream);
+}
+
+int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
+                       uint32_t *mask, hipStream_t stream) {
+    if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R)
+        return SWITCHSD_ESHAPE;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!dn || !mask)
+        return SWITCHSD_EINVAL;
+    const int64_t per = ((int64_t)R * ((R + 31) / 32) + kThreads - 1) / kThreads;
+    if (!grid_ok((int64_t)B * per))
+        return SWITCHSD_ESHAPE;
+    return launch_tree_mask_kernel(dpar, dn, B, R, mask, stream);
 }
 
 }  // extern "C"

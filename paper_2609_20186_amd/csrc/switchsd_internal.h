@@ -20,6 +20,8 @@ constexpr int kScanTile = 4096;
 // one line serialize, and every work-group of a sequence arrives at its line.
 constexpr int kLineU32 = 64;
 constexpr int kLineU64 = 32;
+// Copy candidates per sequence, at most.
+constexpr int kMaxCand = SWITCHSD_MAX_CAND;
 
 enum : int32_t { EPI_NONE = 0, EPI_MATCH = 1, EPI_SELECT = 2 };
 enum : int32_t { ROWS_ALL = 0, ROWS_NEURAL_OR_COPY = 1, ROWS_DRAFT = 2 };
@@ -30,6 +32,10 @@ struct Workspace {
     int32_t *mslot;            // [B] x 256 B: most recent end + 1 per n-gram length
     unsigned long long *keys;  // [B] x key_stride: packed (value key, ~index) row maxima
     int32_t key_stride;        // u64 per sequence (R rounded up to a 256-byte line)
+    int32_t *cand;             // [B] x cand_stride: per scan tile and n-gram length, the
+                               // tile's W most recent ends + 1 (0: none); W > 1 and
+                               // more than one tile only
+    int32_t cand_stride;       // int32 per sequence (whole 256-byte lines)
 };
 
 struct StepParams {
@@ -55,6 +61,7 @@ struct StepParams {
     int32_t kappa;
     int32_t k;
     float theta;
+    int32_t W;  // copy candidates (>= 1)
     // outputs
     int32_t *match_n, *match_end, *copy_len, *copy_tokens;
     float *z;
@@ -80,5 +87,7 @@ struct StepParams {
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_select_kernel(const StepParams &p, hipStream_t stream);
+int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
+                            uint32_t *mask, hipStream_t stream);
 
 }  // namespace switchsd

@@ -43,12 +43,26 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kThreads / 64;
+constexpr int kScanBlocks = kScanTile / kThreads;  // blocks of 64 positions per scan wave
 constexpr uint32_t kNoIdx = 0xFFFFFFFFu;
 
+// Copy candidates being turned into a draft: end, length and first node of
+// candidate c (W > 1).
+struct ChainShared {
+    int32_t e[kMaxCand];
+    int32_t cl[kMaxCand];
+    int32_t st[kMaxCand];
+};
 struct ScanShared {
     int32_t tile[kScanTile + 64];
     int32_t pat[SWITCHSD_MAX_NGRAM_LEN];
     int32_t red[SWITCHSD_MAX_NGRAM];
+    // W > 1: each wave's W most recent ends + 1 per n-gram length, then the
+    // work-group's merged list
+    unsigned long long bm[SWITCHSD_MAX_NGRAM * kWaves * kScanBlocks];  // block masks
+    int32_t cand[SWITCHSD_MAX_NGRAM * kWaves * kMaxCand];
+    int32_t merged[kMaxCand];
+    ChainShared ch;
     double ps[kWaves];  // probe partial sums of the waves (scan tile 0)
     double pc[kWaves];
     int32_t L;
@@ -61,11 +75,11 @@ struct ProbeShared {
     double s[kWaves];
     double c[kWaves];
 };
-struct EpiShared {  // general accept walk, R > 64
+struct EpiShared {  // accept over R > 64 nodes
     int32_t a[SWITCHSD_MAX_R];
     int32_t tok[SWITCHSD_MAX_R];
     int32_t par[SWITCHSD_MAX_R];
-    int32_t dep[SWITCHSD_MAX_R];  // depth if accepted, -1 otherwise
+    uint32_t st[2][SWITCHSD_MAX_R];  // pointer-jumping state, double-buffered (final_epilogue)
 };
 union Shared {
     ScanShared scan;
@@ -258,7 +272,6 @@ struct Prefetch {
 // suffix, and the highest marked lane is the most recent one.  x[e-u] comes
 // from the LDS tile (its 64-position halo covers u < 64), with the 16 blocks'
 // reads issued together: one compare and one 64-bit AND per block and offset.
-constexpr int kScanBlocks = kScanTile / kThreads;  // blocks of 64 positions per wave
 
 __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetch &pre) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -300,6 +313,9 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
         sh.scan.tile[64 * kScanBlocks * wave + 64 * i + lane] = tok[i];
     if (tid < SWITCHSD_MAX_NGRAM)
         sh.scan.red[tid] = 0;
+    if (p.W > 1)
+        for (int i = tid; i < SWITCHSD_MAX_NGRAM * kWaves * kMaxCand; i += kThreads)
+            sh.scan.cand[i] = 0;
     if (tid == 0)
         sh.scan.L = L;
     if (tid < p.nmax)
@@ -348,6 +364,16 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
                 for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
                     if (j == jm)
                         best[j] = e1;
+                if (p.W > 1) {
+                    // keep the block masks of this length for the candidate lists
+                    unsigned long long m = 0ull;
+#pragma unroll
+                    for (int i = 0; i < kScanBlocks; ++i)
+                        if (lane == i)
+                            m = M[i];
+                    if (lane < kScanBlocks)
+                        sh.scan.bm[(jm * kWaves + wave) * kScanBlocks + lane] = m;
+                }
             }
         }
     }
@@ -355,6 +381,31 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
         if (j < p.n_ngram && lane == 0 && best[j] > 0)
             atomicMax(&sh.scan.red[j], best[j]);
+    if (p.W > 1 && elim > 0) {
+        // the wave's W most recent ends per length: lane i < 16 takes block
+        // i's mask and the count of marked ends in later blocks, then lists
+        // its own ends from the highest down
+        for (int j = 0; j < p.n_ngram; ++j) {
+            unsigned long long m =
+                lane < kScanBlocks ? sh.scan.bm[(j * kWaves + wave) * kScanBlocks + lane] : 0ull;
+            const int c0 = __popcll(m);
+            int sfx = c0;  // marked ends in blocks lane..15
+#pragma unroll
+            for (int o = 1; o < kScanBlocks; o <<= 1) {
+                const int y = __shfl_down(sfx, o);
+                if (lane + o < kScanBlocks)
+                    sfx += y;
+            }
+            int r = sfx - c0;
+            int32_t *dst = &sh.scan.cand[(j * kWaves + wave) * kMaxCand];
+            while (m != 0ull && r < p.W) {
+                const int h = 63 - __clzll((long long)m);
+                dst[r] = w0 + 64 * lane + h + 1;
+                m &= ~(1ull << h);
+                ++r;
+            }
+        }
+    }
     __syncthreads();
 }
 
@@ -395,7 +446,8 @@ __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
     if (p.rows_mode == ROWS_DRAFT)
         return (uint32_t)clampi(ld_i32(&p.dn[b]), 1, p.R);
     const int nnb = clampi(p.nn[b], 1, p.R);
-    return (uint32_t)(nnb > p.k + 1 ? nnb : p.k + 1);
+    const int cn = 1 + p.W * p.k;  // the longest copy draft
+    return (uint32_t)(nnb > cn ? nnb : cn);
 }
 
 // One chunk of a segment: vectors [qc0, qc0 + kChunkVecs) of the segment's
@@ -642,13 +694,17 @@ __device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, 
 }
 
 // First length (in the configured order) whose slot holds an occurrence:
-// (match_n, match_end), or (0, -1).  s is lane j's slot value (end + 1).
-__device__ __forceinline__ void pick_match(const StepParams &p, int32_t s, int &mn, int &me) {
+// (match_n, match_end, its index jsel), or (0, -1, -1).  s is lane j's slot
+// value (end + 1).
+__device__ __forceinline__ void pick_match(const StepParams &p, int32_t s, int &mn, int &me,
+                                           int &jsel) {
     const unsigned long long hit = __ballot(s > 0);
     mn = 0;
     me = -1;
+    jsel = -1;
     if (hit) {
         const int j = __ffsll((long long)hit) - 1;
+        jsel = j;
 #pragma unroll
         for (int q = 0; q < SWITCHSD_MAX_NGRAM; ++q)
             if (q == j)
@@ -657,14 +713,119 @@ __device__ __forceinline__ void pick_match(const StepParams &p, int32_t s, int &
     }
 }
 
+// ------------------------------------------------------------- W > 1 copy candidates
+
+// Wave 0: the work-group's W most recent ends + 1 of n-gram length j, merged
+// over its four waves (a higher wave holds later positions).  Lane c < W
+// receives the c-th, 0 past the last occurrence.
+__device__ int merge_waves(const StepParams &p, Shared &sh, int j) {
+    const int lane = threadIdx.x;
+    const int W = p.W;
+    int v = 0;
+    if (lane < kWaves * W) {
+        const int q = lane / W;
+        v = sh.scan.cand[(j * kWaves + (kWaves - 1 - q)) * kMaxCand + (lane - q * W)];
+    }
+    if (lane < W)
+        sh.scan.merged[lane] = 0;
+    const unsigned long long nz = __ballot(v > 0);
+    const int rank = __popcll(nz & ((1ull << lane) - 1ull));
+    if (v > 0 && rank < W)
+        sh.scan.merged[rank] = v;
+    return lane < W ? sh.scan.merged[lane] : 0;
+}
+
+// Wave 0: lays W candidates of lengths cl (lane c) out as chains behind the
+// anchor: ch.cl[c] and ch.st[c] (first node of candidate c).  Returns the node
+// count 1 + sum of the lengths.
+__device__ int chain_layout(const StepParams &p, int cl, ChainShared &ch) {
+    const int lane = threadIdx.x;
+    int inc = cl;  // inclusive prefix sum over lanes 0..W-1 (W <= 16)
+#pragma unroll
+    for (int o = 1; o < kMaxCand; o <<= 1) {
+        const int y = __shfl_up(inc, o);
+        if (lane >= o)
+            inc += y;
+    }
+    if (lane < p.W) {
+        ch.cl[lane] = cl;
+        ch.st[lane] = 1 + inc - cl;
+    }
+    return 1 + __shfl(inc, p.W - 1);
+}
+
+// Wave 0: writes the chosen draft of sequence b (Eq. 4 with the kappa gate);
+// a copy draft is the chains laid out in ch, token j of candidate c being
+// src(c, j).
+template <typename Src>
+__device__ void write_chains(const StepParams &p, int b, int use, int total,
+                             const ChainShared &ch, Src src) {
+    const int lane = threadIdx.x;
+    const int64_t base = (int64_t)b * p.R;
+    const int dnb = use ? total : clampi(p.nn[b], 1, p.R);
+    for (int i = lane; i < p.R; i += 64) {
+        int tok = -1, par = -1;
+        if (i >= 1 && i < dnb) {
+            if (use) {
+                int c = 0;
+                for (int q = 1; q < p.W; ++q)
+                    if (ch.st[q] <= i)
+                        c = q;
+                tok = src(c, i - ch.st[c]);
+                par = i == ch.st[c] ? 0 : i - 1;
+            } else {
+                tok = p.ntok[base + i];
+                par = p.npar ? p.npar[base + i] : i - 1;
+            }
+        }
+        st_i32(&p.dtok[base + i], tok);  // read by the accept epilogue of the same launch
+        st_i32(&p.dpar[base + i], par);
+    }
+    if (lane == 0) {
+        p.use_copy[b] = use;
+        st_i32(&p.dn[b], dnb);
+    }
+}
+
+// Steps 1 and 3 for W > 1 candidates (wave 0).  Lane c < W holds v = end + 1
+// of candidate c (0: none).  Context positions in [lo, hi) are read from this
+// work-group's LDS tile (index = position - t0 + 64), the others from memory.
+__device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L, float zb,
+                               Shared &sh, int t0, int lo, int hi) {
+    const int lane = threadIdx.x;
+    const int W = p.W;
+    const int64_t row = (int64_t)b * p.Lmax;
+    const int cl = (lane < W && v > 0) ? (p.k < L - v ? p.k : L - v) : 0;
+    ChainShared &ch = sh.scan.ch;
+    if (lane < W) {
+        ch.e[lane] = v - 1;
+        p.match_end[(int64_t)b * W + lane] = v - 1;
+        p.copy_len[(int64_t)b * W + lane] = cl;
+    }
+    if (lane == 0)
+        p.match_n[b] = mn;
+    const int total = chain_layout(p, cl, ch);
+    auto src = [&](int c, int j) -> int {
+        const int pos = ch.e[c] + 1 + j;
+        return (pos >= lo && pos < hi) ? sh.scan.tile[pos - t0 + 64] : p.tokens[row + pos];
+    };
+    const int64_t cbase = (int64_t)b * W * p.k;
+    for (int idx = lane; idx < W * p.k; idx += 64) {
+        const int c = idx / p.k, j = idx - c * p.k;
+        p.copy_tokens[cbase + idx] = j < ch.cl[c] ? src(c, j) : -1;
+    }
+    if (p.epi_front == EPI_SELECT)
+        write_chains(p, b, (mn >= p.kappa) && (zb >= p.theta), total, ch, src);
+}
+
 // A context held by one scan tile: everything the switch needs is already in
 // this work-group (match in LDS, probe partial sums in LDS, the copy
 // candidate in the LDS tile, the neural draft prefetched).  No arrival.
 __device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefetch &pre) {
     const int lane = threadIdx.x;
     const int32_t s = lane < p.n_ngram ? sh.scan.red[lane] : 0;
-    int mn, me;
-    pick_match(p, s, mn, me);
+    int mn, me, jsel;
+    pick_match(p, s, mn, me, jsel);
     const int L = sh.scan.L;
     float zb = 0.0f;
     if (p.scan_probe) {
@@ -674,6 +835,11 @@ __device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefet
             p.z[b] = z0;
         }
         zb = __shfl(z0, 0);
+    }
+    if (p.W > 1) {
+        const int v = mn > 0 ? merge_waves(p, sh, jsel) : 0;
+        front_finish_w(p, b, mn, v, L, zb, sh, 0, 0, p.Lmax < kScanTile ? p.Lmax : kScanTile);
+        return;
     }
     const int pos = me + 1 + lane;  // tile index = position + 64 (tile 0)
     const int ct = (mn > 0 && lane < p.k && pos < L) ? sh.scan.tile[pos + 64] : -1;
@@ -691,9 +857,40 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
         st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
     }
     const float zb = p.epi_front == EPI_SELECT ? ld_f32(&p.z[b]) : 0.0f;
-    int mn, me;
-    pick_match(p, s, mn, me);
+    int mn, me, jsel;
+    pick_match(p, s, mn, me, jsel);
     const int L = sh.scan.L;
+    if (p.W > 1) {
+        // the tiles' lists of length jsel, latest tile first: the first W
+        // occurrences in that order are the W most recent
+        const int W = p.W, T = p.scan_tiles;
+        if (lane < W)
+            sh.scan.merged[lane] = 0;
+        if (mn > 0) {
+            const int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride;
+            int cnt = 0;
+            for (int q0 = 0; q0 < T * W && cnt < W; q0 += 64) {
+                const int q = q0 + lane;
+                int v = 0;
+                if (q < T * W) {
+                    const int tq = q / W;
+                    v = ld_i32(&cb[((T - 1 - tq) * SWITCHSD_MAX_NGRAM + jsel) * W + (q - tq * W)]);
+                }
+                const unsigned long long nz = __ballot(v > 0);
+                const int rank = cnt + __popcll(nz & ((1ull << lane) - 1ull));
+                if (v > 0 && rank < W)
+                    sh.scan.merged[rank] = v;
+                cnt += __popcll(nz);
+            }
+        }
+        const int v = lane < W ? sh.scan.merged[lane] : 0;
+        const int t0 = t * kScanTile;
+        front_finish_w(p, b, mn, v, L, zb, sh, t0, t0 - 64 > 0 ? t0 - 64 : 0,
+                       t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax);
+        if (lane == 0)
+            st_u32(&p.ws.tk_front[b * kLineU32], 0u);
+        return;
+    }
     const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
     // this tile's LDS holds positions [t0 - 64, t0 + 4096) (index = position - t0 + 64)
     const int t0 = t * kScanTile;
@@ -803,34 +1000,69 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
                 p.amax[base + i] = a;
         }
         __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_s_waitcnt(0);
-        int best = 0, depth = 0;
-        if (lane == 0) {
-            sh.epi.dep[0] = 0;
-            for (int i = 1; i < dnb; ++i) {
-                const int q = sh.epi.par[i];
-                int d = -1;
-                if (q >= 0 && q < i && sh.epi.dep[q] >= 0 && sh.epi.tok[i] == sh.epi.a[q])
-                    d = sh.epi.dep[q] + 1;
-                sh.epi.dep[i] = d;
-                if (d > depth) {
-                    depth = d;
-                    best = i;
-                }
+        // Pointer jumping over the nodes below dnb.  State of node i: bit 31
+        // = every edge from i up to `anc` holds, bits 16..30 = the number of
+        // those edges, bits 0..15 = anc.  Initially anc is the parent (the
+        // anchor for node 0 and for a node without a valid parent, which also
+        // fails its edge); each round replaces the state by its composition
+        // with the state of anc, doubling the covered path, until every
+        // path reaches the anchor, whose state (holds, 0 edges, itself) is
+        // the identity.
+        for (int i = lane; i < dnb; i += 64) {
+            const int q = sh.epi.par[i];
+            const bool valid = i >= 1 && q >= 0 && q < i;
+            const bool ok = i == 0 || (valid && sh.epi.tok[i] == sh.epi.a[q]);
+            sh.epi.st[0][i] = (ok ? 0x80000000u : 0u) | ((i == 0 ? 0u : 1u) << 16) |
+                              (uint32_t)(valid ? q : 0);
+        }
+        __builtin_amdgcn_wave_barrier();
+        const int rounds = 32 - __clz(dnb - 1);  // 2^rounds >= dnb - 1 edges
+        for (int r = 0; r < rounds; ++r) {
+            const uint32_t *from = sh.epi.st[r & 1];
+            uint32_t *to = sh.epi.st[(r & 1) ^ 1];
+            for (int i = lane; i < dnb; i += 64) {
+                const uint32_t s1 = from[i];
+                const uint32_t s2 = from[s1 & 0xFFFFu];
+                to[i] = (s1 & s2 & 0x80000000u) | ((s1 & 0x7FFF0000u) + (s2 & 0x7FFF0000u)) |
+                        (s2 & 0xFFFFu);
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+        // deepest accepted node, ties to the lowest index
+        uint32_t kb = 0u;
+        for (int i = lane; i < dnb; i += 64) {
+            const uint32_t s1 = sh.epi.st[rounds & 1][i];
+            if (s1 >> 31) {
+                const uint32_t key2 = (((s1 >> 16) & 0x7FFFu) << 16) | (0xFFFFu - (uint32_t)i);
+                kb = key2 > kb ? key2 : kb;
             }
         }
-        best = __shfl(best, 0);
-        depth = __shfl(depth, 0);
+        kb = wave_max_u32(kb);
+        const int best = (int)(0xFFFFu - (kb & 0xFFFFu));
+        const int depth = (int)(kb >> 16);
         const int bon = sh.epi.a[best];
         for (int i = lane; i < p.R; i += 64)
             if (i > depth)
                 p.out_tokens[base + i] = -1;
-        if (lane == 0) {
+        // the path is usually one run of consecutive nodes (a chain, or one
+        // copy candidate): then write it in parallel, else walk it
+        const int first = best - depth + 1;
+        bool bad = false;
+        for (int j = lane; j < depth; j += 64) {
+            const int node = first + j;
+            bad |= node < 1 || sh.epi.par[node] != (j == 0 ? 0 : node - 1);
+        }
+        if (__ballot(bad) == 0ull) {
+            for (int j = lane; j < depth; j += 64)
+                p.out_tokens[base + j] = sh.epi.tok[first + j];
+        } else if (lane == 0) {
             int cur = best;
             for (int pos = depth - 1; pos >= 0; --pos) {
                 p.out_tokens[base + pos] = sh.epi.tok[cur];
                 cur = sh.epi.par[cur];
             }
+        }
+        if (lane == 0) {
             p.out_tokens[base + depth] = bon;
             p.accept_len[b] = depth;
             p.accept_node[b] = best;
@@ -877,6 +1109,15 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
                 atomicMax(&p.ws.mslot[b * kLineU32 + lane], sh.scan.red[lane]);
             if (t == 0 && p.scan_probe && lane == 0)
                 st_f32(&p.z[b], probe_combine(sh.scan.ps, sh.scan.pc, p.bias));
+            if (p.W > 1) {
+                int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride +
+                              (int64_t)t * SWITCHSD_MAX_NGRAM * p.W;
+                for (int j = 0; j < p.n_ngram; ++j) {
+                    const int v = merge_waves(p, sh, j);
+                    if (lane < p.W)
+                        st_i32(&cb[j * p.W + lane], v);
+                }
+            }
             if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front))
                 front_remote(p, b, t, sh, pre);
         }
@@ -889,6 +1130,16 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
 
 __global__ __launch_bounds__(64) void k_select(StepParams p) {
     const int b = blockIdx.x;
+    if (p.W > 1) {
+        __shared__ ChainShared ch;
+        const int lane = threadIdx.x;
+        const int cl = lane < p.W ? clampi(p.copy_len_in[(int64_t)b * p.W + lane], 0, p.k) : 0;
+        const int total = chain_layout(p, cl, ch);
+        const int use = (p.match_n_in[b] >= p.kappa) && (p.z_in[b] >= p.theta);
+        const int32_t *ct = p.copy_tokens_in + (int64_t)b * p.W * p.k;
+        write_chains(p, b, use, total, ch, [&](int c, int j) { return ct[c * p.k + j]; });
+        return;
+    }
     const int mn = p.match_n_in[b];
     const int cl = clampi(p.copy_len_in[b], 0, p.k);
     const float zb = p.z_in[b];
@@ -896,7 +1147,55 @@ __global__ __launch_bounds__(64) void k_select(StepParams p) {
     select_write(p, b, mn, cl, zb, p.copy_tokens_in, (int64_t)b * p.k - 1);
 }
 
+// One work-group of 256 (row, word) cells of sequence b's ancestor mask;
+// dpar of the sequence staged in LDS.  A cell walks its row's path from the
+// node up and keeps the ancestors that fall into its word; indices fall
+// along the path, so the walk stops below the word.
+__global__ __launch_bounds__(kThreads) void k_tree_mask(const int32_t *dpar, const int32_t *dn,
+                                                        int32_t R, int32_t words,
+                                                        int32_t blocks_per_seq,
+                                                        uint32_t *mask) {
+    __shared__ int32_t par[SWITCHSD_MAX_R];
+    const int b = blockIdx.x / blocks_per_seq;
+    const int blk = blockIdx.x - b * blocks_per_seq;
+    const int tid = threadIdx.x;
+    for (int i = tid; i < R; i += kThreads)
+        par[i] = dpar ? dpar[(int64_t)b * R + i] : i - 1;
+    __syncthreads();
+    const int cell = blk * kThreads + tid;
+    if (cell >= R * words)
+        return;
+    const int i = cell / words, w = cell - i * words;
+    const int dnb = clampi(dn[b], 0, R);
+    uint32_t acc = 0u;
+    if (i < dnb && i >= 32 * w) {
+        int node = i;
+        for (;;) {
+            if ((node >> 5) == w)
+                acc |= 1u << (node & 31);
+            if (node == 0)
+                break;
+            const int q = par[node];
+            if (q < 0 || q >= node)
+                break;
+            node = q;
+            if (node < 32 * w)
+                break;
+        }
+    }
+    mask[(int64_t)b * R * words + cell] = acc;
+}
+
 }  // namespace
+
+int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
+                            uint32_t *mask, hipStream_t stream) {
+    const int32_t words = (R + 31) / 32;
+    const int32_t per = (R * words + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(k_tree_mask, dim3((unsigned)((int64_t)B * per)), dim3(kThreads), 0, stream,
+                       dpar, dn, R, words, per, mask);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
     hipLaunchKernelGGL(k_switchsd, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);

@@ -60,6 +60,9 @@ class Workload:
     tree_depth: int = 0
     plant: str = "copy_full_neural_geom"   # | "uniform" | "geom"
     geom_p: float = 0.6
+    n_cand: int = 1              # copy candidates W
+    neural_k: int = 0            # neural chain length (0: k)
+    cand_p: float = 0.5          # accepted copy candidate c: P(c >= j) = cand_p^j
 
     @property
     def chain(self):
@@ -81,6 +84,11 @@ WORKLOADS = {
     "C5": Workload("C5", 5, B=256, L=2048, V=128256, d=4096, k=7, R=60, context="spans",
                    zipf_s=1.1, span_frac=0.2, span_len=(16, 128), draft="tree",
                    tree_nodes=60, tree_depth=7, geom_p=0.6),
+    # the paper's copy setting (W = 10 candidates of D = 20 tokens, Sec. 3.3 and
+    # App. D) on the C2 context and vocabulary, with a 7-token neural chain
+    "C2W10": Workload("C2W10", 6, B=32, L=4096, V=128256, d=4096, k=20, R=201,
+                      context="spans", zipf_s=1.1, span_frac=0.3, span_len=(32, 256),
+                      geom_p=0.6, n_cand=10, neural_k=7),
 }
 
 
@@ -177,12 +185,13 @@ def make_neural_draft(wl, b):
     rng = rng_for(wl, S_DRAFT, b)
     R = wl.R
     ntok = np.full(R, -1, np.int32)
+    kn = wl.neural_k or wl.k
     if wl.draft == "uniform_chain":
-        ntok[1:wl.k + 1] = rng.integers(0, wl.V, wl.k)
-        return ntok, None, wl.k + 1
+        ntok[1:kn + 1] = rng.integers(0, wl.V, kn)
+        return ntok, None, kn + 1
     if wl.draft == "zipf_chain":
-        ntok[1:wl.k + 1] = zipf_tokens(rng, wl.k, wl.zipf_s, wl.V)
-        return ntok, None, wl.k + 1
+        ntok[1:kn + 1] = zipf_tokens(rng, kn, wl.zipf_s, wl.V)
+        return ntok, None, kn + 1
     par = tree_parents(wl).copy()
     n = wl.tree_nodes
     for i in range(1, n):
@@ -259,6 +268,13 @@ def draw_target(wl, b, dpar, dn, use_copy):
     g = int(rng.geometric(1.0 - wl.geom_p)) - 1           # P(g >= j) = p^j
     if wl.plant == "geom":
         steps = g
+    elif use_copy and wl.n_cand > 1:
+        # one candidate accepted in full, the more recent ones more likely
+        starts = _children(dpar, dn, 0)
+        if not starts:
+            return 0
+        c = min(int(rng.geometric(1.0 - wl.cand_p)) - 1, len(starts) - 1)
+        return starts[c + 1] - 1 if c + 1 < len(starts) else last
     elif use_copy:
         return last                                        # copy drafts: accepted in full
     else:

@@ -19,8 +19,8 @@ def say(*a):
     sys.stdout.flush()
 
 
-def ocfg(lens, kappa, k, theta):
-    return oracle.make_cfg(lens, kappa, k, theta)
+def ocfg(lens, kappa, k, theta, n_cand=1):
+    return oracle.make_cfg(lens, kappa, k, theta, n_cand)
 
 
 def planted_workload(name, batch=None):
@@ -28,17 +28,18 @@ def planted_workload(name, batch=None):
     selects (steps 1-3), as the workload recipe prescribes."""
     wl = W.WORKLOADS[name]
     d = W.generate(wl, batch=batch)
-    cfg = ocfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta)
+    cfg = ocfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta, wl.n_cand)
     sel = oracle.front(d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"],
                        d["npar"], d["nn"], cfg)
     d["target"] = W.plant_batch(wl, d, sel)
-    d["cfg"] = dict(lens=wl.ngram_lens, kappa=wl.kappa, k=wl.k, theta=wl.theta)
+    d["cfg"] = dict(lens=wl.ngram_lens, kappa=wl.kappa, k=wl.k, theta=wl.theta,
+                    n_cand=wl.n_cand)
     return d
 
 
 def oracle_step(d, rows=None):
     c = d["cfg"]
-    cfg = ocfg(c["lens"], c["kappa"], c["k"], c["theta"])
+    cfg = ocfg(c["lens"], c["kappa"], c["k"], c["theta"], c.get("n_cand", 1))
     sl = slice(None) if rows is None else rows
     npar = None if d["npar"] is None else d["npar"][sl]
     return oracle.step(d["tokens"][sl], d["lengths"][sl], d["hidden"][sl], d["w"], d["bias"],
@@ -64,16 +65,16 @@ def to_device(d):
 def sd_cfg(d):
     from paper_2609_20186_amd import binding as sd
     c = d["cfg"]
-    return sd.make_cfg(c["lens"], c["kappa"], c["k"], c["theta"])
+    return sd.make_cfg(c["lens"], c["kappa"], c["k"], c["theta"], c.get("n_cand", 1))
 
 
 def gpu_step(dev, d, mode=0, out=None, ws=None):
     import torch
     from paper_2609_20186_amd import binding as sd
     B, R = dev["ntok"].shape
-    k = d["cfg"]["k"]
-    out = out or sd.alloc_outputs(B, R, k)
-    ws = ws if ws is not None else sd.alloc_workspace(B, R)
+    k, W = d["cfg"]["k"], d["cfg"].get("n_cand", 1)
+    out = out or sd.alloc_outputs(B, R, k, W)
+    ws = ws if ws is not None else sd.alloc_workspace(B, R, dev["tokens"].shape[1], W)
     args = sd.build_step_args(dev, out, sd_cfg(d), mode)
     sd.switchsd_step(args, ws)
     torch.cuda.synchronize()
@@ -86,10 +87,10 @@ def gpu_stages(dev, d):
     import torch
     from paper_2609_20186_amd import binding as sd
     B, R = dev["ntok"].shape
-    k = d["cfg"]["k"]
+    k, W = d["cfg"]["k"], d["cfg"].get("n_cand", 1)
     cfg = sd_cfg(d)
-    o = sd.alloc_outputs(B, R, k)
-    ws = sd.alloc_workspace(B, R)
+    o = sd.alloc_outputs(B, R, k, W)
+    ws = sd.alloc_workspace(B, R, dev["tokens"].shape[1], W)
     sd.switchsd_ngram_match(dev["tokens"], dev["lengths"], cfg, o["match_n"], o["match_end"],
                             o["copy_len"], o["copy_tokens"], ws)
     sd.switchsd_probe_score(dev["hidden"], dev["w"], dev["bias"], o["z"])

@@ -24,8 +24,10 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     names = declared_functions()
     assert set(names) >= {"switchsd_ngram_match", "switchsd_probe_score",
-                          "switchsd_select_draft", "switchsd_verify_accept", "switchsd_step",
-                          "switchsd_workspace_bytes", "switchsd_status_string"}
+                          "switchsd_select_draft", "switchsd_verify_accept",
+                          "switchsd_tree_mask", "switchsd_step", "switchsd_workspace_bytes",
+                          "switchsd_status_string"}
+    assert set(names) == set(sd.EXPORTS)
     lib = ctypes.CDLL(sd.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -38,6 +40,12 @@ def test_status_strings_and_workspace_size():
     assert sd.workspace_bytes(32, 8) >= 32 * 8 * 8 + 32 * 8 * 4 + 2 * 32 * 4
     assert sd.workspace_bytes(64, 8) >= sd.workspace_bytes(32, 8)
     assert sd.workspace_bytes(-1, 8) == 0
+    assert sd.workspace_bytes(2, 8, -1, 0) == 0 and sd.workspace_bytes(2, 8, 16, -1) == 0
+    # candidate lists only with several candidates over several 4096-token tiles
+    assert sd.workspace_bytes(2, 8, 4096, 10) == sd.workspace_bytes(2, 8)
+    assert sd.workspace_bytes(2, 8, 4097, 1) == sd.workspace_bytes(2, 8)
+    extra = sd.workspace_bytes(2, 8, 3 * 4096, 10) - sd.workspace_bytes(2, 8)
+    assert extra >= 2 * 3 * 8 * 10 * 4 and extra % 256 == 0
 
 
 # Host buffers stand in for device pointers: every call below fails validation
@@ -66,6 +74,7 @@ def call_step(a, ws=WS, nbytes=4096):
 @pytest.mark.parametrize("kw,code", [
     (dict(B=-1), ESHAPE), (dict(Lmax=0), ESHAPE), (dict(d=-1), ESHAPE), (dict(R=0), ESHAPE),
     (dict(R=2000), ESHAPE), (dict(V=0), ESHAPE), (dict(R=7), ESHAPE),   # k + 1 > R
+    (dict(cfg=sd.make_cfg((3, 2, 1), 1, 7, 0.0, n_cand=2)), ESHAPE),     # 1 + 2 k > R
     (dict(mode=3), EINVAL), (dict(tokens=None), EINVAL), (dict(logits=None), EINVAL),
     (dict(logits=P + 1), EINVAL), (dict(out_tokens=None), EINVAL), (dict(dn=None), EINVAL),
     (dict(hidden=None), EINVAL), (dict(nn=None), EINVAL),
@@ -89,7 +98,8 @@ def test_step_optional_pointers_and_empty_batch():
 @pytest.mark.parametrize("cfg", [
     dict(ngram_lens=(), kappa=1), dict(ngram_lens=(2, 3), kappa=1), dict(ngram_lens=(3, 3)),
     dict(ngram_lens=(65,)), dict(ngram_lens=(0,)), dict(ngram_lens=(3,), kappa=0),
-    dict(ngram_lens=(3,), k=-1),
+    dict(ngram_lens=(3,), k=-1), dict(ngram_lens=(3,), n_cand=-1),
+    dict(ngram_lens=(3,), n_cand=17),
 ])
 def test_bad_cfg(cfg):
     c = sd.make_cfg(**{"kappa": 1, "k": 7, **cfg})
@@ -130,3 +140,16 @@ def test_stage_entry_points_reject():
                                       None) == EINVAL
     assert lib.switchsd_verify_accept(P, 2, 8, 100, P, P, P, P, P, P, P, P, WS, 8,
                                       None) == EWORKSPACE
+    c2 = sd.make_cfg((3, 2, 1), 1, 7, 0.0, n_cand=3)
+    assert lib.switchsd_select_draft(P, P, P, P, P, P, P, 2, 21, ctypes.byref(c2), P, P, P, P,
+                                     None) == ESHAPE           # 1 + W k > R
+    # a multi-candidate match over several tiles needs the candidate lists
+    need1 = sd.workspace_bytes(2, 0, 3 * 4096, 1)
+    assert lib.switchsd_ngram_match(P, P, 2, 3 * 4096, ctypes.byref(c2), P, P, P, P, WS, need1,
+                                    None) == EWORKSPACE
+    assert lib.switchsd_tree_mask(P, P, -1, 8, P, None) == ESHAPE
+    assert lib.switchsd_tree_mask(P, P, 2, 0, P, None) == ESHAPE
+    assert lib.switchsd_tree_mask(P, P, 2, 1025, P, None) == ESHAPE
+    assert lib.switchsd_tree_mask(P, None, 2, 8, P, None) == EINVAL
+    assert lib.switchsd_tree_mask(P, P, 2, 8, None, None) == EINVAL
+    assert lib.switchsd_tree_mask(None, None, 0, 8, None, None) == OK

@@ -88,7 +88,7 @@ SPECIAL = np.array([0x7F80, 0xFF80, 0x7FC0, 0xFFC0, 0x8000, 0x0000, 0x0001], np.
 
 
 def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vocab=None,
-                ragged=True, specials=False, ties=False, repeat_tail=0, plant=False):
+                ragged=True, specials=False, ties=False, repeat_tail=0, plant=False, n_cand=1):
     rng = np.random.default_rng(seed)
     vocab = vocab or V
     tokens = rng.integers(0, vocab, (B, Lmax)).astype(np.int32)
@@ -127,12 +127,12 @@ def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vo
         logits[0, 0, :] = 0x7FC0                            # an all-NaN row
     d_ = {"tokens": tokens, "lengths": lengths, "hidden": hidden, "w": w, "bias": np.float32(0.1),
           "ntok": ntok, "npar": npar, "nn": nn, "logits": logits,
-          "cfg": dict(lens=tuple(lens), kappa=kappa, k=k, theta=theta)}
+          "cfg": dict(lens=tuple(lens), kappa=kappa, k=k, theta=theta, n_cand=n_cand)}
     if plant:
         # plant acceptance up to a random node of the draft the oracle selects
         import oracle
         sel = oracle.front(tokens, lengths, hidden, w, d_["bias"], ntok, npar, nn,
-                           oracle.make_cfg(lens, kappa, k, theta))
+                           oracle.make_cfg(lens, kappa, k, theta, n_cand))
         for b in range(B):
             t = int(rng.integers(0, sel["dn"][b]))
             W.plant(logits[b], sel["dtok"][b], sel["dpar"][b], int(sel["dn"][b]), t)
@@ -170,7 +170,28 @@ CASES = {
                   vocab=3, d=0),
     "d_odd": dict(seed=15, B=3, Lmax=50, V=20, R=3, k=2, lens=(1,), kappa=1, theta=0.0,
                   vocab=3, d=1027),
+    # W copy candidates (Sec. 3.3): W chains behind the anchor
+    "w10_d20_single_tile": dict(seed=40, B=6, Lmax=3000, V=3000, R=204, k=20, lens=(3, 2, 1),
+                                kappa=1, theta=-0.2, vocab=30, n_cand=10, plant=True),
+    "w16_max_ties": dict(seed=41, B=4, Lmax=600, V=500, R=65, k=4, lens=(2, 1), kappa=1,
+                         theta=-np.inf, vocab=6, n_cand=16, ties=True),
+    "w3_short_fused": dict(seed=42, B=8, Lmax=200, V=50, R=16, k=5, lens=(3, 2, 1), kappa=2,
+                           theta=0.0, vocab=4, n_cand=3, plant=True),
+    "w4_tiles_ragged": dict(seed=43, B=5, Lmax=9000, V=70001, R=21, k=5, lens=(3, 2, 1),
+                            kappa=1, theta=0.0, vocab=50, n_cand=4, plant=True),
+    "w10_tree_neural": dict(seed=44, B=5, Lmax=800, V=300, R=120, k=8, lens=(3, 2, 1), kappa=1,
+                            theta=0.0, vocab=8, n_cand=10, tree=True, plant=True),
+    "w2_k0": dict(seed=45, B=3, Lmax=50, V=20, R=2, k=0, lens=(1,), kappa=1, theta=-np.inf,
+                  vocab=3, n_cand=2),
 }
+
+
+def workspace_left_clean(ws, d):
+    """Tickets, slots and row keys are zero again (the candidate lists of long
+    contexts, kept at the end of the workspace, are rewritten before use)."""
+    from paper_2609_20186_amd import binding as sd
+    B, R = d["ntok"].shape
+    return int(ws[:sd.workspace_bytes(B, R)].count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("case", sorted(CASES))
@@ -182,9 +203,104 @@ def test_edge_case_parity(case):
     for mode in (AUTO, FUSED, SPLIT):
         got, ws = gpu_step(dev, d, mode)
         assert_match(got, exp, what=f"{case} mode {mode}")
-        assert int(ws.count_nonzero()) == 0
+        assert workspace_left_clean(ws, d)
     stages, _ = gpu_stages(dev, d)
     assert_match(stages, exp, what=f"{case} stages")
+
+
+def test_multi_candidate_across_tiles():
+    """Occurrences of the suffix 3-gram planted at ends on both sides of the
+    4096-position tile boundaries of a 3-tile context: the W most recent come
+    from different tiles and must be merged latest tile first; a candidate
+    near the end is cut at the context end."""
+    say("[multi] candidates across scan tiles")
+    B, Lmax, Wc, k = 4, 3 * 4096 + 500, 6, 6
+    d = custom_case(seed=46, B=B, Lmax=Lmax, V=1000, R=1 + Wc * k + 2, k=k, lens=(3, 2, 1),
+                    kappa=1, theta=-np.inf, vocab=1 << 20, ragged=False, n_cand=Wc)
+    rng = np.random.default_rng(47)
+    # sequence 2 repeats one token, so its occurrences overlap
+    ends_by_b = [[100, 4094, 4097, 8190, 8193, 12000, Lmax - 4],
+                 [50, 60, 4200],
+                 [4094, 4095, 4096, 4097, 4098, 4099, 4100, 8000],
+                 []]
+    for b, ends in enumerate(ends_by_b):
+        suf = d["tokens"][b, Lmax - 3:].copy() if b != 2 else np.full(3, 777, np.int32)
+        for e in ends:
+            d["tokens"][b, e - 2:e + 1] = suf
+        d["tokens"][b, Lmax - 3:] = suf
+    d["logits"] = W.f32_to_bf16_bits(rng.standard_normal(d["logits"].shape).astype(np.float32))
+    exp = oracle_step(d)
+    assert exp["match_n"][0] == 3 and exp["match_end"][0].tolist() == \
+        [Lmax - 4, 12000, 8193, 8190, 4097, 4094]
+    assert exp["copy_len"][0][0] == 3                       # cut at the context end
+    assert exp["match_end"][2].tolist() == [8000, 4100, 4099, 4098, 4097, 4096]
+    assert exp["match_end"][1].tolist() == [4200, 60, 50, -1, -1, -1]
+    dev = to_device(d)
+    for mode in (AUTO, FUSED, SPLIT):
+        got, ws = gpu_step(dev, d, mode)
+        assert_match(got, exp, what=f"tiles mode {mode}")
+        assert workspace_left_clean(ws, d)
+    stages, _ = gpu_stages(dev, d)
+    assert_match(stages, exp, what="tiles stages")
+
+
+def test_parity_w10_workload_full_size():
+    """The paper's copy setting (W = 10, D = 20) on the C2 context and
+    vocabulary at full size (B = 32, R = 201, V = 128256)."""
+    say("[parity] C2W10 full size")
+    d = planted_workload("C2W10")
+    exp = oracle_step(d)
+    for j in range(len(d["target"])):                      # planted acceptance depth
+        assert exp["accept_len"][j] == W.depth_of(exp["dpar"][j], int(d["target"][j]))
+    dev = to_device(d)
+    got, ws = gpu_step(dev, d, AUTO)
+    assert_match(got, exp, what="C2W10")
+    assert workspace_left_clean(ws, d)
+    say(f"[parity] C2W10: copy on {int(exp['use_copy'].sum())}/32, mean dn "
+        f"{exp['dn'].mean():.1f}, mean accept {exp['accept_len'].mean():.2f}")
+
+
+def test_tree_mask_parity():
+    """The ancestor bit mask against the oracle: random trees with invalid
+    parent links, chains (dpar NULL), ragged dn including 0 and > R, and the
+    W-chain copy drafts of a step."""
+    say("[mask] tree masks")
+    import torch
+    import oracle
+    from paper_2609_20186_amd import binding as sd
+    rng = np.random.default_rng(48)
+    for R in (1, 2, 31, 32, 33, 64, 65, 201, 1024):
+        B = 5
+        words = (R + 31) // 32
+        dpar = np.full((B, R), -1, np.int32)
+        for b in range(B):
+            for i in range(1, R):
+                dpar[b, i] = int(rng.integers(max(0, i - 40), i)) if b != 1 else i - 1
+            if R > 3 and b == 2:
+                dpar[b, R // 2] = int(rng.choice([-1, R // 2, R + 3]))
+        dn = np.array([R, 0, max(1, R // 2), R + 7, 1], np.int32)
+        for use_par in (True, False):
+            exp = np.stack([oracle.tree_mask(dpar[b] if use_par else np.arange(-1, R - 1),
+                                             min(max(int(dn[b]), 0), R), R, words)
+                            for b in range(B)])
+            mask = torch.full((B, R, words), -7, dtype=torch.int32, device="cuda")
+            sd.switchsd_tree_mask(torch.from_numpy(dpar).cuda() if use_par else None,
+                                  torch.from_numpy(dn).cuda(), mask)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(mask.cpu().numpy().view(np.uint32), exp,
+                                          err_msg=f"R={R} dpar={use_par}")
+    # the copy drafts of a multi-candidate step
+    d = custom_case(**CASES["w10_d20_single_tile"])
+    got, _ = gpu_step(to_device(d), d, AUTO)
+    B, R = d["ntok"].shape
+    mask = torch.zeros((B, R, (R + 31) // 32), dtype=torch.int32, device="cuda")
+    sd.switchsd_tree_mask(torch.from_numpy(got["dpar"]).cuda(),
+                          torch.from_numpy(got["dn"]).cuda(), mask)
+    torch.cuda.synchronize()
+    m = mask.cpu().numpy().view(np.uint32)
+    for b in range(B):
+        np.testing.assert_array_equal(m[b], oracle.tree_mask(got["dpar"][b], int(got["dn"][b]),
+                                                             R))
 
 
 def test_misaligned_logits_view():
