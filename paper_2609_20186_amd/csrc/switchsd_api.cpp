@@ -412,10 +412,11 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     // SPLIT: front (scan + probe + select), then verify over the chosen rows
     if ((rc = launch_step_kernel(p, p.n_front_wg, stream)))
         return rc;
-    // a copy draft uses at most 1 + W k of the R rows
+    // rows past a draft are skipped; only short drafts request a row's first
+    // chunk before its need is known
     return verify_launch(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
                          a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
-                         workspace_bytes, 2 * cn >= R, stream);
+                         workspace_bytes, R <= 16, stream);
 }
 
 int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,

@@ -3,11 +3,12 @@
 // One kernel body serves every entry point.  Its work-groups take one of
 // three roles by block index, laid out as [scan tiles | probe | argmax]:
 //
-//   scan    a 4096-position tile of one context, staged in LDS with an
-//           (n_max - 1)-token halo; every lane measures how far the suffix
-//           matches backwards from each of its end positions; the most recent
-//           end per n-gram length is max-reduced over the wave (DPP), the
-//           work-group and (atomicMax) the tiles of the sequence.
+//   scan    a 2048-position tile of one context, staged in LDS with a
+//           64-token halo; ballots over blocks of 64 end positions mark the
+//           occurrences of each suffix n-gram; the most recent end per n-gram
+//           length is max-reduced over the work-group and (atomicMax) the
+//           tiles of the sequence, and with W candidates each wave also lists
+//           its W most recent ends per length, merged latest tile first.
 //           (Sec. 3.3: kappa-gram with a prior occurrence, ranked by recency.)
 //   probe   w . h for one sequence: exact bf16 x float products, summed in
 //           double-double with a fixed reduction order.  (Sec. 3.2, Eq. 3.)
@@ -22,12 +23,12 @@
 //
 // Two last-arriver epilogues close a sequence without a second launch:
 //   front   when its scan tiles and probe are done: pick the match, gather the
-//           copy candidate, apply the switch (Sec. 3.3, Eq. 4) and write the
-//           chosen draft;
+//           copy candidates, apply the switch (Sec. 3.3, Eq. 4) and write the
+//           chosen draft (W candidates: W chains behind the anchor);
 //   final   when every work-group of the sequence is done: decode the row
 //           argmaxes and run the accept walk (Sec. 3.3, Parallel Verification):
-//           a ballot for chains, pointer jumping over the tree, one node per
-//           lane, for trees of up to 64 nodes, a sequential walk beyond.
+//           a ballot for chains and pointer jumping over trees, in registers
+//           (one node per lane) up to 64 nodes and in LDS beyond.
 // Each epilogue resets the workspace slots it consumed, leaving the workspace
 // zeroed for the next call.
 #include <hip/hip_runtime.h>
@@ -63,6 +64,9 @@ struct ScanShared {
     int32_t cand[SWITCHSD_MAX_NGRAM * kWaves * kMaxCand];
     int32_t merged[kMaxCand];
     ChainShared ch;
+    // the neural draft, staged while the scan runs (general select path)
+    int32_t nt[SWITCHSD_MAX_R];
+    int32_t np[SWITCHSD_MAX_R];
     double ps[kWaves];  // probe partial sums of the waves (scan tile 0)
     double pc[kWaves];
     int32_t L;
@@ -249,6 +253,12 @@ __device__ __forceinline__ float probe_combine(const double *ps, const double *p
     return (float)(S + C);
 }
 
+// The chosen draft is written by the general path (LDS-staged neural draft,
+// loops over nodes) rather than one node per lane of wave 0.
+__device__ __forceinline__ bool general_select(const StepParams &p) {
+    return p.W > 1 || p.R > 64 || p.k >= 64;
+}
+
 // The neural draft as handed over, read by wave 0 of a scan work-group before
 // it is needed, so that the switch costs no extra round trip.
 struct Prefetch {
@@ -259,18 +269,19 @@ struct Prefetch {
 
 // ------------------------------------------------------------- scan role
 
-// Tile t of sequence b: end positions e in [t*4096, (t+1)*4096).  Leaves the
-// tile's most recent end + 1 per n-gram length in sh.scan.red, the tokens of
-// positions [t*4096 - 64, t*4096 + 4096) in sh.scan.tile (index = position -
-// t*4096 + 64) and, for tile 0 when the probe rides along, the waves' probe
-// partial sums in sh.scan.ps/pc.
+// Tile t of sequence b: end positions e in [t0, t0 + T) with T = kScanTile
+// and t0 = t*T.  Leaves the tile's most recent end + 1 per n-gram length in
+// sh.scan.red, the tokens of positions [t0 - 64, t0 + T) in sh.scan.tile
+// (index = position - t0 + 64), with W > 1 the W most recent ends + 1 per
+// length and wave in sh.scan.cand and, for tile 0 when the probe rides along,
+// the waves' probe partial sums in sh.scan.ps/pc.
 //
-// Wave w owns the 16 blocks of 64 consecutive positions [t0 + 1024w, +1024),
-// one position per lane.  For suffix offset u, the ballot of
+// Wave w owns the kScanBlocks blocks of 64 consecutive positions starting at
+// t0 + w*T/4, one position per lane.  For suffix offset u, the ballot of
 // (x[e-u] == x[L-1-u]) over a block marks its ends e whose u-th token back
 // matches; AND-ing offsets 0..n-1 marks the ends of occurrences of the n-gram
 // suffix, and the highest marked lane is the most recent one.  x[e-u] comes
-// from the LDS tile (its 64-position halo covers u < 64), with the 16 blocks'
+// from the LDS tile (its 64-position halo covers u < 64), with the blocks'
 // reads issued together: one compare and one 64-bit AND per block and offset.
 
 __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetch &pre) {
@@ -292,12 +303,24 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     const int tp = tid < p.nmax ? tid : 0;
     const int32_t pat_full = p.tokens[row + (p.Lmax - 1 - tp >= 0 ? p.Lmax - 1 - tp : 0)];
     const int L = clampi(p.lengths[b], 0, p.Lmax);
+    const bool stage_neural = p.epi_front == EPI_SELECT && general_select(p);
+    int32_t snt[SWITCHSD_MAX_R / kThreads], snp[SWITCHSD_MAX_R / kThreads];
     if (p.epi_front == EPI_SELECT && tid < 64) {
         const int64_t base = (int64_t)b * p.R;
         const int i = tid < p.R ? tid : 0;
         pre.nnb = clampi(p.nn[b], 1, p.R);
         pre.ntok = p.ntok[base + i];
         pre.npar = p.npar ? p.npar[base + i] : tid - 1;
+    }
+    if (stage_neural) {
+        const int64_t base = (int64_t)b * p.R;
+#pragma unroll
+        for (int q = 0; q < SWITCHSD_MAX_R / kThreads; ++q) {
+            const int i = tid + kThreads * q;
+            const int ic = i < p.R ? i : 0;
+            snt[q] = p.ntok[base + ic];
+            snp[q] = p.npar ? p.npar[base + ic] : i - 1;
+        }
     }
     if (t == 0 && p.scan_probe) {
         double ps, pc;
@@ -311,6 +334,14 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
 #pragma unroll
     for (int i = 0; i <= kScanBlocks; ++i)
         sh.scan.tile[64 * kScanBlocks * wave + 64 * i + lane] = tok[i];
+    if (stage_neural) {
+#pragma unroll
+        for (int q = 0; q < SWITCHSD_MAX_R / kThreads; ++q)
+            if (tid + kThreads * q < p.R) {
+                sh.scan.nt[tid + kThreads * q] = snt[q];
+                sh.scan.np[tid + kThreads * q] = snp[q];
+            }
+    }
     if (tid < SWITCHSD_MAX_NGRAM)
         sh.scan.red[tid] = 0;
     if (p.W > 1)
@@ -339,7 +370,7 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
         const int lx0 = w0 - t0 + 64 + lane;
         for (int u = 0; u < p.nmax; ++u) {
             const int pu = sh.scan.pat[u];
-            // x[e - u] for the 16 blocks: independent LDS reads, issued together
+            // x[e - u] for every block: independent LDS reads, issued together
             int xu[kScanBlocks];
 #pragma unroll
             for (int i = 0; i < kScanBlocks; ++i)
@@ -382,14 +413,14 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
         if (j < p.n_ngram && lane == 0 && best[j] > 0)
             atomicMax(&sh.scan.red[j], best[j]);
     if (p.W > 1 && elim > 0) {
-        // the wave's W most recent ends per length: lane i < 16 takes block
+        // the wave's W most recent ends per length: lane i < kScanBlocks takes block
         // i's mask and the count of marked ends in later blocks, then lists
         // its own ends from the highest down
         for (int j = 0; j < p.n_ngram; ++j) {
             unsigned long long m =
                 lane < kScanBlocks ? sh.scan.bm[(j * kWaves + wave) * kScanBlocks + lane] : 0ull;
             const int c0 = __popcll(m);
-            int sfx = c0;  // marked ends in blocks lane..15
+            int sfx = c0;  // marked ends in blocks lane.. kScanBlocks - 1
 #pragma unroll
             for (int o = 1; o < kScanBlocks; o <<= 1) {
                 const int y = __shfl_down(sfx, o);
@@ -617,35 +648,6 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
 
 // ------------------------------------------------------------- epilogues
 
-// Writes the chosen draft of sequence b (wave 0).  src[off + i] is the i-th
-// copied token (1-based); it is read only for 1 <= i <= copy_len.
-__device__ void select_write(const StepParams &p, int b, int mn, int cl, float zb,
-                             const int32_t *src, int64_t off) {
-    const int lane = threadIdx.x;
-    const int use = (mn >= p.kappa) && (zb >= p.theta);
-    const int nnb = clampi(p.nn[b], 1, p.R);
-    const int dnb = use ? cl + 1 : nnb;
-    const int64_t base = (int64_t)b * p.R;
-    for (int i = lane; i < p.R; i += 64) {
-        int tok = -1, par = -1;
-        if (i >= 1 && i < dnb) {
-            if (use) {
-                tok = src[off + i];
-                par = i - 1;
-            } else {
-                tok = p.ntok[base + i];
-                par = p.npar ? p.npar[base + i] : i - 1;
-            }
-        }
-        st_i32(&p.dtok[base + i], tok);  // read by the accept epilogue of the same launch
-        st_i32(&p.dpar[base + i], par);
-    }
-    if (lane == 0) {
-        p.use_copy[b] = use;
-        st_i32(&p.dn[b], dnb);
-    }
-}
-
 // Steps 1 and 3 for sequence b in wave 0 once the match (mn, me) is known:
 // copy candidate, switch (Eq. 4 with the kappa gate), chosen draft.  When
 // `have_ct`, ct_in is this lane's copied token (read from LDS by the caller);
@@ -662,8 +664,8 @@ __device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, 
         p.match_end[b] = me;
         p.copy_len[b] = cl;
     }
-    if (p.R <= 64 && p.k < 64) {
-        // lane j holds copied token j
+    {
+        // lane j holds copied token j (R <= 64, k < 64, one candidate)
         const int ct = lane < cl ? (have_ct ? ct_in : p.tokens[row + me + 1 + lane]) : -1;
         if (lane < p.k)
             p.copy_tokens[(int64_t)b * p.k + lane] = ct;
@@ -685,11 +687,6 @@ __device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, 
                 st_i32(&p.dn[b], dnb);
             }
         }
-    } else {
-        for (int i = lane; i < p.k; i += 64)
-            p.copy_tokens[(int64_t)b * p.k + i] = i < cl ? p.tokens[row + me + 1 + i] : -1;
-        if (select)  // copied token i (1-based) is x[me + i]
-            select_write(p, b, mn, cl, zb, p.tokens, row + me);
     }
 }
 
@@ -756,13 +753,13 @@ __device__ int chain_layout(const StepParams &p, int cl, ChainShared &ch) {
 
 // Wave 0: writes the chosen draft of sequence b (Eq. 4 with the kappa gate);
 // a copy draft is the chains laid out in ch, token j of candidate c being
-// src(c, j).
-template <typename Src>
-__device__ void write_chains(const StepParams &p, int b, int use, int total,
-                             const ChainShared &ch, Src src) {
+// src(c, j); the neural draft has nnb nodes, node i given by nsrc(i, tok, par).
+template <typename Src, typename NSrc>
+__device__ void write_chains(const StepParams &p, int b, int use, int total, int nnb,
+                             const ChainShared &ch, Src src, NSrc nsrc) {
     const int lane = threadIdx.x;
     const int64_t base = (int64_t)b * p.R;
-    const int dnb = use ? total : clampi(p.nn[b], 1, p.R);
+    const int dnb = use ? total : nnb;
     for (int i = lane; i < p.R; i += 64) {
         int tok = -1, par = -1;
         if (i >= 1 && i < dnb) {
@@ -774,8 +771,7 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total,
                 tok = src(c, i - ch.st[c]);
                 par = i == ch.st[c] ? 0 : i - 1;
             } else {
-                tok = p.ntok[base + i];
-                par = p.npar ? p.npar[base + i] : i - 1;
+                nsrc(i, tok, par);
             }
         }
         st_i32(&p.dtok[base + i], tok);  // read by the accept epilogue of the same launch
@@ -787,11 +783,12 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total,
     }
 }
 
-// Steps 1 and 3 for W > 1 candidates (wave 0).  Lane c < W holds v = end + 1
-// of candidate c (0: none).  Context positions in [lo, hi) are read from this
-// work-group's LDS tile (index = position - t0 + 64), the others from memory.
+// Steps 1 and 3 on the general path (wave 0 of a scan work-group).  Lane
+// c < W holds v = end + 1 of candidate c (0: none).  Context positions in
+// [lo, hi) are read from this work-group's LDS tile (index = position - t0 +
+// 64), the others from memory; the neural draft was staged in LDS.
 __device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L, float zb,
-                               Shared &sh, int t0, int lo, int hi) {
+                               const Prefetch &pre, Shared &sh, int t0, int lo, int hi) {
     const int lane = threadIdx.x;
     const int W = p.W;
     const int64_t row = (int64_t)b * p.Lmax;
@@ -815,7 +812,11 @@ __device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L,
         p.copy_tokens[cbase + idx] = j < ch.cl[c] ? src(c, j) : -1;
     }
     if (p.epi_front == EPI_SELECT)
-        write_chains(p, b, (mn >= p.kappa) && (zb >= p.theta), total, ch, src);
+        write_chains(p, b, (mn >= p.kappa) && (zb >= p.theta), total, pre.nnb, ch, src,
+                     [&](int i, int &tok, int &par) {
+                         tok = sh.scan.nt[i];
+                         par = sh.scan.np[i];
+                     });
 }
 
 // A context held by one scan tile: everything the switch needs is already in
@@ -836,9 +837,10 @@ __device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefet
         }
         zb = __shfl(z0, 0);
     }
-    if (p.W > 1) {
-        const int v = mn > 0 ? merge_waves(p, sh, jsel) : 0;
-        front_finish_w(p, b, mn, v, L, zb, sh, 0, 0, p.Lmax < kScanTile ? p.Lmax : kScanTile);
+    if (general_select(p)) {
+        const int v = mn <= 0 ? 0 : (p.W > 1 ? merge_waves(p, sh, jsel) : (lane == 0 ? me + 1 : 0));
+        front_finish_w(p, b, mn, v, L, zb, pre, sh, 0, 0,
+                       p.Lmax < kScanTile ? p.Lmax : kScanTile);
         return;
     }
     const int pos = me + 1 + lane;  // tile index = position + 64 (tile 0)
@@ -860,13 +862,13 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
     int mn, me, jsel;
     pick_match(p, s, mn, me, jsel);
     const int L = sh.scan.L;
-    if (p.W > 1) {
-        // the tiles' lists of length jsel, latest tile first: the first W
-        // occurrences in that order are the W most recent
+    if (general_select(p)) {
+        // W > 1: the tiles' lists of length jsel, latest tile first: the first
+        // W occurrences in that order are the W most recent
         const int W = p.W, T = p.scan_tiles;
         if (lane < W)
-            sh.scan.merged[lane] = 0;
-        if (mn > 0) {
+            sh.scan.merged[lane] = lane == 0 && mn > 0 ? me + 1 : 0;
+        if (mn > 0 && W > 1) {
             const int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride;
             int cnt = 0;
             for (int q0 = 0; q0 < T * W && cnt < W; q0 += 64) {
@@ -885,14 +887,14 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
         }
         const int v = lane < W ? sh.scan.merged[lane] : 0;
         const int t0 = t * kScanTile;
-        front_finish_w(p, b, mn, v, L, zb, sh, t0, t0 - 64 > 0 ? t0 - 64 : 0,
+        front_finish_w(p, b, mn, v, L, zb, pre, sh, t0, t0 - 64 > 0 ? t0 - 64 : 0,
                        t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax);
         if (lane == 0)
             st_u32(&p.ws.tk_front[b * kLineU32], 0u);
         return;
     }
     const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
-    // this tile's LDS holds positions [t0 - 64, t0 + 4096) (index = position - t0 + 64)
+    // this tile's LDS holds positions [t0 - 64, t0 + T) (index = position - t0 + 64)
     const int t0 = t * kScanTile;
     const int lo = t0 - 64 > 0 ? t0 - 64 : 0;
     const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
@@ -1129,22 +1131,20 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
 }
 
 __global__ __launch_bounds__(64) void k_select(StepParams p) {
+    __shared__ ChainShared ch;
     const int b = blockIdx.x;
-    if (p.W > 1) {
-        __shared__ ChainShared ch;
-        const int lane = threadIdx.x;
-        const int cl = lane < p.W ? clampi(p.copy_len_in[(int64_t)b * p.W + lane], 0, p.k) : 0;
-        const int total = chain_layout(p, cl, ch);
-        const int use = (p.match_n_in[b] >= p.kappa) && (p.z_in[b] >= p.theta);
-        const int32_t *ct = p.copy_tokens_in + (int64_t)b * p.W * p.k;
-        write_chains(p, b, use, total, ch, [&](int c, int j) { return ct[c * p.k + j]; });
-        return;
-    }
-    const int mn = p.match_n_in[b];
-    const int cl = clampi(p.copy_len_in[b], 0, p.k);
-    const float zb = p.z_in[b];
-    // copied token i (1-based) is copy_tokens[b, i-1]
-    select_write(p, b, mn, cl, zb, p.copy_tokens_in, (int64_t)b * p.k - 1);
+    const int lane = threadIdx.x;
+    const int cl = lane < p.W ? clampi(p.copy_len_in[(int64_t)b * p.W + lane], 0, p.k) : 0;
+    const int total = chain_layout(p, cl, ch);
+    const int use = (p.match_n_in[b] >= p.kappa) && (p.z_in[b] >= p.theta);
+    const int32_t *ct = p.copy_tokens_in + (int64_t)b * p.W * p.k;
+    const int64_t base = (int64_t)b * p.R;
+    write_chains(p, b, use, total, clampi(p.nn[b], 1, p.R), ch,
+                 [&](int c, int j) { return ct[c * p.k + j]; },
+                 [&](int i, int &tok, int &par) {
+                     tok = p.ntok[base + i];
+                     par = p.npar ? p.npar[base + i] : i - 1;
+                 });
 }
 
 // One work-group of 256 (row, word) cells of sequence b's ancestor mask;

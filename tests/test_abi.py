@@ -41,10 +41,10 @@ def test_status_strings_and_workspace_size():
     assert sd.workspace_bytes(64, 8) >= sd.workspace_bytes(32, 8)
     assert sd.workspace_bytes(-1, 8) == 0
     assert sd.workspace_bytes(2, 8, -1, 0) == 0 and sd.workspace_bytes(2, 8, 16, -1) == 0
-    # candidate lists only with several candidates over several 4096-token tiles
-    assert sd.workspace_bytes(2, 8, 4096, 10) == sd.workspace_bytes(2, 8)
-    assert sd.workspace_bytes(2, 8, 4097, 1) == sd.workspace_bytes(2, 8)
-    extra = sd.workspace_bytes(2, 8, 3 * 4096, 10) - sd.workspace_bytes(2, 8)
+    # candidate lists only with several candidates over several 2048-token tiles
+    assert sd.workspace_bytes(2, 8, 2048, 10) == sd.workspace_bytes(2, 8)
+    assert sd.workspace_bytes(2, 8, 2049, 1) == sd.workspace_bytes(2, 8)
+    extra = sd.workspace_bytes(2, 8, 3 * 2048, 10) - sd.workspace_bytes(2, 8)
     assert extra >= 2 * 3 * 8 * 10 * 4 and extra % 256 == 0
 
 
@@ -144,8 +144,8 @@ def test_stage_entry_points_reject():
     assert lib.switchsd_select_draft(P, P, P, P, P, P, P, 2, 21, ctypes.byref(c2), P, P, P, P,
                                      None) == ESHAPE           # 1 + W k > R
     # a multi-candidate match over several tiles needs the candidate lists
-    need1 = sd.workspace_bytes(2, 0, 3 * 4096, 1)
-    assert lib.switchsd_ngram_match(P, P, 2, 3 * 4096, ctypes.byref(c2), P, P, P, P, WS, need1,
+    need1 = sd.workspace_bytes(2, 0, 3 * 2048, 1)
+    assert lib.switchsd_ngram_match(P, P, 2, 3 * 2048, ctypes.byref(c2), P, P, P, P, WS, need1,
                                     None) == EWORKSPACE
     assert lib.switchsd_tree_mask(P, P, -1, 8, P, None) == ESHAPE
     assert lib.switchsd_tree_mask(P, P, 2, 0, P, None) == ESHAPE

@@ -94,7 +94,7 @@ def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vo
     tokens = rng.integers(0, vocab, (B, Lmax)).astype(np.int32)
     if repeat_tail:
         # the last `repeat_tail` tokens also occur ending at position 4100, so a
-        # long match straddles the boundary between the first two scan tiles
+        # long match straddles the scan-tile boundary at 4096
         tokens[:, 4101 - repeat_tail:4101] = tokens[:, Lmax - repeat_tail:]
     lengths = np.full(B, Lmax, np.int32)
     if ragged:
@@ -210,9 +210,9 @@ def test_edge_case_parity(case):
 
 def test_multi_candidate_across_tiles():
     """Occurrences of the suffix 3-gram planted at ends on both sides of the
-    4096-position tile boundaries of a 3-tile context: the W most recent come
-    from different tiles and must be merged latest tile first; a candidate
-    near the end is cut at the context end."""
+    scan-tile boundaries (multiples of 2048) of a 12788-token context: the W
+    most recent come from different tiles and must be merged latest tile
+    first; a candidate near the end is cut at the context end."""
     say("[multi] candidates across scan tiles")
     B, Lmax, Wc, k = 4, 3 * 4096 + 500, 6, 6
     d = custom_case(seed=46, B=B, Lmax=Lmax, V=1000, R=1 + Wc * k + 2, k=k, lens=(3, 2, 1),
