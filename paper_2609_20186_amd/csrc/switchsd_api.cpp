@@ -292,11 +292,24 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
     StepParams p;
     memset(&p, 0, sizeof p);
     p.W = 1;
-    if ((rc = set_segments(p, (int64_t)B * R, V)))
-        return rc;
-    const int64_t grid = (int64_t)B * R * p.segs;
-    if (!grid_ok(grid))
-        return SWITCHSD_ESHAPE;
+    int64_t grid = 0;
+    if (R > 64 && B <= kListMaxB && V % 8 == 0 && ((uintptr_t)logits & 15) == 0 &&
+        (int64_t)B * R * ((V / 8 + kChunkVecs - 1) / kChunkVecs) < 0x7FFFFFFFll) {
+        // long drafts use few of their rows: a fixed grid streams the chunks
+        // of the drafted rows, split evenly
+        int cus = 0;
+        if ((rc = cu_count(&cus)))
+            return rc;
+        p.segs = (V / 8 + kChunkVecs - 1) / kChunkVecs;  // chunks per row
+        p.list_mode = 1;
+        grid = 4 * (int64_t)cus;
+    } else {
+        if ((rc = set_segments(p, (int64_t)B * R, V)))
+            return rc;
+        grid = (int64_t)B * R * p.segs;
+        if (!grid_ok(grid))
+            return SWITCHSD_ESHAPE;
+    }
     p.logits = logits;
     p.B = B;
     p.R = R;
@@ -310,8 +323,8 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
     p.out_tokens = out_tokens;
     p.amax = amax;
     p.ws = carve(workspace, B, R, 0, 0);
-    p.rows_mode = ROWS_DRAFT;
-    p.speculate = speculate ? 1 : 0;
+    p.rows_mode = p.list_mode ? ROWS_LISTED : ROWS_DRAFT;
+    p.speculate = speculate && !p.list_mode ? 1 : 0;
     p.epi_accept = 1;
     p.exp_all = (uint32_t)(R * p.segs);
     return launch_step_kernel(p, grid, stream);

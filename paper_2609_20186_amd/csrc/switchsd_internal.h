@@ -24,7 +24,10 @@ constexpr int kLineU64 = 32;
 constexpr int kMaxCand = SWITCHSD_MAX_CAND;
 
 enum : int32_t { EPI_NONE = 0, EPI_MATCH = 1, EPI_SELECT = 2 };
-enum : int32_t { ROWS_ALL = 0, ROWS_NEURAL_OR_COPY = 1, ROWS_DRAFT = 2 };
+enum : int32_t { ROWS_ALL = 0, ROWS_NEURAL_OR_COPY = 1, ROWS_DRAFT = 2, ROWS_LISTED = 3 };
+// Sequences a work-list verify launch handles (its item prefix sums live in
+// four registers per lane).
+constexpr int kListMaxB = 256;
 
 struct Workspace {
     uint32_t *tk_front;        // [B] x 256 B: arrivals of the scan/probe work-groups
@@ -81,6 +84,8 @@ struct StepParams {
     int32_t speculate;   // 1: issue a row's first chunk before reading whether it is needed
     int32_t epi_front;
     int32_t epi_accept;
+    int32_t list_mode;   // 1: verify only, a fixed grid streaming the chunks of the drafted
+                         // rows r < dn[b] (segs = chunks per row)
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all
 };

@@ -155,7 +155,8 @@ __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, uint32_t id, Op 
 }
 __device__ __forceinline__ float wave_max_f32(float v) {
     auto op = [](uint32_t a, uint32_t b) {
-        return __float_as_uint(__builtin_elementwise_maximum(__uint_as_float(a), __uint_as_float(b)));
+        return __float_as_uint(
+            __builtin_elementwise_maximum(__uint_as_float(a), __uint_as_float(b)));
     };
     return __uint_as_float(wave_reduce_u32(__float_as_uint(v), 0xFF800000u, op));
 }
@@ -293,7 +294,8 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     // The tokens, the length, the suffix of a full-length context and the
     // neural draft do not depend on each other: issue all of them at once
     // (indices clamped into range, so that no load sits behind a branch).
-    int32_t tok[kScanBlocks + 1];  // tok[i + 1]: position w0 + 64 i + lane; tok[0]: the block before
+    // tok[i + 1]: position w0 + 64 i + lane; tok[0]: the block before
+    int32_t tok[kScanBlocks + 1];
 #pragma unroll
     for (int i = 0; i <= kScanBlocks; ++i) {
         int x = w0 + 64 * (i - 1) + lane;
@@ -472,7 +474,7 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 }
 
 __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
-    if (p.rows_mode == ROWS_ALL)
+    if (p.rows_mode == ROWS_ALL || p.rows_mode == ROWS_LISTED)
         return (uint32_t)p.R;
     if (p.rows_mode == ROWS_DRAFT)
         return (uint32_t)clampi(ld_i32(&p.dn[b]), 1, p.R);
@@ -990,53 +992,133 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         }
     } else {
         const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
-        for (int i = lane; i < p.R; i += 64) {
-            const unsigned long long key = ld_u64(&keys[i]);
-            if (key)
-                st_u64(&keys[i], 0ull);
-            const int a = i < dnb ? decode_key(key) : -1;
-            sh.epi.a[i] = a;
-            sh.epi.tok[i] = ld_i32(&p.dtok[base + i]);
-            sh.epi.par[i] = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
-            if (p.amax)
-                p.amax[base + i] = a;
+        // the draft and the row maxima into LDS, 256 nodes at a time with all
+        // of their loads in flight together
+        for (int i0 = 0; i0 < p.R; i0 += 4 * 64) {
+            unsigned long long kq[4];
+            int tq[4], pq[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = i0 + lane + 64 * q;
+                kq[q] = 0ull;
+                tq[q] = -1;
+                pq[q] = -1;
+                if (i < p.R) {
+                    kq[q] = ld_u64(&keys[i]);
+                    tq[q] = ld_i32(&p.dtok[base + i]);
+                    pq[q] = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = i0 + lane + 64 * q;
+                if (i < p.R) {
+                    if (kq[q])
+                        st_u64(&keys[i], 0ull);
+                    const int a = i < dnb ? decode_key(kq[q]) : -1;
+                    sh.epi.a[i] = a;
+                    sh.epi.tok[i] = tq[q];
+                    sh.epi.par[i] = pq[q];
+                    if (p.amax)
+                        p.amax[base + i] = a;
+                }
+            }
         }
         __builtin_amdgcn_wave_barrier();
-        // Pointer jumping over the nodes below dnb.  State of node i: bit 31
-        // = every edge from i up to `anc` holds, bits 16..30 = the number of
-        // those edges, bits 0..15 = anc.  Initially anc is the parent (the
-        // anchor for node 0 and for a node without a valid parent, which also
-        // fails its edge); each round replaces the state by its composition
-        // with the state of anc, doubling the covered path, until every
-        // path reaches the anchor, whose state (holds, 0 edges, itself) is
-        // the identity.
+        // key of the deepest accepted node, ties to the lowest index:
+        // (depth << 16) | (0xFFFF - node); the anchor's is 0xFFFF
+        uint32_t kb = lane == 0 ? 0xFFFFu : 0u;
+        bool other = false;  // some node hangs off neither the anchor nor its predecessor
         for (int i = lane; i < dnb; i += 64) {
             const int q = sh.epi.par[i];
-            const bool valid = i >= 1 && q >= 0 && q < i;
-            const bool ok = i == 0 || (valid && sh.epi.tok[i] == sh.epi.a[q]);
-            sh.epi.st[0][i] = (ok ? 0x80000000u : 0u) | ((i == 0 ? 0u : 1u) << 16) |
-                              (uint32_t)(valid ? q : 0);
+            other |= i >= 1 && q != 0 && q != i - 1;
         }
-        __builtin_amdgcn_wave_barrier();
-        const int rounds = 32 - __clz(dnb - 1);  // 2^rounds >= dnb - 1 edges
-        for (int r = 0; r < rounds; ++r) {
-            const uint32_t *from = sh.epi.st[r & 1];
-            uint32_t *to = sh.epi.st[(r & 1) ^ 1];
+        if (__ballot(other) == 0ull) {
+            // Runs of consecutive nodes, each starting at a child of the
+            // anchor (one chain, or W copy candidates): node i is accepted iff
+            // no edge fails between the start of its run and i, and its depth
+            // is its distance to that start.  One ballot pair per 64 nodes.
+            int S = 0, F = -1;  // last run start / failed edge of earlier blocks
+            for (int i0 = 0; i0 < dnb; i0 += 64) {
+                const int i = i0 + lane;
+                bool st = false, fl = false;
+                if (i >= 1 && i < dnb) {
+                    const int q = sh.epi.par[i];
+                    st = q == 0;
+                    fl = sh.epi.tok[i] != sh.epi.a[q];
+                }
+                const unsigned long long sm = __ballot(st), fm = __ballot(fl);
+                const unsigned long long le = lane == 63 ? ~0ull : ((2ull << lane) - 1ull);
+                const int si = (sm & le) ? i0 + 63 - __clzll((long long)(sm & le)) : S;
+                const int fi = (fm & le) ? i0 + 63 - __clzll((long long)(fm & le)) : F;
+                if (i >= 1 && i < dnb && fi < si) {
+                    const uint32_t key2 =
+                        ((uint32_t)(i - si + 1) << 16) | (0xFFFFu - (uint32_t)i);
+                    kb = key2 > kb ? key2 : kb;
+                }
+                if (sm)
+                    S = i0 + 63 - __clzll((long long)sm);
+                if (fm)
+                    F = i0 + 63 - __clzll((long long)fm);
+            }
+        } else {
+            // Pointer jumping over the nodes below dnb.  State of node i: bit 31
+            // = every edge from i up to `anc` holds, bits 16..30 = the number of
+            // those edges, bits 0..15 = anc.  Initially anc is the parent (the
+            // anchor for node 0 and for a node without a valid parent, which also
+            // fails its edge); each round replaces the state by its composition
+            // with the state of anc, doubling the covered path, until every path
+            // reaches the anchor, whose state (holds, 0 edges, itself) is the
+            // identity.
+            bool open = false;  // some path of this lane's nodes not yet at the anchor
             for (int i = lane; i < dnb; i += 64) {
-                const uint32_t s1 = from[i];
-                const uint32_t s2 = from[s1 & 0xFFFFu];
-                to[i] = (s1 & s2 & 0x80000000u) | ((s1 & 0x7FFF0000u) + (s2 & 0x7FFF0000u)) |
-                        (s2 & 0xFFFFu);
+                const int q = sh.epi.par[i];
+                const bool valid = i >= 1 && q >= 0 && q < i;
+                const bool ok = i == 0 || (valid && sh.epi.tok[i] == sh.epi.a[q]);
+                sh.epi.st[0][i] = (ok ? 0x80000000u : 0u) | ((i == 0 ? 0u : 1u) << 16) |
+                                  (uint32_t)(valid ? q : 0);
+                open |= valid && q != 0;
             }
             __builtin_amdgcn_wave_barrier();
-        }
-        // deepest accepted node, ties to the lowest index
-        uint32_t kb = 0u;
-        for (int i = lane; i < dnb; i += 64) {
-            const uint32_t s1 = sh.epi.st[rounds & 1][i];
-            if (s1 >> 31) {
-                const uint32_t key2 = (((s1 >> 16) & 0x7FFFu) << 16) | (0xFFFFu - (uint32_t)i);
-                kb = key2 > kb ? key2 : kb;
+            int cur = 0;
+            while (__ballot(open)) {
+                const uint32_t *from = sh.epi.st[cur];
+                uint32_t *to = sh.epi.st[cur ^ 1];
+                open = false;
+                for (int i0 = 0; i0 < dnb; i0 += 4 * 64) {
+                    uint32_t s1[4], s2[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int i = i0 + lane + 64 * q;
+                        s1[q] = i < dnb ? from[i] : 0u;
+                    }
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        s2[q] = from[s1[q] & 0xFFFFu];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int i = i0 + lane + 64 * q;
+                        if (i < dnb) {
+                            const uint32_t nv =
+                                (s1[q] & s2[q] & 0x80000000u) |
+                                ((s1[q] & 0x7FFF0000u) + (s2[q] & 0x7FFF0000u)) |
+                                (s2[q] & 0xFFFFu);
+                            to[i] = nv;
+                            open |= (nv & 0xFFFFu) != 0u;
+                        }
+                    }
+                }
+                cur ^= 1;
+                __builtin_amdgcn_wave_barrier();
+            }
+            // deepest accepted node
+            for (int i = lane; i < dnb; i += 64) {
+                const uint32_t s1 = sh.epi.st[cur][i];
+                if (s1 >> 31) {
+                    const uint32_t key2 =
+                        (((s1 >> 16) & 0x7FFFu) << 16) | (0xFFFFu - (uint32_t)i);
+                    kb = key2 > kb ? key2 : kb;
+                }
             }
         }
         kb = wave_max_u32(kb);
@@ -1073,6 +1155,130 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
     }
     if (lane == 0)
         st_u32(&p.ws.tk_all[b * kLineU32], 0u);
+}
+
+// ------------------------------------------------------------- streamed verify
+
+// Arrival of n units of work at a ticket expecting `expected` in all (wave 0).
+__device__ __forceinline__ bool arrive_n(uint32_t *ticket, uint32_t n, uint32_t expected) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0);
+    uint32_t old = 0;
+    if (threadIdx.x == 0)
+        old = __hip_atomic_fetch_add(ticket, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    old = __shfl(old, 0);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    return old + n == expected;
+}
+
+// Verify over the drafted rows only, for 16-byte aligned rows (V % 8 == 0 and
+// an aligned tensor).  The units of work are the 16 KB chunks of the rows
+// r < dn[b], sequence by sequence, row by row (p.segs chunks per row); work-
+// group g streams the contiguous units [U g / G, U (g + 1) / G) with the next
+// chunk in flight while one is reduced, across row boundaries.  At the end of
+// a row piece each wave max-combines its (value, index) into the row's key; at
+// the end of a sequence piece the work-group arrives with its unit count, and
+// the last arrival (dn[b] * chunks per row in all) runs the accept epilogue.
+__device__ void verify_stream(const StepParams &p, Shared &sh) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    constexpr int Q = kListMaxB / 64;
+    const int cpr = p.segs;
+    // first unit of sequence b = lane + 64 q (exclusive prefix) and its dn
+    int first[Q], dnq[Q];
+    int carry = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int b = lane + 64 * q;
+        dnq[q] = b < p.B ? clampi(ld_i32(&p.dn[b]), 1, p.R) : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int cnt = dnq[q] * cpr;
+        int inc = cnt;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(inc, o);
+            if (lane >= o)
+                inc += y;
+        }
+        first[q] = carry + inc - cnt;
+        carry += __shfl(inc, 63);
+    }
+    const int64_t U = carry;
+    const int u0 = (int)(U * blockIdx.x / gridDim.x), u1 = (int)(U * (blockIdx.x + 1) / gridDim.x);
+    if (u0 >= u1)
+        return;
+    // coordinates of unit u0: the last sequence starting at or before it
+    int b = 0, fb = 0, dnb = 1;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const unsigned long long m = __ballot(lane + 64 * q < p.B && first[q] <= u0);
+        if (m) {
+            const int l = 63 - __clzll((long long)m);
+            b = 64 * q + l;
+            fb = __shfl(first[q], l);
+            dnb = __shfl(dnq[q], l);
+        }
+    }
+    int r = (u0 - fb) / cpr, c = u0 - fb - r * cpr;
+    const int nq = p.V >> 3;
+    auto row_vecs = [&](int bb, int rr) {
+        return reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)bb * p.R + rr) * p.V);
+    };
+    u32x4 A[kUnroll], Bv[kUnroll];
+    load_chunk(A, row_vecs(b, r), c * kChunkVecs, nq);
+    float runM = -__builtin_inff();
+    uint32_t runI = kNoIdx;
+    int done_b = 0;  // units of sequence b streamed here
+    for (int u = u0; u < u1; ++u) {
+        // the next unit
+        int nb = b, nr = r, nc = c + 1, ndn = dnb;
+        if (nc == cpr) {
+            nc = 0;
+            if (++nr == dnb) {
+                nr = 0;
+                ++nb;
+                if (u + 1 < u1) {  // the next sequence's dn (identical in every lane)
+                    const int q = nb >> 6, l = nb & 63;
+                    int v = 0;
+#pragma unroll
+                    for (int qq = 0; qq < Q; ++qq)
+                        if (qq == q)
+                            v = __shfl(dnq[qq], l);
+                    ndn = v;
+                }
+            }
+        }
+        if (u + 1 < u1)
+            load_chunk(Bv, row_vecs(nb, nr), nc * kChunkVecs, nq);
+        argmax_chunk(A, c * kChunkVecs, nq, 0u, false, 0.0f, 0u, runM, runI);
+        ++done_b;
+        const bool last_unit = u + 1 == u1;
+        if (c == cpr - 1 || last_unit) {  // end of this row's piece
+            if (lane == 0 && runI != kNoIdx) {
+                const unsigned long long key =
+                    ((unsigned long long)order_key(runM) << 32) | (0xFFFFFFFFu - runI);
+                atomicMax(&p.ws.keys[(int64_t)b * p.ws.key_stride + r], key);
+            }
+            runM = -__builtin_inff();
+            runI = kNoIdx;
+        }
+        if (nb != b || last_unit) {  // end of this sequence's piece
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (tid < 64 && arrive_n(&p.ws.tk_all[b * kLineU32], (uint32_t)done_b,
+                                     (uint32_t)(dnb * cpr)))
+                final_epilogue(p, b, sh);
+            done_b = 0;
+        }
+        b = nb;
+        r = nr;
+        c = nc;
+        dnb = ndn;
+#pragma unroll
+        for (int q = 0; q < kUnroll; ++q)
+            A[q] = Bv[q];
+    }
 }
 
 // ------------------------------------------------------------- kernels
@@ -1128,6 +1334,11 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
         if (arrive(&p.ws.tk_all[b * kLineU32], p.exp_all))
             final_epilogue(p, b, sh);
     }
+}
+
+__global__ __launch_bounds__(kThreads) void k_verify_stream(StepParams p) {
+    __shared__ Shared sh;
+    verify_stream(p, sh);
 }
 
 __global__ __launch_bounds__(64) void k_select(StepParams p) {
@@ -1198,7 +1409,10 @@ int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, i
 }
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
-    hipLaunchKernelGGL(k_switchsd, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+    if (p.list_mode)
+        hipLaunchKernelGGL(k_verify_stream, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL(k_switchsd, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 
