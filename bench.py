@@ -10,9 +10,10 @@ shaped copy-heavy batch (B=32, L=4096, V=128256, d=4096, k=7).  Input sets
 are rotated so that more than 512 MB is touched between two uses of one set:
 the 256 MB Infinity Cache cannot serve a step from the previous one.
 
-Prints ONE JSON line (steps/s, ms/step, the fused kernel against the HBM
+Prints ONE JSON line (steps/s, ms/step, the dominant kernel against the HBM
 roofline, the verify-argmax rate, and the CPU oracle timed on a bounded sample
-of the same workload on this host).
+of the same workload on this host).  ``--workload C2W10`` measures the paper's
+multi-candidate copy setting (W = 10 candidates of D = 20 tokens, R = 201).
 """
 import argparse
 import hashlib
@@ -145,7 +146,15 @@ def main():
     sel = plant_with_library(wl, d, sd)
 
     base = upload(d)
-    step_bytes = d["logits"].nbytes + d["tokens"].nbytes + d["hidden"].nbytes
+    # bytes one step reads (the drafted rows for a split step, every row the
+    # fused launch reads otherwise): enough copies that > 512 MB lie between
+    # two uses of one copy
+    cn = 1 + max(1, wl.n_cand) * wl.k
+    if resolve_mode(wl, args.mode) == sd.MODE_FUSED:
+        rows0 = np.maximum(np.clip(d["nn"], 1, wl.R), cn) if cn < wl.R else np.full(wl.B, wl.R)
+    else:
+        rows0 = sel["dn"]
+    step_bytes = int(np.sum(rows0)) * wl.V * 2 + d["tokens"].nbytes + d["hidden"].nbytes
     nrot = max(1, math.ceil(ROTATE_BYTES / step_bytes))
     sets = [base] + [{k: (v.clone() if hasattr(v, "clone") else v) for k, v in base.items()}
                      for _ in range(nrot - 1)]

@@ -6,7 +6,7 @@ import it.  The product path never does, and it shares no code with it.
 
 The arithmetic lives in ``switchsd_oracle.c`` (plain scalar C); this module
 only marshals numpy arrays through ctypes.  Each function cites the passage
-of the paper it follows (see the C source for the readings R1-R8).
+of the paper it follows (see the C source for the readings R1-R8, R13-R15).
 """
 import ctypes
 import os

@@ -23,7 +23,14 @@
  *   R7  node 0 of a draft is the anchor; a node whose parent index is not in
  *       [0, i) is never accepted; among accepted nodes the deepest wins, ties
  *       to the lowest node index;
- *   R8  lengths are clamped to [0, Lmax] and neural node counts to [1, R].
+ *   R8  lengths are clamped to [0, Lmax] and neural node counts to [1, R];
+ *   R13 W candidates are the W largest ends of the matched length, most
+ *       recent first; each is its own chain behind the anchor (no merging of
+ *       equal prefixes); empty slots add no nodes;
+ *   R14 among equally deep accepted nodes the lowest index wins, i.e. the
+ *       most recent candidate;
+ *   R15 the verification mask covers draft nodes only (the prefix, seen by
+ *       every drafted token, is implied); a walk stops at an invalid parent.
  */
 #include "switchsd_oracle.h"
 

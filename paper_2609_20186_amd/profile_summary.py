@@ -2,15 +2,17 @@
 
     python -m paper_2609_20186_amd.profile_summary trace  <dir> <out.md> "<command>"
     python -m paper_2609_20186_amd.profile_summary traffic <fetch_dir> <write_dir> <copy_mb> \\
-        <out.md> <out.json> "<fetch command>" "<write command>"
+        <out.md> <out.json> "<fetch command>" "<write command>" [<workload> <kernel> <label>]
 
 ``trace`` reads a ``--kernel-trace --stats`` run and lists per-kernel
 dispatch counts and durations.  ``traffic`` reads two ``--pmc`` runs
 (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), scales both by what the same
 counters read for the plain device copy of ``copy_mb`` MB that
 ``bench.py --copy-calibration-mb`` runs, and writes the HBM bytes per launch
-of the fused step kernel (with the hash of the kernel source the counters were
-taken on, so that ``bench.py`` drops the figure once the kernel changes).
+of the named kernel (default: the fused step kernel ``k_switchsd`` of C2; the
+largest grid of that kernel dispatched at least 10 times), with the hash of the kernel
+source the counters were taken on, so that ``bench.py`` drops the figure once
+the kernel changes.
 """
 import csv
 import glob
@@ -20,7 +22,6 @@ import os
 import statistics
 import sys
 
-KERNEL = "k_switchsd"
 COPY = "copyBuffer"
 
 
@@ -54,7 +55,7 @@ def trace(d, out, cmd):
              "| kernel | work-groups | dispatches | median us | mean us | min us | max us |",
              "|---|---|---|---|---|---|---|"]
     for (name, wgs), ds in sorted(by.items(), key=lambda kv: -sum(kv[1])):
-        short = name.split("(")[0][-60:]
+        short = name.replace("(anonymous namespace)::", "").split("(")[0][-60:]
         lines.append(f"| `{short}` | {wgs} | {len(ds)} | {statistics.median(ds):.2f} | "
                      f"{statistics.mean(ds):.2f} | {min(ds):.2f} | {max(ds):.2f} |")
     with open(out, "w") as f:
@@ -62,14 +63,14 @@ def trace(d, out, cmd):
     print("\n".join(lines))
 
 
-def _counter(d, counter):
+def _counter(d, counter, kernel):
     rows = _rows(d, "*counter_collection.csv")
     k, c = [], []
     for r in rows:
         if r.get("Counter_Name") != counter:
             continue
         v = float(r["Counter_Value"])
-        if KERNEL in r["Kernel_Name"]:
+        if kernel + "(" in r["Kernel_Name"] or r["Kernel_Name"].endswith(kernel):
             grid = int(r.get("Grid_Size", 0) or 0)
             k.append((grid, v))
         elif COPY in r["Kernel_Name"]:
@@ -77,15 +78,17 @@ def _counter(d, counter):
     return k, c
 
 
-def traffic(fdir, wdir, copy_mb, out_md, out_json, fcmd, wcmd):
+def traffic(fdir, wdir, copy_mb, out_md, out_json, fcmd, wcmd, workload="C2",
+            kernel="k_switchsd", label="fused step kernel"):
     copy_bytes = copy_mb << 20
-    kf, cf = _counter(fdir, "FETCH_SIZE")
-    kw, cw = _counter(wdir, "WRITE_SIZE")
-    # the fused step kernel is the most frequent grid of the benchmark
+    kf, cf = _counter(fdir, "FETCH_SIZE", kernel)
+    kw, cw = _counter(wdir, "WRITE_SIZE", kernel)
+    # the kernel's largest grid dispatched at least 10 times: the timed launch
+    # (the fused step is larger than the benchmark's verify-only launches)
     grids = {}
     for g, _ in kf:
         grids[g] = grids.get(g, 0) + 1
-    g = max(grids, key=grids.get)
+    g = max(gg for gg, n in grids.items() if n >= 10)
     fetch_kib = statistics.median([v for gg, v in kf if gg == g])
     write_kib = statistics.median([v for gg, v in kw if gg == g])
     copy_fetch = statistics.median(sorted(cf)[-5:])   # the large calibration copies
@@ -94,18 +97,18 @@ def traffic(fdir, wdir, copy_mb, out_md, out_json, fcmd, wcmd):
     sw = copy_write * 1024 / copy_bytes
     fetch_b = fetch_kib * 1024 / sf
     write_b = write_kib * 1024 / sw
-    res = {"workload": "C2", "kernel_sha": kernel_sha(), "grid_threads": g,
+    res = {"workload": workload, "kernel": kernel, "kernel_sha": kernel_sha(), "grid_threads": g,
            "fetch_kib_per_launch": fetch_kib, "write_kib_per_launch": write_kib,
            "copy_mb": copy_mb, "copy_fetch_kib": copy_fetch, "copy_write_kib": copy_write,
            "fetch_scale": sf, "write_scale": sw,
            "hbm_bytes_per_launch": int(round(fetch_b + write_b))}
     with open(out_json, "w") as f:
         json.dump(res, f, indent=1)
-    lines = [f"# HBM traffic: fused step kernel, C2 (B=32, V=128256)", "",
+    lines = [f"# HBM traffic: {label} (`{kernel}`), {workload}", "",
              f"FETCH_SIZE command: `{fcmd}`", "", f"WRITE_SIZE command: `{wcmd}`", "",
              "| quantity | value |", "|---|---|",
-             f"| fused step kernel FETCH_SIZE per dispatch | {fetch_kib:.0f} KiB |",
-             f"| fused step kernel WRITE_SIZE per dispatch | {write_kib:.1f} KiB |",
+             f"| {label} FETCH_SIZE per dispatch | {fetch_kib:.0f} KiB |",
+             f"| {label} WRITE_SIZE per dispatch | {write_kib:.1f} KiB |",
              f"| plain copy of {copy_mb} MB: FETCH_SIZE | {copy_fetch:.0f} KiB (scale {sf:.4f}) |",
              f"| plain copy of {copy_mb} MB: WRITE_SIZE | {copy_write:.0f} KiB (scale {sw:.4f}) |",
              f"| scaled HBM bytes per launch (read + write) | {fetch_b + write_b:,.0f} B |",
@@ -120,4 +123,4 @@ if __name__ == "__main__":
         trace(sys.argv[2], sys.argv[3], sys.argv[4])
     else:
         traffic(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5], sys.argv[6],
-                sys.argv[7], sys.argv[8])
+                sys.argv[7], sys.argv[8], *sys.argv[9:12])
