@@ -65,7 +65,13 @@ def _load():
         _lib.oracle_accept.argtypes = [P, P, i32, P, i32, P, P, P, P]
         _lib.oracle_tree_mask.argtypes = [P, i32, i32, i32, P]
         _lib.oracle_step.argtypes = [i32, i32, i32, i32, i32] + [P] * 4 + [ctypes.c_float] + \
-            [P] * 5 + [P] * 14 + [i32]
+            [P] * 5 + [P] * 14 + [ctypes.c_float, P, i32]
+        _lib.oracle_sample_scale.argtypes = [ctypes.c_float]
+        _lib.oracle_sample_scale.restype = ctypes.c_float
+        _lib.oracle_sample_weight.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float]
+        _lib.oracle_sample_weight.restype = ctypes.c_uint32
+        _lib.oracle_sample_row.argtypes = [P, i32, ctypes.c_float, ctypes.c_uint32]
+        _lib.oracle_sample_row.restype = i32
         _lib.oracle_step.restype = i32
     return _lib
 
@@ -132,6 +138,24 @@ def argmax_row(row_bf16):
     return int(lib.oracle_argmax_row(_p(r), int(r.size)))
 
 
+def sample_scale(temperature):
+    """c = log2(e) / T rounded to float (App. A, sampling temperature)."""
+    return np.float32(_load().oracle_sample_scale(float(temperature)))
+
+
+def sample_weight(l, m, c):
+    """Fixed-point weight trunc(2^20 * 2^((l - m) c)) of one logit (see the C source)."""
+    return int(_load().oracle_sample_weight(float(l), float(m), float(c)))
+
+
+def sample_row(row_bf16, temperature, u):
+    """Token drawn from softmax(l / T) by inverse CDF with the 32-bit uniform u."""
+    lib = _load()
+    r = _c(row_bf16, np.uint16)
+    return int(lib.oracle_sample_row(_p(r), int(r.size), float(sample_scale(temperature)),
+                                     int(u)))
+
+
 def accept(dtok, dpar, dn, amax, R):
     """Step 4b (Sec. 3.3): deepest accepted node, its path and the bonus."""
     lib = _load()
@@ -165,12 +189,15 @@ STEP_OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_cop
                 "out_tokens")
 
 
-def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=1):
+def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=1,
+         temperature=0.0, uniforms=None):
     """The whole step for B sequences (steps 1-4 in the paper's order).
 
     tokens [B,Lmax] int32, lengths [B] int32, hidden [B,d] bf16 bits (uint16),
     w [d] float32, ntok/npar [B,R] int32 (npar None = chains), nn [B] int32,
-    logits [B,R,V] bf16 bits (uint16).  Returns a dict of numpy outputs.
+    logits [B,R,V] bf16 bits (uint16).  temperature > 0 draws each row's
+    token with uniforms [B,R] uint32 (App. A); amax then holds the drawn
+    tokens.  Returns a dict of numpy outputs.
     """
     lib = _load()
     tokens = _c(tokens, np.int32)
@@ -198,9 +225,13 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=
         "accept_len": np.zeros(B, np.int32), "accept_node": np.zeros(B, np.int32),
         "bonus": np.zeros(B, np.int32), "out_tokens": np.zeros((B, R), np.int32),
     }
+    un = _c(uniforms, np.uint32) if uniforms is not None else None
+    if temperature > 0:
+        assert un is not None and un.size == B * R
     rc = lib.oracle_step(B, Lmax, d, R, V, _p(tokens), _p(lengths), _p(hidden), _p(w),
                          float(bias), _p(ntok), _p(npar_a), _p(nn), _p(logits),
-                         ctypes.byref(cfg), *[_p(o[k]) for k in STEP_OUTPUTS], int(threads))
+                         ctypes.byref(cfg), *[_p(o[k]) for k in STEP_OUTPUTS],
+                         float(temperature), _p(un), int(threads))
     if rc != 0:
         raise ValueError("oracle_step rejected its arguments")
     o["copy_tokens"] = o["copy_tokens"][:, :, :K]

@@ -176,6 +176,72 @@ int32_t oracle_argmax_row(const uint16_t *row_bf16, int32_t V)
     return best < 0 ? 0 : best;
 }
 
+/* Step 4a at T > 0 -- App. A measures SwitchSD at sampling temperatures
+ * T > 0 with standard speculative sampling.  The drafts here are tokens (copy
+ * candidates are deterministic; neural drafts come without their
+ * distribution), so the draft distribution is one-hot, and the
+ * speculative-sampling rule (accept token x with probability p(x) / q(x),
+ * else draw from the normalized residual max(0, p - q)) yields the same
+ * distribution of the emitted token as drawing y from p and accepting x iff
+ * x == y.  p = softmax(l / T) is realized with fixed-point weights (see the
+ * header) so that the draw is exact integer arithmetic. */
+float oracle_sample_scale(float temperature)
+{
+    return (float)(1.4426950408889634 / (double)temperature);
+}
+
+/* 2^t for t in [-24, 0] as 2^k * P(f), k = rint(t), f = t - k in
+ * [-1/2, 1/2] (exact), P(f) = sum_n (f ln 2)^n / n! up to n = 6, evaluated by
+ * Horner's rule with one rounding per step (fused multiply-add); the weight is
+ * that value times 2^20, truncated to an integer. */
+uint32_t oracle_sample_weight(float l, float m, float c)
+{
+    const float t = (l - m) * c;
+    if (!(t >= -24.0f))
+        return 0u;
+    const float k = rintf(t);
+    const float f = t - k;
+    float p = 0x1.430912p-13f;          /* ln2^6 / 6! */
+    p = fmaf(p, f, 0x1.5d87fep-10f);    /* ln2^5 / 5! */
+    p = fmaf(p, f, 0x1.3b2ab6p-7f);     /* ln2^4 / 4! */
+    p = fmaf(p, f, 0x1.c6b08ep-5f);     /* ln2^3 / 3! */
+    p = fmaf(p, f, 0x1.ebfbe0p-3f);     /* ln2^2 / 2! */
+    p = fmaf(p, f, 0x1.62e430p-1f);     /* ln2 */
+    p = fmaf(p, f, 1.0f);
+    return (uint32_t)ldexpf(p, (int)k + 20);
+}
+
+int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint32_t u)
+{
+    float m = 0.0f;
+    int have = 0;
+    for (int32_t v = 0; v < V; ++v) {
+        const float f = bf16_to_float(row_bf16[v]);
+        if (isnan(f))
+            continue;
+        if (!have || f > m)
+            m = f;
+        have = 1;
+    }
+    if (!have || !isfinite(m))
+        return oracle_argmax_row(row_bf16, V);
+    uint64_t Z = 0;
+    for (int32_t v = 0; v < V; ++v) {
+        const float f = bf16_to_float(row_bf16[v]);
+        Z += isnan(f) ? 0u : oracle_sample_weight(f, m, c);
+    }
+    /* floor(u * Z / 2^32) in exact integer arithmetic */
+    const uint64_t target = (uint64_t)u * (Z >> 32) + (((uint64_t)u * (Z & 0xFFFFFFFFu)) >> 32);
+    uint64_t prefix = 0;
+    for (int32_t v = 0; v < V; ++v) {
+        const float f = bf16_to_float(row_bf16[v]);
+        prefix += isnan(f) ? 0u : oracle_sample_weight(f, m, c);
+        if (prefix > target)
+            return v;
+    }
+    return V - 1; /* not reached: target < Z */
+}
+
 /* Step 4b -- Sec. 3.3 (select the longest validated continuation): a node is
  * accepted when its parent is accepted and its token equals the target's
  * choice at the parent.  The result is the deepest accepted node, the tokens
@@ -255,6 +321,8 @@ typedef struct {
     float *z;
     int32_t *use_copy, *dtok, *dpar, *dn, *amax;
     int32_t *accept_len, *accept_node, *bonus, *out_tokens;
+    float temperature;
+    const uint32_t *uniforms;
 } step_job;
 
 static void step_range(const step_job *j)
@@ -276,9 +344,16 @@ static void step_range(const step_job *j)
                                        j->npar ? j->npar + b * R : NULL, j->nn[b], j->R,
                                        j->cfg, j->dtok + b * R, j->dpar + b * R, &j->dn[b]);
         int32_t *am = j->amax + b * R;
-        for (int32_t r = 0; r < j->R; ++r)
-            am[r] = r < j->dn[b] ? oracle_argmax_row(j->logits + ((int64_t)b * R + r) * V, j->V)
-                                 : -1;
+        const float c = j->temperature > 0.0f ? oracle_sample_scale(j->temperature) : 0.0f;
+        for (int32_t r = 0; r < j->R; ++r) {
+            const uint16_t *row = j->logits + ((int64_t)b * R + r) * V;
+            if (r >= j->dn[b])
+                am[r] = -1;
+            else if (j->temperature > 0.0f)
+                am[r] = oracle_sample_row(row, j->V, c, j->uniforms[b * R + r]);
+            else
+                am[r] = oracle_argmax_row(row, j->V);
+        }
         oracle_accept(j->dtok + b * R, j->dpar + b * R, j->dn[b], am, j->R,
                       &j->accept_len[b], &j->accept_node[b], &j->bonus[b],
                       j->out_tokens + b * R);
@@ -300,12 +375,15 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 int32_t *copy_tokens, float *z, int32_t *use_copy,
                 int32_t *dtok, int32_t *dpar, int32_t *dn, int32_t *amax,
                 int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
-                int32_t *out_tokens, int32_t threads)
+                int32_t *out_tokens, float temperature, const uint32_t *uniforms,
+                int32_t threads)
 {
     if (B < 0 || Lmax < 1 || d < 0 || R < 1 || V < 1 || !cfg || cfg->k < 0 ||
         n_cand_of(cfg) * cfg->k + 1 > R)
         return -1;
     if (cfg->n_ngram < 1 || cfg->n_ngram > ORACLE_MAX_NGRAM)
+        return -1;
+    if (temperature > 0.0f && !uniforms)
         return -1;
     if (threads < 1)
         threads = 1;
@@ -313,7 +391,8 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
         threads = B > 0 ? B : 1;
     step_job base = {0, 0, Lmax, d, R, V, tokens, lengths, hidden, w, bias, ntok, npar, nn,
                      logits, cfg, match_n, match_end, copy_len, copy_tokens, z, use_copy,
-                     dtok, dpar, dn, amax, accept_len, accept_node, bonus, out_tokens};
+                     dtok, dpar, dn, amax, accept_len, accept_node, bonus, out_tokens,
+                     temperature, uniforms};
     if (threads == 1) {
         base.b0 = 0;
         base.b1 = B;

@@ -64,6 +64,25 @@ int32_t oracle_select(int32_t match_n, const int32_t *copy_len, const int32_t *c
 /* Step 4a: lowest index of the largest bf16 value of one row. */
 int32_t oracle_argmax_row(const uint16_t *row_bf16, int32_t V);
 
+/* Step 4a at T > 0 (App. A, sampling temperature; deterministic drafts, so
+ * the draft distribution is one-hot and speculative sampling reduces to: draw
+ * the target's token y from softmax(l / T) at the parent, accept the child iff
+ * its token is y).  The draw is an inverse-CDF sample over fixed-point
+ * weights, so that the decision is exact integer arithmetic:
+ *   c   = (float)(log2(e) / T)                     (oracle_sample_scale)
+ *   m   = the largest non-NaN value of the row
+ *   t_j = (l_j - m) * c  in float; w_j = 0 unless t_j >= -24, else
+ *   w_j = trunc(2^(t_j) * 2^20) with 2^(t_j) evaluated as 2^k * P(t_j - k),
+ *         k = rint(t_j), P the degree-6 Taylor polynomial of 2^f, Horner in
+ *         float with fused multiply-adds                 (oracle_sample_weight)
+ *   Z   = sum_j w_j (exact, 64-bit); target = floor(u * Z / 2^32)
+ *   y   = the smallest j with w_0 + ... + w_j > target.
+ * A row whose maximum is not finite (all NaN, -inf or +inf present) takes the
+ * greedy choice. */
+float oracle_sample_scale(float temperature);
+uint32_t oracle_sample_weight(float l, float m, float c);
+int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint32_t u);
+
 /* Step 4b: accept walk over a chosen draft given the argmax of every
  * draft row.  Writes accept_len, accept_node, bonus and out_tokens[R]. */
 void oracle_accept(const int32_t *dtok, const int32_t *dpar, int32_t dn,
@@ -82,6 +101,9 @@ void oracle_tree_mask(const int32_t *dpar, int32_t dn, int32_t R, int32_t words,
  * POSIX threads (sequences are independent).  npar may be NULL (chains).
  * amax [B,R] receives the argmax of rows r < dn[b] and -1 elsewhere.
  * match_end and copy_len are [B,W], copy_tokens [B,W,k] (W = max(1, n_cand)).
+ * temperature > 0 draws each row's token with oracle_sample_row and
+ * uniforms[b,r] (amax then holds the drawn tokens); temperature <= 0 is the
+ * greedy step and uniforms may be NULL.
  * Returns 0, or -1 on a bad argument. */
 int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 const int32_t *tokens, const int32_t *lengths,
@@ -92,7 +114,8 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 int32_t *copy_tokens, float *z, int32_t *use_copy,
                 int32_t *dtok, int32_t *dpar, int32_t *dn, int32_t *amax,
                 int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
-                int32_t *out_tokens, int32_t threads);
+                int32_t *out_tokens, float temperature, const uint32_t *uniforms,
+                int32_t threads);
 
 #ifdef __cplusplus
 }
