@@ -22,8 +22,9 @@ MODE_AUTO, MODE_FUSED, MODE_SPLIT = 0, 1, 2
 STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE"}
 
 EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
-           "switchsd_verify_accept", "switchsd_tree_mask", "switchsd_step",
-           "switchsd_workspace_bytes", "switchsd_status_string")
+           "switchsd_verify_accept", "switchsd_verify_sample", "switchsd_tree_mask",
+           "switchsd_step", "switchsd_workspace_bytes", "switchsd_sample_workspace_bytes",
+           "switchsd_status_string")
 
 
 class SwitchsdError(RuntimeError):
@@ -66,7 +67,8 @@ class StepArgs(ctypes.Structure):
                 ("match_n", _P), ("match_end", _P), ("copy_len", _P), ("copy_tokens", _P),
                 ("z", _P), ("use_copy", _P), ("dtok", _P), ("dpar", _P), ("dn", _P),
                 ("amax", _P), ("accept_len", _P), ("accept_node", _P), ("bonus", _P),
-                ("out_tokens", _P)]
+                ("out_tokens", _P), ("temperature", ctypes.c_float), ("uniforms", _P),
+                ("sample_workspace", _P), ("sample_workspace_bytes", ctypes.c_size_t)]
 
 
 def _load():
@@ -82,6 +84,10 @@ def _load():
     lib.switchsd_verify_accept.argtypes = [_P, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                            S, _P]
     lib.switchsd_tree_mask.argtypes = [_P, _P, _I, _I, _P, _P]
+    lib.switchsd_verify_sample.argtypes = [_P, _I, _I, _I, ctypes.c_float, _P, _P, _P, _P, _P,
+                                           _P, _P, _P, _P, _P, S, _P, S, _P]
+    lib.switchsd_sample_workspace_bytes.argtypes = [_I, _I, _I]
+    lib.switchsd_sample_workspace_bytes.restype = S
     lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
     lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
     lib.switchsd_workspace_bytes.restype = S
@@ -101,6 +107,10 @@ def status_string(status):
 
 def workspace_bytes(B, R, Lmax=0, n_cand=0):
     return int(lib.switchsd_workspace_bytes(int(B), int(R), int(Lmax), int(n_cand)))
+
+
+def sample_workspace_bytes(B, R, V):
+    return int(lib.switchsd_sample_workspace_bytes(int(B), int(R), int(V)))
 
 
 _DT = {"i32": (torch.int32,), "f32": (torch.float32,),
@@ -172,6 +182,22 @@ def switchsd_verify_accept(logits, dtok, dpar, dn, accept_len, accept_node, bonu
         workspace.numel(), _stream(stream)))
 
 
+def switchsd_verify_sample(logits, temperature, uniforms, dtok, dpar, dn, accept_len,
+                           accept_node, bonus, out_tokens, amax, workspace, sample_workspace,
+                           stream=None):
+    """uniforms: uint32 (or int32 holding the same bits) [B, R]."""
+    B, R, V = logits.shape
+    _check("switchsd_verify_sample", lib.switchsd_verify_sample(
+        _ptr(logits, "bf16", "logits"), B, R, V, float(temperature),
+        _ptr(uniforms, "u32", "uniforms"), _ptr(dtok, "i32", "dtok"),
+        _ptr(dpar, "i32", "dpar", True), _ptr(dn, "i32", "dn"),
+        _ptr(accept_len, "i32", "accept_len"), _ptr(accept_node, "i32", "accept_node"),
+        _ptr(bonus, "i32", "bonus"), _ptr(out_tokens, "i32", "out_tokens"),
+        _ptr(amax, "i32", "amax", True), _ptr(workspace, "u8", "workspace"),
+        workspace.numel(), _ptr(sample_workspace, "u8", "sample_workspace"),
+        sample_workspace.numel(), _stream(stream)))
+
+
 def switchsd_tree_mask(dpar, dn, mask, stream=None):
     """mask: uint32 (or int32 holding the same bits) [B, R, (R + 31) // 32]."""
     B, R = mask.shape[0], mask.shape[1]
@@ -201,16 +227,24 @@ def alloc_outputs(B, R, k, n_cand=1, device="cuda"):
             "out_tokens": torch.empty((B, R), **i32)}
 
 
+def alloc_sample_workspace(B, R, V, device="cuda"):
+    return torch.empty(max(sample_workspace_bytes(B, R, V), 256), dtype=torch.uint8,
+                       device=device)
+
+
 def alloc_workspace(B, R, Lmax=0, n_cand=0, device="cuda"):
     """Zeroed once here; the kernels keep it usable for every later call."""
     return torch.zeros(max(workspace_bytes(B, R, Lmax, n_cand), 256), dtype=torch.uint8,
                        device=device)
 
 
-def build_step_args(inp, out, cfg, mode=MODE_AUTO):
+def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=None,
+                    sample_workspace=None):
     """StepArgs for switchsd_step.  ``inp`` holds device tensors tokens [B,Lmax],
     lengths [B], hidden [B,d], w [d], ntok [B,R], npar [B,R] or None, nn [B],
-    logits [B,R,V] and the float ``bias``; ``out`` is from alloc_outputs."""
+    logits [B,R,V] and the float ``bias``; ``out`` is from alloc_outputs.
+    temperature > 0 draws the rows' tokens with ``uniforms`` [B,R] (uint32
+    bits) and ``sample_workspace`` (alloc_sample_workspace)."""
     tokens, logits, hidden = inp["tokens"], inp["logits"], inp["hidden"]
     B, Lmax = tokens.shape
     R, V = logits.shape[1], logits.shape[2]
@@ -230,6 +264,11 @@ def build_step_args(inp, out, cfg, mode=MODE_AUTO):
     for name in OUTPUTS:
         setattr(a, name, _ptr(out[name], "f32" if name == "z" else "i32", name,
                               optional=(name == "amax" or name == "copy_tokens")))
+    a.temperature = float(temperature)
+    if temperature != 0.0:
+        a.uniforms = _ptr(uniforms, "u32", "uniforms")
+        a.sample_workspace = _ptr(sample_workspace, "u8", "sample_workspace")
+        a.sample_workspace_bytes = sample_workspace.numel()
     return a
 
 

@@ -272,13 +272,68 @@ int switchsd_select_draft(const int32_t *match_n, const int32_t *copy_len,
 
 namespace {
 
-// Verify launch shared by the entry point and the split step.  `speculate`:
+// Arguments of a verification at T > 0.
+struct SampleArgs {
+    float temperature;
+    const uint32_t *uniforms;
+    void *ws;
+    size_t bytes;
+};
+
+int64_t chunks_per_row(int32_t V) { return ((int64_t)V / 8 + kChunkVecs - 1) / kChunkVecs; }
+
+int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_t R, int32_t V) {
+    if (!(sa->temperature > 0.0f) || !isfinite(sa->temperature) || !sa->uniforms)
+        return SWITCHSD_EINVAL;
+    if (V % 8 != 0 || ((uintptr_t)logits & 15))
+        return SWITCHSD_EINVAL;
+    if (chunks_per_row(V) * (kThreads / 64) > kThreads)
+        return SWITCHSD_ESHAPE;
+    if (!sa->ws || ((uintptr_t)sa->ws & (kAlign - 1)) ||
+        sa->bytes < switchsd_sample_workspace_bytes(B, R, V))
+        return SWITCHSD_EWORKSPACE;
+    return SWITCHSD_OK;
+}
+
+// After the row maxima are in the row keys: the weight-sum launch and the pick
+// launch (which runs the accept epilogue).  `p` carries the rows, the draft,
+// the outputs and the carved workspace.
+int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_t stream) {
+    int cus = 0;
+    int rc = cu_count(&cus);
+    if (rc)
+        return rc;
+    p.list_mode = 0;
+    p.uniforms = sa->uniforms;
+    p.samp_c = (float)(1.4426950408889634 / (double)sa->temperature);
+    p.csum = (uint32_t *)sa->ws;
+    p.cpr = (int32_t)chunks_per_row(p.V);
+    const int64_t rows = (int64_t)p.B * p.R;
+    int64_t segs = (2 * (int64_t)cus + rows - 1) / rows;
+    if (segs > p.cpr)
+        segs = p.cpr;
+    if (segs < 1)
+        segs = 1;
+    p.seg_chunks = (int32_t)((p.cpr + segs - 1) / segs);
+    p.segs = (int32_t)((p.cpr + p.seg_chunks - 1) / p.seg_chunks);
+    p.speculate = speculate ? 1 : 0;
+    const int64_t grid = rows * p.segs;
+    if (!grid_ok(grid) || !grid_ok(rows))
+        return SWITCHSD_ESHAPE;
+    if ((rc = launch_sample_sums_kernel(p, grid, stream)))
+        return rc;
+    return launch_sample_pick_kernel(p, stream);
+}
+
+// Verify launch shared by the entry points and the split step.  `speculate`:
 // most rows of the drafts are expected to be read (chains), so a row's first
-// chunk is requested before its need is known.
+// chunk is requested before its need is known.  With `sa`, the launch only
+// leaves the row maxima and the draw at T > 0 follows.
 int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const int32_t *dtok,
                   const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
                   int32_t *accept_node, int32_t *bonus, int32_t *out_tokens, int32_t *amax,
-                  void *workspace, size_t workspace_bytes, bool speculate, hipStream_t stream) {
+                  void *workspace, size_t workspace_bytes, bool speculate,
+                  const SampleArgs *sa, hipStream_t stream) {
     if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || V < 1)
         return SWITCHSD_ESHAPE;
     if (B == 0)
@@ -288,6 +343,8 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
         return SWITCHSD_EINVAL;
     int rc = check_workspace(workspace, workspace_bytes, B, R, 0, 0);
     if (rc)
+        return rc;
+    if (sa && (rc = check_sample(sa, logits, B, R, V)))
         return rc;
     StepParams p;
     memset(&p, 0, sizeof p);
@@ -325,9 +382,11 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
     p.ws = carve(workspace, B, R, 0, 0);
     p.rows_mode = p.list_mode ? ROWS_LISTED : ROWS_DRAFT;
     p.speculate = speculate && !p.list_mode ? 1 : 0;
-    p.epi_accept = 1;
+    p.epi_accept = sa ? 0 : 1;
     p.exp_all = (uint32_t)(R * p.segs);
-    return launch_step_kernel(p, grid, stream);
+    if ((rc = launch_step_kernel(p, grid, stream)) || !sa)
+        return rc;
+    return sample_finish(p, sa, speculate, stream);
 }
 
 }  // namespace
@@ -342,7 +401,28 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
     // chains and short drafts usually use every row
     const bool speculate = dpar == nullptr || R <= 16;
     return verify_launch(logits, B, R, V, dtok, dpar, dn, accept_len, accept_node, bonus,
-                         out_tokens, amax, workspace, workspace_bytes, speculate, stream);
+                         out_tokens, amax, workspace, workspace_bytes, speculate, nullptr,
+                         stream);
+}
+
+int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
+                           float temperature, const uint32_t *uniforms, const int32_t *dtok,
+                           const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
+                           int32_t *accept_node, int32_t *bonus, int32_t *out_tokens,
+                           int32_t *amax, void *workspace, size_t workspace_bytes,
+                           void *sample_workspace, size_t sample_workspace_bytes,
+                           hipStream_t stream) {
+    const SampleArgs sa = {temperature, uniforms, sample_workspace, sample_workspace_bytes};
+    const bool speculate = dpar == nullptr || R <= 16;
+    return verify_launch(logits, B, R, V, dtok, dpar, dn, accept_len, accept_node, bonus,
+                         out_tokens, amax, workspace, workspace_bytes, speculate, &sa, stream);
+}
+
+size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
+    if (B < 0 || R < 0 || V < 0)
+        return 0;
+    const size_t n = (size_t)B * R * chunks_per_row(V) * (kThreads / 64) * 4;
+    return (n + kAlign - 1) / kAlign * kAlign;
 }
 
 int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace_bytes,
@@ -370,6 +450,11 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     memset(&p, 0, sizeof p);
     fill_cfg(p, &a->cfg);
     if ((rc = check_workspace(workspace, workspace_bytes, B, R, a->Lmax, p.W)))
+        return rc;
+    const bool sampled = a->temperature != 0.0f;
+    const SampleArgs sa = {a->temperature, a->uniforms, a->sample_workspace,
+                           a->sample_workspace_bytes};
+    if (sampled && (rc = check_sample(&sa, a->logits, B, R, V)))
         return rc;
     p.tokens = a->tokens;
     p.lengths = a->lengths;
@@ -418,9 +503,11 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         if (!grid_ok(grid))
             return SWITCHSD_ESHAPE;
         p.rows_mode = cn >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;
-        p.epi_accept = 1;
+        p.epi_accept = sampled ? 0 : 1;
         p.exp_all = p.exp_front + (uint32_t)(R * p.segs);
-        return launch_step_kernel(p, grid, stream);
+        if ((rc = launch_step_kernel(p, grid, stream)) || !sampled)
+            return rc;
+        return sample_finish(p, &sa, true, stream);
     }
     // SPLIT: front (scan + probe + select), then verify over the chosen rows
     if ((rc = launch_step_kernel(p, p.n_front_wg, stream)))
@@ -429,7 +516,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     // chunk before its need is known
     return verify_launch(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
                          a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
-                         workspace_bytes, R <= 16, stream);
+                         workspace_bytes, R <= 16, sampled ? &sa : nullptr, stream);
 }
 
 int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,

@@ -86,12 +86,20 @@ struct StepParams {
     int32_t epi_accept;
     int32_t list_mode;   // 1: verify only, a fixed grid streaming the chunks of the drafted
                          // rows r < dn[b] (segs = chunks per row)
+    // draws at T > 0 (sum and pick launches)
+    const uint32_t *uniforms;  // [B, R]
+    float samp_c;              // log2(e) / T
+    uint32_t *csum;            // [B, R, cpr, waves] fixed-point weight sums per chunk
+    int32_t cpr;               // 16 KB chunks per row
+    int32_t seg_chunks;        // chunks per work-group of the sum launch
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all
 };
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_select_kernel(const StepParams &p, hipStream_t stream);
+int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
+int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream);
 int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                             uint32_t *mask, hipStream_t stream);
 

@@ -85,11 +85,19 @@ struct EpiShared {  // accept over R > 64 nodes
     int32_t par[SWITCHSD_MAX_R];
     uint32_t st[2][SWITCHSD_MAX_R];  // pointer-jumping state, double-buffered (final_epilogue)
 };
+struct PickShared {  // one row's draw at T > 0
+    uint32_t cw[kThreads];             // per-chunk, per-wave weight sums
+    uint32_t tot[kWaves][kUnroll];     // per-wave totals of the chosen chunk's vector blocks
+    uint32_t wsum[kWaves];             // per-wave totals within the chosen block
+    unsigned long long target;         // remaining target inside the chosen chunk / block
+    int32_t cstar, ustar, qstar, y;
+};
 union Shared {
     ScanShared scan;
     ArgmaxShared am;
     ProbeShared probe;
     EpiShared epi;
+    PickShared pick;
 };
 
 // ------------------------------------------------------------- atomics
@@ -1263,7 +1271,7 @@ __device__ void verify_stream(const StepParams &p, Shared &sh) {
             runM = -__builtin_inff();
             runI = kNoIdx;
         }
-        if (nb != b || last_unit) {  // end of this sequence's piece
+        if ((nb != b || last_unit) && p.epi_accept) {  // end of this sequence's piece
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid < 64 && arrive_n(&p.ws.tk_all[b * kLineU32], (uint32_t)done_b,
@@ -1279,6 +1287,242 @@ __device__ void verify_stream(const StepParams &p, Shared &sh) {
         for (int q = 0; q < kUnroll; ++q)
             A[q] = Bv[q];
     }
+}
+
+// ------------------------------------------------------------- draws at T > 0
+
+// Sampling temperature T > 0 (App. A).  The drafts are tokens, so the draft
+// distribution is one-hot and speculative sampling emits the same token
+// distribution as: draw y from softmax(l / T) at each drafted row, accept a
+// child iff its token is y.  The draw is an inverse-CDF sample with the row's
+// uniform over fixed-point weights w_j = trunc(2^20 * 2^((l_j - m) c)),
+// c = log2(e) / T, m the row maximum, so that the sums are exact integers and
+// the drawn index does not depend on the reduction order.  Three launches
+// after the draft is chosen: the row maxima (the greedy argmax pass), the
+// per-chunk weight sums, and the pick, which also closes the sequence with the
+// accept epilogue.
+
+// The row's maximum from its packed argmax key; false when the row has no
+// finite maximum (no key: every value NaN; -inf; +inf present), and then the
+// row keeps the greedy choice.
+__device__ __forceinline__ bool key_max(unsigned long long key, float &m) {
+    if (!key)
+        return false;
+    const uint32_t k = (uint32_t)(key >> 32);
+    m = __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+    return __builtin_isfinite(m);
+}
+
+// 2^t for t = (l - m) c in [-24, 0] as 2^k * P(t - k), k = rint(t), with P
+// the degree-6 Taylor polynomial of 2^f = e^(f ln 2) on [-1/2, 1/2] by
+// Horner's rule in fused multiply-adds; the weight is that times 2^20,
+// truncated.  0 unless t >= -24 (so NaN and -inf weigh nothing).
+__device__ __forceinline__ uint32_t samp_weight(float l, float m, float c) {
+    const float t = (l - m) * c;
+    const bool on = t >= -24.0f;
+    const float tc = on ? t : 0.0f;
+    const float k = __builtin_rintf(tc);
+    const float f = tc - k;
+    float q = 0x1.430912p-13f;               // ln2^6 / 6!
+    q = __builtin_fmaf(q, f, 0x1.5d87fep-10f);  // ln2^5 / 5!
+    q = __builtin_fmaf(q, f, 0x1.3b2ab6p-7f);   // ln2^4 / 4!
+    q = __builtin_fmaf(q, f, 0x1.c6b08ep-5f);   // ln2^3 / 3!
+    q = __builtin_fmaf(q, f, 0x1.ebfbe0p-3f);   // ln2^2 / 2!
+    q = __builtin_fmaf(q, f, 0x1.62e430p-1f);   // ln2
+    q = __builtin_fmaf(q, f, 1.0f);
+    const uint32_t w = (uint32_t)__builtin_ldexpf(q, (int)k + 20);
+    return on ? w : 0u;
+}
+
+// Weight sum of the 8 elements of one 16-byte vector (< 2^24).
+__device__ __forceinline__ uint32_t vec_weight(const u32x4 &v, float m, float c) {
+    uint32_t s = 0;
+#pragma unroll
+    for (int w4 = 0; w4 < 4; ++w4)
+        s += samp_weight(lo_f(v[w4]), m, c) + samp_weight(hi_f(v[w4]), m, c);
+    return s;
+}
+
+// Sum launch: work-group (row, segment) adds up the weights of each 16 KB
+// chunk of its segment, per wave (a wave's chunk share is < 2^32).  Rows at
+// and beyond dn and rows without a finite maximum are skipped.
+__global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int rowi = blockIdx.x / p.segs;
+    const int s = blockIdx.x - rowi * p.segs;
+    const int b = rowi / p.R, r = rowi - b * p.R;
+    const int nq = p.V >> 3;
+    const int c0 = s * p.seg_chunks;
+    const int c1 = c0 + p.seg_chunks < p.cpr ? c0 + p.seg_chunks : p.cpr;
+    if (c0 >= c1)
+        return;
+    const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
+    u32x4 A[kUnroll], Bv[kUnroll];
+    if (p.speculate)
+        load_chunk(A, vp, c0 * kChunkVecs, nq);
+    float m = 0.0f;
+    if (r >= clampi(ld_i32(&p.dn[b]), 1, p.R) ||
+        !key_max(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]), m)) {
+        __builtin_amdgcn_s_waitcnt(0);
+        return;
+    }
+    if (!p.speculate)
+        load_chunk(A, vp, c0 * kChunkVecs, nq);
+    uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+    for (int c = c0; c < c1; ++c) {
+        if (c + 1 < c1)
+            load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
+        uint32_t sum = 0;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (c * kChunkVecs + u * kThreads + tid < nq)
+                sum += vec_weight(A[u], m, p.samp_c);
+        sum = wave_reduce_u32(sum, 0u, [](uint32_t a, uint32_t x) { return a + x; });
+        if (lane == 0)
+            cs[c * kWaves + wave] = sum;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            A[u] = Bv[u];
+    }
+}
+
+// floor(u * Z / 2^32), exactly.
+__device__ __forceinline__ unsigned long long scaled_target(uint32_t u, unsigned long long Z) {
+    return (unsigned long long)u * (Z >> 32) +
+           (((unsigned long long)u * (Z & 0xFFFFFFFFull)) >> 32);
+}
+
+// Pick launch: one work-group per row.  The draw is the smallest index j with
+// w_0 + ... + w_j > floor(u Z / 2^32): the chunk from the chunk sums, the
+// vector block (256 vectors) and vector from the re-read chunk, the element
+// within the vector.  The drawn token replaces the row's argmax key; then the
+// row arrives at its sequence, and the last row runs the accept epilogue.
+__global__ __launch_bounds__(kThreads) void k_sample_pick(StepParams p) {
+    __shared__ Shared sh;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int b = blockIdx.x / p.R, r = blockIdx.x - b * p.R;
+    unsigned long long *keyp = &p.ws.keys[(int64_t)b * p.ws.key_stride + r];
+    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    float m = 0.0f;
+    if (r < dnb && key_max(ld_u64(keyp), m)) {
+        const uint32_t uni = p.uniforms[(int64_t)b * p.R + r];
+        const uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+        sh.pick.cw[tid] = tid < p.cpr * kWaves ? cs[tid] : 0u;
+        __syncthreads();
+        if (wave == 0) {
+            // chunk totals, their inclusive prefix, the target and its chunk
+            unsigned long long cc = 0;
+            if (lane < p.cpr)
+                cc = (unsigned long long)sh.pick.cw[4 * lane] + sh.pick.cw[4 * lane + 1] +
+                     sh.pick.cw[4 * lane + 2] + sh.pick.cw[4 * lane + 3];
+            unsigned long long inc = cc;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const unsigned long long y = __shfl_up(inc, o);
+                if (lane >= o)
+                    inc += y;
+            }
+            const unsigned long long Z = __shfl(inc, 63);
+            const unsigned long long target = scaled_target(uni, Z);
+            const unsigned long long hit = __ballot(lane < p.cpr && inc > target);
+            const int cst = __ffsll((long long)hit) - 1;  // exists: target < Z
+            const unsigned long long before = __shfl(inc - cc, cst);
+            if (lane == 0) {
+                sh.pick.cstar = cst;
+                sh.pick.target = target - before;
+            }
+        }
+        __syncthreads();
+        const int cst = sh.pick.cstar;
+        const int nq = p.V >> 3;
+        const u32x4 *vp =
+            reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
+        u32x4 A[kUnroll];
+        load_chunk(A, vp, cst * kChunkVecs, nq);
+        uint32_t vs[kUnroll];  // weight of vector q = chunk start + u * 256 + tid
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            vs[u] = cst * kChunkVecs + u * kThreads + tid < nq ? vec_weight(A[u], m, p.samp_c)
+                                                                : 0u;
+        // totals of the four blocks of 256 vectors (each < 2^32)
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint32_t t = wave_reduce_u32(vs[u], 0u, [](uint32_t a, uint32_t x) { return a + x; });
+            if (lane == 0)
+                sh.pick.tot[wave][u] = t;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            unsigned long long tg = sh.pick.target;
+            int us = kUnroll - 1;
+            for (int u = 0; u < kUnroll; ++u) {
+                const unsigned long long t = (unsigned long long)sh.pick.tot[0][u] +
+                                             sh.pick.tot[1][u] + sh.pick.tot[2][u] +
+                                             sh.pick.tot[3][u];
+                if (tg < t) {
+                    us = u;
+                    break;
+                }
+                tg -= t;
+            }
+            sh.pick.ustar = us;
+            sh.pick.target = tg;
+            sh.pick.qstar = kThreads;
+        }
+        __syncthreads();
+        // within the block: inclusive prefix over the 256 vectors in order
+        const int us = sh.pick.ustar;
+        uint32_t mine = 0;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (u == us)
+                mine = vs[u];
+        uint32_t inc = mine;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = __shfl_up(inc, o);
+            if (lane >= o)
+                inc += y;
+        }
+        if (lane == 63)
+            sh.pick.wsum[wave] = inc;
+        __syncthreads();
+        unsigned long long off = 0;
+        for (int w = 0; w < wave; ++w)
+            off += sh.pick.wsum[w];
+        const unsigned long long tg = sh.pick.target;
+        const unsigned long long hit = __ballot(off + inc > tg);
+        if (hit && lane == __ffsll((long long)hit) - 1)
+            atomicMin(&sh.pick.qstar, tid);
+        __syncthreads();
+        if (tid == sh.pick.qstar) {
+            // the element within this thread's vector
+            unsigned long long run = off + inc - mine;
+            const int q = cst * kChunkVecs + us * kThreads + tid;
+            u32x4 v = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                if (u == us)
+                    v = A[u];
+            int e = 7;
+            for (int j = 0; j < 8; ++j) {
+                const uint32_t x = v[j >> 1];
+                run += samp_weight((j & 1) ? hi_f(x) : lo_f(x), m, p.samp_c);
+                if (run > tg) {
+                    e = j;
+                    break;
+                }
+            }
+            sh.pick.y = q * 8 + e;
+        }
+        __syncthreads();
+        if (tid == 0)
+            st_u64(keyp, (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)sh.pick.y));
+    }
+    if (tid >= 64)
+        return;
+    if (arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)p.R))
+        final_epilogue(p, b, sh);
 }
 
 // ------------------------------------------------------------- kernels
@@ -1413,6 +1657,17 @@ int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
         hipLaunchKernelGGL(k_verify_stream, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
     else
         hipLaunchKernelGGL(k_switchsd, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
+    hipLaunchKernelGGL(k_sample_sums, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream) {
+    hipLaunchKernelGGL(k_sample_pick, dim3((unsigned)((int64_t)p.B * p.R)), dim3(kThreads), 0,
+                       stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 

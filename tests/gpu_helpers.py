@@ -42,9 +42,11 @@ def oracle_step(d, rows=None):
     cfg = ocfg(c["lens"], c["kappa"], c["k"], c["theta"], c.get("n_cand", 1))
     sl = slice(None) if rows is None else rows
     npar = None if d["npar"] is None else d["npar"][sl]
+    T = d.get("T", 0.0)
+    un = d["uniforms"][sl] if T > 0 else None
     return oracle.step(d["tokens"][sl], d["lengths"][sl], d["hidden"][sl], d["w"], d["bias"],
                        d["ntok"][sl], npar, d["nn"][sl], d["logits"][sl], cfg,
-                       threads=ORACLE_THREADS)
+                       threads=ORACLE_THREADS, temperature=T, uniforms=un)
 
 
 def to_device(d):
@@ -59,7 +61,19 @@ def to_device(d):
            "nn": torch.from_numpy(np.ascontiguousarray(d["nn"])).cuda(),
            "logits": torch.from_numpy(np.ascontiguousarray(d["logits"]).view(np.int16)).cuda(),
            "bias": float(d["bias"])}
+    if d.get("T", 0.0) > 0:
+        dev["uniforms"] = torch.from_numpy(
+            np.ascontiguousarray(d["uniforms"], dtype=np.uint32).view(np.int32)).cuda()
     return dev
+
+
+def with_temperature(d, T, seed):
+    """The same inputs at sampling temperature T with seeded row uniforms."""
+    d = dict(d)
+    d["T"] = float(T)
+    B, R = d["ntok"].shape
+    d["uniforms"] = np.random.default_rng(seed).integers(0, 2 ** 32, (B, R), dtype=np.uint32)
+    return d
 
 
 def sd_cfg(d):
@@ -75,7 +89,9 @@ def gpu_step(dev, d, mode=0, out=None, ws=None):
     k, W = d["cfg"]["k"], d["cfg"].get("n_cand", 1)
     out = out or sd.alloc_outputs(B, R, k, W)
     ws = ws if ws is not None else sd.alloc_workspace(B, R, dev["tokens"].shape[1], W)
-    args = sd.build_step_args(dev, out, sd_cfg(d), mode)
+    T = d.get("T", 0.0)
+    sws = sd.alloc_sample_workspace(B, R, dev["logits"].shape[2]) if T > 0 else None
+    args = sd.build_step_args(dev, out, sd_cfg(d), mode, T, dev.get("uniforms"), sws)
     sd.switchsd_step(args, ws)
     torch.cuda.synchronize()
     res = {k2: v.cpu().numpy() for k2, v in out.items()}
@@ -97,8 +113,16 @@ def gpu_stages(dev, d):
     sd.switchsd_select_draft(o["match_n"], o["copy_len"], o["copy_tokens"], o["z"], dev["ntok"],
                              dev["npar"], dev["nn"], cfg, o["use_copy"], o["dtok"], o["dpar"],
                              o["dn"])
-    sd.switchsd_verify_accept(dev["logits"], o["dtok"], o["dpar"], o["dn"], o["accept_len"],
-                              o["accept_node"], o["bonus"], o["out_tokens"], o["amax"], ws)
+    T = d.get("T", 0.0)
+    if T > 0:
+        sd.switchsd_verify_sample(dev["logits"], T, dev["uniforms"], o["dtok"], o["dpar"],
+                                  o["dn"], o["accept_len"], o["accept_node"], o["bonus"],
+                                  o["out_tokens"], o["amax"], ws,
+                                  sd.alloc_sample_workspace(B, R, dev["logits"].shape[2]))
+    else:
+        sd.switchsd_verify_accept(dev["logits"], o["dtok"], o["dpar"], o["dn"],
+                                  o["accept_len"], o["accept_node"], o["bonus"],
+                                  o["out_tokens"], o["amax"], ws)
     torch.cuda.synchronize()
     return {k2: v.cpu().numpy() for k2, v in o.items()}, ws
 

@@ -58,7 +58,8 @@ WS = (P + 255) & ~255
 def step_args(**kw):
     a = sd.StepArgs()
     for f, _ in sd.StepArgs._fields_:
-        if f not in ("B", "Lmax", "d", "R", "V", "bias", "cfg", "mode"):
+        if f not in ("B", "Lmax", "d", "R", "V", "bias", "cfg", "mode", "temperature",
+                     "uniforms", "sample_workspace", "sample_workspace_bytes"):
             setattr(a, f, P)
     a.B, a.Lmax, a.d, a.R, a.V = 2, 16, 8, 8, 100
     a.cfg = sd.make_cfg((3, 2, 1), 1, 7, 0.0)
@@ -153,3 +154,32 @@ def test_stage_entry_points_reject():
     assert lib.switchsd_tree_mask(P, None, 2, 8, P, None) == EINVAL
     assert lib.switchsd_tree_mask(P, P, 2, 8, None, None) == EINVAL
     assert lib.switchsd_tree_mask(None, None, 0, 8, None, None) == OK
+
+
+def test_sample_entry_point_rejects():
+    lib = sd.lib
+    A16 = (P + 15) & ~15
+    SW = WS
+    need = sd.sample_workspace_bytes(2, 8, 128)
+    assert need >= 2 * 8 * 1 * 4 * 4 and need % 256 == 0
+    assert sd.sample_workspace_bytes(2, 8, 128256) == 2 * 8 * 16 * 4 * 4
+    assert sd.sample_workspace_bytes(-1, 8, 8) == 0
+
+    def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS, wsn=4096):
+        return lib.switchsd_verify_sample(logits, 2, 8, V, T, uni, P, P, P, P, P, P, P, P, ws,
+                                          wsn, sw, swn, None)
+    for T in (0.0, -0.5, float("nan"), float("inf")):
+        assert call(T=T) == EINVAL
+    assert call(uni=None) == EINVAL
+    assert call(V=100) == EINVAL                       # rows not 16-byte aligned
+    assert call(logits=A16 + 2) == EINVAL
+    assert call(V=64 * 8192 + 8) == ESHAPE             # more than 64 chunks per row
+    assert call(sw=None) == EWORKSPACE
+    assert call(sw=SW + 4) == EWORKSPACE
+    assert call(swn=need - 1) == EWORKSPACE
+    assert call(wsn=8) == EWORKSPACE
+    assert lib.switchsd_verify_sample(P, 0, 8, 128, 0.5, None, None, None, None, None, None,
+                                      None, None, None, None, 0, None, 0, None) == OK
+    a = step_args(temperature=0.7)                     # sampled step without uniforms
+    a.uniforms = None
+    assert call_step(a, nbytes=1 << 15) == EINVAL
