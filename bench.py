@@ -124,6 +124,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="C2", choices=sorted(W.WORKLOADS))
     ap.add_argument("--mode", type=int, default=0, help="0 auto, 1 fused, 2 split")
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="> 0: verification draws the rows' tokens at this sampling "
+                         "temperature (App. A) with seeded uniforms")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -161,7 +164,15 @@ def main():
     cfg = sd.make_cfg(wl.ngram_lens, wl.kappa, wl.k, wl.theta, wl.n_cand)
     outs = [sd.alloc_outputs(wl.B, wl.R, wl.k, wl.n_cand) for _ in range(nrot)]
     ws = sd.alloc_workspace(wl.B, wl.R, wl.L, wl.n_cand)
-    step_args = [sd.build_step_args(s, o, cfg, args.mode) for s, o in zip(sets, outs)]
+    T = args.temperature
+    if T > 0:
+        uni = torch.from_numpy(np.random.default_rng(20186).integers(
+            0, 2 ** 32, (wl.B, wl.R), dtype=np.uint32).view(np.int32)).cuda()
+        sws = sd.alloc_sample_workspace(wl.B, wl.R, wl.V)
+        step_args = [sd.build_step_args(s, o, cfg, args.mode, T, uni, sws)
+                     for s, o in zip(sets, outs)]
+    else:
+        step_args = [sd.build_step_args(s, o, cfg, args.mode) for s, o in zip(sets, outs)]
     import ctypes
     lib = sd.lib
     stream = torch.cuda.current_stream()
@@ -201,17 +212,27 @@ def main():
     alg, alg_logits = algorithmic_bytes(wl, rows_read)
     step_gbps = alg / (ms * 1e-3) / 1e9
 
-    # verify-argmax alone (stage entry point), rows of the chosen draft
-    vargs = [(st["logits"].data_ptr(), wl.B, wl.R, wl.V, o["dtok"].data_ptr(),
-              o["dpar"].data_ptr(), o["dn"].data_ptr(), o["accept_len"].data_ptr(),
-              o["accept_node"].data_ptr(), o["bonus"].data_ptr(), o["out_tokens"].data_ptr(),
-              o["amax"].data_ptr(), wsp, wsn, sptr) for st, o in zip(sets, outs)]
+    # verification alone (stage entry point), rows of the chosen draft
+    if T > 0:
+        vargs = [(st["logits"].data_ptr(), wl.B, wl.R, wl.V, T, uni.data_ptr(),
+                  o["dtok"].data_ptr(), o["dpar"].data_ptr(), o["dn"].data_ptr(),
+                  o["accept_len"].data_ptr(), o["accept_node"].data_ptr(), o["bonus"].data_ptr(),
+                  o["out_tokens"].data_ptr(), o["amax"].data_ptr(), wsp, wsn, sws.data_ptr(),
+                  sws.numel(), sptr) for st, o in zip(sets, outs)]
+        vfn, vname = lib.switchsd_verify_sample, "switchsd_verify_sample"
+    else:
+        vargs = [(st["logits"].data_ptr(), wl.B, wl.R, wl.V, o["dtok"].data_ptr(),
+                  o["dpar"].data_ptr(), o["dn"].data_ptr(), o["accept_len"].data_ptr(),
+                  o["accept_node"].data_ptr(), o["bonus"].data_ptr(),
+                  o["out_tokens"].data_ptr(), o["amax"].data_ptr(), wsp, wsn, sptr)
+                 for st, o in zip(sets, outs)]
+        vfn, vname = lib.switchsd_verify_accept, "switchsd_verify_accept"
 
     def run_verify(n):
         for i in range(n):
-            rc = lib.switchsd_verify_accept(*vargs[i % nrot])
+            rc = vfn(*vargs[i % nrot])
             if rc:
-                raise sd.SwitchsdError("switchsd_verify_accept", rc)
+                raise sd.SwitchsdError(vname, rc)
 
     nv = max(200, args.steps // 4)
     run_verify(20)
@@ -234,8 +255,13 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # the dominant kernel: the fused launch, or the verify launch of a split step
-    if mode == sd.MODE_FUSED:
+    # the dominant kernel: the fused launch, or the verify launch of a split step;
+    # at T > 0 the verification's three launches together
+    if T > 0:
+        dom = {"kernel": "sampled verification (row maxima + weight sums + pick, 3 launches)",
+               "gbps": v_gbps, "bytes": vbytes,
+               "traffic_file": f"traffic_sampled_verify_{wl.name}.json"}
+    elif mode == sd.MODE_FUSED:
         dom = {"kernel": "k_switchsd (fused step)", "gbps": step_gbps, "bytes": alg,
                "traffic_file": f"traffic_fused_step_{wl.name}.json"}
     else:
@@ -256,9 +282,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: B={wl.B} L={wl.L} V={wl.V} d={wl.d} k={wl.k} R={wl.R}"
                                f" W={max(1, wl.n_cand)} ngram={list(wl.ngram_lens)}"
-                               f" kappa={wl.kappa}",
+                               f" kappa={wl.kappa}" + (f" T={T}" if T > 0 else ""),
                    "global_batch": wl.B, "seq_len": wl.L, "parallelism": "none (1 GPU)",
-                   "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode],
+                   "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode] +
+                             (" + 2 kernels for the draw at T > 0" if T > 0 else ""),
                    "rotation_sets": nrot},
         "roofline": {"bound": "hbm", "achieved": round(dom["gbps"], 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(dom["gbps"] / HBM_PEAK_GBPS, 4),

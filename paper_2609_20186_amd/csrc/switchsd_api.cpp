@@ -303,13 +303,14 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     int rc = cu_count(&cus);
     if (rc)
         return rc;
-    p.list_mode = 0;
+    // long drafts: the sums stream the drafted rows' chunks over a fixed grid
+    const bool stream_sums = p.R > 64 && p.B <= kListMaxB;
     p.uniforms = sa->uniforms;
     p.samp_c = (float)(1.4426950408889634 / (double)sa->temperature);
     p.csum = (uint32_t *)sa->ws;
     p.cpr = (int32_t)chunks_per_row(p.V);
     const int64_t rows = (int64_t)p.B * p.R;
-    int64_t segs = (2 * (int64_t)cus + rows - 1) / rows;
+    int64_t segs = (4 * (int64_t)cus + rows - 1) / rows;
     if (segs > p.cpr)
         segs = p.cpr;
     if (segs < 1)
@@ -317,11 +318,13 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     p.seg_chunks = (int32_t)((p.cpr + segs - 1) / segs);
     p.segs = (int32_t)((p.cpr + p.seg_chunks - 1) / p.seg_chunks);
     p.speculate = speculate ? 1 : 0;
-    const int64_t grid = rows * p.segs;
+    p.list_mode = stream_sums ? 1 : 0;
+    const int64_t grid = stream_sums ? 4 * (int64_t)cus : rows * p.segs;
     if (!grid_ok(grid) || !grid_ok(rows))
         return SWITCHSD_ESHAPE;
     if ((rc = launch_sample_sums_kernel(p, grid, stream)))
         return rc;
+    p.list_mode = 0;
     return launch_sample_pick_kernel(p, stream);
 }
 

@@ -1316,22 +1316,23 @@ __device__ __forceinline__ bool key_max(unsigned long long key, float &m) {
 // 2^t for t = (l - m) c in [-24, 0] as 2^k * P(t - k), k = rint(t), with P
 // the degree-6 Taylor polynomial of 2^f = e^(f ln 2) on [-1/2, 1/2] by
 // Horner's rule in fused multiply-adds; the weight is that times 2^20,
-// truncated.  0 unless t >= -24 (so NaN and -inf weigh nothing).
+// truncated, and 0 unless t >= -24 (so NaN and -inf weigh nothing).  Two
+// rewrites give the same bits with fewer operations: the coefficients carry
+// the factor 2^20 (scaling by a power of two commutes with every rounding
+// step here), and t is clamped to >= -25 instead of tested (every t below -24,
+// NaN included, then yields 2^(20 + t') < 1/16, which truncates to 0).
 __device__ __forceinline__ uint32_t samp_weight(float l, float m, float c) {
-    const float t = (l - m) * c;
-    const bool on = t >= -24.0f;
-    const float tc = on ? t : 0.0f;
-    const float k = __builtin_rintf(tc);
-    const float f = tc - k;
-    float q = 0x1.430912p-13f;               // ln2^6 / 6!
-    q = __builtin_fmaf(q, f, 0x1.5d87fep-10f);  // ln2^5 / 5!
-    q = __builtin_fmaf(q, f, 0x1.3b2ab6p-7f);   // ln2^4 / 4!
-    q = __builtin_fmaf(q, f, 0x1.c6b08ep-5f);   // ln2^3 / 3!
-    q = __builtin_fmaf(q, f, 0x1.ebfbe0p-3f);   // ln2^2 / 2!
-    q = __builtin_fmaf(q, f, 0x1.62e430p-1f);   // ln2
-    q = __builtin_fmaf(q, f, 1.0f);
-    const uint32_t w = (uint32_t)__builtin_ldexpf(q, (int)k + 20);
-    return on ? w : 0u;
+    const float t = __builtin_fmaxf((l - m) * c, -25.0f);
+    const float k = __builtin_rintf(t);
+    const float f = t - k;
+    float q = 0x1.430912p+7f;                  // 2^20 ln2^6 / 6!
+    q = __builtin_fmaf(q, f, 0x1.5d87fep+10f);  // 2^20 ln2^5 / 5!
+    q = __builtin_fmaf(q, f, 0x1.3b2ab6p+13f);  // 2^20 ln2^4 / 4!
+    q = __builtin_fmaf(q, f, 0x1.c6b08ep+15f);  // 2^20 ln2^3 / 3!
+    q = __builtin_fmaf(q, f, 0x1.ebfbe0p+17f);  // 2^20 ln2^2 / 2!
+    q = __builtin_fmaf(q, f, 0x1.62e430p+19f);  // 2^20 ln2
+    q = __builtin_fmaf(q, f, 0x1p+20f);         // 2^20
+    return (uint32_t)__builtin_ldexpf(q, (int)k);
 }
 
 // Weight sum of the 8 elements of one 16-byte vector (< 2^24).
@@ -1383,6 +1384,103 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
             A[u] = Bv[u];
+    }
+}
+
+// Sum launch for long drafts (p.list_mode): the chunks of the drafted rows,
+// sequence by sequence and row by row, split evenly over a fixed grid as in
+// the streamed verify; a row's maximum is requested together with the
+// prefetch of its first chunk.
+__global__ __launch_bounds__(kThreads) void k_sample_sums_stream(StepParams p) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int Q = kListMaxB / 64;
+    const int cpr = p.cpr;
+    int first[Q], dnq[Q];
+    int carry = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int b = lane + 64 * q;
+        dnq[q] = b < p.B ? clampi(ld_i32(&p.dn[b]), 1, p.R) : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int cnt = dnq[q] * cpr;
+        int inc = cnt;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(inc, o);
+            if (lane >= o)
+                inc += y;
+        }
+        first[q] = carry + inc - cnt;
+        carry += __shfl(inc, 63);
+    }
+    const int64_t U = carry;
+    const int u0 = (int)(U * blockIdx.x / gridDim.x), u1 = (int)(U * (blockIdx.x + 1) / gridDim.x);
+    if (u0 >= u1)
+        return;
+    int b = 0, fb = 0, dnb = 1;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const unsigned long long m = __ballot(lane + 64 * q < p.B && first[q] <= u0);
+        if (m) {
+            const int l = 63 - __clzll((long long)m);
+            b = 64 * q + l;
+            fb = __shfl(first[q], l);
+            dnb = __shfl(dnq[q], l);
+        }
+    }
+    int r = (u0 - fb) / cpr, c = u0 - fb - r * cpr;
+    const int nq = p.V >> 3;
+    auto row_vecs = [&](int bb, int rr) {
+        return reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)bb * p.R + rr) * p.V);
+    };
+    u32x4 A[kUnroll], Bv[kUnroll];
+    load_chunk(A, row_vecs(b, r), c * kChunkVecs, nq);
+    unsigned long long key = ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]);
+    for (int u = u0; u < u1; ++u) {
+        int nb = b, nr = r, nc = c + 1, ndn = dnb;
+        if (nc == cpr) {
+            nc = 0;
+            if (++nr == dnb) {
+                nr = 0;
+                ++nb;
+                if (u + 1 < u1) {
+                    const int q = nb >> 6, l = nb & 63;
+                    int v = 0;
+#pragma unroll
+                    for (int qq = 0; qq < Q; ++qq)
+                        if (qq == q)
+                            v = __shfl(dnq[qq], l);
+                    ndn = v;
+                }
+            }
+        }
+        unsigned long long nkey = key;
+        if (u + 1 < u1) {
+            load_chunk(Bv, row_vecs(nb, nr), nc * kChunkVecs, nq);
+            if (nc == 0)
+                nkey = ld_u64(&p.ws.keys[(int64_t)nb * p.ws.key_stride + nr]);
+        }
+        float m;
+        if (key_max(key, m)) {
+            uint32_t sum = 0;
+#pragma unroll
+            for (int q = 0; q < kUnroll; ++q)
+                if (c * kChunkVecs + q * kThreads + (int)threadIdx.x < nq)
+                    sum += vec_weight(A[q], m, p.samp_c);
+            sum = wave_reduce_u32(sum, 0u, [](uint32_t a, uint32_t x) { return a + x; });
+            if (lane == 0)
+                p.csum[(((int64_t)b * p.R + r) * cpr + c) * kWaves + wave] = sum;
+        }
+        b = nb;
+        r = nr;
+        c = nc;
+        dnb = ndn;
+        key = nkey;
+#pragma unroll
+        for (int q = 0; q < kUnroll; ++q)
+            A[q] = Bv[q];
     }
 }
 
@@ -1661,7 +1759,11 @@ int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
 }
 
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
-    hipLaunchKernelGGL(k_sample_sums, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+    if (p.list_mode)
+        hipLaunchKernelGGL(k_sample_sums_stream, dim3((unsigned)grid), dim3(kThreads), 0,
+                           stream, p);
+    else
+        hipLaunchKernelGGL(k_sample_sums, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 
