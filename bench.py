@@ -31,6 +31,13 @@ sys.path.insert(0, ROOT)
 from paper_2609_20186_amd import workloads as W  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
+# VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a wave64 op takes 4
+# cycles on one SIMD) = 39.3 T lane-ops/s; one FMA is one op here
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# VALU ops per logit of the draw at T > 0: about 1.5 in the row-maximum pass,
+# 16 for the fixed-point weight (unpack, shift, scale, clamp, rint, reduce,
+# 7 fused multiply-adds, convert, ldexp, convert, accumulate) in the sum pass
+SAMPLE_OPS_PER_LOGIT = 17.5
 METRIC = "speculation-control steps/s + verify-argmax HBM GB/s (% peak), B=32 V=128256"
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_20186_amd", "csrc", "switchsd_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
@@ -259,7 +266,9 @@ def main():
     # at T > 0 the verification's three launches together
     if T > 0:
         dom = {"kernel": "sampled verification (row maxima + weight sums + pick, 3 launches)",
-               "gbps": v_gbps, "bytes": vbytes,
+               "bound": "alu", "unit": "TOP/s (VALU lane-ops)", "peak": round(VALU_PEAK_TOPS, 1),
+               "gbps": vbytes / 2 * SAMPLE_OPS_PER_LOGIT / (vms * 1e-3) / 1e12,
+               "bytes": int(vbytes / 2 * SAMPLE_OPS_PER_LOGIT),
                "traffic_file": f"traffic_sampled_verify_{wl.name}.json"}
     elif mode == sd.MODE_FUSED:
         dom = {"kernel": "k_switchsd (fused step)", "gbps": step_gbps, "bytes": alg,
@@ -287,12 +296,15 @@ def main():
                    "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode] +
                              (" + 2 kernels for the draw at T > 0" if T > 0 else ""),
                    "rotation_sets": nrot},
-        "roofline": {"bound": "hbm", "achieved": round(dom["gbps"], 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(dom["gbps"] / HBM_PEAK_GBPS, 4),
+        "roofline": {"bound": dom.get("bound", "hbm"), "achieved": round(dom["gbps"], 1),
+                     "peak": dom.get("peak", HBM_PEAK_GBPS), "unit": dom.get("unit", "GB/s"),
+                     "frac": round(dom["gbps"] / dom.get("peak", HBM_PEAK_GBPS), 4),
                      "traffic": traffic, "kernel": dom["kernel"],
-                     "algorithmic_bytes_per_launch": dom["bytes"]},
+                     ("algorithmic_ops_per_call" if T > 0 else "algorithmic_bytes_per_launch"):
+                         dom["bytes"]},
         "step_GBps": round(step_gbps, 1),
-        "verify_argmax": {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),
+        ("verify_sampled" if T > 0 else "verify_argmax"):
+            {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),
                           "us_per_call": round(vms * 1e3, 2), "bytes_per_call": vbytes},
         "copy_fraction": round(float(np.mean(sel["use_copy"])), 3),
         "mean_accept_len": round(float(o0["accept_len"].float().mean()), 3),
