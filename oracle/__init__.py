@@ -66,6 +66,7 @@ def _load():
         _lib.oracle_tree_mask.argtypes = [P, i32, i32, i32, P]
         _lib.oracle_step.argtypes = [i32, i32, i32, i32, i32] + [P] * 4 + [ctypes.c_float] + \
             [P] * 5 + [P] * 14 + [ctypes.c_float, P, i32]
+        _lib.oracle_commit.argtypes = [P, P, i32, P, i32, i32, P, P]
         _lib.oracle_sample_scale.argtypes = [ctypes.c_float]
         _lib.oracle_sample_scale.restype = ctypes.c_float
         _lib.oracle_sample_weight.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float]
@@ -182,6 +183,26 @@ def tree_mask(dpar, dn, R, words=None):
     m = np.zeros((R, words), np.uint32)
     lib.oracle_tree_mask(_p(dpar), int(dn), int(R), int(words), _p(m))
     return m
+
+
+def commit(tokens, lengths, draft_pos, res):
+    """Sec. 3.3 (KV Cache Synchronization): append every sequence's accepted
+    tokens and bonus (res from step()) to tokens/lengths in place and update
+    draft_pos; returns lag [B]."""
+    lib = _load()
+    B, Lmax = tokens.shape
+    assert tokens.dtype == np.int32 and tokens.flags.c_contiguous
+    lag = np.zeros(B, np.int32)
+    for b in range(B):
+        ln = np.array([lengths[b]], np.int32)
+        dp = np.array([draft_pos[b]], np.int32)
+        lg = np.zeros(1, np.int32)
+        out = _c(res["out_tokens"][b], np.int32)
+        row = tokens[b]
+        lib.oracle_commit(_p(row), _p(ln), int(Lmax), _p(out), int(res["accept_len"][b]),
+                          int(res["use_copy"][b]), _p(dp), _p(lg))
+        lengths[b], draft_pos[b], lag[b] = ln[0], dp[0], lg[0]
+    return lag
 
 
 STEP_OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_copy",

@@ -307,6 +307,33 @@ void oracle_tree_mask(const int32_t *dpar, int32_t dn, int32_t R, int32_t words,
     }
 }
 
+/* Sec. 3.3 (KV Cache Synchronization): when a copy draft is accepted the
+ * draft model's cache lags behind; the accepted tokens are passed through the
+ * draft model in its next forward pass.  This is the bookkeeping of that
+ * rule plus the append of the step's tokens to the context. */
+void oracle_commit(int32_t *x, int32_t *length, int32_t Lmax, const int32_t *out_tokens,
+                   int32_t accept_len, int32_t use_copy, int32_t *draft_pos, int32_t *lag)
+{
+    int32_t L = *length;
+    if (L < 0)
+        L = 0;
+    if (L > Lmax)
+        L = Lmax;
+    int32_t Lnew = L + accept_len + 1;
+    if (Lnew > Lmax)
+        Lnew = Lmax;
+    for (int32_t i = 0; L + i < Lnew; ++i)
+        x[L + i] = out_tokens[i];
+    int32_t pos = use_copy ? *draft_pos : L + accept_len;
+    if (pos < 0)
+        pos = 0;
+    if (pos > Lnew)
+        pos = Lnew;
+    *length = Lnew;
+    *draft_pos = pos;
+    *lag = Lnew - pos;
+}
+
 typedef struct {
     int32_t b0, b1;
     int32_t Lmax, d, R, V;

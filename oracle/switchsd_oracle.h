@@ -97,6 +97,18 @@ void oracle_accept(const int32_t *dtok, const int32_t *dpar, int32_t dn,
 void oracle_tree_mask(const int32_t *dpar, int32_t dn, int32_t R, int32_t words,
                       uint32_t *mask);
 
+/* Commit of one sequence after its step (Sec. 3.3, KV Cache Synchronization:
+ * lazy propagation).  The accept_len accepted tokens and the bonus
+ * (out_tokens[0..accept_len]) are appended to the context x at L =
+ * clamp(*length, 0, Lmax); the context stops at Lmax (tokens past it are
+ * dropped).  The draft model's cache position: after a copy step it is
+ * unchanged (the draft model saw nothing new); after a neural step it is L +
+ * accept_len (it drafted the accepted tokens itself; the bonus is new to it);
+ * it is clamped to [0, new length].  lag = new length - draft position, the
+ * tokens the next neural drafting pass must consume first. */
+void oracle_commit(int32_t *x, int32_t *length, int32_t Lmax, const int32_t *out_tokens,
+                   int32_t accept_len, int32_t use_copy, int32_t *draft_pos, int32_t *lag);
+
 /* The whole step for B sequences; threads > 1 splits the batch across
  * POSIX threads (sequences are independent).  npar may be NULL (chains).
  * amax [B,R] receives the argmax of rows r < dn[b] and -1 elsewhere.
