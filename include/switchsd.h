@@ -236,6 +236,12 @@ typedef struct {
     const uint32_t *uniforms;  /* [B, R] */
     void *sample_workspace;
     size_t sample_workspace_bytes;
+    /* decode loop: commit != 0 appends the accepted tokens and the bonus to
+     * tokens/lengths in the same launch (they are then read-write) and
+     * updates draft_pos and lag as switchsd_commit does */
+    int32_t commit;
+    int32_t *draft_pos;      /* [B] in/out */
+    int32_t *lag;            /* [B] out    */
 } switchsd_step_args;
 
 /* One whole step.  Results are identical to calling the four stage entry
@@ -243,6 +249,23 @@ typedef struct {
  * MODE_FUSED does the greedy step in one kernel launch. */
 int switchsd_step(const switchsd_step_args *args, void *workspace, size_t workspace_bytes,
                   hipStream_t stream);
+
+/* Decode-loop commit of a finished step -- Sec. 3.3, KV Cache
+ * Synchronization (lazy propagation).  For each sequence, with
+ * L = clamp(lengths[b], 0, Lmax) and a = clamp(accept_len[b], 0, R - 1): the
+ * accepted tokens and the bonus out_tokens[b, 0..a] are appended at
+ * tokens[b, L..], cut at Lmax; lengths[b] = min(L + a + 1, Lmax).  The draft
+ * model's cache position draft_pos[b] stays after a copy step (the draft model
+ * saw nothing new) and becomes L + a after a neural step (it drafted the
+ * accepted tokens; the bonus is new to it), clamped to [0, lengths[b]];
+ * lag[b] = lengths[b] - draft_pos[b] is the number of tokens the next neural
+ * drafting pass must consume first.
+ *   tokens [B, Lmax], lengths, draft_pos [B] int32 in/out; out_tokens [B, R],
+ *   accept_len, use_copy [B] int32 in; lag [B] int32 out. */
+int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,
+                    const int32_t *out_tokens, int32_t R, const int32_t *accept_len,
+                    const int32_t *use_copy, int32_t *draft_pos, int32_t *lag,
+                    hipStream_t stream);
 
 /* Workspace bytes needed by calls with B sequences of R rows, contexts of up
  * to Lmax tokens and n_cand copy candidates (pass 0 for what a call does not

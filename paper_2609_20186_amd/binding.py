@@ -23,7 +23,8 @@ STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE"}
 
 EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
            "switchsd_verify_accept", "switchsd_verify_sample", "switchsd_tree_mask",
-           "switchsd_step", "switchsd_workspace_bytes", "switchsd_sample_workspace_bytes",
+           "switchsd_commit", "switchsd_step", "switchsd_workspace_bytes",
+           "switchsd_sample_workspace_bytes",
            "switchsd_status_string")
 
 
@@ -68,7 +69,8 @@ class StepArgs(ctypes.Structure):
                 ("z", _P), ("use_copy", _P), ("dtok", _P), ("dpar", _P), ("dn", _P),
                 ("amax", _P), ("accept_len", _P), ("accept_node", _P), ("bonus", _P),
                 ("out_tokens", _P), ("temperature", ctypes.c_float), ("uniforms", _P),
-                ("sample_workspace", _P), ("sample_workspace_bytes", ctypes.c_size_t)]
+                ("sample_workspace", _P), ("sample_workspace_bytes", ctypes.c_size_t),
+                ("commit", _I), ("draft_pos", _P), ("lag", _P)]
 
 
 def _load():
@@ -87,6 +89,7 @@ def _load():
     lib.switchsd_verify_sample.argtypes = [_P, _I, _I, _I, ctypes.c_float, _P, _P, _P, _P, _P,
                                            _P, _P, _P, _P, _P, S, _P, S, _P]
     lib.switchsd_sample_workspace_bytes.argtypes = [_I, _I, _I]
+    lib.switchsd_commit.argtypes = [_P, _P, _I, _I, _P, _I, _P, _P, _P, _P, _P]
     lib.switchsd_sample_workspace_bytes.restype = S
     lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
     lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
@@ -198,6 +201,17 @@ def switchsd_verify_sample(logits, temperature, uniforms, dtok, dpar, dn, accept
         sample_workspace.numel(), _stream(stream)))
 
 
+def switchsd_commit(tokens, lengths, out_tokens, accept_len, use_copy, draft_pos, lag,
+                    stream=None):
+    B, Lmax = tokens.shape
+    R = out_tokens.shape[1]
+    _check("switchsd_commit", lib.switchsd_commit(
+        _ptr(tokens, "i32", "tokens"), _ptr(lengths, "i32", "lengths"), B, Lmax,
+        _ptr(out_tokens, "i32", "out_tokens"), R, _ptr(accept_len, "i32", "accept_len"),
+        _ptr(use_copy, "i32", "use_copy"), _ptr(draft_pos, "i32", "draft_pos"),
+        _ptr(lag, "i32", "lag"), _stream(stream)))
+
+
 def switchsd_tree_mask(dpar, dn, mask, stream=None):
     """mask: uint32 (or int32 holding the same bits) [B, R, (R + 31) // 32]."""
     B, R = mask.shape[0], mask.shape[1]
@@ -239,12 +253,14 @@ def alloc_workspace(B, R, Lmax=0, n_cand=0, device="cuda"):
 
 
 def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=None,
-                    sample_workspace=None):
+                    sample_workspace=None, draft_pos=None, lag=None):
     """StepArgs for switchsd_step.  ``inp`` holds device tensors tokens [B,Lmax],
     lengths [B], hidden [B,d], w [d], ntok [B,R], npar [B,R] or None, nn [B],
     logits [B,R,V] and the float ``bias``; ``out`` is from alloc_outputs.
     temperature > 0 draws the rows' tokens with ``uniforms`` [B,R] (uint32
-    bits) and ``sample_workspace`` (alloc_sample_workspace)."""
+    bits) and ``sample_workspace`` (alloc_sample_workspace).  With ``draft_pos``
+    and ``lag`` [B] the step also commits (decode loop): tokens and lengths are
+    then updated in place."""
     tokens, logits, hidden = inp["tokens"], inp["logits"], inp["hidden"]
     B, Lmax = tokens.shape
     R, V = logits.shape[1], logits.shape[2]
@@ -264,6 +280,10 @@ def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=Non
     for name in OUTPUTS:
         setattr(a, name, _ptr(out[name], "f32" if name == "z" else "i32", name,
                               optional=(name == "amax" or name == "copy_tokens")))
+    if draft_pos is not None:
+        a.commit = 1
+        a.draft_pos = _ptr(draft_pos, "i32", "draft_pos")
+        a.lag = _ptr(lag, "i32", "lag")
     a.temperature = float(temperature)
     if temperature != 0.0:
         a.uniforms = _ptr(uniforms, "u32", "uniforms")

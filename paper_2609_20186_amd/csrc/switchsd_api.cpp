@@ -336,7 +336,7 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
                   const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
                   int32_t *accept_node, int32_t *bonus, int32_t *out_tokens, int32_t *amax,
                   void *workspace, size_t workspace_bytes, bool speculate,
-                  const SampleArgs *sa, hipStream_t stream) {
+                  const SampleArgs *sa, const StepParams *loop, hipStream_t stream) {
     if (!shape_ok_B(B) || R < 1 || R > SWITCHSD_MAX_R || V < 1)
         return SWITCHSD_ESHAPE;
     if (B == 0)
@@ -386,6 +386,15 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
     p.rows_mode = p.list_mode ? ROWS_LISTED : ROWS_DRAFT;
     p.speculate = speculate && !p.list_mode ? 1 : 0;
     p.epi_accept = sa ? 0 : 1;
+    if (loop && loop->commit) {  // the decode loop's commit rides on the accept epilogue
+        p.commit = 1;
+        p.ctok = loop->ctok;
+        p.clen = loop->clen;
+        p.draft_pos = loop->draft_pos;
+        p.lag = loop->lag;
+        p.Lmax = loop->Lmax;
+        p.use_copy = loop->use_copy;
+    }
     p.exp_all = (uint32_t)(R * p.segs);
     if ((rc = launch_step_kernel(p, grid, stream)) || !sa)
         return rc;
@@ -405,7 +414,7 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
     const bool speculate = dpar == nullptr || R <= 16;
     return verify_launch(logits, B, R, V, dtok, dpar, dn, accept_len, accept_node, bonus,
                          out_tokens, amax, workspace, workspace_bytes, speculate, nullptr,
-                         stream);
+                         nullptr, stream);
 }
 
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
@@ -418,7 +427,8 @@ int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t
     const SampleArgs sa = {temperature, uniforms, sample_workspace, sample_workspace_bytes};
     const bool speculate = dpar == nullptr || R <= 16;
     return verify_launch(logits, B, R, V, dtok, dpar, dn, accept_len, accept_node, bonus,
-                         out_tokens, amax, workspace, workspace_bytes, speculate, &sa, stream);
+                         out_tokens, amax, workspace, workspace_bytes, speculate, &sa, nullptr,
+                         stream);
 }
 
 size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
@@ -447,7 +457,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         !a->nn || !a->logits || ((uintptr_t)a->logits & 1) || !a->match_n || !a->match_end ||
         !a->copy_len || (a->cfg.k > 0 && !a->copy_tokens) || !a->z || !a->use_copy ||
         !a->dtok || !a->dpar || !a->dn || !a->accept_len || !a->accept_node || !a->bonus ||
-        !a->out_tokens)
+        !a->out_tokens || (a->commit && (!a->draft_pos || !a->lag)))
         return SWITCHSD_EINVAL;
     StepParams p;
     memset(&p, 0, sizeof p);
@@ -487,6 +497,13 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.accept_node = a->accept_node;
     p.bonus = a->bonus;
     p.out_tokens = a->out_tokens;
+    if (a->commit) {
+        p.commit = 1;
+        p.ctok = const_cast<int32_t *>(a->tokens);
+        p.clen = const_cast<int32_t *>(a->lengths);
+        p.draft_pos = a->draft_pos;
+        p.lag = a->lag;
+    }
     p.ws = carve(workspace, B, R, a->Lmax, p.W);
     if ((rc = set_scan(p, B, a->Lmax)))
         return rc;
@@ -519,7 +536,32 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     // chunk before its need is known
     return verify_launch(a->logits, B, R, V, a->dtok, a->dpar, a->dn, a->accept_len,
                          a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
-                         workspace_bytes, R <= 16, sampled ? &sa : nullptr, stream);
+                         workspace_bytes, R <= 16, sampled ? &sa : nullptr, &p, stream);
+}
+
+int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,
+                    const int32_t *out_tokens, int32_t R, const int32_t *accept_len,
+                    const int32_t *use_copy, int32_t *draft_pos, int32_t *lag,
+                    hipStream_t stream) {
+    if (!shape_ok_B(B) || Lmax < 1 || R < 1 || R > SWITCHSD_MAX_R)
+        return SWITCHSD_ESHAPE;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!tokens || !lengths || !out_tokens || !accept_len || !use_copy || !draft_pos || !lag)
+        return SWITCHSD_EINVAL;
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    p.B = B;
+    p.R = R;
+    p.Lmax = Lmax;
+    p.ctok = tokens;
+    p.clen = lengths;
+    p.out_tokens = const_cast<int32_t *>(out_tokens);
+    p.accept_len = const_cast<int32_t *>(accept_len);
+    p.use_copy = const_cast<int32_t *>(use_copy);
+    p.draft_pos = draft_pos;
+    p.lag = lag;
+    return launch_commit_kernel(p, stream);
 }
 
 int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,

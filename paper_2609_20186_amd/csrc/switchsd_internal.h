@@ -86,6 +86,12 @@ struct StepParams {
     int32_t epi_accept;
     int32_t list_mode;   // 1: verify only, a fixed grid streaming the chunks of the drafted
                          // rows r < dn[b] (segs = chunks per row)
+    // decode loop: the accept epilogue appends to the context (read-write)
+    int32_t commit;
+    int32_t *ctok;       // [B, Lmax] the context, written at positions >= its length
+    int32_t *clen;       // [B] its length
+    int32_t *draft_pos;  // [B] draft-model cache position (in/out)
+    int32_t *lag;        // [B] tokens the next neural drafting pass must consume first
     // draws at T > 0 (sum and pick launches)
     const uint32_t *uniforms;  // [B, R]
     float samp_c;              // log2(e) / T
@@ -98,6 +104,7 @@ struct StepParams {
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_select_kernel(const StepParams &p, hipStream_t stream);
+int launch_commit_kernel(const StepParams &p, hipStream_t stream);
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream);
 int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,

@@ -693,7 +693,7 @@ __device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, 
                 st_i32(&p.dpar[base + lane], par);
             }
             if (lane == 0) {
-                p.use_copy[b] = use;
+                st_i32(&p.use_copy[b], use);  // read by the commit of this launch
                 st_i32(&p.dn[b], dnb);
             }
         }
@@ -788,7 +788,7 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total, int
         st_i32(&p.dpar[base + i], par);
     }
     if (lane == 0) {
-        p.use_copy[b] = use;
+        st_i32(&p.use_copy[b], use);  // read by the commit of this launch
         st_i32(&p.dn[b], dnb);
     }
 }
@@ -925,6 +925,22 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
     const int lane = threadIdx.x;
     const int64_t base = (int64_t)b * p.R;
     unsigned long long *keys = p.ws.keys + (int64_t)b * p.ws.key_stride;
+    // decode loop (Sec. 3.3, KV Cache Synchronization): the accepted tokens and
+    // the bonus also go to the context at its length cL
+    int cL = 0, cdp = 0, cuc = 0;
+    if (p.commit) {
+        cL = clampi(p.clen[b], 0, p.Lmax);
+        cdp = p.draft_pos[b];
+        cuc = ld_i32(&p.use_copy[b]);
+    }
+    const int64_t crow = (int64_t)b * p.Lmax;
+    // output position j of the accepted path (then the bonus) holds v
+    auto emit = [&](int j, int v) {
+        p.out_tokens[base + j] = v;
+        if (p.commit && cL + j < p.Lmax)
+            p.ctok[crow + cL + j] = v;
+    };
+    int acc = 0;  // accepted length (uniform over the wave)
     if (p.R <= 64) {
         const int i = lane;
         // the draft and the row maxima, all requested at once
@@ -987,9 +1003,9 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         const int bon = __shfl(a, best);
         if (i < p.R) {
             if ((onpath >> i) & 1ull)
-                p.out_tokens[base + dep - 1] = tok;
+                emit(dep - 1, tok);
             if (i == depth)
-                p.out_tokens[base + i] = bon;
+                emit(i, bon);
             else if (i > depth)
                 p.out_tokens[base + i] = -1;
         }
@@ -998,6 +1014,7 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
             p.accept_node[b] = best;
             p.bonus[b] = bon;
         }
+        acc = depth;
     } else {
         const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
         // the draft and the row maxima into LDS, 256 nodes at a time with all
@@ -1146,20 +1163,28 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         }
         if (__ballot(bad) == 0ull) {
             for (int j = lane; j < depth; j += 64)
-                p.out_tokens[base + j] = sh.epi.tok[first + j];
+                emit(j, sh.epi.tok[first + j]);
         } else if (lane == 0) {
             int cur = best;
             for (int pos = depth - 1; pos >= 0; --pos) {
-                p.out_tokens[base + pos] = sh.epi.tok[cur];
+                emit(pos, sh.epi.tok[cur]);
                 cur = sh.epi.par[cur];
             }
         }
         if (lane == 0) {
-            p.out_tokens[base + depth] = bon;
+            emit(depth, bon);
             p.accept_len[b] = depth;
             p.accept_node[b] = best;
             p.bonus[b] = bon;
         }
+        acc = depth;
+    }
+    if (p.commit && lane == 0) {
+        const int Lnew = cL + acc + 1 < p.Lmax ? cL + acc + 1 : p.Lmax;
+        const int pos = clampi(cuc ? cdp : cL + acc, 0, Lnew);
+        p.clen[b] = Lnew;
+        p.draft_pos[b] = pos;
+        p.lag[b] = Lnew - pos;
     }
     if (lane == 0)
         st_u32(&p.ws.tk_all[b * kLineU32], 0u);
@@ -1683,6 +1708,22 @@ __global__ __launch_bounds__(kThreads) void k_verify_stream(StepParams p) {
     verify_stream(p, sh);
 }
 
+// Stand-alone commit of a finished step (one wave per sequence).
+__global__ __launch_bounds__(64) void k_commit(StepParams p) {
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int L = clampi(p.clen[b], 0, p.Lmax);
+    const int a = clampi(p.accept_len[b], 0, p.R - 1);
+    const int Lnew = L + a + 1 < p.Lmax ? L + a + 1 : p.Lmax;
+    for (int j = lane; L + j < Lnew; j += 64)
+        p.ctok[(int64_t)b * p.Lmax + L + j] = p.out_tokens[(int64_t)b * p.R + j];
+    if (lane == 0) {
+        const int pos = clampi(p.use_copy[b] ? p.draft_pos[b] : L + a, 0, Lnew);
+        p.clen[b] = Lnew;
+        p.draft_pos[b] = pos;
+        p.lag[b] = Lnew - pos;
+    }
+}
+
 __global__ __launch_bounds__(64) void k_select(StepParams p) {
     __shared__ ChainShared ch;
     const int b = blockIdx.x;
@@ -1770,6 +1811,11 @@ int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t str
 int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream) {
     hipLaunchKernelGGL(k_sample_pick, dim3((unsigned)((int64_t)p.B * p.R)), dim3(kThreads), 0,
                        stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_commit_kernel(const StepParams &p, hipStream_t stream) {
+    hipLaunchKernelGGL(k_commit, dim3((unsigned)p.B), dim3(64), 0, stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 

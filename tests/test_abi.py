@@ -59,7 +59,8 @@ def step_args(**kw):
     a = sd.StepArgs()
     for f, _ in sd.StepArgs._fields_:
         if f not in ("B", "Lmax", "d", "R", "V", "bias", "cfg", "mode", "temperature",
-                     "uniforms", "sample_workspace", "sample_workspace_bytes"):
+                     "uniforms", "sample_workspace", "sample_workspace_bytes", "commit",
+                     "draft_pos", "lag"):
             setattr(a, f, P)
     a.B, a.Lmax, a.d, a.R, a.V = 2, 16, 8, 8, 100
     a.cfg = sd.make_cfg((3, 2, 1), 1, 7, 0.0)
@@ -182,4 +183,15 @@ def test_sample_entry_point_rejects():
                                       None, None, None, None, 0, None, 0, None) == OK
     a = step_args(temperature=0.7)                     # sampled step without uniforms
     a.uniforms = None
+    assert call_step(a, nbytes=1 << 15) == EINVAL
+
+
+def test_commit_entry_point_rejects():
+    lib = sd.lib
+    assert lib.switchsd_commit(P, P, -1, 16, P, 8, P, P, P, P, None) == ESHAPE
+    assert lib.switchsd_commit(P, P, 2, 0, P, 8, P, P, P, P, None) == ESHAPE
+    assert lib.switchsd_commit(P, P, 2, 16, P, 0, P, P, P, P, None) == ESHAPE
+    assert lib.switchsd_commit(P, P, 2, 16, P, 8, P, P, None, P, None) == EINVAL
+    assert lib.switchsd_commit(None, None, 0, 16, None, 8, None, None, None, None, None) == OK
+    a = step_args(commit=1)                            # loop step without its counters
     assert call_step(a, nbytes=1 << 15) == EINVAL
