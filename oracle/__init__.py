@@ -67,6 +67,7 @@ def _load():
         _lib.oracle_step.argtypes = [i32, i32, i32, i32, i32] + [P] * 4 + [ctypes.c_float] + \
             [P] * 5 + [P] * 14 + [ctypes.c_float, P, i32]
         _lib.oracle_commit.argtypes = [P, P, i32, P, i32, i32, P, P]
+        _lib.oracle_copy_labels.argtypes = [P, i32, i32, i32, P]
         _lib.oracle_sample_scale.argtypes = [ctypes.c_float]
         _lib.oracle_sample_scale.restype = ctypes.c_float
         _lib.oracle_sample_weight.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float]
@@ -203,6 +204,19 @@ def commit(tokens, lengths, draft_pos, res):
                           int(res["use_copy"][b]), _p(dp), _p(lg))
         lengths[b], draft_pos[b], lag[b] = ln[0], dp[0], lg[0]
     return lag
+
+
+def copy_labels(tokens, lengths, n):
+    """Sec. 3.2: copy-mode label of every position ([B, Lmax] uint8)."""
+    lib = _load()
+    tokens = _c(tokens, np.int32)
+    B, Lmax = tokens.shape
+    out = np.zeros((B, Lmax), np.uint8)
+    for b in range(B):
+        L = max(0, min(int(lengths[b]), Lmax))
+        row = out[b]
+        lib.oracle_copy_labels(_p(tokens[b]), L, Lmax, int(n), _p(row))
+    return out
 
 
 STEP_OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_copy",

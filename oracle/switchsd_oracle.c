@@ -334,6 +334,36 @@ void oracle_commit(int32_t *x, int32_t *length, int32_t Lmax, const int32_t *out
     *lag = Lnew - pos;
 }
 
+/* Sec. 3.2 (Problem Formulation): the training label of the copy-intent
+ * probe.  A verbatim span of at least n tokens that appears earlier contains
+ * windows of exactly n tokens that appear earlier at the same offsets, and
+ * such a window is itself a span of n tokens, so the rule is: j is covered by
+ * an n-token window that is not the first occurrence of its tokens. */
+void oracle_copy_labels(const int32_t *x, int32_t L, int32_t Lmax, int32_t n,
+                        uint8_t *labels)
+{
+    for (int32_t j = 0; j < Lmax; ++j)
+        labels[j] = 0;
+    if (n < 1 || L > Lmax)
+        return;
+    for (int32_t s = 1; s + n <= L; ++s) {
+        int earlier = 0;
+        for (int32_t s2 = 0; s2 < s && !earlier; ++s2) {
+            int same = 1;
+            for (int32_t t = 0; t < n; ++t) {
+                if (x[s2 + t] != x[s + t]) {
+                    same = 0;
+                    break;
+                }
+            }
+            earlier = same;
+        }
+        if (earlier)
+            for (int32_t t = 0; t < n; ++t)
+                labels[s + t] = 1;
+    }
+}
+
 typedef struct {
     int32_t b0, b1;
     int32_t Lmax, d, R, V;

@@ -109,6 +109,15 @@ void oracle_tree_mask(const int32_t *dpar, int32_t dn, int32_t R, int32_t words,
 void oracle_commit(int32_t *x, int32_t *length, int32_t Lmax, const int32_t *out_tokens,
                    int32_t accept_len, int32_t use_copy, int32_t *draft_pos, int32_t *lag);
 
+/* Copy-mode labels of one sequence x[0..L-1] (Sec. 3.2, Problem
+ * Formulation): position j is copy-mode (labels[j] = 1) iff it lies inside a
+ * window of n consecutive tokens that also occurs earlier, i.e. some window
+ * x[s..s+n-1] with s <= j <= s+n-1, s+n-1 <= L-1, equals x[s'..s'+n-1] for
+ * some s' < s (overlap allowed); else 0.  labels[j] = 0 for j >= L, up to
+ * Lmax. */
+void oracle_copy_labels(const int32_t *x, int32_t L, int32_t Lmax, int32_t n,
+                        uint8_t *labels);
+
 /* The whole step for B sequences; threads > 1 splits the batch across
  * POSIX threads (sequences are independent).  npar may be NULL (chains).
  * amax [B,R] receives the argmax of rows r < dn[b] and -1 elsewhere.
