@@ -267,6 +267,22 @@ int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,
                     const int32_t *use_copy, int32_t *draft_pos, int32_t *lag,
                     hipStream_t stream);
 
+/* Copy-mode labels for training the copy-intent probe -- Sec. 3.2, Problem
+ * Formulation: position j of sequence b (L = clamp(lengths[b], 0, Lmax)) is
+ * copy-mode, labels[b, j] = 1, iff it lies inside a verbatim span of at least
+ * n tokens that appears earlier in the context, i.e. some window
+ * x[s..s+n-1] with s <= j <= s+n-1 <= L-1 equals x[s'..s'+n-1] for some
+ * s' < s (overlap allowed); 0 otherwise and for j >= L.  The paper's setting
+ * is n = 5.  Offline (whole sequences, not per decoding step).
+ *   tokens [B, Lmax] int32, lengths [B] int32, 1 <= n <= 64;
+ *   output labels [B, Lmax] uint8; workspace of
+ *   switchsd_label_workspace_bytes(B, Lmax) bytes, 256-byte aligned, zeroed
+ *   once by the caller (left zeroed by every call).  Two launches. */
+int switchsd_copy_labels(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
+                         int32_t n, uint8_t *labels, void *workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+size_t switchsd_label_workspace_bytes(int32_t B, int32_t Lmax);
+
 /* Workspace bytes needed by calls with B sequences of R rows, contexts of up
  * to Lmax tokens and n_cand copy candidates (pass 0 for what a call does not
  * take: R for the match stage, Lmax for verification).  0 for a negative

@@ -23,8 +23,9 @@ STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE"}
 
 EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
            "switchsd_verify_accept", "switchsd_verify_sample", "switchsd_tree_mask",
-           "switchsd_commit", "switchsd_step", "switchsd_workspace_bytes",
-           "switchsd_sample_workspace_bytes",
+           "switchsd_commit", "switchsd_step", "switchsd_copy_labels",
+           "switchsd_workspace_bytes", "switchsd_sample_workspace_bytes",
+           "switchsd_label_workspace_bytes",
            "switchsd_status_string")
 
 
@@ -90,6 +91,9 @@ def _load():
                                            _P, _P, _P, _P, _P, S, _P, S, _P]
     lib.switchsd_sample_workspace_bytes.argtypes = [_I, _I, _I]
     lib.switchsd_commit.argtypes = [_P, _P, _I, _I, _P, _I, _P, _P, _P, _P, _P]
+    lib.switchsd_copy_labels.argtypes = [_P, _P, _I, _I, _I, _P, _P, S, _P]
+    lib.switchsd_label_workspace_bytes.argtypes = [_I, _I]
+    lib.switchsd_label_workspace_bytes.restype = S
     lib.switchsd_sample_workspace_bytes.restype = S
     lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
     lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
@@ -210,6 +214,19 @@ def switchsd_commit(tokens, lengths, out_tokens, accept_len, use_copy, draft_pos
         _ptr(out_tokens, "i32", "out_tokens"), R, _ptr(accept_len, "i32", "accept_len"),
         _ptr(use_copy, "i32", "use_copy"), _ptr(draft_pos, "i32", "draft_pos"),
         _ptr(lag, "i32", "lag"), _stream(stream)))
+
+
+def label_workspace_bytes(B, Lmax):
+    return int(lib.switchsd_label_workspace_bytes(int(B), int(Lmax)))
+
+
+def switchsd_copy_labels(tokens, lengths, n, labels, workspace, stream=None):
+    """labels: uint8 [B, Lmax]; workspace: zeroed uint8 of label_workspace_bytes."""
+    B, Lmax = tokens.shape
+    _check("switchsd_copy_labels", lib.switchsd_copy_labels(
+        _ptr(tokens, "i32", "tokens"), _ptr(lengths, "i32", "lengths"), B, Lmax, int(n),
+        _ptr(labels, "u8", "labels"), _ptr(workspace, "u8", "workspace"), workspace.numel(),
+        _stream(stream)))
 
 
 def switchsd_tree_mask(dpar, dn, mask, stream=None):

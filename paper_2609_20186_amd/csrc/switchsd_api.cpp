@@ -539,6 +539,40 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
                          workspace_bytes, R <= 16, sampled ? &sa : nullptr, &p, stream);
 }
 
+size_t switchsd_label_workspace_bytes(int32_t B, int32_t Lmax) {
+    if (B < 0 || Lmax < 0)
+        return 0;
+    const size_t n = (size_t)B * (((size_t)Lmax + 63) / 64) * 8;
+    return (n + kAlign - 1) / kAlign * kAlign;
+}
+
+int switchsd_copy_labels(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
+                         int32_t n, uint8_t *labels, void *workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+    if (!shape_ok_B(B) || Lmax < 1 || (int64_t)B * ((Lmax + 63) / 64) * 8 > (1ll << 40))
+        return SWITCHSD_ESHAPE;
+    if (n < 1 || n > 64)
+        return SWITCHSD_EINVAL;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!tokens || !lengths || !labels)
+        return SWITCHSD_EINVAL;
+    if (!workspace || ((uintptr_t)workspace & (kAlign - 1)) ||
+        workspace_bytes < switchsd_label_workspace_bytes(B, Lmax))
+        return SWITCHSD_EWORKSPACE;
+    StepParams p;
+    memset(&p, 0, sizeof p);
+    p.tokens = tokens;
+    p.lengths = lengths;
+    p.B = B;
+    p.Lmax = Lmax;
+    const int64_t nblocks = (Lmax + 63) / 64;
+    const int64_t grid = (int64_t)B * ((nblocks + 15) / 16) * ((Lmax - 1 + 255) / 256 + 1);
+    if (!grid_ok(grid))
+        return SWITCHSD_ESHAPE;
+    return launch_label_kernels(p, n, workspace, labels, stream);
+}
+
 int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,
                     const int32_t *out_tokens, int32_t R, const int32_t *accept_len,
                     const int32_t *use_copy, int32_t *draft_pos, int32_t *lag,

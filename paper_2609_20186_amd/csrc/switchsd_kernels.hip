@@ -1648,6 +1648,114 @@ __global__ __launch_bounds__(kThreads) void k_sample_pick(StepParams p) {
         final_epilogue(p, b, sh);
 }
 
+// ------------------------------------------------------------- copy-mode labels
+
+// Copy-mode labels for probe training (Sec. 3.2, Problem Formulation):
+// position j is copy-mode iff an n-token window covering it repeats an
+// earlier window.  For a distance delta >= 1, bit l of the ballot D over the
+// block of end positions 64w..64w+63 is x[j] == x[j - delta]; a window
+// starting at s repeats the one at s - delta iff bits s..s+n-1 are all set, so
+// the starts of repeated windows are the AND of D shifted by 0..n-1 (carrying
+// in the next block's ballot) -- scalar mask operations per (delta, block).
+// The starts of all distances are OR-ed into the workspace (one bit per
+// position), then widened by n - 1 positions into the labels.
+
+constexpr int kLabelBlocks = 16;   // 64-position blocks per work-group
+constexpr int kLabelDeltas = 256;  // distances per work-group
+
+__global__ __launch_bounds__(kThreads) void k_label_starts(StepParams p, int32_t n, int32_t nbg,
+                                                           int32_t ndg,
+                                                           unsigned long long *starts) {
+    // xb: positions of the range and the next block; xa: those positions
+    // moved back by every distance of the group
+    __shared__ int32_t xb[64 * kLabelBlocks + 64];
+    __shared__ int32_t xa[64 * kLabelBlocks + 64 + kLabelDeltas];
+    __shared__ unsigned long long acc_s[kLabelBlocks];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int dg = blockIdx.x % ndg;
+    const int bg = (blockIdx.x / ndg) % nbg;
+    const int b = blockIdx.x / (ndg * nbg);
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+    const int nblocks = (p.Lmax + 63) >> 6;
+    const int w_lo = bg * kLabelBlocks;
+    const int w_hi = w_lo + kLabelBlocks < nblocks ? w_lo + kLabelBlocks : nblocks;  // excl.
+    const int d_lo = dg * kLabelDeltas + 1;
+    const int d_hi = d_lo + kLabelDeltas - 1 < L - 1 ? d_lo + kLabelDeltas - 1 : L - 1;  // incl.
+    // distances that reach no position of the range (or past the context)
+    if (d_lo > d_hi || d_lo > 64 * w_hi - 1)
+        return;
+    const int b_len = 64 * (w_hi + 1 - w_lo);       // <= 64 * kLabelBlocks + 64
+    const int a_lo = 64 * w_lo - d_hi;                // may be negative
+    const int a_len = b_len + (d_hi - d_lo);          // <= 64 * kLabelBlocks + 64 + kLabelDeltas
+    const int64_t row = (int64_t)b * p.Lmax;
+    for (int i = tid; i < b_len; i += kThreads) {
+        const int x = 64 * w_lo + i;
+        xb[i] = x < L ? p.tokens[row + x] : 0;
+    }
+    for (int i = tid; i < a_len; i += kThreads) {
+        const int x = a_lo + i;
+        xa[i] = x >= 0 && x < L ? p.tokens[row + x] : 0;
+    }
+    if (tid < kLabelBlocks)
+        acc_s[tid] = 0ull;
+    __syncthreads();
+    // ballot of x[j] == x[j - d] over block w
+    auto diag = [&](int w, int d) -> unsigned long long {
+        const int j = 64 * w + lane;
+        const bool ok = j < L && j - d >= 0 && xb[j - 64 * w_lo] == xa[j - d - a_lo];
+        return __ballot(ok);
+    };
+    unsigned long long acc[kLabelBlocks];
+#pragma unroll
+    for (int i = 0; i < kLabelBlocks; ++i)
+        acc[i] = 0ull;
+    for (int d = d_lo + wave; d <= d_hi; d += kWaves) {
+        unsigned long long Dn = w_hi < nblocks ? diag(w_hi, d) : 0ull;
+#pragma unroll
+        for (int i = kLabelBlocks - 1; i >= 0; --i) {
+            const int w = w_lo + i;
+            if (w >= w_hi)
+                continue;
+            const unsigned long long D = diag(w, d);
+            unsigned long long S = D;
+            for (int u = 1; u < n && S; ++u)
+                S &= (D >> u) | (Dn << (64 - u));
+            acc[i] |= S;
+            Dn = D;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kLabelBlocks; ++i)
+        if (lane == 0 && acc[i])
+            atomicOr(&acc_s[i], acc[i]);
+    __syncthreads();
+    if (tid < kLabelBlocks && w_lo + tid < w_hi && acc_s[tid])
+        atomicOr(&starts[(int64_t)b * nblocks + w_lo + tid], acc_s[tid]);
+}
+
+// Labels of one sequence: position j is copy-mode iff a repeated window
+// starts in [j - n + 1, j]; the start bits are cleared again afterwards.
+__global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t n,
+                                                          unsigned long long *starts,
+                                                          uint8_t *labels) {
+    const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int nblocks = (p.Lmax + 63) >> 6;
+    unsigned long long *st = starts + (int64_t)b * nblocks;
+    for (int w = wave; w < nblocks; w += kWaves) {
+        const unsigned long long E = ld_u64(&st[w]);
+        const unsigned long long Ep = w > 0 ? ld_u64(&st[w - 1]) : 0ull;
+        unsigned long long Y = E;
+        for (int u = 1; u < n; ++u)
+            Y |= (E << u) | (Ep >> (64 - u));
+        const int j = 64 * w + lane;
+        if (j < p.Lmax)
+            labels[(int64_t)b * p.Lmax + j] = (uint8_t)((Y >> lane) & 1ull);
+    }
+    __syncthreads();
+    for (int w = tid; w < nblocks; w += kThreads)
+        st_u64(&st[w], 0ull);
+}
+
 // ------------------------------------------------------------- kernels
 
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
@@ -1816,6 +1924,21 @@ int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream) {
 
 int launch_commit_kernel(const StepParams &p, hipStream_t stream) {
     hipLaunchKernelGGL(k_commit, dim3((unsigned)p.B), dim3(64), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_label_kernels(const StepParams &p, int32_t n, void *starts, uint8_t *labels,
+                         hipStream_t stream) {
+    const int nblocks = (p.Lmax + 63) / 64;
+    const int nbg = (nblocks + kLabelBlocks - 1) / kLabelBlocks;
+    const int ndg = p.Lmax > 1 ? (p.Lmax - 1 + kLabelDeltas - 1) / kLabelDeltas : 1;
+    const int64_t grid = (int64_t)p.B * nbg * ndg;
+    hipLaunchKernelGGL(k_label_starts, dim3((unsigned)grid), dim3(kThreads), 0, stream, p, n,
+                       nbg, ndg, (unsigned long long *)starts);
+    if (hipGetLastError() != hipSuccess)
+        return SWITCHSD_EHIP;
+    hipLaunchKernelGGL(k_label_write, dim3((unsigned)p.B), dim3(kThreads), 0, stream, p, n,
+                       (unsigned long long *)starts, labels);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 

@@ -186,6 +186,21 @@ def test_sample_entry_point_rejects():
     assert call_step(a, nbytes=1 << 15) == EINVAL
 
 
+def test_label_entry_point_rejects():
+    lib = sd.lib
+    need = sd.label_workspace_bytes(2, 100)
+    assert need == 256 and sd.label_workspace_bytes(3, 4096) == 3 * 64 * 8
+    assert sd.label_workspace_bytes(-1, 5) == 0
+    assert lib.switchsd_copy_labels(P, P, -1, 100, 5, P, WS, need, None) == ESHAPE
+    assert lib.switchsd_copy_labels(P, P, 2, 0, 5, P, WS, need, None) == ESHAPE
+    assert lib.switchsd_copy_labels(P, P, 2, 100, 0, P, WS, need, None) == EINVAL
+    assert lib.switchsd_copy_labels(P, P, 2, 100, 65, P, WS, need, None) == EINVAL
+    assert lib.switchsd_copy_labels(P, None, 2, 100, 5, P, WS, need, None) == EINVAL
+    assert lib.switchsd_copy_labels(P, P, 2, 100, 5, P, WS + 8, need, None) == EWORKSPACE
+    assert lib.switchsd_copy_labels(P, P, 2, 4096, 5, P, WS, need, None) == EWORKSPACE
+    assert lib.switchsd_copy_labels(None, None, 0, 100, 5, None, None, 0, None) == OK
+
+
 def test_commit_entry_point_rejects():
     lib = sd.lib
     assert lib.switchsd_commit(P, P, -1, 16, P, 8, P, P, P, P, None) == ESHAPE
