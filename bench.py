@@ -124,6 +124,72 @@ def cpu_baseline(wl_name, budget_s):
                       f"{threads} threads"}
 
 
+def decode_loop(args, wl, d, sets, cfg, sd, torch, T, uni, sws):
+    """K steps with commit captured in one HIP graph, cycling over the input
+    copies (the contexts, lengths and draft-model positions are shared and
+    grow); each replay starts from the initial contexts (restored outside the
+    timed region)."""
+    K = args.loop
+    B, R = wl.B, wl.R
+    Lmax = wl.L + K * R
+    tokens = torch.zeros((B, Lmax), dtype=torch.int32, device="cuda")
+    tokens[:, :wl.L] = sets[0]["tokens"]
+    lengths0 = sets[0]["lengths"].clone()
+    lengths = lengths0.clone()
+    draft_pos = lengths0.clone()
+    lag = torch.zeros(B, dtype=torch.int32, device="cuda")
+    tokens0 = tokens.clone()
+    nset = len(sets)
+    outs = [sd.alloc_outputs(B, R, wl.k, wl.n_cand) for _ in range(nset)]
+    ws = sd.alloc_workspace(B, R, Lmax, wl.n_cand)
+    args_l = []
+    for st, o in zip(sets, outs):
+        inp = dict(st)
+        inp["tokens"], inp["lengths"] = tokens, lengths
+        args_l.append(sd.build_step_args(inp, o, cfg, args.mode, T, uni, sws, draft_pos, lag))
+
+    def run_steps():
+        for i in range(K):
+            sd.switchsd_step(args_l[i % nset], ws)
+
+    def reset():
+        tokens.copy_(tokens0)
+        lengths.copy_(lengths0)
+        draft_pos.copy_(lengths0)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run_steps()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    eager_len = lengths.clone()
+    reset()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_steps()
+    reps = max(3, args.steps // K)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    total = 0.0
+    for rep in range(reps + 1):
+        reset()
+        torch.cuda.synchronize()
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if rep > 0:                      # the first replay is a warm-up
+            total += e0.elapsed_time(e1)
+        assert torch.equal(lengths, eager_len), "graph replay disagrees with the eager loop"
+    us = total / reps / K * 1e3
+    grown = (eager_len - lengths0).float().mean().item()
+    return {"steps_per_graph": K, "replays": reps, "us_per_step": round(us, 2),
+            "steps_per_s": round(1e6 / us, 1),
+            "tokens_appended_per_sequence_per_step": round(grown / K, 3),
+            "note": "contexts grow in place; inputs cycle over the rotation copies"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,6 +200,12 @@ def main():
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="> 0: verification draws the rows' tokens at this sampling "
                          "temperature (App. A) with seeded uniforms")
+    ap.add_argument("--loop", type=int, default=0,
+                    help="also time the decode loop: this many steps with commit (append "
+                         "the accepted tokens, draft-model lag) captured in one HIP graph")
+    ap.add_argument("--labels", type=int, default=0,
+                    help="also time the copy-mode labels (Sec. 3.2) of the workload's "
+                         "contexts with this window length n (the paper's is 5)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -252,6 +324,30 @@ def main():
     vbytes = int(np.sum(sel["dn"])) * wl.V * 2
     v_gbps = vbytes / (vms * 1e-3) / 1e9
 
+    loop_res = None
+    if args.loop > 0:
+        loop_res = decode_loop(args, wl, d, sets, cfg, sd, torch, T,
+                               uni if T > 0 else None, sws if T > 0 else None)
+
+    label_res = None
+    if args.labels > 0:
+        lab = torch.empty(base["tokens"].shape, dtype=torch.uint8, device="cuda")
+        lws = torch.zeros(max(sd.label_workspace_bytes(wl.B, wl.L), 256), dtype=torch.uint8,
+                          device="cuda")
+        for _ in range(3):
+            sd.switchsd_copy_labels(base["tokens"], base["lengths"], args.labels, lab, lws)
+        torch.cuda.synchronize()
+        nl = 20
+        e0.record(stream)
+        for _ in range(nl):
+            sd.switchsd_copy_labels(base["tokens"], base["lengths"], args.labels, lab, lws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        lus = e0.elapsed_time(e1) / nl * 1e3
+        label_res = {"n": args.labels, "us_per_call": round(lus, 1),
+                     "positions_per_s": round(wl.B * wl.L / (lus * 1e-6), 1),
+                     "copy_mode_share": round(float(lab.float().mean().item()), 4)}
+
     if args.copy_calibration_mb > 0:
         n = args.copy_calibration_mb << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
@@ -310,6 +406,10 @@ def main():
         "mean_accept_len": round(float(o0["accept_len"].float().mean()), 3),
         "kernel_sha": kernel_sha(),
     }
+    if loop_res:
+        res["decode_loop"] = loop_res
+    if label_res:
+        res["copy_labels"] = label_res
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl.name, args.cpu_seconds)
