@@ -16,7 +16,15 @@
  *   4. greedy verification -- Sec. 2 (Speculative Decoding) and App. A
  *      (T = 0): the target's token at each drafted position is the argmax of
  *      its logits, and the longest validated continuation is kept (Sec. 3.3,
- *      Parallel Verification) together with the target's next token (bonus).
+ *      Parallel Verification) together with the target's next token (bonus);
+ *      at sampling temperature T > 0 the target's tokens are drawn instead
+ *      (App. A; switchsd_verify_sample).
+ *
+ * Around the step: the verification mask of the drafts (switchsd_tree_mask),
+ * the decode loop's commit with the draft model's lazy-propagation counters
+ * (switchsd_commit, or `commit` in switchsd_step; Sec. 3.3, KV Cache
+ * Synchronization), and the copy-mode labels the probe is trained on
+ * (switchsd_copy_labels; Sec. 3.2).
  *
  * Conventions for every entry point:
  *   - All array pointers are DEVICE pointers owned by the caller; arrays are
@@ -36,7 +44,7 @@
  *     [1, R], and a node whose parent is not in [0, i) is never accepted.
  *   - Host-side validation runs before any HIP call; on failure a negative
  *     status is returned and nothing is launched.  B = 0 is a valid no-op.
- *   - Calls that take a workspace need
+ *   - Calls that take a workspace (the step and its stages) need
  *     `switchsd_workspace_bytes(B, R, Lmax, cfg.n_cand)` bytes, 256-byte
  *     aligned, zeroed once by the caller at allocation.  Every kernel leaves
  *     its tickets, slots and row keys zeroed again when it completes (the

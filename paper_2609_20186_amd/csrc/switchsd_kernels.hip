@@ -1,7 +1,8 @@
 // switchsd_kernels.hip -- gfx950 kernels of SwitchSD's speculation-control step.
 //
-// One kernel body serves every entry point.  Its work-groups take one of
-// three roles by block index, laid out as [scan tiles | probe | argmax]:
+// One kernel body (k_switchsd) serves the greedy step and its stages.  Its
+// work-groups take one of three roles by block index, laid out as
+// [scan tiles | probe | argmax]:
 //
 //   scan    a 2048-position tile of one context, staged in LDS with a
 //           64-token halo; ballots over blocks of 64 end positions mark the
@@ -29,8 +30,15 @@
 //           argmaxes and run the accept walk (Sec. 3.3, Parallel Verification):
 //           a ballot for chains and pointer jumping over trees, in registers
 //           (one node per lane) up to 64 nodes and in LDS beyond.
-// Each epilogue resets the workspace slots it consumed, leaving the workspace
-// zeroed for the next call.
+// With the decode loop's commit the final epilogue also appends the accepted
+// tokens and the bonus to the context.  Each epilogue resets the workspace
+// slots it consumed, leaving them zeroed for the next call.
+//
+// Further kernels: k_verify_stream (verification of long drafts over a fixed
+// grid), k_sample_sums / k_sample_sums_stream / k_sample_pick (verification at
+// sampling temperature T > 0), k_select and k_commit (stage entry points),
+// k_tree_mask (the verification mask), k_label_starts / k_label_write
+// (copy-mode labels for probe training).
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -293,6 +301,9 @@ struct Prefetch {
 // from the LDS tile (its 64-position halo covers u < 64), with the blocks'
 // reads issued together: one compare and one 64-bit AND per block and offset.
 
+// kMulti: the W > 1 candidate lists are compiled in (the host launches the
+// instantiation that matches the configuration).
+template <bool kMulti>
 __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetch &pre) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int64_t row = (int64_t)b * p.Lmax;
@@ -354,7 +365,7 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     }
     if (tid < SWITCHSD_MAX_NGRAM)
         sh.scan.red[tid] = 0;
-    if (p.W > 1)
+    if (kMulti && p.W > 1)
         for (int i = tid; i < SWITCHSD_MAX_NGRAM * kWaves * kMaxCand; i += kThreads)
             sh.scan.cand[i] = 0;
     if (tid == 0)
@@ -405,7 +416,7 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
                 for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
                     if (j == jm)
                         best[j] = e1;
-                if (p.W > 1) {
+                if (kMulti && p.W > 1) {
                     // keep the block masks of this length for the candidate lists
                     unsigned long long m = 0ull;
 #pragma unroll
@@ -422,7 +433,7 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
         if (j < p.n_ngram && lane == 0 && best[j] > 0)
             atomicMax(&sh.scan.red[j], best[j]);
-    if (p.W > 1 && elim > 0) {
+    if (kMulti && p.W > 1 && elim > 0) {
         // the wave's W most recent ends per length: lane i < kScanBlocks takes block
         // i's mask and the count of marked ends in later blocks, then lists
         // its own ends from the highest down
@@ -921,6 +932,8 @@ __device__ __forceinline__ int32_t decode_key(unsigned long long key) {
     return key ? (int32_t)(0xFFFFFFFFu - (uint32_t)key) : 0;
 }
 
+// kCommit: the decode loop's commit is compiled in.
+template <bool kCommit>
 __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
     const int lane = threadIdx.x;
     const int64_t base = (int64_t)b * p.R;
@@ -928,7 +941,7 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
     // decode loop (Sec. 3.3, KV Cache Synchronization): the accepted tokens and
     // the bonus also go to the context at its length cL
     int cL = 0, cdp = 0, cuc = 0;
-    if (p.commit) {
+    if (kCommit) {
         cL = clampi(p.clen[b], 0, p.Lmax);
         cdp = p.draft_pos[b];
         cuc = ld_i32(&p.use_copy[b]);
@@ -937,7 +950,7 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
     // output position j of the accepted path (then the bonus) holds v
     auto emit = [&](int j, int v) {
         p.out_tokens[base + j] = v;
-        if (p.commit && cL + j < p.Lmax)
+        if (kCommit && cL + j < p.Lmax)
             p.ctok[crow + cL + j] = v;
     };
     int acc = 0;  // accepted length (uniform over the wave)
@@ -1179,7 +1192,7 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         }
         acc = depth;
     }
-    if (p.commit && lane == 0) {
+    if (kCommit && lane == 0) {
         const int Lnew = cL + acc + 1 < p.Lmax ? cL + acc + 1 : p.Lmax;
         const int pos = clampi(cuc ? cdp : cL + acc, 0, Lnew);
         p.clen[b] = Lnew;
@@ -1212,6 +1225,7 @@ __device__ __forceinline__ bool arrive_n(uint32_t *ticket, uint32_t n, uint32_t 
 // a row piece each wave max-combines its (value, index) into the row's key; at
 // the end of a sequence piece the work-group arrives with its unit count, and
 // the last arrival (dn[b] * chunks per row in all) runs the accept epilogue.
+template <bool kCommit>
 __device__ void verify_stream(const StepParams &p, Shared &sh) {
     const int tid = threadIdx.x, lane = tid & 63;
     constexpr int Q = kListMaxB / 64;
@@ -1301,7 +1315,7 @@ __device__ void verify_stream(const StepParams &p, Shared &sh) {
             __syncthreads();
             if (tid < 64 && arrive_n(&p.ws.tk_all[b * kLineU32], (uint32_t)done_b,
                                      (uint32_t)(dnb * cpr)))
-                final_epilogue(p, b, sh);
+                final_epilogue<kCommit>(p, b, sh);
             done_b = 0;
         }
         b = nb;
@@ -1520,6 +1534,7 @@ __device__ __forceinline__ unsigned long long scaled_target(uint32_t u, unsigned
 // vector block (256 vectors) and vector from the re-read chunk, the element
 // within the vector.  The drawn token replaces the row's argmax key; then the
 // row arrives at its sequence, and the last row runs the accept epilogue.
+template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_pick(StepParams p) {
     __shared__ Shared sh;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -1645,7 +1660,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_pick(StepParams p) {
     if (tid >= 64)
         return;
     if (arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)p.R))
-        final_epilogue(p, b, sh);
+        final_epilogue<kCommit>(p, b, sh);
 }
 
 // ------------------------------------------------------------- copy-mode labels
@@ -1758,6 +1773,7 @@ __global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t 
 
 // ------------------------------------------------------------- kernels
 
+template <bool kMulti, bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     __shared__ Shared sh;
     const int blk = blockIdx.x;
@@ -1767,7 +1783,7 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     if (blk < p.n_scan_wg) {
         b = blk / p.scan_tiles;
         t = blk - b * p.scan_tiles;
-        scan_role(p, b, t, sh, pre);
+        scan_role<kMulti>(p, b, t, sh, pre);
         role = 0;
     } else if (blk < p.n_front_wg) {
         b = blk - p.n_scan_wg;
@@ -1792,7 +1808,7 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
                 atomicMax(&p.ws.mslot[b * kLineU32 + lane], sh.scan.red[lane]);
             if (t == 0 && p.scan_probe && lane == 0)
                 st_f32(&p.z[b], probe_combine(sh.scan.ps, sh.scan.pc, p.bias));
-            if (p.W > 1) {
+            if (kMulti && p.W > 1) {
                 int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride +
                               (int64_t)t * SWITCHSD_MAX_NGRAM * p.W;
                 for (int j = 0; j < p.n_ngram; ++j) {
@@ -1807,13 +1823,14 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     }
     if (p.epi_accept && role != 1) {
         if (arrive(&p.ws.tk_all[b * kLineU32], p.exp_all))
-            final_epilogue(p, b, sh);
+            final_epilogue<kCommit>(p, b, sh);
     }
 }
 
+template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_verify_stream(StepParams p) {
     __shared__ Shared sh;
-    verify_stream(p, sh);
+    verify_stream<kCommit>(p, sh);
 }
 
 // Stand-alone commit of a finished step (one wave per sequence).
@@ -1901,9 +1918,24 @@ int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, i
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
     if (p.list_mode)
-        hipLaunchKernelGGL(k_verify_stream, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+        if (p.commit)
+            hipLaunchKernelGGL((k_verify_stream<true>), dim3((unsigned)grid), dim3(kThreads), 0,
+                               stream, p);
+        else
+            hipLaunchKernelGGL((k_verify_stream<false>), dim3((unsigned)grid), dim3(kThreads), 0,
+                               stream, p);
+    else if (p.W > 1 && p.commit)
+        hipLaunchKernelGGL((k_switchsd<true, true>), dim3((unsigned)grid), dim3(kThreads), 0,
+                           stream, p);
+    else if (p.W > 1)
+        hipLaunchKernelGGL((k_switchsd<true, false>), dim3((unsigned)grid), dim3(kThreads), 0,
+                           stream, p);
+    else if (p.commit)
+        hipLaunchKernelGGL((k_switchsd<false, true>), dim3((unsigned)grid), dim3(kThreads), 0,
+                           stream, p);
     else
-        hipLaunchKernelGGL(k_switchsd, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL((k_switchsd<false, false>), dim3((unsigned)grid), dim3(kThreads), 0,
+                           stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 
@@ -1917,8 +1949,11 @@ int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t str
 }
 
 int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream) {
-    hipLaunchKernelGGL(k_sample_pick, dim3((unsigned)((int64_t)p.B * p.R)), dim3(kThreads), 0,
-                       stream, p);
+    const dim3 grid((unsigned)((int64_t)p.B * p.R));
+    if (p.commit)
+        hipLaunchKernelGGL((k_sample_pick<true>), grid, dim3(kThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL((k_sample_pick<false>), grid, dim3(kThreads), 0, stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 

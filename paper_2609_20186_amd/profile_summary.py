@@ -70,7 +70,9 @@ def _counter(d, counter, kernel):
         if r.get("Counter_Name") != counter:
             continue
         v = float(r["Counter_Value"])
-        if kernel + "(" in r["Kernel_Name"] or r["Kernel_Name"].endswith(kernel):
+        name = r["Kernel_Name"]
+        # plain or templated (k_switchsd<false, false>) instantiations
+        if kernel + "(" in name or kernel + "<" in name or name.endswith(kernel):
             grid = int(r.get("Grid_Size", 0) or 0)
             k.append((grid, v))
         elif COPY in r["Kernel_Name"]:
