@@ -15,7 +15,7 @@ constexpr int kUnroll = 4;
 // 16-byte vectors in one chunk (16 KB); two chunks are in flight per work-group.
 constexpr int kChunkVecs = kThreads * kUnroll;
 // Context end positions covered by one scan work-group.
-constexpr int kScanTile = 2048;
+constexpr int kScanTile = 1024;
 // Per-sequence workspace slots live on their own 256-byte lines: atomics to
 // one line serialize, and every work-group of a sequence arrives at its line.
 constexpr int kLineU32 = 64;

@@ -482,7 +482,6 @@ __device__ __forceinline__ float hi_f(uint32_t x) { return __uint_as_float(x & 0
 __device__ __forceinline__ float max3n(float a, float b, float c) {
     return __builtin_elementwise_maximum(a, __builtin_elementwise_maximum(b, c));
 }
-__device__ __forceinline__ float fmax_nonan(float m, float x) { return x > m ? x : m; }
 
 // Order-preserving key of a float; -0 is folded onto +0.
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -502,15 +501,57 @@ __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
     return (uint32_t)(nnb > cn ? nnb : cn);
 }
 
-// One chunk of a segment: vectors [qc0, qc0 + kChunkVecs) of the segment's
-// aligned interior (nq vectors; row-relative element index of vector q is
-// ebase + 8q), plus this lane's head or tail element when `x_on`.  Updates
-// the wave's running maximum runM and the lowest row-relative index runI
-// holding it (kNoIdx: no candidate yet).  Chunks arrive in increasing index
-// order, so an equal maximum in a later chunk never replaces runI.
-__device__ __forceinline__ void argmax_chunk(u32x4 (&v)[kUnroll], int qc0, int nq, uint32_t ebase,
-                                             bool x_on, float xv, uint32_t xi, float &runM,
-                                             uint32_t &runI) {
+// Running argmax of one lane over the 16 KB chunks it reduces, in increasing
+// index order.  Per chunk only the lane's maximum is taken; the chunk that
+// raised it is kept, and the lowest index holding the maximum is looked up
+// once at the end (lazy_index), so the streaming loop carries no cross-lane
+// work.  best is NaN while the lane has seen no non-NaN element.  The kept
+// chunk sits in registers (LazyMax) or, where registers are short, in LDS
+// (LazyMaxLds: vector u of lane t at d[u * kThreads + t]).
+struct LazyMax {
+    float best;
+    int q0;                 // first vector index of the kept chunk
+    u32x4 d[kUnroll];       // the kept chunk
+    __device__ __forceinline__ u32x4 get(int u) const { return d[u]; }
+    __device__ __forceinline__ void keep(bool upd, const u32x4 (&v)[kUnroll]) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+            for (int w4 = 0; w4 < 4; ++w4)
+                d[u][w4] = upd ? v[u][w4] : d[u][w4];
+    }
+};
+struct LazyMaxLds {
+    float best;
+    int q0;
+    u32x4 *d;
+    __device__ __forceinline__ u32x4 get(int u) const { return d[u * kThreads + threadIdx.x]; }
+    __device__ __forceinline__ void keep(bool upd, const u32x4 (&v)[kUnroll]) {
+        if (upd) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                d[u * kThreads + threadIdx.x] = v[u];
+        }
+    }
+};
+
+template <typename S>
+__device__ __forceinline__ void lazy_init(S &s) {
+    s.best = __builtin_nanf("");
+    s.q0 = 0;
+}
+
+// Maximum ignoring NaN; NaN only when both are NaN (or m is and x is).
+__device__ __forceinline__ float fmax_first(float m, float x) {
+    return (m != m || x > m) ? x : m;
+}
+
+// Chunk [qc0, qc0 + kChunkVecs) of a row piece of nq vectors; vectors past nq
+// read as -inf and are never reported (lazy_index checks q < nq).  A later
+// chunk replaces the kept one only with a strictly larger maximum, so ties
+// stay with the earliest chunk.
+template <typename S>
+__device__ __forceinline__ void lazy_chunk(u32x4 (&v)[kUnroll], int qc0, int nq, S &s) {
     const int tid = threadIdx.x;
     if (qc0 + kChunkVecs > nq) {
 #pragma unroll
@@ -518,7 +559,7 @@ __device__ __forceinline__ void argmax_chunk(u32x4 (&v)[kUnroll], int qc0, int n
             if (qc0 + u * kThreads + tid >= nq)
                 v[u] = u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
     }
-    float m = x_on ? xv : -__builtin_inff();
+    float m = -__builtin_inff();
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
         m = max3n(m, lo_f(v[u][0]), hi_f(v[u][0]));
@@ -528,43 +569,52 @@ __device__ __forceinline__ void argmax_chunk(u32x4 (&v)[kUnroll], int qc0, int n
     }
     if (__any(m != m)) {  // a NaN somewhere: recompute those lanes ignoring NaN
         if (m != m) {
-            m = x_on ? fmax_nonan(-__builtin_inff(), xv) : -__builtin_inff();
+            m = __builtin_nanf("");
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
                 for (int w4 = 0; w4 < 4; ++w4) {
-                    m = fmax_nonan(m, lo_f(v[u][w4]));
-                    m = fmax_nonan(m, hi_f(v[u][w4]));
+                    m = fmax_first(m, lo_f(v[u][w4]));
+                    m = fmax_first(m, hi_f(v[u][w4]));
                 }
         }
     }
-    if (runI == kNoIdx || __any(m > runM)) {
-        const float W = wave_max_f32(m);
-        if (runI == kNoIdx || W > runM) {
-            uint32_t idx = kNoIdx;
-            if (m == W) {
-                if (x_on && xv == W)
-                    idx = xi;
+    const bool upd = m == m && !(m <= s.best);
+    s.best = upd ? m : s.best;
+    s.q0 = upd ? qc0 : s.q0;
+    s.keep(upd, v);
+}
+
+// Lowest row-relative index (vector q is at ebase + 8q) of an element equal to
+// the lane's maximum in its kept chunk; kNoIdx when the lane has none.  -0 and
+// +0 compare equal.
+template <typename S>
+__device__ __forceinline__ uint32_t lazy_index(const S &s, int nq, uint32_t ebase) {
+    uint32_t idx = kNoIdx;
+    if (s.best == s.best) {
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    const int q = qc0 + u * kThreads + tid;
-                    const uint32_t e = ebase + (uint32_t)q * 8u;
+        for (int u = kUnroll - 1; u >= 0; --u) {  // descending: the last hit is the lowest
+            const int q = s.q0 + u * kThreads + (int)threadIdx.x;
+            const uint32_t e = ebase + (uint32_t)q * 8u;
+            const u32x4 d = s.get(u);
 #pragma unroll
-                    for (int w4 = 0; w4 < 4; ++w4) {
-                        if (q < nq && lo_f(v[u][w4]) == W && e + w4 * 2u < idx)
-                            idx = e + w4 * 2u;
-                        if (q < nq && hi_f(v[u][w4]) == W && e + w4 * 2u + 1u < idx)
-                            idx = e + w4 * 2u + 1u;
-                    }
-                }
-            }
-            idx = wave_min_u32(idx);
-            if (idx != kNoIdx) {  // W is a real element (not only -inf padding)
-                runM = W;
-                runI = idx;
+            for (int w4 = 3; w4 >= 0; --w4) {
+                if (q < nq && hi_f(d[w4]) == s.best)
+                    idx = e + w4 * 2u + 1u;
+                if (q < nq && lo_f(d[w4]) == s.best)
+                    idx = e + w4 * 2u;
             }
         }
     }
+    return idx;
+}
+
+// Wave argmax of (value, index) pairs, index kNoIdx meaning none: the largest
+// value, ties to the lowest index.  Returns the index (kNoIdx when the wave has
+// none) and the value in W.
+__device__ __forceinline__ uint32_t wave_argmax(float v, uint32_t idx, float &W) {
+    W = wave_max_f32(idx != kNoIdx ? v : -__builtin_inff());
+    return wave_min_u32(idx != kNoIdx && v == W ? idx : kNoIdx);
 }
 
 __device__ __forceinline__ void load_chunk(u32x4 (&v)[kUnroll], const u32x4 *vp, int qc0, int nq) {
@@ -602,11 +652,10 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
         xg = a1 + (tid - nhead);
     const float xv = xg >= 0 ? lo_f((uint32_t)p.logits[xg]) : -__builtin_inff();
     const uint32_t xi = (uint32_t)(xg - rowoff);
-    const bool is_head = tid < nhead;
     const bool has_x = xg >= 0;
 
-    float runM = -__builtin_inff();
-    uint32_t runI = kNoIdx;
+    LazyMax st;
+    lazy_init(st);
     const int nch = (nq + kChunkVecs - 1) / kChunkVecs;
     // Whether the row is needed at all may depend on the draft (a global read);
     // with `speculate` the first chunk is already in flight meanwhile.
@@ -618,29 +667,33 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
         __builtin_amdgcn_s_waitcnt(0);
         return;
     }
-    if (nch == 0) {
-        u32x4 v[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            v[u] = u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
-        argmax_chunk(v, 0, 0, ebase, has_x, xv, xi, runM, runI);
-    } else {
-        // double buffer: chunk c + 1 is in flight while chunk c is reduced; the
-        // head element joins the first chunk, the tail element the last one
+    if (nch > 0) {
+        // double buffer: chunk c + 1 is in flight while chunk c is reduced.
+        // The loop body has a single exit at its end, so that no path reaches
+        // the next iteration with the other buffer's loads still pending (the
+        // compiler would then wait for every load at the top of the loop).
+        // A load past the last chunk reads the last vector again (clamped).
         if (!spec)
             load_chunk(A, vp, 0, nq);
-        for (int c = 0; c < nch; c += 2) {
+        int c = 0;
+        for (; c + 1 < nch; c += 2) {
             load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
-            argmax_chunk(A, c * kChunkVecs, nq, ebase,
-                         has_x && ((is_head && c == 0) || (!is_head && c == nch - 1)), xv, xi,
-                         runM, runI);
-            if (c + 1 >= nch)
-                break;
+            lazy_chunk(A, c * kChunkVecs, nq, st);
             load_chunk(A, vp, (c + 2) * kChunkVecs, nq);
-            argmax_chunk(Bv, (c + 1) * kChunkVecs, nq, ebase, has_x && !is_head && c + 1 == nch - 1,
-                         xv, xi, runM, runI);
+            lazy_chunk(Bv, (c + 1) * kChunkVecs, nq, st);
         }
+        if (c < nch)  // odd count: the last chunk
+            lazy_chunk(A, c * kChunkVecs, nq, st);
     }
+    // the head and tail elements (lower and higher indices than the interior)
+    float lv = st.best;
+    uint32_t li = lazy_index(st, nq, ebase);
+    if (has_x && xv == xv && (li == kNoIdx || xv > lv || (xv == lv && xi < li))) {
+        lv = xv;
+        li = xi;
+    }
+    float runM;
+    const uint32_t runI = wave_argmax(lv, li, runM);
     const int wave = tid >> 6, lane = tid & 63;
     if (lane == 0) {
         sh.am.wmax[wave] = runM;
@@ -1226,7 +1279,7 @@ __device__ __forceinline__ bool arrive_n(uint32_t *ticket, uint32_t n, uint32_t 
 // the end of a sequence piece the work-group arrives with its unit count, and
 // the last arrival (dn[b] * chunks per row in all) runs the accept epilogue.
 template <bool kCommit>
-__device__ void verify_stream(const StepParams &p, Shared &sh) {
+__device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
     const int tid = threadIdx.x, lane = tid & 63;
     constexpr int Q = kListMaxB / 64;
     const int cpr = p.segs;
@@ -1274,8 +1327,9 @@ __device__ void verify_stream(const StepParams &p, Shared &sh) {
     };
     u32x4 A[kUnroll], Bv[kUnroll];
     load_chunk(A, row_vecs(b, r), c * kChunkVecs, nq);
-    float runM = -__builtin_inff();
-    uint32_t runI = kNoIdx;
+    LazyMaxLds st;
+    st.d = keep;
+    lazy_init(st);
     int done_b = 0;  // units of sequence b streamed here
     for (int u = u0; u < u1; ++u) {
         // the next unit
@@ -1298,17 +1352,18 @@ __device__ void verify_stream(const StepParams &p, Shared &sh) {
         }
         if (u + 1 < u1)
             load_chunk(Bv, row_vecs(nb, nr), nc * kChunkVecs, nq);
-        argmax_chunk(A, c * kChunkVecs, nq, 0u, false, 0.0f, 0u, runM, runI);
+        lazy_chunk(A, c * kChunkVecs, nq, st);
         ++done_b;
         const bool last_unit = u + 1 == u1;
         if (c == cpr - 1 || last_unit) {  // end of this row's piece
+            float runM;
+            const uint32_t runI = wave_argmax(st.best, lazy_index(st, nq, 0u), runM);
             if (lane == 0 && runI != kNoIdx) {
                 const unsigned long long key =
                     ((unsigned long long)order_key(runM) << 32) | (0xFFFFFFFFu - runI);
                 atomicMax(&p.ws.keys[(int64_t)b * p.ws.key_stride + r], key);
             }
-            runM = -__builtin_inff();
-            runI = kNoIdx;
+            lazy_init(st);
         }
         if ((nb != b || last_unit) && p.epi_accept) {  // end of this sequence's piece
             __builtin_amdgcn_s_waitcnt(0);
@@ -1827,10 +1882,13 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     }
 }
 
+// The grid is four work-groups per compute unit, all resident at once.
 template <bool kCommit>
-__global__ __launch_bounds__(kThreads) void k_verify_stream(StepParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void
+k_verify_stream(StepParams p) {
     __shared__ Shared sh;
-    verify_stream<kCommit>(p, sh);
+    __shared__ u32x4 keep[kChunkVecs];  // each lane's kept chunk (running argmax)
+    verify_stream<kCommit>(p, sh, keep);
 }
 
 // Stand-alone commit of a finished step (one wave per sequence).
