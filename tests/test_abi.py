@@ -41,10 +41,12 @@ def test_status_strings_and_workspace_size():
     assert sd.workspace_bytes(64, 8) >= sd.workspace_bytes(32, 8)
     assert sd.workspace_bytes(-1, 8) == 0
     assert sd.workspace_bytes(2, 8, -1, 0) == 0 and sd.workspace_bytes(2, 8, 16, -1) == 0
-    # candidate lists only with several candidates over several 2048-token tiles
-    assert sd.workspace_bytes(2, 8, 2048, 10) == sd.workspace_bytes(2, 8)
-    assert sd.workspace_bytes(2, 8, 2049, 1) == sd.workspace_bytes(2, 8)
-    extra = sd.workspace_bytes(2, 8, 3 * 2048, 10) - sd.workspace_bytes(2, 8)
+    # candidate lists only with several candidates over several scan tiles
+    # (1024 positions each)
+    assert sd.workspace_bytes(2, 8, 1024, 10) == sd.workspace_bytes(2, 8)
+    assert sd.workspace_bytes(2, 8, 1025, 1) == sd.workspace_bytes(2, 8)
+    assert sd.workspace_bytes(2, 8, 1025, 10) > sd.workspace_bytes(2, 8)
+    extra = sd.workspace_bytes(2, 8, 3 * 1024, 10) - sd.workspace_bytes(2, 8)
     assert extra >= 2 * 3 * 8 * 10 * 4 and extra % 256 == 0
 
 

@@ -210,7 +210,7 @@ def test_edge_case_parity(case):
 
 def test_multi_candidate_across_tiles():
     """Occurrences of the suffix 3-gram planted at ends on both sides of the
-    scan-tile boundaries (multiples of 2048) of a 12788-token context: the W
+    scan-tile boundaries (multiples of 1024) of a 12788-token context: the W
     most recent come from different tiles and must be merged latest tile
     first; a candidate near the end is cut at the context end."""
     say("[multi] candidates across scan tiles")
@@ -220,7 +220,7 @@ def test_multi_candidate_across_tiles():
     rng = np.random.default_rng(47)
     # sequence 2 repeats one token, so its occurrences overlap
     ends_by_b = [[100, 4094, 4097, 8190, 8193, 12000, Lmax - 4],
-                 [50, 60, 4200],
+                 [50, 60, 1022, 1025, 3071, 4200],
                  [4094, 4095, 4096, 4097, 4098, 4099, 4100, 8000],
                  []]
     for b, ends in enumerate(ends_by_b):
