@@ -626,7 +626,7 @@ __device__ __forceinline__ void load_chunk(u32x4 (&v)[kUnroll], const u32x4 *vp,
 }
 
 // Segment s of row r of sequence b.
-__device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh) {
+__device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh, u32x4 *keep) {
     const int tid = threadIdx.x;
     const int64_t rowoff = ((int64_t)b * p.R + r) * p.V;
     const int64_t e0 = (int64_t)s * p.seg_elems;
@@ -654,7 +654,8 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
     const uint32_t xi = (uint32_t)(xg - rowoff);
     const bool has_x = xg >= 0;
 
-    LazyMax st;
+    LazyMaxLds st;
+    st.d = keep;
     lazy_init(st);
     const int nch = (nq + kChunkVecs - 1) / kChunkVecs;
     // Whether the row is needed at all may depend on the draft (a global read);
@@ -1831,6 +1832,7 @@ __global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t 
 template <bool kMulti, bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     __shared__ Shared sh;
+    __shared__ u32x4 keep[kChunkVecs];  // argmax role: each lane's kept chunk
     const int blk = blockIdx.x;
     int b, t = 0;
     int role;  // 0 scan, 1 stand-alone probe, 2 argmax
@@ -1849,7 +1851,7 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
         const int rowi = idx / p.segs;
         const int s = idx - rowi * p.segs;
         b = rowi / p.R;
-        argmax_role(p, b, rowi - b * p.R, s, sh);
+        argmax_role(p, b, rowi - b * p.R, s, sh, keep);
         role = 2;
     }
     if (threadIdx.x >= 64)

@@ -234,7 +234,7 @@ def test_multi_candidate_across_tiles():
         [Lmax - 4, 12000, 8193, 8190, 4097, 4094]
     assert exp["copy_len"][0][0] == 3                       # cut at the context end
     assert exp["match_end"][2].tolist() == [8000, 4100, 4099, 4098, 4097, 4096]
-    assert exp["match_end"][1].tolist() == [4200, 60, 50, -1, -1, -1]
+    assert exp["match_end"][1].tolist() == [4200, 3071, 1025, 1022, 60, 50]
     dev = to_device(d)
     for mode in (AUTO, FUSED, SPLIT):
         got, ws = gpu_step(dev, d, mode)
