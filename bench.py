@@ -371,7 +371,11 @@ def main():
         dom = {"kernel": "k_switchsd (fused step)", "gbps": step_gbps, "bytes": alg,
                "traffic_file": f"traffic_fused_step_{wl.name}.json"}
     else:
-        dom = {"kernel": "k_switchsd (verify launch of the split step)", "gbps": v_gbps,
+        # long drafts of up to 256 sequences with 16-byte aligned rows: the
+        # streamed verify kernel; otherwise the step kernel's argmax role
+        streamed = wl.R > 64 and wl.B <= 256 and wl.V % 8 == 0
+        kname = "k_verify_stream" if streamed else "k_switchsd"
+        dom = {"kernel": f"{kname} (verify launch of the split step)", "gbps": v_gbps,
                "bytes": vbytes, "traffic_file": f"traffic_verify_{wl.name}.json"}
     traffic = None
     tf = os.path.join(PROFILES, dom["traffic_file"])
