@@ -16,7 +16,6 @@ of the same workload on this host).  ``--workload C2W10`` measures the paper's
 multi-candidate copy setting (W = 10 candidates of D = 20 tokens, R = 201).
 """
 import argparse
-import hashlib
 import json
 import math
 import os
@@ -39,14 +38,13 @@ VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 # 7 fused multiply-adds, convert, ldexp, convert, accumulate) in the sum pass
 SAMPLE_OPS_PER_LOGIT = 17.5
 METRIC = "speculation-control steps/s + verify-argmax HBM GB/s (% peak), B=32 V=128256"
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_20186_amd", "csrc", "switchsd_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 ROTATE_BYTES = 512 << 20
 
 
 def kernel_sha():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    from paper_2609_20186_amd.profile_summary import kernel_sha as sha
+    return sha()
 
 
 def algorithmic_bytes(wl, rows_read, d_sel=None):

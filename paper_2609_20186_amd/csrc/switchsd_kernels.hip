@@ -4,7 +4,7 @@
 // work-groups take one of three roles by block index, laid out as
 // [scan tiles | probe | argmax]:
 //
-//   scan    a 2048-position tile of one context, staged in LDS with a
+//   scan    a 1024-position tile of one context, staged in LDS with a
 //           64-token halo; ballots over blocks of 64 end positions mark the
 //           occurrences of each suffix n-gram; the most recent end per n-gram
 //           length is max-reduced over the work-group and (atomicMax) the

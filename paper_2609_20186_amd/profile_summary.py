@@ -19,6 +19,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 
@@ -37,9 +38,18 @@ def _rows(d, pattern):
 
 
 def kernel_sha():
-    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "switchsd_kernels.hip")
-    with open(src, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the code (comments and blank space dropped) of the kernels, their
+    launch configuration and the constants they share: a counter reading stays
+    valid while none of these changes."""
+    h = hashlib.sha256()
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+    for name in ("switchsd_kernels.hip", "switchsd_api.cpp", "switchsd_internal.h"):
+        with open(os.path.join(csrc, name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
+    return h.hexdigest()[:16]
 
 
 def trace(d, out, cmd):
@@ -114,7 +124,7 @@ def traffic(fdir, wdir, copy_mb, out_md, out_json, fcmd, wcmd, workload="C2",
              f"| plain copy of {copy_mb} MB: FETCH_SIZE | {copy_fetch:.0f} KiB (scale {sf:.4f}) |",
              f"| plain copy of {copy_mb} MB: WRITE_SIZE | {copy_write:.0f} KiB (scale {sw:.4f}) |",
              f"| scaled HBM bytes per launch (read + write) | {fetch_b + write_b:,.0f} B |",
-             f"| kernel source sha256[:16] | {res['kernel_sha']} |"]
+             f"| kernel code sha256[:16] (comments dropped) | {res['kernel_sha']} |"]
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
