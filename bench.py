@@ -358,9 +358,9 @@ def main():
         del src, dst
 
     # the dominant kernel: the fused launch, or the verify launch of a split step;
-    # at T > 0 the verification's three launches together
+    # at T > 0 the verification's two launches together
     if T > 0:
-        dom = {"kernel": "sampled verification (row maxima + weight sums + pick, 3 launches)",
+        dom = {"kernel": "sampled verification (row maxima, then weight sums with the draw: 2 launches)",
                "bound": "alu", "unit": "TOP/s (VALU lane-ops)", "peak": round(VALU_PEAK_TOPS, 1),
                "gbps": vbytes / 2 * SAMPLE_OPS_PER_LOGIT / (vms * 1e-3) / 1e12,
                "bytes": int(vbytes / 2 * SAMPLE_OPS_PER_LOGIT),
@@ -393,7 +393,7 @@ def main():
                                f" kappa={wl.kappa}" + (f" T={T}" if T > 0 else ""),
                    "global_batch": wl.B, "seq_len": wl.L, "parallelism": "none (1 GPU)",
                    "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode] +
-                             (" + 2 kernels for the draw at T > 0" if T > 0 else ""),
+                             (" + 1 kernel for the weight sums and the draw at T > 0" if T > 0 else ""),
                    "rotation_sets": nrot},
         "roofline": {"bound": dom.get("bound", "hbm"), "achieved": round(dom["gbps"], 1),
                      "peak": dom.get("peak", HBM_PEAK_GBPS), "unit": dom.get("unit", "GB/s"),

@@ -184,7 +184,8 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
  *   are read); logits [B, R, V] bf16 bits, 16-byte aligned, V % 8 == 0 and
  *   V <= 524288; sample_workspace of switchsd_sample_workspace_bytes(B, R, V)
  *   bytes, 256-byte aligned, no initialization needed; other arguments as in
- *   switchsd_verify_accept.  Three launches. */
+ *   switchsd_verify_accept.  Two launches: the row maxima, then the weight
+ *   sums, whose last work-group per row draws the row's token. */
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
                            float temperature, const uint32_t *uniforms, const int32_t *dtok,
                            const int32_t *dpar, const int32_t *dn, int32_t *accept_len,

@@ -67,6 +67,10 @@ int32_t key_stride_for(int32_t R) {
     return (int32_t)(((int64_t)R + kLineU64 - 1) / kLineU64 * kLineU64);
 }
 
+int32_t rtk_stride_for(int32_t R) {
+    return (int32_t)(((int64_t)R + kLineU32 - 1) / kLineU32 * kLineU32);
+}
+
 int scan_tiles_for(int32_t Lmax) { return (int)((Lmax + kScanTile - 1) / kScanTile); }
 
 // int32 per sequence of the candidate lists: every scan tile keeps W ends per
@@ -87,7 +91,9 @@ Workspace carve(void *ws, int32_t B, int32_t R, int32_t Lmax, int32_t W) {
     w.mslot = (int32_t *)(base + 2 * (size_t)B * line);
     w.keys = (unsigned long long *)(base + 3 * (size_t)B * line);
     w.key_stride = key_stride_for(R);
-    w.cand = (int32_t *)(base + 3 * (size_t)B * line + (size_t)B * w.key_stride * 8);
+    w.rtk = (uint32_t *)(base + 3 * (size_t)B * line + (size_t)B * w.key_stride * 8);
+    w.rtk_stride = rtk_stride_for(R);
+    w.cand = (int32_t *)((char *)w.rtk + (size_t)B * w.rtk_stride * 4);
     w.cand_stride = (int32_t)cand_stride_for(Lmax, W);
     return w;
 }
@@ -153,9 +159,11 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
     if (B < 0 || R < 0 || Lmax < 0 || n_cand < 0)
         return 0;
     // per sequence: three 256-byte lines (two tickets, the n-gram slots), the
-    // row keys and the candidate lists, each rounded up to whole lines
+    // row keys, the row tickets of the draw at T > 0 and the candidate lists,
+    // each rounded up to whole lines
     const int64_t W = n_cand > SWITCHSD_MAX_CAND ? SWITCHSD_MAX_CAND : n_cand_of(n_cand);
     return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8 +
+                        (size_t)rtk_stride_for(R) * 4 +
                         (size_t)cand_stride_for(Lmax, (int32_t)W) * 4);
 }
 
@@ -322,10 +330,9 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     const int64_t grid = stream_sums ? 4 * (int64_t)cus : rows * p.segs;
     if (!grid_ok(grid) || !grid_ok(rows))
         return SWITCHSD_ESHAPE;
-    if ((rc = launch_sample_sums_kernel(p, grid, stream)))
-        return rc;
-    p.list_mode = 0;
-    return launch_sample_pick_kernel(p, stream);
+    // the last work-group of each drafted row also draws its token, and the
+    // last drafted row of a sequence runs the accept epilogue
+    return launch_sample_sums_kernel(p, grid, stream);
 }
 
 // Verify launch shared by the entry points and the split step.  `speculate`:

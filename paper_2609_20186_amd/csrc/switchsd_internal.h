@@ -35,6 +35,9 @@ struct Workspace {
     int32_t *mslot;            // [B] x 256 B: most recent end + 1 per n-gram length
     unsigned long long *keys;  // [B] x key_stride: packed (value key, ~index) row maxima
     int32_t key_stride;        // u64 per sequence (R rounded up to a 256-byte line)
+    uint32_t *rtk;             // [B] x rtk_stride: arrivals of the sum work-groups per row
+                               // (draw at T > 0)
+    int32_t rtk_stride;        // u32 per sequence (R rounded up to a 256-byte line)
     int32_t *cand;             // [B] x cand_stride: per scan tile and n-gram length, the
                                // tile's W most recent ends + 1 (0: none); W > 1 and
                                // more than one tile only
@@ -108,7 +111,6 @@ int launch_commit_kernel(const StepParams &p, hipStream_t stream);
 int launch_label_kernels(const StepParams &p, int32_t n, void *starts, uint8_t *labels,
                          hipStream_t stream);
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
-int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream);
 int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                             uint32_t *mask, hipStream_t stream);
 

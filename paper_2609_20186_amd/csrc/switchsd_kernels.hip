@@ -35,7 +35,7 @@
 // slots it consumed, leaving them zeroed for the next call.
 //
 // Further kernels: k_verify_stream (verification of long drafts over a fixed
-// grid), k_sample_sums / k_sample_sums_stream / k_sample_pick (verification at
+// grid), k_sample_sums / k_sample_sums_stream (verification at
 // sampling temperature T > 0), k_select and k_commit (stage entry points),
 // k_tree_mask (the verification mask), k_label_starts / k_label_write
 // (copy-mode labels for probe training).
@@ -99,6 +99,7 @@ struct PickShared {  // one row's draw at T > 0
     uint32_t wsum[kWaves];             // per-wave totals within the chosen block
     unsigned long long target;         // remaining target inside the chosen chunk / block
     int32_t cstar, ustar, qstar, y;
+    int32_t last;                      // this work-group completed the row (row_done)
 };
 union Shared {
     ScanShared scan;
@@ -1439,33 +1440,197 @@ __device__ __forceinline__ uint32_t vec_weight(const u32x4 &v, float m, float c)
     return s;
 }
 
+// floor(u * Z / 2^32), exactly.
+__device__ __forceinline__ unsigned long long scaled_target(uint32_t u, unsigned long long Z) {
+    return (unsigned long long)u * (Z >> 32) +
+           (((unsigned long long)u * (Z & 0xFFFFFFFFull)) >> 32);
+}
+
+// The draw of row r of sequence b (its maximum m): the chunk sums give Z and
+// the target floor(u Z / 2^32) and its chunk; the chunk is read again, the
+// 256-vector block and the vector are found by prefix sums and the element by
+// a scan of 8 weights.  The drawn token replaces the row's key (key_max reads
+// it as a finite maximum of index y).  Every thread of the work-group takes
+// part.
+__device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned long long *keyp,
+                         Shared &sh) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const uint32_t uni = p.uniforms[(int64_t)b * p.R + r];
+    const uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+    sh.pick.cw[tid] = tid < p.cpr * kWaves ? (uint32_t)ld_i32((const int32_t *)&cs[tid]) : 0u;
+    __syncthreads();
+    if (wave == 0) {
+        // chunk totals, their inclusive prefix, the target and its chunk
+        unsigned long long cc = 0;
+        if (lane < p.cpr)
+            cc = (unsigned long long)sh.pick.cw[4 * lane] + sh.pick.cw[4 * lane + 1] +
+                 sh.pick.cw[4 * lane + 2] + sh.pick.cw[4 * lane + 3];
+        unsigned long long inc = cc;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const unsigned long long y = __shfl_up(inc, o);
+            if (lane >= o)
+                inc += y;
+        }
+        const unsigned long long Z = __shfl(inc, 63);
+        const unsigned long long target = scaled_target(uni, Z);
+        const unsigned long long hit = __ballot(lane < p.cpr && inc > target);
+        const int cst = __ffsll((long long)hit) - 1;  // exists: target < Z
+        const unsigned long long before = __shfl(inc - cc, cst);
+        if (lane == 0) {
+            sh.pick.cstar = cst;
+            sh.pick.target = target - before;
+        }
+    }
+    __syncthreads();
+    const int cst = sh.pick.cstar;
+    const int nq = p.V >> 3;
+    const u32x4 *vp =
+        reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
+    u32x4 A[kUnroll];
+    load_chunk(A, vp, cst * kChunkVecs, nq);
+    uint32_t vs[kUnroll];  // weight of vector q = chunk start + u * 256 + tid
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        vs[u] = cst * kChunkVecs + u * kThreads + tid < nq ? vec_weight(A[u], m, p.samp_c)
+                                                            : 0u;
+    // totals of the four blocks of 256 vectors (each < 2^32)
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t t = wave_reduce_u32(vs[u], 0u, [](uint32_t a, uint32_t x) { return a + x; });
+        if (lane == 0)
+            sh.pick.tot[wave][u] = t;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        unsigned long long tg = sh.pick.target;
+        int us = kUnroll - 1;
+        for (int u = 0; u < kUnroll; ++u) {
+            const unsigned long long t = (unsigned long long)sh.pick.tot[0][u] +
+                                         sh.pick.tot[1][u] + sh.pick.tot[2][u] +
+                                         sh.pick.tot[3][u];
+            if (tg < t) {
+                us = u;
+                break;
+            }
+            tg -= t;
+        }
+        sh.pick.ustar = us;
+        sh.pick.target = tg;
+        sh.pick.qstar = kThreads;
+    }
+    __syncthreads();
+    // within the block: inclusive prefix over the 256 vectors in order
+    const int us = sh.pick.ustar;
+    uint32_t mine = 0;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        if (u == us)
+            mine = vs[u];
+    uint32_t inc = mine;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= o)
+            inc += y;
+    }
+    if (lane == 63)
+        sh.pick.wsum[wave] = inc;
+    __syncthreads();
+    unsigned long long off = 0;
+    for (int w = 0; w < wave; ++w)
+        off += sh.pick.wsum[w];
+    const unsigned long long tg = sh.pick.target;
+    const unsigned long long hit = __ballot(off + inc > tg);
+    if (hit && lane == __ffsll((long long)hit) - 1)
+        atomicMin(&sh.pick.qstar, tid);
+    __syncthreads();
+    if (tid == sh.pick.qstar) {
+        // the element within this thread's vector
+        unsigned long long run = off + inc - mine;
+        const int q = cst * kChunkVecs + us * kThreads + tid;
+        u32x4 v = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (u == us)
+                v = A[u];
+        int e = 7;
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t x = v[j >> 1];
+            run += samp_weight((j & 1) ? hi_f(x) : lo_f(x), m, p.samp_c);
+            if (run > tg) {
+                e = j;
+                break;
+            }
+        }
+        sh.pick.y = q * 8 + e;
+    }
+    __syncthreads();
+    if (tid == 0)
+        st_u64(keyp, (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)sh.pick.y));
+}
+
+// The sum work-groups of a drafted row arrive with the units (16 KB chunks or
+// work-groups) they covered; the last one draws the row's token, then arrives
+// for the sequence, and the last of its dn[b] drafted rows runs the accept
+// epilogue (wave 0).  Every thread of the work-group calls this together; all
+// of them continue afterwards.
+template <bool kCommit>
+__device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t units,
+                         uint32_t expected, bool active, float m, Shared &sh) {
+    const int tid = threadIdx.x;
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's chunk sums are out
+    __syncthreads();
+    uint32_t *rt = &p.ws.rtk[(int64_t)b * p.ws.rtk_stride + r];
+    if (tid < 64) {
+        const bool last = arrive_n(rt, units, expected);
+        if (tid == 0)
+            sh.pick.last = last ? 1 : 0;
+    }
+    __syncthreads();
+    const bool last = sh.pick.last != 0;
+    __syncthreads();
+    if (!last)
+        return;
+    if (tid == 0)
+        st_u32(rt, 0u);
+    if (active)
+        pick_row(p, b, r, m, &p.ws.keys[(int64_t)b * p.ws.key_stride + r], sh);
+    if (tid < 64 && arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)dnb))
+        final_epilogue<kCommit>(p, b, sh);
+    __syncthreads();
+}
+
 // Sum launch: work-group (row, segment) adds up the weights of each 16 KB
 // chunk of its segment, per wave (a wave's chunk share is < 2^32).  Rows at
 // and beyond dn and rows without a finite maximum are skipped.
+template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
+    __shared__ Shared sh;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int rowi = blockIdx.x / p.segs;
     const int s = blockIdx.x - rowi * p.segs;
     const int b = rowi / p.R, r = rowi - b * p.R;
     const int nq = p.V >> 3;
+    // every work-group of the row covers at least one chunk (segs = chunks
+    // per row / chunks per work-group, rounded up)
     const int c0 = s * p.seg_chunks;
     const int c1 = c0 + p.seg_chunks < p.cpr ? c0 + p.seg_chunks : p.cpr;
-    if (c0 >= c1)
-        return;
     const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
     u32x4 A[kUnroll], Bv[kUnroll];
     if (p.speculate)
         load_chunk(A, vp, c0 * kChunkVecs, nq);
-    float m = 0.0f;
-    if (r >= clampi(ld_i32(&p.dn[b]), 1, p.R) ||
-        !key_max(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]), m)) {
+    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    if (r >= dnb) {  // not drafted: no part in the draw
         __builtin_amdgcn_s_waitcnt(0);
         return;
     }
-    if (!p.speculate)
+    float m = 0.0f;
+    const bool active = key_max(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]), m);
+    if (active && !p.speculate)
         load_chunk(A, vp, c0 * kChunkVecs, nq);
     uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
-    for (int c = c0; c < c1; ++c) {
+    for (int c = c0; active && c < c1; ++c) {
         if (c + 1 < c1)
             load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
         uint32_t sum = 0;
@@ -1475,18 +1640,23 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
                 sum += vec_weight(A[u], m, p.samp_c);
         sum = wave_reduce_u32(sum, 0u, [](uint32_t a, uint32_t x) { return a + x; });
         if (lane == 0)
-            cs[c * kWaves + wave] = sum;
+            st_u32(&cs[c * kWaves + wave], sum);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
             A[u] = Bv[u];
     }
+    row_done<kCommit>(p, b, r, dnb, 1u, (uint32_t)p.segs, active, m, sh);
 }
 
 // Sum launch for long drafts (p.list_mode): the chunks of the drafted rows,
 // sequence by sequence and row by row, split evenly over a fixed grid as in
 // the streamed verify; a row's maximum is requested together with the
 // prefetch of its first chunk.
-__global__ __launch_bounds__(kThreads) void k_sample_sums_stream(StepParams p) {
+// The grid is four work-groups per compute unit, all resident at once.
+template <bool kCommit>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void
+k_sample_sums_stream(StepParams p) {
+    __shared__ Shared sh;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     constexpr int Q = kListMaxB / 64;
     const int cpr = p.cpr;
@@ -1533,6 +1703,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums_stream(StepParams p) {
     u32x4 A[kUnroll], Bv[kUnroll];
     load_chunk(A, row_vecs(b, r), c * kChunkVecs, nq);
     unsigned long long key = ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]);
+    uint32_t done_r = 0;  // units of row (b, r) streamed here
     for (int u = u0; u < u1; ++u) {
         int nb = b, nr = r, nc = c + 1, ndn = dnb;
         if (nc == cpr) {
@@ -1557,8 +1728,9 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums_stream(StepParams p) {
             if (nc == 0)
                 nkey = ld_u64(&p.ws.keys[(int64_t)nb * p.ws.key_stride + nr]);
         }
-        float m;
-        if (key_max(key, m)) {
+        float m = 0.0f;
+        const bool active = key_max(key, m);
+        if (active) {
             uint32_t sum = 0;
 #pragma unroll
             for (int q = 0; q < kUnroll; ++q)
@@ -1566,7 +1738,12 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums_stream(StepParams p) {
                     sum += vec_weight(A[q], m, p.samp_c);
             sum = wave_reduce_u32(sum, 0u, [](uint32_t a, uint32_t x) { return a + x; });
             if (lane == 0)
-                p.csum[(((int64_t)b * p.R + r) * cpr + c) * kWaves + wave] = sum;
+                st_u32(&p.csum[(((int64_t)b * p.R + r) * cpr + c) * kWaves + wave], sum);
+        }
+        ++done_r;
+        if (c == cpr - 1 || u + 1 == u1) {  // end of this row's piece
+            row_done<kCommit>(p, b, r, dnb, done_r, (uint32_t)cpr, active, m, sh);
+            done_r = 0;
         }
         b = nb;
         r = nr;
@@ -1579,146 +1756,12 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums_stream(StepParams p) {
     }
 }
 
-// floor(u * Z / 2^32), exactly.
-__device__ __forceinline__ unsigned long long scaled_target(uint32_t u, unsigned long long Z) {
-    return (unsigned long long)u * (Z >> 32) +
-           (((unsigned long long)u * (Z & 0xFFFFFFFFull)) >> 32);
-}
 
 // Pick launch: one work-group per row.  The draw is the smallest index j with
 // w_0 + ... + w_j > floor(u Z / 2^32): the chunk from the chunk sums, the
 // vector block (256 vectors) and vector from the re-read chunk, the element
 // within the vector.  The drawn token replaces the row's argmax key; then the
 // row arrives at its sequence, and the last row runs the accept epilogue.
-template <bool kCommit>
-__global__ __launch_bounds__(kThreads) void k_sample_pick(StepParams p) {
-    __shared__ Shared sh;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int b = blockIdx.x / p.R, r = blockIdx.x - b * p.R;
-    unsigned long long *keyp = &p.ws.keys[(int64_t)b * p.ws.key_stride + r];
-    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
-    float m = 0.0f;
-    if (r < dnb && key_max(ld_u64(keyp), m)) {
-        const uint32_t uni = p.uniforms[(int64_t)b * p.R + r];
-        const uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
-        sh.pick.cw[tid] = tid < p.cpr * kWaves ? cs[tid] : 0u;
-        __syncthreads();
-        if (wave == 0) {
-            // chunk totals, their inclusive prefix, the target and its chunk
-            unsigned long long cc = 0;
-            if (lane < p.cpr)
-                cc = (unsigned long long)sh.pick.cw[4 * lane] + sh.pick.cw[4 * lane + 1] +
-                     sh.pick.cw[4 * lane + 2] + sh.pick.cw[4 * lane + 3];
-            unsigned long long inc = cc;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const unsigned long long y = __shfl_up(inc, o);
-                if (lane >= o)
-                    inc += y;
-            }
-            const unsigned long long Z = __shfl(inc, 63);
-            const unsigned long long target = scaled_target(uni, Z);
-            const unsigned long long hit = __ballot(lane < p.cpr && inc > target);
-            const int cst = __ffsll((long long)hit) - 1;  // exists: target < Z
-            const unsigned long long before = __shfl(inc - cc, cst);
-            if (lane == 0) {
-                sh.pick.cstar = cst;
-                sh.pick.target = target - before;
-            }
-        }
-        __syncthreads();
-        const int cst = sh.pick.cstar;
-        const int nq = p.V >> 3;
-        const u32x4 *vp =
-            reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
-        u32x4 A[kUnroll];
-        load_chunk(A, vp, cst * kChunkVecs, nq);
-        uint32_t vs[kUnroll];  // weight of vector q = chunk start + u * 256 + tid
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            vs[u] = cst * kChunkVecs + u * kThreads + tid < nq ? vec_weight(A[u], m, p.samp_c)
-                                                                : 0u;
-        // totals of the four blocks of 256 vectors (each < 2^32)
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const uint32_t t = wave_reduce_u32(vs[u], 0u, [](uint32_t a, uint32_t x) { return a + x; });
-            if (lane == 0)
-                sh.pick.tot[wave][u] = t;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            unsigned long long tg = sh.pick.target;
-            int us = kUnroll - 1;
-            for (int u = 0; u < kUnroll; ++u) {
-                const unsigned long long t = (unsigned long long)sh.pick.tot[0][u] +
-                                             sh.pick.tot[1][u] + sh.pick.tot[2][u] +
-                                             sh.pick.tot[3][u];
-                if (tg < t) {
-                    us = u;
-                    break;
-                }
-                tg -= t;
-            }
-            sh.pick.ustar = us;
-            sh.pick.target = tg;
-            sh.pick.qstar = kThreads;
-        }
-        __syncthreads();
-        // within the block: inclusive prefix over the 256 vectors in order
-        const int us = sh.pick.ustar;
-        uint32_t mine = 0;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            if (u == us)
-                mine = vs[u];
-        uint32_t inc = mine;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t y = __shfl_up(inc, o);
-            if (lane >= o)
-                inc += y;
-        }
-        if (lane == 63)
-            sh.pick.wsum[wave] = inc;
-        __syncthreads();
-        unsigned long long off = 0;
-        for (int w = 0; w < wave; ++w)
-            off += sh.pick.wsum[w];
-        const unsigned long long tg = sh.pick.target;
-        const unsigned long long hit = __ballot(off + inc > tg);
-        if (hit && lane == __ffsll((long long)hit) - 1)
-            atomicMin(&sh.pick.qstar, tid);
-        __syncthreads();
-        if (tid == sh.pick.qstar) {
-            // the element within this thread's vector
-            unsigned long long run = off + inc - mine;
-            const int q = cst * kChunkVecs + us * kThreads + tid;
-            u32x4 v = {0u, 0u, 0u, 0u};
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                if (u == us)
-                    v = A[u];
-            int e = 7;
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t x = v[j >> 1];
-                run += samp_weight((j & 1) ? hi_f(x) : lo_f(x), m, p.samp_c);
-                if (run > tg) {
-                    e = j;
-                    break;
-                }
-            }
-            sh.pick.y = q * 8 + e;
-        }
-        __syncthreads();
-        if (tid == 0)
-            st_u64(keyp, (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)sh.pick.y));
-    }
-    if (tid >= 64)
-        return;
-    if (arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)p.R))
-        final_epilogue<kCommit>(p, b, sh);
-}
-
 // ------------------------------------------------------------- copy-mode labels
 
 // Copy-mode labels for probe training (Sec. 3.2, Problem Formulation):
@@ -2000,20 +2043,15 @@ int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
 }
 
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
-    if (p.list_mode)
-        hipLaunchKernelGGL(k_sample_sums_stream, dim3((unsigned)grid), dim3(kThreads), 0,
-                           stream, p);
+    const dim3 g((unsigned)grid);
+    if (p.list_mode && p.commit)
+        hipLaunchKernelGGL((k_sample_sums_stream<true>), g, dim3(kThreads), 0, stream, p);
+    else if (p.list_mode)
+        hipLaunchKernelGGL((k_sample_sums_stream<false>), g, dim3(kThreads), 0, stream, p);
+    else if (p.commit)
+        hipLaunchKernelGGL((k_sample_sums<true>), g, dim3(kThreads), 0, stream, p);
     else
-        hipLaunchKernelGGL(k_sample_sums, dim3((unsigned)grid), dim3(kThreads), 0, stream, p);
-    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
-}
-
-int launch_sample_pick_kernel(const StepParams &p, hipStream_t stream) {
-    const dim3 grid((unsigned)((int64_t)p.B * p.R));
-    if (p.commit)
-        hipLaunchKernelGGL((k_sample_pick<true>), grid, dim3(kThreads), 0, stream, p);
-    else
-        hipLaunchKernelGGL((k_sample_pick<false>), grid, dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL((k_sample_sums<false>), g, dim3(kThreads), 0, stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 
