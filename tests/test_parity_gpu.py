@@ -162,6 +162,10 @@ CASES = {
                      vocab=2, tree=True, ties=True),
     "tree_r100_general": dict(seed=11, B=4, Lmax=500, V=40, R=100, k=10, lens=(2, 1), kappa=1,
                               theta=0.0, vocab=2, tree=True, ties=True),
+    # more than 256 sequences with long drafts: the per-row verify launch (not
+    # the streamed one) with the accept epilogue over more than 64 nodes
+    "tree_r70_wide_batch": dict(seed=16, B=260, Lmax=96, V=64, R=70, k=5, lens=(2, 1),
+                                kappa=1, theta=0.0, vocab=3, tree=True, ties=True),
     "chain_r100_general": dict(seed=12, B=3, Lmax=300, V=3, R=100, k=99, lens=(1,), kappa=1,
                                theta=-np.inf, vocab=2, ties=True, plant=True),
     "long_halo_ngram64": dict(seed=13, B=3, Lmax=8300, V=100, R=3, k=2, lens=(64, 63, 1),

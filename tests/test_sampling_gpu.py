@@ -59,6 +59,10 @@ SAMPLE_CASES = {
     "multi_chunk_rows": dict(seed=65, B=3, Lmax=900, V=40000, R=4, k=3, lens=(2, 1), kappa=1,
                              theta=-np.inf, vocab=10, plant=True),
     "v8": dict(seed=66, B=5, Lmax=40, V=8, R=3, k=2, lens=(1,), kappa=1, theta=0.0, vocab=3),
+    # more than 256 sequences with long drafts: per-row weight sums (not the
+    # streamed ones), then the accept epilogue over more than 64 nodes
+    "tree70_wide_batch": dict(seed=69, B=260, Lmax=96, V=64, R=70, k=5, lens=(2, 1), kappa=1,
+                              theta=0.0, vocab=3, tree=True, ties=True),
 }
 
 
