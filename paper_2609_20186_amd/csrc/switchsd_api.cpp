@@ -303,9 +303,9 @@ int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_
     return SWITCHSD_OK;
 }
 
-// After the row maxima are in the row keys: the weight-sum launch and the pick
-// launch (which runs the accept epilogue).  `p` carries the rows, the draft,
-// the outputs and the carved workspace.
+// After the row maxima are in the row keys: the weight-sum launch, which also
+// draws each row's token and runs the accept epilogue.  `p` carries the rows,
+// the draft, the outputs and the carved workspace.
 int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_t stream) {
     int cus = 0;
     int rc = cu_count(&cus);

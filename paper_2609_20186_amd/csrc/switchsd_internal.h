@@ -95,7 +95,7 @@ struct StepParams {
     int32_t *clen;       // [B] its length
     int32_t *draft_pos;  // [B] draft-model cache position (in/out)
     int32_t *lag;        // [B] tokens the next neural drafting pass must consume first
-    // draws at T > 0 (sum and pick launches)
+    // draws at T > 0 (the weight-sum launch)
     const uint32_t *uniforms;  // [B, R]
     float samp_c;              // log2(e) / T
     uint32_t *csum;            // [B, R, cpr, waves] fixed-point weight sums per chunk

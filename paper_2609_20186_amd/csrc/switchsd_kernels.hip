@@ -1393,10 +1393,10 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
 // child iff its token is y.  The draw is an inverse-CDF sample with the row's
 // uniform over fixed-point weights w_j = trunc(2^20 * 2^((l_j - m) c)),
 // c = log2(e) / T, m the row maximum, so that the sums are exact integers and
-// the drawn index does not depend on the reduction order.  Three launches
-// after the draft is chosen: the row maxima (the greedy argmax pass), the
-// per-chunk weight sums, and the pick, which also closes the sequence with the
-// accept epilogue.
+// the drawn index does not depend on the reduction order.  Two launches after
+// the draft is chosen: the row maxima (the greedy argmax pass), then the
+// per-chunk weight sums, whose last work-group per row draws the row's token
+// and whose last row closes the sequence with the accept epilogue.
 
 // The row's maximum from its packed argmax key; false when the row has no
 // finite maximum (no key: every value NaN; -inf; +inf present), and then the
