@@ -283,13 +283,16 @@ int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,
  * x[s..s+n-1] with s <= j <= s+n-1 <= L-1 equals x[s'..s'+n-1] for some
  * s' < s (overlap allowed); 0 otherwise and for j >= L.  The paper's setting
  * is n = 5.  Offline (whole sequences, not per decoding step).
- *   tokens [B, Lmax] int32, lengths [B] int32, 1 <= n <= 64;
- *   output labels [B, Lmax] uint8; workspace of
- *   switchsd_label_workspace_bytes(B, Lmax) bytes, 256-byte aligned, zeroed
- *   once by the caller (left zeroed by every call).  Two launches. */
+ *   tokens [B, Lmax] int32, lengths [B] int32, 1 <= n <= 64,
+ *   Lmax <= 2^28; output labels [B, Lmax] uint8; workspace of
+ *   switchsd_label_workspace_bytes(B, Lmax) bytes (a table of the distinct
+ *   windows per sequence), 256-byte aligned, zeroed once by the caller (left
+ *   zeroed by every call).  Three launches; expected time linear in
+ *   B * Lmax * n. */
 int switchsd_copy_labels(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
                          int32_t n, uint8_t *labels, void *workspace, size_t workspace_bytes,
                          hipStream_t stream);
+/* 0 for a negative argument or Lmax > 2^28. */
 size_t switchsd_label_workspace_bytes(int32_t B, int32_t Lmax);
 
 /* Workspace bytes needed by calls with B sequences of R rows, contexts of up

@@ -546,17 +546,33 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
                          workspace_bytes, R <= 16, sampled ? &sa : nullptr, &p, stream);
 }
 
+}  // extern "C"
+
+namespace {
+// Slots of a sequence's window table: a power of two of at least 2 Lmax (the
+// table is at most half full) and 64.
+int64_t label_table_slots(int32_t Lmax) {
+    int64_t t = 64;
+    while (t < 2 * (int64_t)Lmax)
+        t <<= 1;
+    return t;
+}
+}  // namespace
+
+extern "C" {
+
 size_t switchsd_label_workspace_bytes(int32_t B, int32_t Lmax) {
-    if (B < 0 || Lmax < 0)
+    if (B < 0 || Lmax < 0 || Lmax > (1 << 28))
         return 0;
-    const size_t n = (size_t)B * (((size_t)Lmax + 63) / 64) * 8;
-    return (n + kAlign - 1) / kAlign * kAlign;
+    // a table of the distinct windows per sequence
+    return (size_t)((int64_t)B * label_table_slots(Lmax) * 4);
 }
 
 int switchsd_copy_labels(const int32_t *tokens, const int32_t *lengths, int32_t B, int32_t Lmax,
                          int32_t n, uint8_t *labels, void *workspace, size_t workspace_bytes,
                          hipStream_t stream) {
-    if (!shape_ok_B(B) || Lmax < 1 || (int64_t)B * ((Lmax + 63) / 64) * 8 > (1ll << 40))
+    if (!shape_ok_B(B) || Lmax < 1 || Lmax > (1 << 28) ||
+        (int64_t)B * label_table_slots(Lmax) * 4 > (1ll << 40))
         return SWITCHSD_ESHAPE;
     if (n < 1 || n > 64)
         return SWITCHSD_EINVAL;
@@ -573,11 +589,11 @@ int switchsd_copy_labels(const int32_t *tokens, const int32_t *lengths, int32_t 
     p.lengths = lengths;
     p.B = B;
     p.Lmax = Lmax;
-    const int64_t nblocks = (Lmax + 63) / 64;
-    const int64_t grid = (int64_t)B * ((nblocks + 15) / 16) * ((Lmax - 1 + 255) / 256 + 1);
+    const int64_t grid = (int64_t)B * ((Lmax + kThreads - 1) / kThreads);
     if (!grid_ok(grid))
         return SWITCHSD_ESHAPE;
-    return launch_label_kernels(p, n, workspace, labels, stream);
+    return launch_label_kernels(p, n, labels, (int32_t)label_table_slots(Lmax), workspace,
+                                stream);
 }
 
 int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,

@@ -108,8 +108,8 @@ struct StepParams {
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_select_kernel(const StepParams &p, hipStream_t stream);
 int launch_commit_kernel(const StepParams &p, hipStream_t stream);
-int launch_label_kernels(const StepParams &p, int32_t n, void *starts, uint8_t *labels,
-                         hipStream_t stream);
+int launch_label_kernels(const StepParams &p, int32_t n, uint8_t *labels, int32_t tsize,
+                         void *table, hipStream_t stream);
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                             uint32_t *mask, hipStream_t stream);

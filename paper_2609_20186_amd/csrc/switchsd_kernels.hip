@@ -37,8 +37,8 @@
 // Further kernels: k_verify_stream (verification of long drafts over a fixed
 // grid), k_sample_sums / k_sample_sums_stream (verification at
 // sampling temperature T > 0), k_select and k_commit (stage entry points),
-// k_tree_mask (the verification mask), k_label_starts / k_label_write
-// (copy-mode labels for probe training).
+// k_tree_mask (the verification mask), k_label_insert / k_label_write /
+// k_label_clear (copy-mode labels for probe training).
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -1756,118 +1756,155 @@ k_sample_sums_stream(StepParams p) {
     }
 }
 
-
-// Pick launch: one work-group per row.  The draw is the smallest index j with
-// w_0 + ... + w_j > floor(u Z / 2^32): the chunk from the chunk sums, the
-// vector block (256 vectors) and vector from the re-read chunk, the element
-// within the vector.  The drawn token replaces the row's argmax key; then the
-// row arrives at its sequence, and the last row runs the accept epilogue.
 // ------------------------------------------------------------- copy-mode labels
 
 // Copy-mode labels for probe training (Sec. 3.2, Problem Formulation):
 // position j is copy-mode iff an n-token window covering it repeats an
-// earlier window.  For a distance delta >= 1, bit l of the ballot D over the
-// block of end positions 64w..64w+63 is x[j] == x[j - delta]; a window
-// starting at s repeats the one at s - delta iff bits s..s+n-1 are all set, so
-// the starts of repeated windows are the AND of D shifted by 0..n-1 (carrying
-// in the next block's ballot) -- scalar mask operations per (delta, block).
-// The starts of all distances are OR-ed into the workspace (one bit per
-// position), then widened by n - 1 positions into the labels.
+// earlier window, i.e. the window starting at some s in [j - n + 1, j] is not
+// the first occurrence of its n tokens.  An open-addressing table per
+// sequence (linear probing, at most half full) holds one slot per distinct
+// window content with the complement of its earliest start (0: empty):
+// k_label_insert claims a slot with a compare-and-swap or, when the slot's
+// window has the same tokens (compared token by token, never by hash),
+// lowers its start with an atomic max of the complement; k_label_write then
+// marks the starts s whose slot holds an earlier start and widens them into
+// labels, and k_label_clear empties the table.  The hash only spreads
+// the windows over the table: the result does not depend on it.  All windows
+// of one content walk the same probe sequence, and a slot never empties or
+// changes content, so each content ends in exactly one slot and every walk
+// reaches it before any empty slot.
 
-constexpr int kLabelBlocks = 16;   // 64-position blocks per work-group
-constexpr int kLabelDeltas = 256;  // distances per work-group
+// Windows are read 8 tokens at a time, the 8 loads of a group issued together
+// (one memory round trip per group rather than per token).
+constexpr int kWinGroup = 8;
 
-__global__ __launch_bounds__(kThreads) void k_label_starts(StepParams p, int32_t n, int32_t nbg,
-                                                           int32_t ndg,
-                                                           unsigned long long *starts) {
-    // xb: positions of the range and the next block; xa: those positions
-    // moved back by every distance of the group
-    __shared__ int32_t xb[64 * kLabelBlocks + 64];
-    __shared__ int32_t xa[64 * kLabelBlocks + 64 + kLabelDeltas];
-    __shared__ unsigned long long acc_s[kLabelBlocks];
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int dg = blockIdx.x % ndg;
-    const int bg = (blockIdx.x / ndg) % nbg;
-    const int b = blockIdx.x / (ndg * nbg);
-    const int L = clampi(p.lengths[b], 0, p.Lmax);
-    const int nblocks = (p.Lmax + 63) >> 6;
-    const int w_lo = bg * kLabelBlocks;
-    const int w_hi = w_lo + kLabelBlocks < nblocks ? w_lo + kLabelBlocks : nblocks;  // excl.
-    const int d_lo = dg * kLabelDeltas + 1;
-    const int d_hi = d_lo + kLabelDeltas - 1 < L - 1 ? d_lo + kLabelDeltas - 1 : L - 1;  // incl.
-    // distances that reach no position of the range (or past the context)
-    if (d_lo > d_hi || d_lo > 64 * w_hi - 1)
-        return;
-    const int b_len = 64 * (w_hi + 1 - w_lo);       // <= 64 * kLabelBlocks + 64
-    const int a_lo = 64 * w_lo - d_hi;                // may be negative
-    const int a_len = b_len + (d_hi - d_lo);          // <= 64 * kLabelBlocks + 64 + kLabelDeltas
-    const int64_t row = (int64_t)b * p.Lmax;
-    for (int i = tid; i < b_len; i += kThreads) {
-        const int x = 64 * w_lo + i;
-        xb[i] = x < L ? p.tokens[row + x] : 0;
-    }
-    for (int i = tid; i < a_len; i += kThreads) {
-        const int x = a_lo + i;
-        xa[i] = x >= 0 && x < L ? p.tokens[row + x] : 0;
-    }
-    if (tid < kLabelBlocks)
-        acc_s[tid] = 0ull;
-    __syncthreads();
-    // ballot of x[j] == x[j - d] over block w
-    auto diag = [&](int w, int d) -> unsigned long long {
-        const int j = 64 * w + lane;
-        const bool ok = j < L && j - d >= 0 && xb[j - 64 * w_lo] == xa[j - d - a_lo];
-        return __ballot(ok);
-    };
-    unsigned long long acc[kLabelBlocks];
+// Slot of the window at s: a multiplicative mix of its tokens.
+__device__ __forceinline__ uint32_t label_hash(const int32_t *x, int s, int n) {
+    uint32_t h = 0x9E3779B9u;
+    for (int i0 = 0; i0 < n; i0 += kWinGroup) {
+        int32_t t[kWinGroup];
 #pragma unroll
-    for (int i = 0; i < kLabelBlocks; ++i)
-        acc[i] = 0ull;
-    for (int d = d_lo + wave; d <= d_hi; d += kWaves) {
-        unsigned long long Dn = w_hi < nblocks ? diag(w_hi, d) : 0ull;
+        for (int i = 0; i < kWinGroup; ++i)
+            t[i] = i0 + i < n ? x[s + i0 + i] : 0;
 #pragma unroll
-        for (int i = kLabelBlocks - 1; i >= 0; --i) {
-            const int w = w_lo + i;
-            if (w >= w_hi)
-                continue;
-            const unsigned long long D = diag(w, d);
-            unsigned long long S = D;
-            for (int u = 1; u < n && S; ++u)
-                S &= (D >> u) | (Dn << (64 - u));
-            acc[i] |= S;
-            Dn = D;
-        }
+        for (int i = 0; i < kWinGroup; ++i)
+            if (i0 + i < n) {
+                h = (h ^ (uint32_t)t[i]) * 0x85EBCA6Bu;
+                h ^= h >> 15;
+            }
     }
-#pragma unroll
-    for (int i = 0; i < kLabelBlocks; ++i)
-        if (lane == 0 && acc[i])
-            atomicOr(&acc_s[i], acc[i]);
-    __syncthreads();
-    if (tid < kLabelBlocks && w_lo + tid < w_hi && acc_s[tid])
-        atomicOr(&starts[(int64_t)b * nblocks + w_lo + tid], acc_s[tid]);
+    h *= 0xC2B2AE35u;
+    return h ^ (h >> 16);
 }
 
-// Labels of one sequence: position j is copy-mode iff a repeated window
-// starts in [j - n + 1, j]; the start bits are cleared again afterwards.
-__global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t n,
-                                                          unsigned long long *starts,
-                                                          uint8_t *labels) {
-    const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int nblocks = (p.Lmax + 63) >> 6;
-    unsigned long long *st = starts + (int64_t)b * nblocks;
-    for (int w = wave; w < nblocks; w += kWaves) {
-        const unsigned long long E = ld_u64(&st[w]);
-        const unsigned long long Ep = w > 0 ? ld_u64(&st[w - 1]) : 0ull;
-        unsigned long long Y = E;
-        for (int u = 1; u < n; ++u)
-            Y |= (E << u) | (Ep >> (64 - u));
-        const int j = 64 * w + lane;
-        if (j < p.Lmax)
-            labels[(int64_t)b * p.Lmax + j] = (uint8_t)((Y >> lane) & 1ull);
+__device__ __forceinline__ bool same_window(const int32_t *x, int s1, int s2, int n) {
+    for (int i0 = 0; i0 < n; i0 += kWinGroup) {
+        int32_t a[kWinGroup], c[kWinGroup];
+#pragma unroll
+        for (int i = 0; i < kWinGroup; ++i) {
+            a[i] = i0 + i < n ? x[s1 + i0 + i] : 0;
+            c[i] = i0 + i < n ? x[s2 + i0 + i] : 0;
+        }
+        bool eq = true;
+#pragma unroll
+        for (int i = 0; i < kWinGroup; ++i)
+            eq = eq && a[i] == c[i];
+        if (!eq)
+            return false;
+    }
+    return true;
+}
+
+// One lane per window start s <= L - n of sequence b.
+__global__ __launch_bounds__(kThreads) void k_label_insert(StepParams p, int32_t n, int32_t tsize,
+                                                           uint32_t *table) {
+    const int per = (p.Lmax + kThreads - 1) / kThreads;
+    const int b = blockIdx.x / per;
+    const int s = (blockIdx.x - b * per) * kThreads + (int)threadIdx.x;
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+    if (s > L - n)
+        return;
+    const int32_t *x = p.tokens + (int64_t)b * p.Lmax;
+    uint32_t *tab = table + (int64_t)b * tsize;
+    const uint32_t mask = (uint32_t)tsize - 1u;
+    uint32_t slot = label_hash(x, s, n) & mask;
+    const uint32_t mine = ~(uint32_t)s;
+    for (int probe = 0; probe < tsize; ++probe) {
+        // a plain read first: most windows find their content already there
+        uint32_t cur = __hip_atomic_load(&tab[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (cur == 0u) {
+            cur = atomicCAS(&tab[slot], 0u, mine);
+            if (cur == 0u)
+                return;  // first of its content to arrive here
+        }
+        if (same_window(x, (int)~cur, s, n)) {
+            if (cur < mine)  // a later start is there: the earliest one wins
+                atomicMax(&tab[slot], mine);
+            return;
+        }
+        slot = (slot + 1u) & mask;
+    }
+}
+
+// Whether the window at s (s <= L - n) repeats an earlier one: its content's
+// slot holds a start < s.
+__device__ __forceinline__ bool label_repeats(const int32_t *x, const uint32_t *tab,
+                                              uint32_t mask, int s, int n) {
+    uint32_t slot = label_hash(x, s, n) & mask;
+    for (uint32_t probe = 0; probe <= mask; ++probe) {
+        const uint32_t cur = tab[slot];
+        if (cur == 0u)
+            return false;  // unreachable: the window's own insert filled a slot first
+        if (same_window(x, (int)~cur, s, n))
+            return (int)~cur < s;
+        slot = (slot + 1u) & mask;
+    }
+    return false;
+}
+
+// Labels of 256 positions of sequence b (one 64-position block per wave):
+// bit l of block w's ballot E_w says whether the window starting at 64 w + l
+// repeats an earlier one; position j is copy-mode iff such a start lies in
+// [j - n + 1, j], i.e. bit j of E | E << 1 | ... | E << (n - 1) with the
+// previous block's bits carried in (wave 0 also looks up the block before the
+// range).
+__global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t n, int32_t tsize,
+                                                          const uint32_t *table, uint8_t *labels) {
+    __shared__ unsigned long long E[kWaves + 1];  // E[0]: the block before the range
+    const int per = (p.Lmax + kThreads - 1) / kThreads;
+    const int b = blockIdx.x / per;
+    const int g = blockIdx.x - b * per;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int L = clampi(p.lengths[b], 0, p.Lmax);
+    const int32_t *x = p.tokens + (int64_t)b * p.Lmax;
+    const uint32_t *tab = table + (int64_t)b * tsize;
+    const uint32_t mask = (uint32_t)tsize - 1u;
+    const int s = g * kThreads + tid;
+    const unsigned long long m = __ballot(s <= L - n && label_repeats(x, tab, mask, s, n));
+    if (lane == 0)
+        E[wave + 1] = m;
+    if (wave == 0) {
+        const int sp = s - 64;
+        const unsigned long long mp =
+            __ballot(sp >= 0 && sp <= L - n && label_repeats(x, tab, mask, sp, n));
+        if (lane == 0)
+            E[0] = mp;
     }
     __syncthreads();
-    for (int w = tid; w < nblocks; w += kThreads)
-        st_u64(&st[w], 0ull);
+    const unsigned long long Ec = E[wave + 1], Ep = E[wave];
+    unsigned long long Y = Ec;
+    for (int u = 1; u < n; ++u)
+        Y |= (Ec << u) | (Ep >> (64 - u));
+    if (s < p.Lmax)
+        labels[(int64_t)b * p.Lmax + s] = (uint8_t)((Y >> lane) & 1ull);
+}
+
+// Empties the window tables again (after every lookup has finished); the
+// tables are 256-byte aligned and a whole number of 16-byte vectors.
+__global__ __launch_bounds__(kThreads) void k_label_clear(u32x4 *table, int64_t vecs) {
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < vecs;
+         i += (int64_t)gridDim.x * kThreads)
+        table[i] = u32x4{0u, 0u, 0u, 0u};
 }
 
 // ------------------------------------------------------------- kernels
@@ -2060,18 +2097,22 @@ int launch_commit_kernel(const StepParams &p, hipStream_t stream) {
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 
-int launch_label_kernels(const StepParams &p, int32_t n, void *starts, uint8_t *labels,
-                         hipStream_t stream) {
-    const int nblocks = (p.Lmax + 63) / 64;
-    const int nbg = (nblocks + kLabelBlocks - 1) / kLabelBlocks;
-    const int ndg = p.Lmax > 1 ? (p.Lmax - 1 + kLabelDeltas - 1) / kLabelDeltas : 1;
-    const int64_t grid = (int64_t)p.B * nbg * ndg;
-    hipLaunchKernelGGL(k_label_starts, dim3((unsigned)grid), dim3(kThreads), 0, stream, p, n,
-                       nbg, ndg, (unsigned long long *)starts);
+int launch_label_kernels(const StepParams &p, int32_t n, uint8_t *labels, int32_t tsize,
+                         void *table, hipStream_t stream) {
+    const int64_t per = (p.Lmax + kThreads - 1) / kThreads;
+    const dim3 grid((unsigned)((int64_t)p.B * per));
+    hipLaunchKernelGGL(k_label_insert, grid, dim3(kThreads), 0, stream, p, n, tsize,
+                       (uint32_t *)table);
     if (hipGetLastError() != hipSuccess)
         return SWITCHSD_EHIP;
-    hipLaunchKernelGGL(k_label_write, dim3((unsigned)p.B), dim3(kThreads), 0, stream, p, n,
-                       (unsigned long long *)starts, labels);
+    hipLaunchKernelGGL(k_label_write, grid, dim3(kThreads), 0, stream, p, n, tsize,
+                       (const uint32_t *)table, labels);
+    if (hipGetLastError() != hipSuccess)
+        return SWITCHSD_EHIP;
+    const int64_t vecs = (int64_t)p.B * tsize / 4;  // tsize is a multiple of 64
+    const int64_t cgrid = (vecs + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(k_label_clear, dim3((unsigned)(cgrid < 65536 ? cgrid : 65536)),
+                       dim3(kThreads), 0, stream, (u32x4 *)table, vecs);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 
