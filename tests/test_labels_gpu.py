@@ -32,13 +32,16 @@ def gpu_labels(tokens, lengths, n, ws=None):
     return lab.cpu().numpy(), ws
 
 
-@pytest.mark.parametrize("n", [1, 2, 5, 8, 64])
+@pytest.mark.parametrize("n", [1, 2, 5, 8, 9, 64])
 def test_labels_random_parity(n):
-    """Small vocabularies (many repeats), ragged and clamped lengths, contexts
-    crossing the 1024-position and 256-distance work-group boundaries."""
+    """Small vocabularies (many repeats: windows sharing a table slot, and with
+    vocabulary 1 a single content for every window), ragged and clamped
+    lengths, contexts crossing the 256-position work-group boundaries, and
+    windows longer than one 8-token read group (n = 9, 64)."""
     say(f"[labels] random n={n}")
     rng = np.random.default_rng(70 + n)
-    for Lmax, vocab in ((1, 2), (63, 2), (64, 3), (65, 3), (700, 4), (1500, 20), (2600, 2)):
+    for Lmax, vocab in ((1, 2), (63, 2), (64, 3), (65, 3), (300, 1), (700, 4), (1500, 20),
+                        (2600, 2)):
         B = 5
         x = rng.integers(0, vocab, (B, Lmax)).astype(np.int32)
         if n == 64 and Lmax > 200:
