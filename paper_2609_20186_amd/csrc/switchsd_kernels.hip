@@ -16,11 +16,12 @@
 //   argmax  one segment of one logits row, streamed in 16 KB chunks with the
 //           next chunk's nontemporal 16-byte loads in flight while the current
 //           one is reduced.  Lane maxima use the NaN-propagating
-//           v_maximum3_f32 (1.5 VALU ops per element); a ballot asks whether
-//           any lane beat the wave's running maximum, and only then does the
-//           wave reduce and look up the lowest index holding it.  The segment
-//           result is packed as (order key << 32 | ~index) and atomicMax-ed
-//           into the row's slot.  (Sec. 2 / App. A: greedy verification, T = 0.)
+//           v_maximum3_f32 (1.5 VALU ops per element); each lane keeps the
+//           chunk that raised its maximum (in LDS) and looks up the lowest
+//           index holding it once, at the end, before one wave reduction.
+//           The segment result is packed as (order key << 32 | ~index) and
+//           atomicMax-ed into the row's slot.  (Sec. 2 / App. A: greedy
+//           verification, T = 0.)
 //
 // Two last-arriver epilogues close a sequence without a second launch:
 //   front   when its scan tiles and probe are done: pick the match, gather the
