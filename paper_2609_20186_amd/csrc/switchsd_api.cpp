@@ -514,8 +514,15 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.ws = carve(workspace, B, R, a->Lmax, p.W);
     if ((rc = set_scan(p, B, a->Lmax)))
         return rc;
-    p.scan_probe = 1;
-    p.n_front_wg = p.n_scan_wg;
+    // one tile: it computes the probe too; several: the probe has a work-group
+    // of its own (first in the grid) and no tile carries it
+    if (p.scan_tiles > 1) {
+        p.probe_on = 1;
+        p.n_front_wg = p.n_scan_wg + B;
+    } else {
+        p.scan_probe = 1;
+        p.n_front_wg = p.n_scan_wg;
+    }
     p.epi_front = EPI_SELECT;
     p.exp_front = (uint32_t)p.scan_tiles;
 

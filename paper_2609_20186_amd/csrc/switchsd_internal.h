@@ -77,7 +77,7 @@ struct StepParams {
     Workspace ws;
     // grid layout: [scan tiles][probe][argmax row segments]
     int32_t scan_tiles;  // per sequence (0: no scan role)
-    int32_t probe_on;    // 1: one stand-alone probe work-group per sequence
+    int32_t probe_on;    // 1: one probe work-group per sequence, first in the grid
     int32_t scan_probe;  // 1: scan tile 0 of each sequence also computes the probe
     int32_t segs;        // argmax work-groups per row (0: no argmax role)
     int32_t seg_elems;   // logits elements per row segment (multiple of 8)

@@ -83,6 +83,7 @@ struct ScanShared {
 struct ArgmaxShared {
     float wmax[kWaves];
     uint32_t widx[kWaves];
+    u32x4 keep[kChunkVecs];  // each lane's kept chunk (running argmax)
 };
 struct ProbeShared {
     double s[kWaves];
@@ -463,7 +464,16 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     __syncthreads();
 }
 
-// Stand-alone probe work-group (the probe entry point).
+// In the step with several scan tiles per sequence the probe has a
+// work-group of its own, dispatched before every tile (block order), and the
+// last tile waits for this flag before it reads z.  It sits in the last word
+// of the sequence's n-gram slot line (at most 8 n-gram lengths use the line).
+__device__ __forceinline__ uint32_t *probe_flag(const StepParams &p, int b) {
+    return (uint32_t *)&p.ws.mslot[b * kLineU32 + kLineU32 - 1];
+}
+
+// Stand-alone probe work-group (the probe entry point, or the step's probe
+// when a sequence has several scan tiles).
 __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
     double s, c;
     probe_partial(p, b, s, c);
@@ -473,8 +483,13 @@ __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
         sh.probe.c[tid >> 6] = c;
     }
     __syncthreads();
-    if (tid == 0)
+    if (tid == 0) {
         st_f32(&p.z[b], probe_combine(sh.probe.s, sh.probe.c, p.bias));
+        if (p.epi_front == EPI_SELECT) {  // the step: z is ready for the front
+            __builtin_amdgcn_s_waitcnt(0);
+            st_u32(probe_flag(p, b), 1u);
+        }
+    }
 }
 
 // ------------------------------------------------------------- argmax role
@@ -935,7 +950,24 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
         s = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
         st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
     }
-    const float zb = p.epi_front == EPI_SELECT ? ld_f32(&p.z[b]) : 0.0f;
+    float zb = 0.0f;
+    if (p.epi_front == EPI_SELECT) {
+        if (p.probe_on) {
+            // the probe's work-group was dispatched before every tile and
+            // depends on nothing, so the flag is set in bounded time (the cap
+            // only guards against a broken launch)
+            uint32_t *fl = probe_flag(p, b);
+            for (int spin = 0; spin < (1 << 22) && __hip_atomic_load(fl, __ATOMIC_RELAXED,
+                                                                    __HIP_MEMORY_SCOPE_AGENT) == 0u;
+                 ++spin)
+                __builtin_amdgcn_s_sleep(2);
+            zb = ld_f32(&p.z[b]);
+            if (lane == 0)
+                st_u32(fl, 0u);
+        } else {
+            zb = ld_f32(&p.z[b]);
+        }
+    }
     int mn, me, jsel;
     pick_match(p, s, mn, me, jsel);
     const int L = sh.scan.L;
@@ -1912,27 +1944,30 @@ __global__ __launch_bounds__(kThreads) void k_label_clear(u32x4 *table, int64_t 
 
 template <bool kMulti, bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
+    // the argmax role's kept chunks share the union: the role is over (every
+    // wave) before an epilogue of this work-group uses LDS
     __shared__ Shared sh;
-    __shared__ u32x4 keep[kChunkVecs];  // argmax role: each lane's kept chunk
     const int blk = blockIdx.x;
     int b, t = 0;
     int role;  // 0 scan, 1 stand-alone probe, 2 argmax
     Prefetch pre = {1, -1, -1};
-    if (blk < p.n_scan_wg) {
-        b = blk / p.scan_tiles;
-        t = blk - b * p.scan_tiles;
-        scan_role<kMulti>(p, b, t, sh, pre);
-        role = 0;
-    } else if (blk < p.n_front_wg) {
-        b = blk - p.n_scan_wg;
+    // block order: [probe work-groups | scan tiles | argmax segments]
+    const int n_probe = p.n_front_wg - p.n_scan_wg;
+    if (blk < n_probe) {
+        b = blk;
         probe_role(p, b, sh);
         role = 1;
+    } else if (blk < p.n_front_wg) {
+        b = (blk - n_probe) / p.scan_tiles;
+        t = blk - n_probe - b * p.scan_tiles;
+        scan_role<kMulti>(p, b, t, sh, pre);
+        role = 0;
     } else {
         const int idx = blk - p.n_front_wg;
         const int rowi = idx / p.segs;
         const int s = idx - rowi * p.segs;
         b = rowi / p.R;
-        argmax_role(p, b, rowi - b * p.R, s, sh, keep);
+        argmax_role(p, b, rowi - b * p.R, s, sh, sh.am.keep);
         role = 2;
     }
     if (threadIdx.x >= 64)
