@@ -76,6 +76,8 @@ struct ScanShared {
     // the neural draft, staged while the scan runs (general select path)
     int32_t nt[SWITCHSD_MAX_R];
     int32_t np[SWITCHSD_MAX_R];
+    // the copy candidates' tokens, candidate c at c * k (general select path)
+    int32_t ctok[SWITCHSD_MAX_R];
     double ps[kWaves];  // probe partial sums of the waves (scan tile 0)
     double pc[kWaves];
     int32_t L;
@@ -894,15 +896,32 @@ __device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L,
     if (lane == 0)
         p.match_n[b] = mn;
     const int total = chain_layout(p, cl, ch);
-    auto src = [&](int c, int j) -> int {
-        const int pos = ch.e[c] + 1 + j;
-        return (pos >= lo && pos < hi) ? sh.scan.tile[pos - t0 + 64] : p.tokens[row + pos];
-    };
-    const int64_t cbase = (int64_t)b * W * p.k;
-    for (int idx = lane; idx < W * p.k; idx += 64) {
-        const int c = idx / p.k, j = idx - c * p.k;
-        p.copy_tokens[cbase + idx] = j < ch.cl[c] ? src(c, j) : -1;
+    // every candidate's tokens into LDS, four per lane requested together (from
+    // the LDS tile where they lie in it), then the outputs and the chains from
+    // there: one memory round trip for W * k tokens
+    const int ntk = W * p.k;
+    for (int i0 = 0; i0 < ntk; i0 += 4 * 64) {
+        int v4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int idx = i0 + q * 64 + lane;
+            const int c = idx < ntk ? idx / p.k : 0, j = idx - c * p.k;
+            v4[q] = -1;
+            if (idx < ntk && j < ch.cl[c]) {
+                const int pos = ch.e[c] + 1 + j;
+                v4[q] = (pos >= lo && pos < hi) ? sh.scan.tile[pos - t0 + 64] : p.tokens[row + pos];
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (i0 + q * 64 + lane < ntk)
+                sh.scan.ctok[i0 + q * 64 + lane] = v4[q];
     }
+    __builtin_amdgcn_wave_barrier();
+    auto src = [&](int c, int j) -> int { return sh.scan.ctok[c * p.k + j]; };
+    const int64_t cbase = (int64_t)b * W * p.k;
+    for (int idx = lane; idx < ntk; idx += 64)
+        p.copy_tokens[cbase + idx] = sh.scan.ctok[idx];
     if (p.epi_front == EPI_SELECT)
         write_chains(p, b, (mn >= p.kappa) && (zb >= p.theta), total, pre.nnb, ch, src,
                      [&](int i, int &tok, int &par) {
