@@ -854,16 +854,24 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total, int
     const int lane = threadIdx.x;
     const int64_t base = (int64_t)b * p.R;
     const int dnb = use ? total : nnb;
+    // the chains' first nodes in registers (one LDS read each, all at once)
+    int stq[kMaxCand];
+#pragma unroll
+    for (int q = 0; q < kMaxCand; ++q)
+        stq[q] = q < p.W ? ch.st[q] : 0x7FFFFFFF;
     for (int i = lane; i < p.R; i += 64) {
         int tok = -1, par = -1;
         if (i >= 1 && i < dnb) {
             if (use) {
-                int c = 0;
-                for (int q = 1; q < p.W; ++q)
-                    if (ch.st[q] <= i)
+                int c = 0, st = stq[0];  // the last chain starting at or before i
+#pragma unroll
+                for (int q = 1; q < kMaxCand; ++q)
+                    if (stq[q] <= i) {
                         c = q;
-                tok = src(c, i - ch.st[c]);
-                par = i == ch.st[c] ? 0 : i - 1;
+                        st = stq[q];
+                    }
+                tok = src(c, i - st);
+                par = i == st ? 0 : i - 1;
             } else {
                 nsrc(i, tok, par);
             }
