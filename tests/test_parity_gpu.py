@@ -162,6 +162,11 @@ CASES = {
                      vocab=2, tree=True, ties=True),
     "tree_r100_general": dict(seed=11, B=4, Lmax=500, V=40, R=100, k=10, lens=(2, 1), kappa=1,
                               theta=0.0, vocab=2, tree=True, ties=True),
+    # more sequences than work-groups fit on the GPU at once, each with two
+    # scan tiles: every sequence's probe work-group comes first in the grid
+    # and the last tile of each sequence waits for its flag
+    "many_two_tile_contexts": dict(seed=17, B=1600, Lmax=1500, V=24, R=4, k=3, lens=(3, 2, 1),
+                                   kappa=1, theta=0.0, vocab=5),
     # more than 256 sequences with long drafts: the per-row verify launch (not
     # the streamed one) with the accept epilogue over more than 64 nodes
     "tree_r70_wide_batch": dict(seed=16, B=260, Lmax=96, V=64, R=70, k=5, lens=(2, 1),
