@@ -441,7 +441,7 @@ int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t
 size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
     if (B < 0 || R < 0 || V < 0)
         return 0;
-    const size_t n = (size_t)B * R * chunks_per_row(V) * (kThreads / 64) * 4;
+    const size_t n = (size_t)B * R * chunks_per_row(V) * kCsumPerChunk * 4;
     return (n + kAlign - 1) / kAlign * kAlign;
 }
 

@@ -16,6 +16,9 @@ constexpr int kUnroll = 4;
 constexpr int kChunkVecs = kThreads * kUnroll;
 // Context end positions covered by one scan work-group.
 constexpr int kScanTile = 1024;
+// Weight sums per 16 KB chunk of the draw at T > 0: one per block of 256
+// vectors and wave.
+constexpr int kCsumPerChunk = kUnroll * (kThreads / 64);
 // Per-sequence workspace slots live on their own 256-byte lines: atomics to
 // one line serialize, and every work-group of a sequence arrives at its line.
 constexpr int kLineU32 = 64;

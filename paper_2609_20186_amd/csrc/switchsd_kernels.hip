@@ -98,11 +98,7 @@ struct EpiShared {  // accept over R > 64 nodes
     uint32_t st[2][SWITCHSD_MAX_R];  // pointer-jumping state, double-buffered (final_epilogue)
 };
 struct PickShared {  // one row's draw at T > 0
-    uint32_t cw[kThreads];             // per-chunk, per-wave weight sums
-    uint32_t tot[kWaves][kUnroll];     // per-wave totals of the chosen chunk's vector blocks
-    uint32_t wsum[kWaves];             // per-wave totals within the chosen block
-    unsigned long long target;         // remaining target inside the chosen chunk / block
-    int32_t cstar, ustar, qstar, y;
+    uint32_t cw[64 * kCsumPerChunk];   // the row's weight sums per (chunk, block, wave)
     int32_t last;                      // this work-group completed the row (row_done)
 };
 union Shared {
@@ -1506,114 +1502,93 @@ __device__ __forceinline__ unsigned long long scaled_target(uint32_t u, unsigned
            (((unsigned long long)u * (Z & 0xFFFFFFFFull)) >> 32);
 }
 
-// The draw of row r of sequence b (its maximum m): the chunk sums give Z and
-// the target floor(u Z / 2^32) and its chunk; the chunk is read again, the
-// 256-vector block and the vector are found by prefix sums and the element by
-// a scan of 8 weights.  The drawn token replaces the row's key (key_max reads
-// it as a finite maximum of index y).  Every thread of the work-group takes
-// part.
+// Weight sums of chunk c (16 KB) of a row, one per block of 256 vectors and
+// wave (64 vectors), stored at cs[(c * kUnroll + u) * kWaves + wave]: the
+// elements of a chunk in index order are block by block, wave by wave.
+__device__ __forceinline__ void store_block_sums(const u32x4 (&A)[kUnroll], int c, int nq, float m,
+                                                 float samp_c, uint32_t *cs) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        uint32_t w = c * kChunkVecs + u * kThreads + tid < nq ? vec_weight(A[u], m, samp_c) : 0u;
+        w = wave_reduce_u32(w, 0u, [](uint32_t a, uint32_t x) { return a + x; });
+        if (lane == 0)
+            st_u32(&cs[(c * kUnroll + u) * kWaves + wave], w);
+    }
+}
+
+// The draw of row r of sequence b (its maximum m), by wave 0: the block sums
+// give Z and the target floor(u Z / 2^32), then the chunk, the block and the
+// wave's 64 vectors holding it; only those 64 vectors are read again, and the
+// vector and the element are found by a prefix over their weights and a scan
+// of 8.  The drawn token replaces the row's key (key_max reads it as a finite
+// maximum of index y).  Every thread of the work-group calls this (the block
+// sums are staged in LDS by all of them).
 __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned long long *keyp,
                          Shared &sh) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kCsumPerChunk;
+    const int ncs = p.cpr * kCsumPerChunk;  // <= 64 chunks (V <= 524288)
+    for (int i = tid; i < ncs; i += kThreads)
+        sh.pick.cw[i] = (uint32_t)ld_i32((const int32_t *)&cs[i]);
+    __syncthreads();
+    if (wave != 0)
+        return;
     const uint32_t uni = p.uniforms[(int64_t)b * p.R + r];
-    const uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
-    sh.pick.cw[tid] = tid < p.cpr * kWaves ? (uint32_t)ld_i32((const int32_t *)&cs[tid]) : 0u;
-    __syncthreads();
-    if (wave == 0) {
-        // chunk totals, their inclusive prefix, the target and its chunk
-        unsigned long long cc = 0;
-        if (lane < p.cpr)
-            cc = (unsigned long long)sh.pick.cw[4 * lane] + sh.pick.cw[4 * lane + 1] +
-                 sh.pick.cw[4 * lane + 2] + sh.pick.cw[4 * lane + 3];
-        unsigned long long inc = cc;
+    // chunk totals, their inclusive prefix, the target and its chunk
+    unsigned long long cc = 0;
+    if (lane < p.cpr) {
 #pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const unsigned long long y = __shfl_up(inc, o);
-            if (lane >= o)
-                inc += y;
-        }
-        const unsigned long long Z = __shfl(inc, 63);
-        const unsigned long long target = scaled_target(uni, Z);
-        const unsigned long long hit = __ballot(lane < p.cpr && inc > target);
-        const int cst = __ffsll((long long)hit) - 1;  // exists: target < Z
-        const unsigned long long before = __shfl(inc - cc, cst);
-        if (lane == 0) {
-            sh.pick.cstar = cst;
-            sh.pick.target = target - before;
-        }
+        for (int e = 0; e < kCsumPerChunk; ++e)
+            cc += sh.pick.cw[lane * kCsumPerChunk + e];
     }
-    __syncthreads();
-    const int cst = sh.pick.cstar;
-    const int nq = p.V >> 3;
-    const u32x4 *vp =
-        reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
-    u32x4 A[kUnroll];
-    load_chunk(A, vp, cst * kChunkVecs, nq);
-    uint32_t vs[kUnroll];  // weight of vector q = chunk start + u * 256 + tid
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        vs[u] = cst * kChunkVecs + u * kThreads + tid < nq ? vec_weight(A[u], m, p.samp_c)
-                                                            : 0u;
-    // totals of the four blocks of 256 vectors (each < 2^32)
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        const uint32_t t = wave_reduce_u32(vs[u], 0u, [](uint32_t a, uint32_t x) { return a + x; });
-        if (lane == 0)
-            sh.pick.tot[wave][u] = t;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        unsigned long long tg = sh.pick.target;
-        int us = kUnroll - 1;
-        for (int u = 0; u < kUnroll; ++u) {
-            const unsigned long long t = (unsigned long long)sh.pick.tot[0][u] +
-                                         sh.pick.tot[1][u] + sh.pick.tot[2][u] +
-                                         sh.pick.tot[3][u];
-            if (tg < t) {
-                us = u;
-                break;
-            }
-            tg -= t;
-        }
-        sh.pick.ustar = us;
-        sh.pick.target = tg;
-        sh.pick.qstar = kThreads;
-    }
-    __syncthreads();
-    // within the block: inclusive prefix over the 256 vectors in order
-    const int us = sh.pick.ustar;
-    uint32_t mine = 0;
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        if (u == us)
-            mine = vs[u];
-    uint32_t inc = mine;
+    unsigned long long inc = cc;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
+        const unsigned long long y = __shfl_up(inc, o);
         if (lane >= o)
             inc += y;
     }
-    if (lane == 63)
-        sh.pick.wsum[wave] = inc;
-    __syncthreads();
-    unsigned long long off = 0;
-    for (int w = 0; w < wave; ++w)
-        off += sh.pick.wsum[w];
-    const unsigned long long tg = sh.pick.target;
-    const unsigned long long hit = __ballot(off + inc > tg);
-    if (hit && lane == __ffsll((long long)hit) - 1)
-        atomicMin(&sh.pick.qstar, tid);
-    __syncthreads();
-    if (tid == sh.pick.qstar) {
-        // the element within this thread's vector
-        unsigned long long run = off + inc - mine;
-        const int q = cst * kChunkVecs + us * kThreads + tid;
-        u32x4 v = {0u, 0u, 0u, 0u};
+    const unsigned long long Z = __shfl(inc, 63);
+    unsigned long long tg = scaled_target(uni, Z);
+    const unsigned long long hit = __ballot(lane < p.cpr && inc > tg);
+    const int cst = __ffsll((long long)hit) - 1;  // exists: target < Z
+    tg -= __shfl(inc - cc, cst);
+    // within the chunk: the (block, wave) entry holding the target (lanes
+    // 0..15 take the entries in index order)
+    const unsigned long long ce =
+        lane < kCsumPerChunk ? (unsigned long long)sh.pick.cw[cst * kCsumPerChunk + lane] : 0ull;
+    unsigned long long ie = ce;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            if (u == us)
-                v = A[u];
+    for (int o = 1; o < kCsumPerChunk; o <<= 1) {
+        const unsigned long long y = __shfl_up(ie, o);
+        if (lane >= o)
+            ie += y;
+    }
+    const unsigned long long hit2 = __ballot(lane < kCsumPerChunk && ie > tg);
+    const int est = __ffsll((long long)hit2) - 1;  // exists: tg < the chunk's total
+    tg -= __shfl(ie - ce, est);
+    // the entry's 64 vectors: lane l holds vector cst * kChunkVecs + est * 64 + l
+    // (est = block * kWaves + wave, and a block's vectors are wave by wave)
+    const int nq = p.V >> 3;
+    const int q = cst * kChunkVecs + est * 64 + lane;
+    const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (q < nq)
+        v = vp[q];
+    const uint32_t vw = q < nq ? vec_weight(v, m, p.samp_c) : 0u;
+    uint32_t iv = vw;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(iv, o);
+        if (lane >= o)
+            iv += y;
+    }
+    const unsigned long long hit3 = __ballot((unsigned long long)iv > tg);
+    const int lst = __ffsll((long long)hit3) - 1;  // exists: tg < the entry's total
+    if (lane == lst) {
+        // the element within this lane's vector
+        unsigned long long run = (unsigned long long)(iv - vw);
         int e = 7;
         for (int j = 0; j < 8; ++j) {
             const uint32_t x = v[j >> 1];
@@ -1623,11 +1598,9 @@ __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned lo
                 break;
             }
         }
-        sh.pick.y = q * 8 + e;
+        const uint32_t y = (uint32_t)q * 8u + (uint32_t)e;
+        st_u64(keyp, (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - y));
     }
-    __syncthreads();
-    if (tid == 0)
-        st_u64(keyp, (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)sh.pick.y));
 }
 
 // The sum work-groups of a drafted row arrive with the units (16 KB chunks or
@@ -1667,7 +1640,6 @@ __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t un
 template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     __shared__ Shared sh;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int rowi = blockIdx.x / p.segs;
     const int s = blockIdx.x - rowi * p.segs;
     const int b = rowi / p.R, r = rowi - b * p.R;
@@ -1689,18 +1661,11 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     const bool active = key_max(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]), m);
     if (active && !p.speculate)
         load_chunk(A, vp, c0 * kChunkVecs, nq);
-    uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+    uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kCsumPerChunk;
     for (int c = c0; active && c < c1; ++c) {
         if (c + 1 < c1)
             load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
-        uint32_t sum = 0;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            if (c * kChunkVecs + u * kThreads + tid < nq)
-                sum += vec_weight(A[u], m, p.samp_c);
-        sum = wave_reduce_u32(sum, 0u, [](uint32_t a, uint32_t x) { return a + x; });
-        if (lane == 0)
-            st_u32(&cs[c * kWaves + wave], sum);
+        store_block_sums(A, c, nq, m, p.samp_c, cs);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
             A[u] = Bv[u];
@@ -1717,7 +1682,7 @@ template <bool kCommit>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void
 k_sample_sums_stream(StepParams p) {
     __shared__ Shared sh;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
     constexpr int Q = kListMaxB / 64;
     const int cpr = p.cpr;
     int first[Q], dnq[Q];
@@ -1790,16 +1755,9 @@ k_sample_sums_stream(StepParams p) {
         }
         float m = 0.0f;
         const bool active = key_max(key, m);
-        if (active) {
-            uint32_t sum = 0;
-#pragma unroll
-            for (int q = 0; q < kUnroll; ++q)
-                if (c * kChunkVecs + q * kThreads + (int)threadIdx.x < nq)
-                    sum += vec_weight(A[q], m, p.samp_c);
-            sum = wave_reduce_u32(sum, 0u, [](uint32_t a, uint32_t x) { return a + x; });
-            if (lane == 0)
-                st_u32(&p.csum[(((int64_t)b * p.R + r) * cpr + c) * kWaves + wave], sum);
-        }
+        if (active)
+            store_block_sums(A, c, nq, m, p.samp_c,
+                             p.csum + ((int64_t)b * p.R + r) * cpr * kCsumPerChunk);
         ++done_r;
         if (c == cpr - 1 || u + 1 == u1) {  // end of this row's piece
             row_done<kCommit>(p, b, r, dnb, done_r, (uint32_t)cpr, active, m, sh);

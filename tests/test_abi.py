@@ -165,7 +165,8 @@ def test_sample_entry_point_rejects():
     SW = WS
     need = sd.sample_workspace_bytes(2, 8, 128)
     assert need >= 2 * 8 * 1 * 4 * 4 and need % 256 == 0
-    assert sd.sample_workspace_bytes(2, 8, 128256) == 2 * 8 * 16 * 4 * 4
+    # a 32-bit weight sum per 16 KB chunk, block of 256 vectors (4) and wave (4)
+    assert sd.sample_workspace_bytes(2, 8, 128256) == 2 * 8 * 16 * 4 * 4 * 4
     assert sd.sample_workspace_bytes(-1, 8, 8) == 0
 
     def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS, wsn=4096):
