@@ -67,6 +67,15 @@ int32_t key_stride_for(int32_t R) {
     return (int32_t)(((int64_t)R + kLineU64 - 1) / kLineU64 * kLineU64);
 }
 
+// Slots of a sequence's window table (copy labels): a power of two of at
+// least 2 Lmax (the table is at most half full) and 64.
+int64_t label_table_slots(int32_t Lmax) {
+    int64_t t = 64;
+    while (t < 2 * (int64_t)Lmax)
+        t <<= 1;
+    return t;
+}
+
 int32_t rtk_stride_for(int32_t R) {
     return (int32_t)(((int64_t)R + kLineU32 - 1) / kLineU32 * kLineU32);
 }
@@ -552,21 +561,6 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
                          a->accept_node, a->bonus, a->out_tokens, a->amax, workspace,
                          workspace_bytes, R <= 16, sampled ? &sa : nullptr, &p, stream);
 }
-
-}  // extern "C"
-
-namespace {
-// Slots of a sequence's window table: a power of two of at least 2 Lmax (the
-// table is at most half full) and 64.
-int64_t label_table_slots(int32_t Lmax) {
-    int64_t t = 64;
-    while (t < 2 * (int64_t)Lmax)
-        t <<= 1;
-    return t;
-}
-}  // namespace
-
-extern "C" {
 
 size_t switchsd_label_workspace_bytes(int32_t B, int32_t Lmax) {
     if (B < 0 || Lmax < 0 || Lmax > (1 << 28))
