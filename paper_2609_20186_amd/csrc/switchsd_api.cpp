@@ -68,10 +68,11 @@ int32_t key_stride_for(int32_t R) {
 }
 
 // Slots of a sequence's window table (copy labels): a power of two of at
-// least 2 Lmax (the table is at most half full) and 64.
+// least 4 Lmax (the table is at most a quarter full, which keeps the probe
+// walks short) and 64.
 int64_t label_table_slots(int32_t Lmax) {
     int64_t t = 64;
-    while (t < 2 * (int64_t)Lmax)
+    while (t < 4 * (int64_t)Lmax)
         t <<= 1;
     return t;
 }

@@ -1780,7 +1780,7 @@ k_sample_sums_stream(StepParams p) {
 // position j is copy-mode iff an n-token window covering it repeats an
 // earlier window, i.e. the window starting at some s in [j - n + 1, j] is not
 // the first occurrence of its n tokens.  An open-addressing table per
-// sequence (linear probing, at most half full) holds one slot per distinct
+// sequence (linear probing, at most a quarter full) holds one slot per distinct
 // window content with the complement of its earliest start (0: empty):
 // k_label_insert claims a slot with a compare-and-swap or, when the slot's
 // window has the same tokens (compared token by token, never by hash),

@@ -192,11 +192,11 @@ def test_sample_entry_point_rejects():
 def test_label_entry_point_rejects():
     lib = sd.lib
     need = sd.label_workspace_bytes(2, 100)
-    # a window table per sequence: a power of two of at least 2 Lmax (and 64)
+    # a window table per sequence: a power of two of at least 4 Lmax (and 64)
     # 32-bit slots
-    assert need == 2 * 256 * 4
-    assert sd.label_workspace_bytes(3, 4096) == 3 * 8192 * 4
-    assert sd.label_workspace_bytes(1, 20) == 64 * 4
+    assert need == 2 * 512 * 4
+    assert sd.label_workspace_bytes(3, 4096) == 3 * 16384 * 4
+    assert sd.label_workspace_bytes(1, 10) == 64 * 4
     assert sd.label_workspace_bytes(-1, 5) == 0 and sd.label_workspace_bytes(1, (1 << 28) + 1) == 0
     assert lib.switchsd_copy_labels(P, P, 1, (1 << 28) + 1, 5, P, WS, need, None) == ESHAPE
     assert lib.switchsd_copy_labels(P, P, -1, 100, 5, P, WS, need, None) == ESHAPE
