@@ -1880,14 +1880,17 @@ __device__ __forceinline__ bool label_repeats(const int32_t *x, const uint32_t *
     return false;
 }
 
-// Labels of 256 positions of sequence b (one 64-position block per wave):
-// bit l of block w's ballot E_w says whether the window starting at 64 w + l
-// repeats an earlier one; position j is copy-mode iff such a start lies in
-// [j - n + 1, j], i.e. bit j of E | E << 1 | ... | E << (n - 1) with the
-// previous block's bits carried in (wave 0 also looks up the block before the
-// range).
-__global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t n, int32_t tsize,
-                                                          const uint32_t *table, uint8_t *labels) {
+// Labels of 256 positions of sequence b (one 64-position block per wave of
+// the first four): bit l of block w's ballot E_w says whether the window
+// starting at 64 w + l repeats an earlier one; position j is copy-mode iff
+// such a start lies in [j - n + 1, j], i.e. bit j of E | E << 1 | ... |
+// E << (n - 1) with the previous block's bits carried in.  A fifth wave looks
+// up the block before the range, so that no wave walks two blocks.
+constexpr int kLabelWriteThreads = kThreads + 64;
+__global__ __launch_bounds__(kLabelWriteThreads) void k_label_write(StepParams p, int32_t n,
+                                                                    int32_t tsize,
+                                                                    const uint32_t *table,
+                                                                    uint8_t *labels) {
     __shared__ unsigned long long E[kWaves + 1];  // E[0]: the block before the range
     const int per = (p.Lmax + kThreads - 1) / kThreads;
     const int b = blockIdx.x / per;
@@ -1897,18 +1900,15 @@ __global__ __launch_bounds__(kThreads) void k_label_write(StepParams p, int32_t 
     const int32_t *x = p.tokens + (int64_t)b * p.Lmax;
     const uint32_t *tab = table + (int64_t)b * tsize;
     const uint32_t mask = (uint32_t)tsize - 1u;
-    const int s = g * kThreads + tid;
-    const unsigned long long m = __ballot(s <= L - n && label_repeats(x, tab, mask, s, n));
+    // waves 0..3: starts 256 g + tid; wave 4: the 64 starts before them
+    const int s = wave < kWaves ? g * kThreads + tid : g * kThreads - 64 + lane;
+    const unsigned long long m =
+        __ballot(s >= 0 && s <= L - n && label_repeats(x, tab, mask, s, n));
     if (lane == 0)
-        E[wave + 1] = m;
-    if (wave == 0) {
-        const int sp = s - 64;
-        const unsigned long long mp =
-            __ballot(sp >= 0 && sp <= L - n && label_repeats(x, tab, mask, sp, n));
-        if (lane == 0)
-            E[0] = mp;
-    }
+        E[wave < kWaves ? wave + 1 : 0] = m;
     __syncthreads();
+    if (wave == kWaves)
+        return;
     const unsigned long long Ec = E[wave + 1], Ep = E[wave];
     unsigned long long Y = Ec;
     for (int u = 1; u < n; ++u)
@@ -2126,7 +2126,7 @@ int launch_label_kernels(const StepParams &p, int32_t n, uint8_t *labels, int32_
                        (uint32_t *)table);
     if (hipGetLastError() != hipSuccess)
         return SWITCHSD_EHIP;
-    hipLaunchKernelGGL(k_label_write, grid, dim3(kThreads), 0, stream, p, n, tsize,
+    hipLaunchKernelGGL(k_label_write, grid, dim3(kLabelWriteThreads), 0, stream, p, n, tsize,
                        (const uint32_t *)table, labels);
     if (hipGetLastError() != hipSuccess)
         return SWITCHSD_EHIP;
