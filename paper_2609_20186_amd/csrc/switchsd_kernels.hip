@@ -1848,13 +1848,11 @@ __global__ __launch_bounds__(kThreads) void k_label_insert(StepParams p, int32_t
     uint32_t slot = label_hash(x, s, n) & mask;
     const uint32_t mine = ~(uint32_t)s;
     for (int probe = 0; probe < tsize; ++probe) {
-        // a plain read first: most windows find their content already there
-        uint32_t cur = __hip_atomic_load(&tab[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (cur == 0u) {
-            cur = atomicCAS(&tab[slot], 0u, mine);
-            if (cur == 0u)
-                return;  // first of its content to arrive here
-        }
+        // one compare-and-swap claims an empty slot or returns its start (a
+        // plain read first costs one more round trip for every first window)
+        const uint32_t cur = atomicCAS(&tab[slot], 0u, mine);
+        if (cur == 0u)
+            return;  // first of its content to arrive here
         if (same_window(x, (int)~cur, s, n)) {
             if (cur < mine)  // a later start is there: the earliest one wins
                 atomicMax(&tab[slot], mine);
