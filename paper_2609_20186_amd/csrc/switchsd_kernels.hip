@@ -561,6 +561,33 @@ __device__ __forceinline__ float fmax_first(float m, float x) {
     return (m != m || x > m) ? x : m;
 }
 
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ s16x2 as_s16x2(uint32_t u) { return __builtin_bit_cast(s16x2, u); }
+
+// Maximum of the 8 * kUnroll elements of a lane's chunk as floats, NaN ignored
+// (NaN only when every element is NaN).
+__device__ __forceinline__ float chunk_max(const u32x4 (&v)[kUnroll]) {
+    float m = -__builtin_inff();
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        m = max3n(m, lo_f(v[u][0]), hi_f(v[u][0]));
+        m = max3n(m, lo_f(v[u][1]), hi_f(v[u][1]));
+        m = max3n(m, lo_f(v[u][2]), hi_f(v[u][2]));
+        m = max3n(m, lo_f(v[u][3]), hi_f(v[u][3]));
+    }
+    if (m != m) {  // a NaN somewhere: recompute ignoring NaN
+        m = __builtin_nanf("");
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+            for (int w4 = 0; w4 < 4; ++w4) {
+                m = fmax_first(m, lo_f(v[u][w4]));
+                m = fmax_first(m, hi_f(v[u][w4]));
+            }
+    }
+    return m;
+}
+
 // Chunk [qc0, qc0 + kChunkVecs) of a row piece of nq vectors; vectors past nq
 // read as -inf and are never reported (lazy_index checks q < nq).  A later
 // chunk replaces the kept one only with a strictly larger maximum, so ties
@@ -574,25 +601,26 @@ __device__ __forceinline__ void lazy_chunk(u32x4 (&v)[kUnroll], int qc0, int nq,
             if (qc0 + u * kThreads + tid >= nq)
                 v[u] = u32x4{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
     }
-    float m = -__builtin_inff();
+    // Read as signed 16-bit integers, the bf16 bit patterns of +0 .. +inf keep
+    // their order and sit above every negative pattern, and positive NaNs sit
+    // above +inf; one packed integer maximum per two elements then gives the
+    // chunk's maximum whenever it lies in [+0, +inf].  Otherwise (a positive
+    // NaN, or no element >= +0) the floats are compared, unless the lane
+    // already holds a maximum >= +0 that an all-negative chunk cannot raise.
+    s16x2 t[4];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        m = max3n(m, lo_f(v[u][0]), hi_f(v[u][0]));
-        m = max3n(m, lo_f(v[u][1]), hi_f(v[u][1]));
-        m = max3n(m, lo_f(v[u][2]), hi_f(v[u][2]));
-        m = max3n(m, lo_f(v[u][3]), hi_f(v[u][3]));
-    }
-    if (__any(m != m)) {  // a NaN somewhere: recompute those lanes ignoring NaN
-        if (m != m) {
-            m = __builtin_nanf("");
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-#pragma unroll
-                for (int w4 = 0; w4 < 4; ++w4) {
-                    m = fmax_first(m, lo_f(v[u][w4]));
-                    m = fmax_first(m, hi_f(v[u][w4]));
-                }
-        }
+    for (int w4 = 0; w4 < 4; ++w4)
+        t[w4] = __builtin_elementwise_max(
+            __builtin_elementwise_max(as_s16x2(v[0][w4]), as_s16x2(v[1][w4])),
+            __builtin_elementwise_max(as_s16x2(v[2][w4]), as_s16x2(v[3][w4])));
+    t[0] = __builtin_elementwise_max(__builtin_elementwise_max(t[0], t[1]),
+                                     __builtin_elementwise_max(t[2], t[3]));
+    const int m16 = t[0].x > t[0].y ? t[0].x : t[0].y;
+    float m = m16 >= 0 ? __uint_as_float((uint32_t)m16 << 16) : -__builtin_inff();
+    const bool exact = m16 > 0x7F80 || (m16 < 0 && !(s.best >= 0.0f));
+    if (__any(exact)) {
+        if (exact)
+            m = chunk_max(v);
     }
     const bool upd = m == m && !(m <= s.best);
     s.best = upd ? m : s.best;

@@ -88,7 +88,8 @@ SPECIAL = np.array([0x7F80, 0xFF80, 0x7FC0, 0xFFC0, 0x8000, 0x0000, 0x0001], np.
 
 
 def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vocab=None,
-                ragged=True, specials=False, ties=False, repeat_tail=0, plant=False, n_cand=1):
+                ragged=True, specials=False, ties=False, repeat_tail=0, plant=False, n_cand=1,
+                neg=False):
     rng = np.random.default_rng(seed)
     vocab = vocab or V
     tokens = rng.integers(0, vocab, (B, Lmax)).astype(np.int32)
@@ -121,6 +122,21 @@ def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vo
     else:
         logits = W.f32_to_bf16_bits(np.clip(rng.standard_normal((B, R, V)), -7.5, 7.5)
                                     .astype(np.float32))
+    if neg:
+        # every element <= -0, except in the last tenth of the odd rows (a
+        # running maximum that stays negative over many chunks, then turns
+        # positive late); negative NaN and -0 sprinkled in
+        logits = W.f32_to_bf16_bits(-np.abs(np.clip(rng.standard_normal((B, R, V)), -7.5, 7.5))
+                                    .astype(np.float32)) | np.uint16(0x8000)
+        logits[:, 1::2, V - max(V // 10, 1):] &= np.uint16(0x7FFF)
+        m = rng.random((B, R, V)) < 0.02
+        logits[m] = rng.choice(np.array([0xFFC0, 0x8000, 0xFF80], np.uint16), int(m.sum()))
+        logits[0, 0, :] = 0xFF80                            # all -inf: index 0
+        if R > 2:
+            logits[0, 2, :] = 0xFFC0                        # all negative NaN: index 0
+        if B > 1:
+            logits[1, 0, :] = 0x8000                        # -0 everywhere, one +0 late:
+            logits[1, 0, V - 1] = 0x0000                    # ties at index 0
     if specials:
         m = rng.random((B, R, V)) < 0.05
         logits[m] = rng.choice(SPECIAL, int(m.sum()))
@@ -175,6 +191,12 @@ CASES = {
                                theta=-np.inf, vocab=2, ties=True, plant=True),
     "long_halo_ngram64": dict(seed=13, B=3, Lmax=8300, V=100, R=3, k=2, lens=(64, 63, 1),
                               kappa=1, theta=0.0, vocab=2, ragged=False, repeat_tail=80),
+    # rows with no element above -0 over many chunks (the argmax must compare
+    # the floats there), and rows that only turn positive near their end
+    "negative_rows_multi_chunk": dict(seed=18, B=3, Lmax=200, V=70001, R=4, k=3, lens=(2, 1),
+                                      kappa=1, theta=0.0, vocab=10, neg=True),
+    "negative_rows_short": dict(seed=19, B=4, Lmax=100, V=3001, R=5, k=4, lens=(2, 1),
+                                kappa=1, theta=0.0, vocab=10, neg=True),
     "k0_d0": dict(seed=14, B=4, Lmax=50, V=20, R=2, k=0, lens=(1,), kappa=1, theta=-np.inf,
                   vocab=3, d=0),
     "d_odd": dict(seed=15, B=3, Lmax=50, V=20, R=3, k=2, lens=(1,), kappa=1, theta=0.0,

@@ -58,6 +58,8 @@ SAMPLE_CASES = {
                     theta=-0.2, vocab=30, n_cand=10, plant=True),
     "multi_chunk_rows": dict(seed=65, B=3, Lmax=900, V=40000, R=4, k=3, lens=(2, 1), kappa=1,
                              theta=-np.inf, vocab=10, plant=True),
+    "negative_rows": dict(seed=70, B=3, Lmax=200, V=40000, R=4, k=3, lens=(2, 1), kappa=1,
+                          theta=0.0, vocab=10, neg=True),
     "v8": dict(seed=66, B=5, Lmax=40, V=8, R=3, k=2, lens=(1,), kappa=1, theta=0.0, vocab=3),
     # more than 256 sequences with long drafts: per-row weight sums (not the
     # streamed ones), then the accept epilogue over more than 64 nodes
