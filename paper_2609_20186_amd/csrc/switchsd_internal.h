@@ -78,7 +78,7 @@ struct StepParams {
     int32_t *amax;
     int32_t *accept_len, *accept_node, *bonus, *out_tokens;
     Workspace ws;
-    // grid layout: [scan tiles][probe][argmax row segments]
+    // grid layout: [probe][scan tiles][argmax row segments, segment-major]
     int32_t scan_tiles;  // per sequence (0: no scan role)
     int32_t probe_on;    // 1: one probe work-group per sequence, first in the grid
     int32_t scan_probe;  // 1: scan tile 0 of each sequence also computes the probe

@@ -1668,8 +1668,10 @@ __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t un
 template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     __shared__ Shared sh;
-    const int rowi = blockIdx.x / p.segs;
-    const int s = blockIdx.x - rowi * p.segs;
+    // segment-major, as the argmax role of the step kernel
+    const int nrows = p.B * p.R;
+    const int s = blockIdx.x / nrows;
+    const int rowi = blockIdx.x - s * nrows;
     const int b = rowi / p.R, r = rowi - b * p.R;
     const int nq = p.V >> 3;
     // every work-group of the row covers at least one chunk (segs = chunks
@@ -1974,9 +1976,15 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
         scan_role<kMulti>(p, b, t, sh, pre);
         role = 0;
     } else {
+        // segment-major: the first B * R work-groups take every row's first
+        // segment, the next B * R the second ...  Work-groups later in the
+        // dispatch stream more slowly (they share their CUs with ones issued
+        // earlier), and a sequence waits for its slowest segment; so every
+        // sequence gets segments from the whole dispatch order.
         const int idx = blk - p.n_front_wg;
-        const int rowi = idx / p.segs;
-        const int s = idx - rowi * p.segs;
+        const int nrows = p.B * p.R;
+        const int s = idx / nrows;
+        const int rowi = idx - s * nrows;
         b = rowi / p.R;
         argmax_role(p, b, rowi - b * p.R, s, sh, sh.am.keep);
         role = 2;
