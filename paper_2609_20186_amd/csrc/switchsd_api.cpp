@@ -328,7 +328,10 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     p.csum = (uint32_t *)sa->ws;
     p.cpr = (int32_t)chunks_per_row(p.V);
     const int64_t rows = (int64_t)p.B * p.R;
-    int64_t segs = (4 * (int64_t)cus + rows - 1) / rows;
+    // about eight sum work-groups per CU: the kernel needs few registers, and
+    // eight resident work-groups (their LDS fills the CU's 160 KB) hide the
+    // load latency behind the weight arithmetic better than four
+    int64_t segs = (8 * (int64_t)cus + rows - 1) / rows;
     if (segs > p.cpr)
         segs = p.cpr;
     if (segs < 1)
