@@ -54,6 +54,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kThreads / 64;
 constexpr int kScanBlocks = kScanTile / kThreads;  // blocks of 64 positions per scan wave
+constexpr int kScanOffsets = 4;  // offsets u whose LDS reads are issued together
 constexpr uint32_t kNoIdx = 0xFFFFFFFFu;
 
 // Copy candidates being turned into a draft: end, length and first node of
@@ -69,7 +70,6 @@ struct ScanShared {
     int32_t red[SWITCHSD_MAX_NGRAM];
     // W > 1: each wave's W most recent ends + 1 per n-gram length, then the
     // work-group's merged list
-    unsigned long long bm[SWITCHSD_MAX_NGRAM * kWaves * kScanBlocks];  // block masks
     int32_t cand[SWITCHSD_MAX_NGRAM * kWaves * kMaxCand];
     int32_t merged[kMaxCand];
     ChainShared ch;
@@ -390,42 +390,60 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
         }
         // LDS index of position w0 + 64 i + lane is lx0 + 64 i
         const int lx0 = w0 - t0 + 64 + lane;
-        for (int u = 0; u < p.nmax; ++u) {
-            const int pu = sh.scan.pat[u];
-            // x[e - u] for every block: independent LDS reads, issued together
-            int xu[kScanBlocks];
+        for (int u0 = 0; u0 < p.nmax; u0 += kScanOffsets) {
+            // x[e - u] for kScanOffsets offsets u and every block: independent
+            // LDS reads, issued together (one LDS wait per batch of offsets)
+            int pu[kScanOffsets], xu[kScanOffsets][kScanBlocks];
 #pragma unroll
-            for (int i = 0; i < kScanBlocks; ++i)
-                xu[i] = u == 0 ? tok[i + 1] : sh.scan.tile[lx0 + 64 * i - u];
-            // positions e < u have no u-th token back (only in the context's first block)
-#pragma unroll
-            for (int i = 0; i < kScanBlocks; ++i)
-                M[i] &= __ballot(xu[i] == pu && (i > 0 || w0 > 0 || lane >= u));
-            // record the length equal to u + 1, if it is one of the lengths
-            int jm = -1;
-#pragma unroll
-            for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
-                if (j < p.n_ngram && p.lens[j] == u + 1)
-                    jm = j;
-            if (jm >= 0) {
-                int e1 = 0;
+            for (int du = 0; du < kScanOffsets; ++du) {
+                const int u = u0 + du < p.nmax ? u0 + du : p.nmax - 1;
+                pu[du] = sh.scan.pat[u];
 #pragma unroll
                 for (int i = 0; i < kScanBlocks; ++i)
-                    if (M[i])
-                        e1 = w0 + 64 * i + 64 - __clzll((long long)M[i]);  // highest end + 1
+                    xu[du][i] = u == 0 ? tok[i + 1] : sh.scan.tile[lx0 + 64 * i - u];
+            }
+#pragma unroll
+            for (int du = 0; du < kScanOffsets; ++du) {
+                const int u = u0 + du;
+                if (u >= p.nmax)
+                    break;
+                // positions e < u have no u-th token back (only in the context's
+                // first block)
+#pragma unroll
+                for (int i = 0; i < kScanBlocks; ++i)
+                    M[i] &= __ballot(xu[du][i] == pu[du] && (i > 0 || w0 > 0 || lane >= u));
+                // record the length equal to u + 1, if it is one of the lengths
+                int jm = -1;
 #pragma unroll
                 for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
-                    if (j == jm)
-                        best[j] = e1;
-                if (kMulti && p.W > 1) {
-                    // keep the block masks of this length for the candidate lists
-                    unsigned long long m = 0ull;
+                    if (j < p.n_ngram && p.lens[j] == u + 1)
+                        jm = j;
+                if (jm >= 0) {
+                    int e1 = 0;
 #pragma unroll
                     for (int i = 0; i < kScanBlocks; ++i)
-                        if (lane == i)
-                            m = M[i];
-                    if (lane < kScanBlocks)
-                        sh.scan.bm[(jm * kWaves + wave) * kScanBlocks + lane] = m;
+                        if (M[i])
+                            e1 = w0 + 64 * i + 64 - __clzll((long long)M[i]);  // highest end + 1
+#pragma unroll
+                    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+                        if (j == jm)
+                            best[j] = e1;
+                    if (kMulti && p.W > 1) {
+                        // this wave's W most recent ends of this length: each
+                        // lane writes its own end at its rank among the ends
+                        // at later positions (later blocks, then higher lanes)
+                        int32_t *dst = &sh.scan.cand[(jm * kWaves + wave) * kMaxCand];
+                        int later = 0;
+#pragma unroll
+                        for (int i = kScanBlocks - 1; i >= 0; --i) {
+                            const unsigned long long above =
+                                lane == 63 ? 0ull : (M[i] >> (lane + 1));
+                            const int rank = later + __popcll(above);
+                            if (((M[i] >> lane) & 1ull) && rank < p.W)
+                                dst[rank] = w0 + 64 * i + lane + 1;
+                            later += __popcll(M[i]);
+                        }
+                    }
                 }
             }
         }
@@ -434,31 +452,6 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
         if (j < p.n_ngram && lane == 0 && best[j] > 0)
             atomicMax(&sh.scan.red[j], best[j]);
-    if (kMulti && p.W > 1 && elim > 0) {
-        // the wave's W most recent ends per length: lane i < kScanBlocks takes block
-        // i's mask and the count of marked ends in later blocks, then lists
-        // its own ends from the highest down
-        for (int j = 0; j < p.n_ngram; ++j) {
-            unsigned long long m =
-                lane < kScanBlocks ? sh.scan.bm[(j * kWaves + wave) * kScanBlocks + lane] : 0ull;
-            const int c0 = __popcll(m);
-            int sfx = c0;  // marked ends in blocks lane.. kScanBlocks - 1
-#pragma unroll
-            for (int o = 1; o < kScanBlocks; o <<= 1) {
-                const int y = __shfl_down(sfx, o);
-                if (lane + o < kScanBlocks)
-                    sfx += y;
-            }
-            int r = sfx - c0;
-            int32_t *dst = &sh.scan.cand[(j * kWaves + wave) * kMaxCand];
-            while (m != 0ull && r < p.W) {
-                const int h = 63 - __clzll((long long)m);
-                dst[r] = w0 + 64 * lane + h + 1;
-                m &= ~(1ull << h);
-                ++r;
-            }
-        }
-    }
     __syncthreads();
 }
 
@@ -1417,6 +1410,13 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
     st.d = keep;
     lazy_init(st);
     int done_b = 0;  // units of sequence b streamed here
+    // sequences whose last arrival was this work-group's: their accept
+    // epilogues run after the stream (inline they held this work-group's
+    // remaining chunks back by the epilogue's round trips under full load)
+    unsigned long long pend[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        pend[q] = 0ull;
     for (int u = u0; u < u1; ++u) {
         // the next unit
         int nb = b, nr = r, nc = c + 1, ndn = dnb;
@@ -1455,8 +1455,12 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid < 64 && arrive_n(&p.ws.tk_all[b * kLineU32], (uint32_t)done_b,
-                                     (uint32_t)(dnb * cpr)))
-                final_epilogue<kCommit>(p, b, sh);
+                                     (uint32_t)(dnb * cpr))) {
+#pragma unroll
+                for (int q = 0; q < Q; ++q)
+                    if (q == (b >> 6))
+                        pend[q] |= 1ull << (b & 63);
+            }
             done_b = 0;
         }
         b = nb;
@@ -1466,6 +1470,12 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
 #pragma unroll
         for (int q = 0; q < kUnroll; ++q)
             A[q] = Bv[q];
+    }
+    if (tid < 64) {
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            for (unsigned long long m = pend[q]; m != 0ull; m &= m - 1ull)
+                final_epilogue<kCommit>(p, 64 * q + __ffsll((long long)m) - 1, sh);
     }
 }
 
