@@ -375,6 +375,13 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
         sh.scan.pat[tid] = tid >= L ? 0 : (L == p.Lmax ? pat_full : p.tokens[row + L - 1 - tid]);
     __syncthreads();
 
+    // bit n - 1 set for each configured length n; the lengths are strictly
+    // descending, so length n is number popcount(bits above n - 1) in the list
+    unsigned long long lenbits = 0ull;
+#pragma unroll
+    for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
+        if (j < p.n_ngram)
+            lenbits |= 1ull << (p.lens[j] - 1);
     int32_t best[SWITCHSD_MAX_NGRAM];
 #pragma unroll
     for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
@@ -413,12 +420,8 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
                 for (int i = 0; i < kScanBlocks; ++i)
                     M[i] &= __ballot(xu[du][i] == pu[du] && (i > 0 || w0 > 0 || lane >= u));
                 // record the length equal to u + 1, if it is one of the lengths
-                int jm = -1;
-#pragma unroll
-                for (int j = 0; j < SWITCHSD_MAX_NGRAM; ++j)
-                    if (j < p.n_ngram && p.lens[j] == u + 1)
-                        jm = j;
-                if (jm >= 0) {
+                if ((lenbits >> u) & 1ull) {
+                    const int jm = u == 63 ? 0 : __popcll(lenbits >> (u + 1));
                     int e1 = 0;
 #pragma unroll
                     for (int i = 0; i < kScanBlocks; ++i)
