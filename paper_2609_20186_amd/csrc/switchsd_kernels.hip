@@ -2,23 +2,26 @@
 //
 // One kernel body (k_switchsd) serves the greedy step and its stages.  Its
 // work-groups take one of three roles by block index, laid out as
-// [scan tiles | probe | argmax]:
+// [probe | scan tiles | argmax segments, segment-major]:
 //
 //   scan    a 1024-position tile of one context, staged in LDS with a
 //           64-token halo; ballots over blocks of 64 end positions mark the
 //           occurrences of each suffix n-gram; the most recent end per n-gram
 //           length is max-reduced over the work-group and (atomicMax) the
-//           tiles of the sequence, and with W candidates each wave also lists
-//           its W most recent ends per length, merged latest tile first.
+//           tiles of the sequence, and with W candidates each marked end is
+//           written at its recency rank (the W most recent per wave and
+//           length), merged latest wave and latest tile first.
 //           (Sec. 3.3: kappa-gram with a prior occurrence, ranked by recency.)
 //   probe   w . h for one sequence: exact bf16 x float products, summed in
 //           double-double with a fixed reduction order.  (Sec. 3.2, Eq. 3.)
 //   argmax  one segment of one logits row, streamed in 16 KB chunks with the
 //           next chunk's nontemporal 16-byte loads in flight while the current
-//           one is reduced.  Lane maxima use the NaN-propagating
-//           v_maximum3_f32 (1.5 VALU ops per element); each lane keeps the
-//           chunk that raised its maximum (in LDS) and looks up the lowest
-//           index holding it once, at the end, before one wave reduction.
+//           one is reduced.  Lane maxima of a chunk are packed 16-bit integer
+//           maxima of the bf16 bit patterns (0.5 VALU ops per element), with
+//           a float path for chunks holding a positive NaN or nothing >= +0;
+//           each lane keeps the chunk that raised its maximum (in LDS) and
+//           looks up the lowest index holding it once, at the end, before
+//           one wave reduction.
 //           The segment result is packed as (order key << 32 | ~index) and
 //           atomicMax-ed into the row's slot.  (Sec. 2 / App. A: greedy
 //           verification, T = 0.)
@@ -603,6 +606,7 @@ __device__ __forceinline__ void lazy_chunk(u32x4 (&v)[kUnroll], int qc0, int nq,
     // chunk's maximum whenever it lies in [+0, +inf].  Otherwise (a positive
     // NaN, or no element >= +0) the floats are compared, unless the lane
     // already holds a maximum >= +0 that an all-negative chunk cannot raise.
+    static_assert(kUnroll == 4, "the packed maximum below takes four vectors per lane");
     s16x2 t[4];
 #pragma unroll
     for (int w4 = 0; w4 < 4; ++w4)
