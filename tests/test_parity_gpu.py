@@ -87,6 +87,16 @@ def test_determinism_repeats():
 SPECIAL = np.array([0x7F80, 0xFF80, 0x7FC0, 0xFFC0, 0x8000, 0x0000, 0x0001], np.uint16)
 
 
+def _reaches_anchor(par, t):
+    """Node t's parent links lead back to node 0 (each parent precedes its child)."""
+    while t > 0:
+        q = int(par[t])
+        if q < 0 or q >= t:
+            return False
+        t = q
+    return True
+
+
 def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vocab=None,
                 ragged=True, specials=False, ties=False, repeat_tail=0, plant=False, n_cand=1,
                 neg=False):
@@ -151,6 +161,8 @@ def custom_case(seed, B, Lmax, V, R, k, lens, kappa, theta, d=64, tree=False, vo
                            oracle.make_cfg(lens, kappa, k, theta, n_cand))
         for b in range(B):
             t = int(rng.integers(0, sel["dn"][b]))
+            while not _reaches_anchor(sel["dpar"][b], t):  # e.g. the invalid parent link
+                t = int(rng.integers(0, sel["dn"][b]))
             W.plant(logits[b], sel["dtok"][b], sel["dpar"][b], int(sel["dn"][b]), t)
     return d_
 
