@@ -78,3 +78,29 @@ def test_random_config_parity(seed):
             got, ws = gpu_step(devt, dt, mode)
             assert_match(got, expt, what=f"random {seed} T={T} mode {mode}")
             assert workspace_left_clean(ws, dt)
+
+
+MAX_CASES = {
+    # the largest vocabulary the draw at T > 0 accepts, on the streamed path
+    # (R > 64), with 16 copy candidates
+    "max_vocab": dict(seed=90, B=2, Lmax=2000, V=524288, R=65, k=4, lens=(3, 2, 1), kappa=1,
+                      theta=-0.2, vocab=20, n_cand=16, plant=True),
+    # the most rows per sequence: 16 candidates of 63 tokens (1009 nodes) in
+    # 1024 rows, accept walks over hundreds of nodes
+    "max_rows": dict(seed=91, B=3, Lmax=3000, V=64, R=1024, k=63, lens=(3, 2, 1), kappa=1,
+                     theta=-0.2, vocab=3, n_cand=16, plant=True),
+}
+
+
+@pytest.mark.parametrize("case", sorted(MAX_CASES))
+def test_maximum_sizes(case):
+    say(f"[max] {case}")
+    d = custom_case(**MAX_CASES[case])
+    for T in (0.0, 0.7):
+        dt = with_temperature(d, T, seed=40_000) if T > 0 else d
+        exp = oracle_step(dt)
+        dev = to_device(dt)
+        for mode in (AUTO, FUSED, SPLIT):
+            got, ws = gpu_step(dev, dt, mode)
+            assert_match(got, exp, what=f"{case} T={T} mode {mode}")
+            assert workspace_left_clean(ws, dt)
