@@ -89,6 +89,12 @@ LOOP_CASES = {
                            theta=-0.3, vocab=6, plant=True), 0.6),
     "tiles_capacity": (dict(seed=84, B=3, Lmax=4200, V=256, R=9, k=8, lens=(3, 2, 1),
                             kappa=1, theta=-np.inf, vocab=5, ragged=False, plant=True), 0.0),
+    # long drafts at T > 0: the streamed weight sums close the step and commit
+    "w10_long_sampled": (dict(seed=85, B=3, Lmax=2500, V=1024, R=204, k=20, lens=(3, 2, 1),
+                              kappa=1, theta=-0.2, vocab=20, n_cand=10, plant=True), 0.6),
+    # more sequences than the streamed launches take: per-row sums with commit
+    "wide_batch_sampled": (dict(seed=86, B=260, Lmax=96, V=64, R=70, k=5, lens=(2, 1),
+                                kappa=1, theta=0.0, vocab=3, tree=True, plant=True), 0.6),
 }
 
 
