@@ -213,7 +213,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the speculation-control step shards by sequence with "
-              "no exchange, and this build runs on a single MI355X. Use --gpus 1.",
+              "no exchange between GPUs, so one GPU's throughput is the measure. Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
