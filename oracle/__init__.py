@@ -65,16 +65,22 @@ def _load():
         _lib.oracle_accept.argtypes = [P, P, i32, P, i32, P, P, P, P]
         _lib.oracle_tree_mask.argtypes = [P, i32, i32, i32, P]
         _lib.oracle_step.argtypes = [i32, i32, i32, i32, i32] + [P] * 4 + [ctypes.c_float] + \
-            [P] * 5 + [P] * 14 + [ctypes.c_float, P, i32]
+            [P] * 5 + [P] * 14 + [ctypes.c_float, P, P, P, i32]
         _lib.oracle_commit.argtypes = [P, P, i32, P, i32, i32, P, P]
         _lib.oracle_copy_labels.argtypes = [P, i32, i32, i32, P]
         _lib.oracle_sample_scale.argtypes = [ctypes.c_float]
         _lib.oracle_sample_scale.restype = ctypes.c_float
         _lib.oracle_sample_weight.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float]
-        _lib.oracle_sample_weight.restype = ctypes.c_uint32
-        _lib.oracle_sample_row.argtypes = [P, i32, ctypes.c_float, ctypes.c_uint32]
+        _lib.oracle_sample_weight.restype = ctypes.c_uint64
+        _lib.oracle_row_weights.argtypes = [P, i32, ctypes.c_float, P]
+        _lib.oracle_row_weights.restype = ctypes.c_uint64
+        _lib.oracle_sample_row.argtypes = [P, i32, ctypes.c_float, ctypes.c_uint64]
         _lib.oracle_sample_row.restype = i32
         _lib.oracle_step.restype = i32
+        _lib.oracle_spec_accept.argtypes = [P, P, i32, ctypes.c_float, i32, ctypes.c_uint64]
+        _lib.oracle_spec_accept.restype = i32
+        _lib.oracle_residual_row.argtypes = [P, P, i32, ctypes.c_float, ctypes.c_uint64]
+        _lib.oracle_residual_row.restype = i32
     return _lib
 
 
@@ -146,16 +152,46 @@ def sample_scale(temperature):
 
 
 def sample_weight(l, m, c):
-    """Fixed-point weight trunc(2^20 * 2^((l - m) c)) of one logit (see the C source)."""
+    """Integer weight floor(2^40 * 2^((l - m) c)) of one logit (see the C source)."""
     return int(_load().oracle_sample_weight(float(l), float(m), float(c)))
 
 
+def row_weights(row_bf16, temperature):
+    """The integer weights of a row (uint64 [V]) and their sum Z (App. A)."""
+    lib = _load()
+    r = _c(row_bf16, np.uint16)
+    w = np.zeros(max(r.size, 1), np.uint64)
+    Z = lib.oracle_row_weights(_p(r), int(r.size), float(sample_scale(temperature)), _p(w))
+    return w[:r.size], int(Z)
+
+
 def sample_row(row_bf16, temperature, u):
-    """Token drawn from softmax(l / T) by inverse CDF with the 32-bit uniform u."""
+    """Token drawn from softmax(l / T) by inverse CDF with the 64-bit uniform u."""
     lib = _load()
     r = _c(row_bf16, np.uint16)
     return int(lib.oracle_sample_row(_p(r), int(r.size), float(sample_scale(temperature)),
                                      int(u)))
+
+
+def spec_accept(p_row, q_row, temperature, x, u):
+    """Speculative-sampling test (Sec. 2; App. A): is the drafted token x
+    accepted at a row with target logits p_row and draft logits q_row, with
+    the 64-bit uniform u?  (u Q_x Zp < 2^64 P_x Zq.)"""
+    lib = _load()
+    pr, qr = _c(p_row, np.uint16), _c(q_row, np.uint16)
+    assert pr.size == qr.size
+    return bool(lib.oracle_spec_accept(_p(pr), _p(qr), int(pr.size),
+                                       float(sample_scale(temperature)), int(x), int(u)))
+
+
+def residual_row(p_row, q_row, temperature, u):
+    """Token drawn from the normalized residual max(0, p - q) with the 64-bit
+    uniform u (Sec. 2; App. A)."""
+    lib = _load()
+    pr, qr = _c(p_row, np.uint16), _c(q_row, np.uint16)
+    assert pr.size == qr.size
+    return int(lib.oracle_residual_row(_p(pr), _p(qr), int(pr.size),
+                                       float(sample_scale(temperature)), int(u)))
 
 
 def accept(dtok, dpar, dn, amax, R):
@@ -225,14 +261,17 @@ STEP_OUTPUTS = ("match_n", "match_end", "copy_len", "copy_tokens", "z", "use_cop
 
 
 def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=1,
-         temperature=0.0, uniforms=None):
+         temperature=0.0, uniforms=None, draft_logits=None, accept_uniforms=None):
     """The whole step for B sequences (steps 1-4 in the paper's order).
 
     tokens [B,Lmax] int32, lengths [B] int32, hidden [B,d] bf16 bits (uint16),
     w [d] float32, ntok/npar [B,R] int32 (npar None = chains), nn [B] int32,
     logits [B,R,V] bf16 bits (uint16).  temperature > 0 draws each row's
-    token with uniforms [B,R] uint32 (App. A); amax then holds the drawn
-    tokens.  Returns a dict of numpy outputs.
+    token with uniforms [B,R] uint64 (App. A); amax then holds the drawn
+    tokens.  draft_logits [B,R,V] bf16 bits (chains, T > 0) with
+    accept_uniforms [B,R] uint64: sequences verifying their neural draft use
+    speculative sampling with that draft distribution (see the C header).
+    Returns a dict of numpy outputs.
     """
     lib = _load()
     tokens = _c(tokens, np.int32)
@@ -260,13 +299,17 @@ def step(tokens, lengths, hidden, w, bias, ntok, npar, nn, logits, cfg, threads=
         "accept_len": np.zeros(B, np.int32), "accept_node": np.zeros(B, np.int32),
         "bonus": np.zeros(B, np.int32), "out_tokens": np.zeros((B, R), np.int32),
     }
-    un = _c(uniforms, np.uint32) if uniforms is not None else None
+    un = _c(uniforms, np.uint64) if uniforms is not None else None
     if temperature > 0:
         assert un is not None and un.size == B * R
+    ql = _c(draft_logits, np.uint16) if draft_logits is not None else None
+    ua = _c(accept_uniforms, np.uint64) if accept_uniforms is not None else None
+    if ql is not None:
+        assert ql.size == B * R * V and ua is not None and ua.size == B * R
     rc = lib.oracle_step(B, Lmax, d, R, V, _p(tokens), _p(lengths), _p(hidden), _p(w),
                          float(bias), _p(ntok), _p(npar_a), _p(nn), _p(logits),
                          ctypes.byref(cfg), *[_p(o[k]) for k in STEP_OUTPUTS],
-                         float(temperature), _p(un), int(threads))
+                         float(temperature), _p(un), _p(ql), _p(ua), int(threads))
     if rc != 0:
         raise ValueError("oracle_step rejected its arguments")
     o["copy_tokens"] = o["copy_tokens"][:, :, :K]

@@ -177,27 +177,24 @@ int32_t oracle_argmax_row(const uint16_t *row_bf16, int32_t V)
 }
 
 /* Step 4a at T > 0 -- App. A measures SwitchSD at sampling temperatures
- * T > 0 with standard speculative sampling.  The drafts here are tokens (copy
- * candidates are deterministic; neural drafts come without their
- * distribution), so the draft distribution is one-hot, and the
- * speculative-sampling rule (accept token x with probability p(x) / q(x),
- * else draw from the normalized residual max(0, p - q)) yields the same
- * distribution of the emitted token as drawing y from p and accepting x iff
- * x == y.  p = softmax(l / T) is realized with fixed-point weights (see the
- * header) so that the draw is exact integer arithmetic. */
+ * T > 0 with standard speculative sampling.  The target's distribution at a
+ * drafted position is p = softmax(l / T).  It is realized with integer
+ * weights w_j (see the header) so that every sum and every decision below is
+ * exact integer arithmetic and does not depend on an order of summation. */
 float oracle_sample_scale(float temperature)
 {
     return (float)(1.4426950408889634 / (double)temperature);
 }
 
-/* 2^t for t in [-24, 0] as 2^k * P(f), k = rint(t), f = t - k in
+/* 2^t for t in [-41, 0] as 2^k * P(f), k = rint(t), f = t - k in
  * [-1/2, 1/2] (exact), P(f) = sum_n (f ln 2)^n / n! up to n = 6, evaluated by
- * Horner's rule with one rounding per step (fused multiply-add); the weight is
- * that value times 2^20, truncated to an integer. */
-uint32_t oracle_sample_weight(float l, float m, float c)
+ * Horner's rule with one rounding per step (fused multiply-add).  The weight
+ * is floor(2^40 * 2^k * P(f)); below t = -41 that is 0, and so is the weight
+ * of NaN and -inf. */
+uint64_t oracle_sample_weight(float l, float m, float c)
 {
     const float t = (l - m) * c;
-    if (!(t >= -24.0f))
+    if (!(t >= -41.0f))
         return 0u;
     const float k = rintf(t);
     const float f = t - k;
@@ -208,10 +205,15 @@ uint32_t oracle_sample_weight(float l, float m, float c)
     p = fmaf(p, f, 0x1.ebfbe0p-3f);     /* ln2^2 / 2! */
     p = fmaf(p, f, 0x1.62e430p-1f);     /* ln2 */
     p = fmaf(p, f, 1.0f);
-    return (uint32_t)ldexpf(p, (int)k + 20);
+    const float e = ldexpf(p, (int)k);  /* exact: a power-of-two scaling of a normal float */
+    return (uint64_t)floor(ldexp((double)e, 40));
 }
 
-int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint32_t u)
+/* The weights of one row and their sum.  m is the largest non-NaN value.  A
+ * row without a finite maximum (every value NaN, -inf, or +inf present) has
+ * the one-hot weights 2^40 at its greedy choice (the lowest index of its
+ * largest value) and 0 elsewhere. */
+uint64_t oracle_row_weights(const uint16_t *row_bf16, int32_t V, float c, uint64_t *w)
 {
     float m = 0.0f;
     int have = 0;
@@ -223,23 +225,151 @@ int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint32_t
             m = f;
         have = 1;
     }
-    if (!have || !isfinite(m))
-        return oracle_argmax_row(row_bf16, V);
     uint64_t Z = 0;
+    if (!have || !isfinite(m)) {
+        const int32_t g = oracle_argmax_row(row_bf16, V);
+        for (int32_t v = 0; v < V; ++v)
+            w[v] = v == g ? ((uint64_t)1 << 40) : 0u;
+        return (uint64_t)1 << 40;
+    }
     for (int32_t v = 0; v < V; ++v) {
         const float f = bf16_to_float(row_bf16[v]);
-        Z += isnan(f) ? 0u : oracle_sample_weight(f, m, c);
+        w[v] = isnan(f) ? 0u : oracle_sample_weight(f, m, c);
+        Z += w[v];
     }
-    /* floor(u * Z / 2^32) in exact integer arithmetic */
-    const uint64_t target = (uint64_t)u * (Z >> 32) + (((uint64_t)u * (Z & 0xFFFFFFFFu)) >> 32);
+    return Z;
+}
+
+/* Inverse CDF: the smallest j with w_0 + ... + w_j > floor(u * Z / 2^64). */
+int32_t oracle_draw(const uint64_t *w, int32_t V, uint64_t Z, uint64_t u)
+{
+    const uint64_t target = (uint64_t)(((unsigned __int128)u * Z) >> 64);
     uint64_t prefix = 0;
     for (int32_t v = 0; v < V; ++v) {
-        const float f = bf16_to_float(row_bf16[v]);
-        prefix += isnan(f) ? 0u : oracle_sample_weight(f, m, c);
+        prefix += w[v];
         if (prefix > target)
             return v;
     }
     return V - 1; /* not reached: target < Z */
+}
+
+int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint64_t u)
+{
+    uint64_t *w = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)(V > 0 ? V : 1));
+    const uint64_t Z = oracle_row_weights(row_bf16, V, c, w);
+    const int32_t y = oracle_draw(w, V, Z, u);
+    free(w);
+    return y;
+}
+
+/* 192-bit product of a 128-bit and a 64-bit unsigned integer, as its upper
+ * 128 bits (hi) and lower 64 bits (lo). */
+static void mul_128_64(unsigned __int128 a, uint64_t b, unsigned __int128 *hi, uint64_t *lo)
+{
+    const unsigned __int128 plo = (unsigned __int128)(uint64_t)a * b;
+    const unsigned __int128 phi = (unsigned __int128)(uint64_t)(a >> 64) * b;
+    *lo = (uint64_t)plo;
+    *hi = phi + (plo >> 64);
+}
+
+/* Speculative sampling with the draft's own distribution q (Sec. 2,
+ * Speculative Decoding; App. A at T > 0): the drafted token x is accepted with
+ * probability min(1, p(x) / q(x)), p and q being the target's and the
+ * draft's distributions at the parent position, both softmax(. / T) realized
+ * with the integer weights above (P_j / Zp and Q_j / Zq).  With a 64-bit
+ * uniform u the test is u / 2^64 < p(x) / q(x), i.e. in integers
+ *   u * Q_x * Zp < 2^64 * P_x * Zq.
+ * A token outside [0, V) has P_x = Q_x = 0 and is rejected. */
+int32_t oracle_spec_accept(const uint16_t *p_row, const uint16_t *q_row, int32_t V, float c,
+                           int32_t x, uint64_t u)
+{
+    uint64_t *P = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)V);
+    uint64_t *Q = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)V);
+    const uint64_t Zp = oracle_row_weights(p_row, V, c, P);
+    const uint64_t Zq = oracle_row_weights(q_row, V, c, Q);
+    const uint64_t Px = (x >= 0 && x < V) ? P[x] : 0u;
+    const uint64_t Qx = (x >= 0 && x < V) ? Q[x] : 0u;
+    free(P);
+    free(Q);
+    unsigned __int128 lhi;
+    uint64_t llo;
+    mul_128_64((unsigned __int128)u * Qx, Zp, &lhi, &llo);   /* u Q_x Zp */
+    const unsigned __int128 rhi = (unsigned __int128)Px * Zq; /* 2^64 P_x Zq = (rhi, 0) */
+    return lhi < rhi;
+}
+
+/* After a rejection the emitted token is drawn from the normalized residual
+ * max(0, p - q) (Sec. 2; App. A), in integers
+ *   R_j = max(0, P_j * Zq - Q_j * Zp),
+ * by inverse CDF: the smallest j with R_0 + ... + R_j > floor(u * sum R / 2^64).
+ * The residual has positive mass whenever a rejection is possible (p(x) < q(x)
+ * for the drafted x); a row with none gives the draw from p instead. */
+int32_t oracle_residual_row(const uint16_t *p_row, const uint16_t *q_row, int32_t V, float c,
+                            uint64_t u)
+{
+    uint64_t *P = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)V);
+    uint64_t *Q = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)V);
+    const uint64_t Zp = oracle_row_weights(p_row, V, c, P);
+    const uint64_t Zq = oracle_row_weights(q_row, V, c, Q);
+    unsigned __int128 S = 0;
+    for (int32_t j = 0; j < V; ++j) {
+        const unsigned __int128 a = (unsigned __int128)P[j] * Zq;
+        const unsigned __int128 b = (unsigned __int128)Q[j] * Zp;
+        S += a > b ? a - b : 0;
+    }
+    int32_t y = V - 1;
+    if (S == 0) {
+        y = oracle_draw(P, V, Zp, u);
+    } else {
+        unsigned __int128 target;
+        uint64_t lo;
+        mul_128_64(S, u, &target, &lo);  /* floor(u S / 2^64) */
+        unsigned __int128 prefix = 0;
+        for (int32_t j = 0; j < V; ++j) {
+            const unsigned __int128 a = (unsigned __int128)P[j] * Zq;
+            const unsigned __int128 b = (unsigned __int128)Q[j] * Zp;
+            prefix += a > b ? a - b : 0;
+            if (prefix > target) {
+                y = j;
+                break;
+            }
+        }
+    }
+    free(P);
+    free(Q);
+    return y;
+}
+
+/* A chain drafted with distribution q (rows r of draft_logits: the draft
+ * model's logits at node r, from which node r + 1 was drawn).  Rows are
+ * tested in order; the first rejection at row r ends the step with the
+ * residual draw there (accept_len = r); with no rejection the bonus is drawn
+ * from p at the last drafted row.  amax[r] receives the token emitted at row
+ * r (the drafted token when accepted, then the residual draw or the bonus)
+ * and -1 at the rows after it. */
+static void spec_chain(const uint16_t *logits, const uint16_t *qlogits, int64_t V, int32_t R,
+                       const int32_t *dtok, int32_t dn, float c, const uint64_t *un,
+                       const uint64_t *ua, int32_t *am, int32_t *accept_len,
+                       int32_t *accept_node, int32_t *bonus, int32_t *out_tokens)
+{
+    int32_t a = dn - 1;
+    for (int32_t r = 0; r + 1 < dn; ++r) {
+        if (!oracle_spec_accept(logits + r * V, qlogits + r * V, (int32_t)V, c, dtok[r + 1],
+                                ua[r])) {
+            a = r;
+            break;
+        }
+    }
+    const int32_t y = a + 1 < dn ? oracle_residual_row(logits + a * V, qlogits + a * V,
+                                                       (int32_t)V, c, un[a])
+                                 : oracle_sample_row(logits + a * V, (int32_t)V, c, un[a]);
+    for (int32_t r = 0; r < R; ++r) {
+        am[r] = r < a ? dtok[r + 1] : (r == a ? y : -1);
+        out_tokens[r] = r < a ? dtok[r + 1] : (r == a ? y : -1);
+    }
+    *accept_len = a;
+    *accept_node = a;
+    *bonus = y;
 }
 
 /* Step 4b -- Sec. 3.3 (select the longest validated continuation): a node is
@@ -379,7 +509,9 @@ typedef struct {
     int32_t *use_copy, *dtok, *dpar, *dn, *amax;
     int32_t *accept_len, *accept_node, *bonus, *out_tokens;
     float temperature;
-    const uint32_t *uniforms;
+    const uint64_t *uniforms;
+    const uint16_t *qlogits;
+    const uint64_t *accept_uniforms;
 } step_job;
 
 static void step_range(const step_job *j)
@@ -402,6 +534,14 @@ static void step_range(const step_job *j)
                                        j->cfg, j->dtok + b * R, j->dpar + b * R, &j->dn[b]);
         int32_t *am = j->amax + b * R;
         const float c = j->temperature > 0.0f ? oracle_sample_scale(j->temperature) : 0.0f;
+        if (j->temperature > 0.0f && j->qlogits && !j->use_copy[b]) {
+            /* a neural chain with its distribution: speculative sampling */
+            spec_chain(j->logits + (int64_t)b * R * V, j->qlogits + (int64_t)b * R * V, V,
+                       j->R, j->dtok + b * R, j->dn[b], c, j->uniforms + b * R,
+                       j->accept_uniforms + b * R, am, &j->accept_len[b],
+                       &j->accept_node[b], &j->bonus[b], j->out_tokens + b * R);
+            continue;
+        }
         for (int32_t r = 0; r < j->R; ++r) {
             const uint16_t *row = j->logits + ((int64_t)b * R + r) * V;
             if (r >= j->dn[b])
@@ -432,7 +572,8 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 int32_t *copy_tokens, float *z, int32_t *use_copy,
                 int32_t *dtok, int32_t *dpar, int32_t *dn, int32_t *amax,
                 int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
-                int32_t *out_tokens, float temperature, const uint32_t *uniforms,
+                int32_t *out_tokens, float temperature, const uint64_t *uniforms,
+                const uint16_t *draft_logits, const uint64_t *accept_uniforms,
                 int32_t threads)
 {
     if (B < 0 || Lmax < 1 || d < 0 || R < 1 || V < 1 || !cfg || cfg->k < 0 ||
@@ -442,6 +583,8 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
         return -1;
     if (temperature > 0.0f && !uniforms)
         return -1;
+    if (draft_logits && (!(temperature > 0.0f) || !accept_uniforms || npar))
+        return -1;
     if (threads < 1)
         threads = 1;
     if (threads > B)
@@ -449,7 +592,7 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
     step_job base = {0, 0, Lmax, d, R, V, tokens, lengths, hidden, w, bias, ntok, npar, nn,
                      logits, cfg, match_n, match_end, copy_len, copy_tokens, z, use_copy,
                      dtok, dpar, dn, amax, accept_len, accept_node, bonus, out_tokens,
-                     temperature, uniforms};
+                     temperature, uniforms, draft_logits, accept_uniforms};
     if (threads == 1) {
         base.b0 = 0;
         base.b1 = B;

@@ -64,24 +64,43 @@ int32_t oracle_select(int32_t match_n, const int32_t *copy_len, const int32_t *c
 /* Step 4a: lowest index of the largest bf16 value of one row. */
 int32_t oracle_argmax_row(const uint16_t *row_bf16, int32_t V);
 
-/* Step 4a at T > 0 (App. A, sampling temperature; deterministic drafts, so
- * the draft distribution is one-hot and speculative sampling reduces to: draw
- * the target's token y from softmax(l / T) at the parent, accept the child iff
- * its token is y).  The draw is an inverse-CDF sample over fixed-point
- * weights, so that the decision is exact integer arithmetic:
+/* Step 4a at T > 0 (App. A, sampling temperature).  The target's
+ * distribution p = softmax(l / T) at a drafted position is realized with
+ * integer weights, so that every sum and decision is exact:
  *   c   = (float)(log2(e) / T)                     (oracle_sample_scale)
  *   m   = the largest non-NaN value of the row
- *   t_j = (l_j - m) * c  in float; w_j = 0 unless t_j >= -24, else
- *   w_j = trunc(2^(t_j) * 2^20) with 2^(t_j) evaluated as 2^k * P(t_j - k),
- *         k = rint(t_j), P the degree-6 Taylor polynomial of 2^f, Horner in
- *         float with fused multiply-adds                 (oracle_sample_weight)
- *   Z   = sum_j w_j (exact, 64-bit); target = floor(u * Z / 2^32)
- *   y   = the smallest j with w_0 + ... + w_j > target.
- * A row whose maximum is not finite (all NaN, -inf or +inf present) takes the
- * greedy choice. */
+ *   t_j = (l_j - m) * c  in float
+ *   w_j = floor(2^40 * 2^k * P(t_j - k)), k = rint(t_j), P the degree-6
+ *         Taylor polynomial of 2^f, Horner in float with fused multiply-adds;
+ *         0 for t_j < -41, NaN or -inf              (oracle_sample_weight)
+ *   Z   = sum_j w_j (exact, 64-bit)                  (oracle_row_weights)
+ *   y   = the smallest j with w_0 + ... + w_j > floor(u * Z / 2^64) for a
+ *         64-bit uniform u                           (oracle_draw)
+ * A row whose maximum is not finite (all NaN, -inf or +inf present) has
+ * one-hot weights 2^40 at its greedy choice.  One-hot drafts (copy drafts,
+ * trees, drafts without their distribution): the target's token y_r is drawn
+ * at every drafted row r, and node i is accepted iff its parent is accepted
+ * and its token equals y at the parent (speculative sampling with a one-hot
+ * draft distribution emits tokens with the same law). */
 float oracle_sample_scale(float temperature);
-uint32_t oracle_sample_weight(float l, float m, float c);
-int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint32_t u);
+uint64_t oracle_sample_weight(float l, float m, float c);
+uint64_t oracle_row_weights(const uint16_t *row_bf16, int32_t V, float c, uint64_t *w);
+int32_t oracle_draw(const uint64_t *w, int32_t V, uint64_t Z, uint64_t u);
+int32_t oracle_sample_row(const uint16_t *row_bf16, int32_t V, float c, uint64_t u);
+
+/* Speculative sampling with the draft's own distribution q (Sec. 2; App. A),
+ * for drafts that come with it (a neural chain; row r of the draft logits is
+ * the draft model's output at node r, from which node r + 1 was drawn, taken
+ * at the same temperature and with the same integer weights, Q_j / Zq):
+ *   accept x  iff  u * Q_x * Zp < 2^64 * P_x * Zq       (oracle_spec_accept)
+ * (probability min(1, p(x) / q(x)) for a uniform 64-bit u; x outside [0, V)
+ * is rejected), and after a rejection the emitted token is drawn from
+ *   R_j = max(0, P_j * Zq - Q_j * Zp)                   (oracle_residual_row)
+ * by inverse CDF with floor(u * sum R / 2^64) (exact 128/192-bit integers). */
+int32_t oracle_spec_accept(const uint16_t *p_row, const uint16_t *q_row, int32_t V, float c,
+                           int32_t x, uint64_t u);
+int32_t oracle_residual_row(const uint16_t *p_row, const uint16_t *q_row, int32_t V, float c,
+                            uint64_t u);
 
 /* Step 4b: accept walk over a chosen draft given the argmax of every
  * draft row.  Writes accept_len, accept_node, bonus and out_tokens[R]. */
@@ -124,7 +143,12 @@ void oracle_copy_labels(const int32_t *x, int32_t L, int32_t Lmax, int32_t n,
  * match_end and copy_len are [B,W], copy_tokens [B,W,k] (W = max(1, n_cand)).
  * temperature > 0 draws each row's token with oracle_sample_row and
  * uniforms[b,r] (amax then holds the drawn tokens); temperature <= 0 is the
- * greedy step and uniforms may be NULL.
+ * greedy step and uniforms may be NULL.  draft_logits [B,R,V] (T > 0 and
+ * chain drafts only, with accept_uniforms [B,R]): a sequence whose neural
+ * draft is chosen is verified by speculative sampling with that q (rows tested
+ * in order with accept_uniforms[b,r]; the residual or the bonus drawn with
+ * uniforms[b,r] at the row where the step ends; amax[r] = the emitted token at
+ * row r, -1 after it); a copy draft keeps the one-hot rule.
  * Returns 0, or -1 on a bad argument. */
 int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 const int32_t *tokens, const int32_t *lengths,
@@ -135,7 +159,8 @@ int oracle_step(int32_t B, int32_t Lmax, int32_t d, int32_t R, int32_t V,
                 int32_t *copy_tokens, float *z, int32_t *use_copy,
                 int32_t *dtok, int32_t *dpar, int32_t *dn, int32_t *amax,
                 int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
-                int32_t *out_tokens, float temperature, const uint32_t *uniforms,
+                int32_t *out_tokens, float temperature, const uint64_t *uniforms,
+                const uint16_t *draft_logits, const uint64_t *accept_uniforms,
                 int32_t threads);
 
 #ifdef __cplusplus

@@ -63,7 +63,7 @@ def to_device(d):
            "bias": float(d["bias"])}
     if d.get("T", 0.0) > 0:
         dev["uniforms"] = torch.from_numpy(
-            np.ascontiguousarray(d["uniforms"], dtype=np.uint32).view(np.int32)).cuda()
+            np.ascontiguousarray(d["uniforms"], dtype=np.uint64).view(np.int64)).cuda()
     return dev
 
 
@@ -72,7 +72,7 @@ def with_temperature(d, T, seed):
     d = dict(d)
     d["T"] = float(T)
     B, R = d["ntok"].shape
-    d["uniforms"] = np.random.default_rng(seed).integers(0, 2 ** 32, (B, R), dtype=np.uint32)
+    d["uniforms"] = np.random.default_rng(seed).integers(0, 2 ** 64, (B, R), dtype=np.uint64)
     return d
 
 
