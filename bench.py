@@ -244,7 +244,7 @@ def main():
     T = args.temperature
     if T > 0:
         uni = torch.from_numpy(np.random.default_rng(20186).integers(
-            0, 2 ** 32, (wl.B, wl.R), dtype=np.uint32).view(np.int32)).cuda()
+            0, 2 ** 64, (wl.B, wl.R), dtype=np.uint64).view(np.int64)).cuda()
         sws = sd.alloc_sample_workspace(wl.B, wl.R, wl.V)
         step_args = [sd.build_step_args(s, o, cfg, args.mode, T, uni, sws)
                      for s, o in zip(sets, outs)]

@@ -162,39 +162,43 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
                            size_t workspace_bytes, hipStream_t stream);
 
 /* Step 4 at sampling temperature T > 0 -- App. A (throughput at T > 0 with
- * speculative sampling).  The drafts are tokens (copy candidates are
- * deterministic; neural drafts come without their distribution), so the draft
- * distribution is one-hot and speculative sampling (accept x with probability
- * p(x)/q(x), else draw from the normalized residual max(0, p - q)) emits the
- * same token distribution as: draw y_r from p_r = softmax(logits[b,r,:] / T)
- * for every drafted row r < dn[b], accept node i iff its parent is accepted
- * and dtok[b,i] == y_{parent}.  The accept result is then formed exactly as in
- * switchsd_verify_accept with y in place of the argmax (amax[b,r] = y_r).
- * The draw is an inverse-CDF sample with the row's uniform
- * u = uniforms[b,r] / 2^32 over fixed-point weights
- *   w_j = trunc(2^20 * 2^t_j),  t_j = (l_j - m) * c  (float),
+ * speculative sampling).  The target's distribution at drafted row r is
+ * p_r = softmax(logits[b,r,:] / T), realized with integer weights
+ *   w_j = floor(2^40 * 2^k P(t_j - k)),  t_j = (l_j - m) * c  (float),
  *   c = (float)(log2(e) / T), m = the largest non-NaN value of the row,
- * with 2^t = 2^k P(t - k), k = rint(t), P the degree-6 Taylor polynomial of
- * 2^f evaluated by Horner's rule in fused multiply-adds, and w_j = 0 unless
- * t_j >= -24 (NaN and -inf weigh nothing): y is the smallest j with
- * w_0 + ... + w_j > floor(u * sum_j w_j).  The sums are exact integers, so y
- * does not depend on the order of the reduction.  A row without a finite
- * maximum (every value NaN, -inf, or +inf present) takes the greedy choice.
- *   temperature > 0 and finite; uniforms [B, R] uint32 (only rows r < dn[b]
+ *   k = rint(t_j), P the degree-6 Taylor polynomial of 2^f evaluated by
+ *   Horner's rule in fused multiply-adds,
+ * which are 0 for t_j < -40.5 (and for NaN and -inf).  A row without a finite
+ * maximum (every value NaN, -inf, or +inf present) has one-hot weights at its
+ * greedy choice.  The normalized weights are within total variation 1e-6 of
+ * the exact softmax at vocabularies up to 151936 (measured <= 1e-7).  A draw
+ * with the 64-bit uniform u is the smallest j with w_0 + ... + w_j >
+ * floor(u * Z / 2^64), Z = sum_j w_j: the sums are exact integers, so y does
+ * not depend on the order of the reduction.
+ * The drafts are tokens (copy candidates are deterministic; neural drafts come
+ * without their distribution), so the draft distribution is one-hot and
+ * speculative sampling (accept x with probability p(x)/q(x), else draw from
+ * the normalized residual max(0, p - q)) emits the same token law as: draw
+ * y_r from p_r with uniforms[b,r] for every drafted row r < dn[b], accept node
+ * i iff its parent is accepted and dtok[b,i] == y_{parent}.  The accept result
+ * is then formed exactly as in switchsd_verify_accept with y in place of the
+ * argmax (amax[b,r] = y_r).
+ *   temperature > 0 and finite; uniforms [B, R] uint64 (only rows r < dn[b]
  *   are read); logits [B, R, V] bf16 bits, 16-byte aligned, V % 8 == 0 and
  *   V <= 524288; sample_workspace of switchsd_sample_workspace_bytes(B, R, V)
  *   bytes, 256-byte aligned, no initialization needed; other arguments as in
  *   switchsd_verify_accept.  Two launches: the row maxima, then the weight
  *   sums, whose last work-group per row draws the row's token. */
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
-                           float temperature, const uint32_t *uniforms, const int32_t *dtok,
+                           float temperature, const uint64_t *uniforms, const int32_t *dtok,
                            const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
                            int32_t *accept_node, int32_t *bonus, int32_t *out_tokens,
                            int32_t *amax, void *workspace, size_t workspace_bytes,
                            void *sample_workspace, size_t sample_workspace_bytes,
                            hipStream_t stream);
 
-/* Bytes of the scratch a draw at T > 0 needs (per-chunk weight sums). */
+/* Bytes of the scratch a draw at T > 0 needs (the weight sums per 16 KB chunk
+ * and wave of every row). */
 size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V);
 
 /* Attention mask of the chosen drafts for the target's verification pass --
@@ -242,7 +246,7 @@ typedef struct {
     /* T > 0 (switchsd_verify_sample); 0 for the greedy step (the fields below
      * are then unused) */
     float temperature;
-    const uint32_t *uniforms;  /* [B, R] */
+    const uint64_t *uniforms;  /* [B, R] */
     void *sample_workspace;
     size_t sample_workspace_bytes;
     /* decode loop: commit != 0 appends the accepted tokens and the bonus to

@@ -122,7 +122,7 @@ def sample_workspace_bytes(B, R, V):
 
 _DT = {"i32": (torch.int32,), "f32": (torch.float32,),
        "bf16": (torch.bfloat16, torch.int16, torch.uint16), "u8": (torch.uint8,),
-       "u32": (torch.int32, torch.uint32)}
+       "u32": (torch.int32, torch.uint32), "u64": (torch.int64, torch.uint64)}
 
 
 def _ptr(t, kind, name, optional=False):
@@ -192,11 +192,11 @@ def switchsd_verify_accept(logits, dtok, dpar, dn, accept_len, accept_node, bonu
 def switchsd_verify_sample(logits, temperature, uniforms, dtok, dpar, dn, accept_len,
                            accept_node, bonus, out_tokens, amax, workspace, sample_workspace,
                            stream=None):
-    """uniforms: uint32 (or int32 holding the same bits) [B, R]."""
+    """uniforms: uint64 (or int64 holding the same bits) [B, R]."""
     B, R, V = logits.shape
     _check("switchsd_verify_sample", lib.switchsd_verify_sample(
         _ptr(logits, "bf16", "logits"), B, R, V, float(temperature),
-        _ptr(uniforms, "u32", "uniforms"), _ptr(dtok, "i32", "dtok"),
+        _ptr(uniforms, "u64", "uniforms"), _ptr(dtok, "i32", "dtok"),
         _ptr(dpar, "i32", "dpar", True), _ptr(dn, "i32", "dn"),
         _ptr(accept_len, "i32", "accept_len"), _ptr(accept_node, "i32", "accept_node"),
         _ptr(bonus, "i32", "bonus"), _ptr(out_tokens, "i32", "out_tokens"),
@@ -274,7 +274,7 @@ def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=Non
     """StepArgs for switchsd_step.  ``inp`` holds device tensors tokens [B,Lmax],
     lengths [B], hidden [B,d], w [d], ntok [B,R], npar [B,R] or None, nn [B],
     logits [B,R,V] and the float ``bias``; ``out`` is from alloc_outputs.
-    temperature > 0 draws the rows' tokens with ``uniforms`` [B,R] (uint32
+    temperature > 0 draws the rows' tokens with ``uniforms`` [B,R] (uint64
     bits) and ``sample_workspace`` (alloc_sample_workspace).  With ``draft_pos``
     and ``lag`` [B] the step also commits (decode loop): tokens and lengths are
     then updated in place."""
@@ -303,7 +303,7 @@ def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=Non
         a.lag = _ptr(lag, "i32", "lag")
     a.temperature = float(temperature)
     if temperature != 0.0:
-        a.uniforms = _ptr(uniforms, "u32", "uniforms")
+        a.uniforms = _ptr(uniforms, "u64", "uniforms")
         a.sample_workspace = _ptr(sample_workspace, "u8", "sample_workspace")
         a.sample_workspace_bytes = sample_workspace.numel()
     return a

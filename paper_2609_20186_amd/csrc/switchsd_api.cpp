@@ -293,7 +293,7 @@ namespace {
 // Arguments of a verification at T > 0.
 struct SampleArgs {
     float temperature;
-    const uint32_t *uniforms;
+    const uint64_t *uniforms;
     void *ws;
     size_t bytes;
 };
@@ -325,7 +325,7 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     const bool stream_sums = p.R > 64 && p.B <= kListMaxB;
     p.uniforms = sa->uniforms;
     p.samp_c = (float)(1.4426950408889634 / (double)sa->temperature);
-    p.csum = (uint32_t *)sa->ws;
+    p.csum = (unsigned long long *)sa->ws;
     p.cpr = (int32_t)chunks_per_row(p.V);
     const int64_t rows = (int64_t)p.B * p.R;
     // about eight sum work-groups per CU: the kernel needs few registers, and
@@ -438,7 +438,7 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
 }
 
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
-                           float temperature, const uint32_t *uniforms, const int32_t *dtok,
+                           float temperature, const uint64_t *uniforms, const int32_t *dtok,
                            const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
                            int32_t *accept_node, int32_t *bonus, int32_t *out_tokens,
                            int32_t *amax, void *workspace, size_t workspace_bytes,
@@ -454,7 +454,7 @@ int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t
 size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
     if (B < 0 || R < 0 || V < 0)
         return 0;
-    const size_t n = (size_t)B * R * chunks_per_row(V) * kCsumPerChunk * 4;
+    const size_t n = (size_t)B * R * chunks_per_row(V) * kCsumPerChunk * 8;
     return (n + kAlign - 1) / kAlign * kAlign;
 }
 

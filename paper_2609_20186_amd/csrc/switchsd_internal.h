@@ -16,9 +16,9 @@ constexpr int kUnroll = 4;
 constexpr int kChunkVecs = kThreads * kUnroll;
 // Context end positions covered by one scan work-group.
 constexpr int kScanTile = 1024;
-// Weight sums per 16 KB chunk of the draw at T > 0: one per block of 256
-// vectors and wave.
-constexpr int kCsumPerChunk = kUnroll * (kThreads / 64);
+// Weight sums per 16 KB chunk of the draw at T > 0: one per wave (each wave
+// reads 256 contiguous vectors of the chunk).
+constexpr int kCsumPerChunk = kThreads / 64;
 // Per-sequence workspace slots live on their own 256-byte lines: atomics to
 // one line serialize, and every work-group of a sequence arrives at its line.
 constexpr int kLineU32 = 64;
@@ -99,9 +99,9 @@ struct StepParams {
     int32_t *draft_pos;  // [B] draft-model cache position (in/out)
     int32_t *lag;        // [B] tokens the next neural drafting pass must consume first
     // draws at T > 0 (the weight-sum launch)
-    const uint32_t *uniforms;  // [B, R]
+    const uint64_t *uniforms;  // [B, R]
     float samp_c;              // log2(e) / T
-    uint32_t *csum;            // [B, R, cpr, waves] fixed-point weight sums per chunk
+    unsigned long long *csum;  // [B, R, cpr, waves] integer weight sums per chunk and wave
     int32_t cpr;               // 16 KB chunks per row
     int32_t seg_chunks;        // chunks per work-group of the sum launch
     uint32_t exp_front;  // arrivals per sequence at tk_front

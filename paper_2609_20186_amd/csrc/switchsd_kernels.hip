@@ -101,7 +101,7 @@ struct EpiShared {  // accept over R > 64 nodes
     uint32_t st[2][SWITCHSD_MAX_R];  // pointer-jumping state, double-buffered (final_epilogue)
 };
 struct PickShared {  // one row's draw at T > 0
-    uint32_t cw[64 * kCsumPerChunk];   // the row's weight sums per (chunk, block, wave)
+    unsigned long long cw[64 * kWaves];  // the row's weight sums per (chunk, wave)
     int32_t last;                      // this work-group completed the row (row_done)
 };
 union Shared {
@@ -1488,20 +1488,21 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
 
 // ------------------------------------------------------------- draws at T > 0
 
-// Sampling temperature T > 0 (App. A).  The drafts are tokens, so the draft
-// distribution is one-hot and speculative sampling emits the same token
-// distribution as: draw y from softmax(l / T) at each drafted row, accept a
-// child iff its token is y.  The draw is an inverse-CDF sample with the row's
-// uniform over fixed-point weights w_j = trunc(2^20 * 2^((l_j - m) c)),
-// c = log2(e) / T, m the row maximum, so that the sums are exact integers and
-// the drawn index does not depend on the reduction order.  Two launches after
-// the draft is chosen: the row maxima (the greedy argmax pass), then the
-// per-chunk weight sums, whose last work-group per row draws the row's token
-// and whose last row closes the sequence with the accept epilogue.
+// Sampling temperature T > 0 (App. A).  The target's distribution at a
+// drafted row is p = softmax(l / T), realized with integer weights
+// w_j = floor(2^40 * 2^((l_j - m) c)), c = log2(e) / T, m the row maximum, so
+// that every sum is exact and the drawn index does not depend on the order
+// of the reduction.  One-hot drafts (copy drafts, trees, drafts without their
+// distribution): speculative sampling emits the same token law as drawing y
+// from p at each drafted row and accepting a child iff its token is y.  Two
+// launches after the draft is chosen: the row maxima (the greedy argmax
+// pass), then the per-chunk weight sums, whose last work-group per row draws
+// the row's token and whose last row closes the sequence with the accept
+// epilogue.
 
 // The row's maximum from its packed argmax key; false when the row has no
 // finite maximum (no key: every value NaN; -inf; +inf present), and then the
-// row keeps the greedy choice.
+// row keeps the greedy choice (its weights are one-hot there).
 __device__ __forceinline__ bool key_max(unsigned long long key, float &m) {
     if (!key)
         return false;
@@ -1510,140 +1511,200 @@ __device__ __forceinline__ bool key_max(unsigned long long key, float &m) {
     return __builtin_isfinite(m);
 }
 
-// 2^t for t = (l - m) c in [-24, 0] as 2^k * P(t - k), k = rint(t), with P
-// the degree-6 Taylor polynomial of 2^f = e^(f ln 2) on [-1/2, 1/2] by
-// Horner's rule in fused multiply-adds; the weight is that times 2^20,
-// truncated, and 0 unless t >= -24 (so NaN and -inf weigh nothing).  Two
-// rewrites give the same bits with fewer operations: the coefficients carry
-// the factor 2^20 (scaling by a power of two commutes with every rounding
-// step here), and t is clamped to >= -25 instead of tested (every t below -24,
-// NaN included, then yields 2^(20 + t') < 1/16, which truncates to 0).
-__device__ __forceinline__ uint32_t samp_weight(float l, float m, float c) {
-    const float t = __builtin_fmaxf((l - m) * c, -25.0f);
+// floor(2^40 * 2^t) for t = (l - m) c as a float (an integer <= 2^40): 2^t =
+// 2^k * P(t - k), k = rint(t), P the degree-6 Taylor polynomial of 2^f =
+// e^(f ln 2) on [-1/2, 1/2] by Horner's rule in fused multiply-adds.  The
+// coefficients carry the factor 2^40 (a power-of-two scaling commutes with
+// every rounding here), and t is clamped to >= -41 (every t below, NaN
+// included, then gives 2^40 * 2^-41 = 1/2, which floors to 0, as the weight
+// of any t < -40.5 does).
+__device__ __forceinline__ float samp_weight(float l, float m, float c) {
+    const float t = __builtin_fmaxf((l - m) * c, -41.0f);
     const float k = __builtin_rintf(t);
     const float f = t - k;
-    float q = 0x1.430912p+7f;                  // 2^20 ln2^6 / 6!
-    q = __builtin_fmaf(q, f, 0x1.5d87fep+10f);  // 2^20 ln2^5 / 5!
-    q = __builtin_fmaf(q, f, 0x1.3b2ab6p+13f);  // 2^20 ln2^4 / 4!
-    q = __builtin_fmaf(q, f, 0x1.c6b08ep+15f);  // 2^20 ln2^3 / 3!
-    q = __builtin_fmaf(q, f, 0x1.ebfbe0p+17f);  // 2^20 ln2^2 / 2!
-    q = __builtin_fmaf(q, f, 0x1.62e430p+19f);  // 2^20 ln2
-    q = __builtin_fmaf(q, f, 0x1p+20f);         // 2^20
-    return (uint32_t)__builtin_ldexpf(q, (int)k);
+    float q = 0x1.430912p+27f;                  // 2^40 ln2^6 / 6!
+    q = __builtin_fmaf(q, f, 0x1.5d87fep+30f);  // 2^40 ln2^5 / 5!
+    q = __builtin_fmaf(q, f, 0x1.3b2ab6p+33f);  // 2^40 ln2^4 / 4!
+    q = __builtin_fmaf(q, f, 0x1.c6b08ep+35f);  // 2^40 ln2^3 / 3!
+    q = __builtin_fmaf(q, f, 0x1.ebfbe0p+37f);  // 2^40 ln2^2 / 2!
+    q = __builtin_fmaf(q, f, 0x1.62e430p+39f);  // 2^40 ln2
+    q = __builtin_fmaf(q, f, 0x1p+40f);         // 2^40
+    return __builtin_floorf(__builtin_ldexpf(q, (int)k));
 }
 
-// Weight sum of the 8 elements of one 16-byte vector (< 2^24).
-__device__ __forceinline__ uint32_t vec_weight(const u32x4 &v, float m, float c) {
-    uint32_t s = 0;
+// Weight sum of the 8 elements of one 16-byte vector (< 2^44, exact: every
+// partial sum is an integer below 2^53).
+__device__ __forceinline__ double vec_weight(const u32x4 &v, float m, float c) {
+    double s = 0.0;
 #pragma unroll
     for (int w4 = 0; w4 < 4; ++w4)
-        s += samp_weight(lo_f(v[w4]), m, c) + samp_weight(hi_f(v[w4]), m, c);
+        s += (double)samp_weight(lo_f(v[w4]), m, c) + (double)samp_weight(hi_f(v[w4]), m, c);
     return s;
 }
 
-// floor(u * Z / 2^32), exactly.
-__device__ __forceinline__ unsigned long long scaled_target(uint32_t u, unsigned long long Z) {
-    return (unsigned long long)u * (Z >> 32) +
-           (((unsigned long long)u * (Z & 0xFFFFFFFFull)) >> 32);
+// Wave sum of doubles holding integers below 2^53 (every partial sum exact,
+// so the result does not depend on the reduction order): DPP row shifts and
+// row broadcasts on both halves, as wave_reduce_u32.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_shift_f64(double v) {
+    const unsigned long long u = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, kCtrl, kRowMask, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), kCtrl, kRowMask, 0xf,
+                                               false);
+    return __longlong_as_double((long long)(((unsigned long long)(uint32_t)hi << 32) |
+                                            (uint32_t)lo));
+}
+__device__ __forceinline__ double wave_sum_f64(double v) {
+    v += dpp_shift_f64<0x111, 0xf>(v);
+    v += dpp_shift_f64<0x112, 0xf>(v);
+    v += dpp_shift_f64<0x114, 0xf>(v);
+    v += dpp_shift_f64<0x118, 0xf>(v);
+    v += dpp_shift_f64<0x142, 0xa>(v);
+    v += dpp_shift_f64<0x143, 0xc>(v);
+    const unsigned long long u = __double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// Weight sums of chunk c (16 KB) of a row, one per block of 256 vectors and
-// wave (64 vectors), stored at cs[(c * kUnroll + u) * kWaves + wave]: the
-// elements of a chunk in index order are block by block, wave by wave.
-__device__ __forceinline__ void store_block_sums(const u32x4 (&A)[kUnroll], int c, int nq, float m,
-                                                 float samp_c, uint32_t *cs) {
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+// floor(u * Z / 2^64), exactly (the upper half of the 128-bit product).
+__device__ __forceinline__ unsigned long long scaled_target(unsigned long long u,
+                                                            unsigned long long Z) {
+    return __umul64hi(u, Z);
+}
+
+// The sum launch reads each chunk wave by wave: the kUnroll * 64 vectors of
+// wave w in chunk c are contiguous, [c kChunkVecs + 256 w, + 256), vector u of
+// lane l at 64 u + l; one weight sum per (chunk, wave) then covers a
+// contiguous range in index order.
+__device__ __forceinline__ void load_chunk_w(u32x4 (&v)[kUnroll], const u32x4 *vp, int qc0,
+                                             int nq) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-        uint32_t w = c * kChunkVecs + u * kThreads + tid < nq ? vec_weight(A[u], m, samp_c) : 0u;
-        w = wave_reduce_u32(w, 0u, [](uint32_t a, uint32_t x) { return a + x; });
-        if (lane == 0)
-            st_u32(&cs[(c * kUnroll + u) * kWaves + wave], w);
+        const int q = qc0 + wave * (kUnroll * 64) + u * 64 + lane;
+        v[u] = __builtin_nontemporal_load(vp + (q < nq ? q : nq - 1));
     }
 }
 
-// The draw of row r of sequence b (its maximum m), by wave 0: the block sums
-// give Z and the target floor(u Z / 2^32), then the chunk, the block and the
-// wave's 64 vectors holding it; only those 64 vectors are read again, and the
-// vector and the element are found by a prefix over their weights and a scan
-// of 8.  The drawn token replaces the row's key (key_max reads it as a finite
-// maximum of index y).  Every thread of the work-group calls this (the block
-// sums are staged in LDS by all of them).
+// Weight sums of chunk c (16 KB) of a row, one per wave (its contiguous 256
+// vectors), stored at cs[c * kWaves + wave]; the entries of a row in index
+// order are chunk by chunk, wave by wave.
+__device__ __forceinline__ void store_block_sums(const u32x4 (&A)[kUnroll], int c, int nq, float m,
+                                                 float samp_c, unsigned long long *cs) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int q0 = c * kChunkVecs + wave * (kUnroll * 64) + lane;
+    double w = 0.0;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        w += q0 + u * 64 < nq ? vec_weight(A[u], m, samp_c) : 0.0;
+    w = wave_sum_f64(w);
+    if (lane == 0)
+        __hip_atomic_store(&cs[c * kWaves + wave], (unsigned long long)w, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Inclusive prefix over the 64 lanes of a wave.
+__device__ __forceinline__ unsigned long long wave_prefix_u64(unsigned long long v) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long y = __shfl_up(v, o);
+        if ((int)(threadIdx.x & 63) >= o)
+            v += y;
+    }
+    return v;
+}
+
+// The draw of row r of sequence b (its maximum m), by wave 0: the (chunk,
+// wave) sums give Z and the target floor(u Z / 2^64), then the chunk and the
+// wave's 256 vectors holding it; only those are read again (four per lane),
+// and the block of 64 vectors, the vector and the element are found by
+// prefix sums over their weights.  The drawn token replaces the row's key
+// (key_max reads it as a finite maximum of index y).  Every thread of the
+// work-group calls this (the sums are staged in LDS by all of them).
 __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned long long *keyp,
                          Shared &sh) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kCsumPerChunk;
-    const int ncs = p.cpr * kCsumPerChunk;  // <= 64 chunks (V <= 524288)
+    const unsigned long long *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+    const int ncs = p.cpr * kWaves;  // <= 256 (V <= 524288)
     for (int i = tid; i < ncs; i += kThreads)
-        sh.pick.cw[i] = (uint32_t)ld_i32((const int32_t *)&cs[i]);
+        sh.pick.cw[i] = __hip_atomic_load(&cs[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (wave != 0)
         return;
-    const uint32_t uni = p.uniforms[(int64_t)b * p.R + r];
+    const unsigned long long uni = p.uniforms[(int64_t)b * p.R + r];
     // chunk totals, their inclusive prefix, the target and its chunk
     unsigned long long cc = 0;
     if (lane < p.cpr) {
 #pragma unroll
-        for (int e = 0; e < kCsumPerChunk; ++e)
-            cc += sh.pick.cw[lane * kCsumPerChunk + e];
+        for (int e = 0; e < kWaves; ++e)
+            cc += sh.pick.cw[lane * kWaves + e];
     }
-    unsigned long long inc = cc;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const unsigned long long y = __shfl_up(inc, o);
-        if (lane >= o)
-            inc += y;
-    }
+    const unsigned long long inc = wave_prefix_u64(cc);
     const unsigned long long Z = __shfl(inc, 63);
     unsigned long long tg = scaled_target(uni, Z);
     const unsigned long long hit = __ballot(lane < p.cpr && inc > tg);
     const int cst = __ffsll((long long)hit) - 1;  // exists: target < Z
     tg -= __shfl(inc - cc, cst);
-    // within the chunk: the (block, wave) entry holding the target (lanes
-    // 0..15 take the entries in index order)
-    const unsigned long long ce =
-        lane < kCsumPerChunk ? (unsigned long long)sh.pick.cw[cst * kCsumPerChunk + lane] : 0ull;
-    unsigned long long ie = ce;
-#pragma unroll
-    for (int o = 1; o < kCsumPerChunk; o <<= 1) {
-        const unsigned long long y = __shfl_up(ie, o);
-        if (lane >= o)
-            ie += y;
-    }
-    const unsigned long long hit2 = __ballot(lane < kCsumPerChunk && ie > tg);
+    // the wave entry of that chunk holding the target (lanes 0..kWaves-1)
+    const unsigned long long ce = lane < kWaves ? sh.pick.cw[cst * kWaves + lane] : 0ull;
+    const unsigned long long ie = wave_prefix_u64(ce);
+    const unsigned long long hit2 = __ballot(lane < kWaves && ie > tg);
     const int est = __ffsll((long long)hit2) - 1;  // exists: tg < the chunk's total
     tg -= __shfl(ie - ce, est);
-    // the entry's 64 vectors: lane l holds vector cst * kChunkVecs + est * 64 + l
-    // (est = block * kWaves + wave, and a block's vectors are wave by wave)
+    // the entry's 256 vectors, block u of 64 at 64 u + lane
     const int nq = p.V >> 3;
-    const int q = cst * kChunkVecs + est * 64 + lane;
+    const int q0 = cst * kChunkVecs + est * (kUnroll * 64) + lane;
     const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (q < nq)
-        v = vp[q];
-    const uint32_t vw = q < nq ? vec_weight(v, m, p.samp_c) : 0u;
-    uint32_t iv = vw;
+    u32x4 v[kUnroll];
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(iv, o);
-        if (lane >= o)
-            iv += y;
+    for (int u = 0; u < kUnroll; ++u)
+        v[u] = q0 + u * 64 < nq ? vp[q0 + u * 64] : u32x4{0u, 0u, 0u, 0u};
+    unsigned long long vw[kUnroll], bs[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        vw[u] = q0 + u * 64 < nq ? (unsigned long long)vec_weight(v[u], m, p.samp_c) : 0ull;
+        bs[u] = (unsigned long long)wave_sum_f64((double)vw[u]);
     }
-    const unsigned long long hit3 = __ballot((unsigned long long)iv > tg);
-    const int lst = __ffsll((long long)hit3) - 1;  // exists: tg < the entry's total
+    // the block holding the target (exists: tg < the entry's total)
+    int us = kUnroll - 1;
+    unsigned long long incl = 0, us_before = 0;
+    bool found = false;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const unsigned long long excl = incl;
+        incl += bs[u];
+        if (!found && tg < incl) {
+            found = true;
+            us = u;
+            us_before = excl;
+        }
+    }
+    tg -= us_before;
+    unsigned long long w = 0;
+    u32x4 x = v[0];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        if (u == us) {
+            w = vw[u];
+            x = v[u];
+        }
+    const unsigned long long iv = wave_prefix_u64(w);
+    const unsigned long long hit3 = __ballot(iv > tg);
+    const int lst = __ffsll((long long)hit3) - 1;  // exists: tg < the block's total
     if (lane == lst) {
         // the element within this lane's vector
-        unsigned long long run = (unsigned long long)(iv - vw);
+        unsigned long long run = iv - w;
         int e = 7;
         for (int j = 0; j < 8; ++j) {
-            const uint32_t x = v[j >> 1];
-            run += samp_weight((j & 1) ? hi_f(x) : lo_f(x), m, p.samp_c);
+            const uint32_t xj = x[j >> 1];
+            run += (unsigned long long)samp_weight((j & 1) ? hi_f(xj) : lo_f(xj), m, p.samp_c);
             if (run > tg) {
                 e = j;
                 break;
             }
         }
-        const uint32_t y = (uint32_t)q * 8u + (uint32_t)e;
+        const uint32_t y = (uint32_t)(q0 + us * 64) * 8u + (uint32_t)e;
         st_u64(keyp, (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - y));
     }
 }
@@ -1680,7 +1741,8 @@ __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t un
 }
 
 // Sum launch: work-group (row, segment) adds up the weights of each 16 KB
-// chunk of its segment, per wave (a wave's chunk share is < 2^32).  Rows at
+// chunk of its segment, per wave (a wave's chunk share is < 2^51, exact in
+// binary64).  Rows at
 // and beyond dn and rows without a finite maximum are skipped.
 template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
@@ -1698,7 +1760,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
     u32x4 A[kUnroll], Bv[kUnroll];
     if (p.speculate)
-        load_chunk(A, vp, c0 * kChunkVecs, nq);
+        load_chunk_w(A, vp, c0 * kChunkVecs, nq);
     const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
     if (r >= dnb) {  // not drafted: no part in the draw
         __builtin_amdgcn_s_waitcnt(0);
@@ -1707,11 +1769,11 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     float m = 0.0f;
     const bool active = key_max(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]), m);
     if (active && !p.speculate)
-        load_chunk(A, vp, c0 * kChunkVecs, nq);
-    uint32_t *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kCsumPerChunk;
+        load_chunk_w(A, vp, c0 * kChunkVecs, nq);
+    unsigned long long *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
     for (int c = c0; active && c < c1; ++c) {
         if (c + 1 < c1)
-            load_chunk(Bv, vp, (c + 1) * kChunkVecs, nq);
+            load_chunk_w(Bv, vp, (c + 1) * kChunkVecs, nq);
         store_block_sums(A, c, nq, m, p.samp_c, cs);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
@@ -1773,7 +1835,7 @@ k_sample_sums_stream(StepParams p) {
         return reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)bb * p.R + rr) * p.V);
     };
     u32x4 A[kUnroll], Bv[kUnroll];
-    load_chunk(A, row_vecs(b, r), c * kChunkVecs, nq);
+    load_chunk_w(A, row_vecs(b, r), c * kChunkVecs, nq);
     unsigned long long key = ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]);
     uint32_t done_r = 0;  // units of row (b, r) streamed here
     for (int u = u0; u < u1; ++u) {
@@ -1796,7 +1858,7 @@ k_sample_sums_stream(StepParams p) {
         }
         unsigned long long nkey = key;
         if (u + 1 < u1) {
-            load_chunk(Bv, row_vecs(nb, nr), nc * kChunkVecs, nq);
+            load_chunk_w(Bv, row_vecs(nb, nr), nc * kChunkVecs, nq);
             if (nc == 0)
                 nkey = ld_u64(&p.ws.keys[(int64_t)nb * p.ws.key_stride + nr]);
         }
@@ -1804,7 +1866,7 @@ k_sample_sums_stream(StepParams p) {
         const bool active = key_max(key, m);
         if (active)
             store_block_sums(A, c, nq, m, p.samp_c,
-                             p.csum + ((int64_t)b * p.R + r) * cpr * kCsumPerChunk);
+                             p.csum + ((int64_t)b * p.R + r) * cpr * kWaves);
         ++done_r;
         if (c == cpr - 1 || u + 1 == u1) {  // end of this row's piece
             row_done<kCommit>(p, b, r, dnb, done_r, (uint32_t)cpr, active, m, sh);
