@@ -183,19 +183,38 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
  * i iff its parent is accepted and dtok[b,i] == y_{parent}.  The accept result
  * is then formed exactly as in switchsd_verify_accept with y in place of the
  * argmax (amax[b,r] = y_r).
+ * Drafts that come with their distribution q (draft_logits != NULL; chains
+ * only, dpar == NULL): row r of draft_logits holds the draft model's logits
+ * at node r, from which node r + 1 was drawn; q_r = softmax(draft_logits[b,r]
+ * / T) with the same integer weights (Q_j / Zq, p_r being P_j / Zp).  This is
+ * speculative sampling proper (Sec. 2): rows r = 0, 1, ... are tested in
+ * order, node r + 1 with token x being accepted iff
+ *   accept_uniforms[b,r] * Q_x * Zp < 2^64 * P_x * Zq
+ * (probability min(1, p(x)/q(x)); x outside [0, V) is rejected); at the first
+ * rejected row a the emitted token is drawn with uniforms[b,a] from the
+ * residual R_j = max(0, P_j * Zq - Q_j * Zp) (from p if the residual is empty),
+ * and with no rejection the bonus is drawn from p at row dn - 1.  Then
+ * accept_len = accept_node = a, out_tokens = the accepted tokens and the
+ * emitted one, amax[b,r] = the token emitted at row r (-1 after a).  The
+ * emitted tokens follow p exactly up to the weights' error and the uniforms'
+ * 2^-64 resolution.
  *   temperature > 0 and finite; uniforms [B, R] uint64 (only rows r < dn[b]
- *   are read); logits [B, R, V] bf16 bits, 16-byte aligned, V % 8 == 0 and
- *   V <= 524288; sample_workspace of switchsd_sample_workspace_bytes(B, R, V)
- *   bytes, 256-byte aligned, no initialization needed; other arguments as in
- *   switchsd_verify_accept.  Two launches: the row maxima, then the weight
- *   sums, whose last work-group per row draws the row's token. */
+ *   are read); accept_uniforms [B, R] uint64 (with draft_logits, else
+ *   ignored); logits and draft_logits [B, R, V] bf16 bits, 16-byte aligned,
+ *   V % 8 == 0 and V <= 524288; sample_workspace of
+ *   switchsd_sample_workspace_bytes(B, R, V) bytes, 256-byte aligned, no
+ *   initialization needed; other arguments as in switchsd_verify_accept.
+ *   Launches: the row maxima, then the weight sums, whose last work-group per
+ *   row draws the row's token; with q also the q row maxima (second) and the
+ *   residual draw (last). */
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
-                           float temperature, const uint64_t *uniforms, const int32_t *dtok,
-                           const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
-                           int32_t *accept_node, int32_t *bonus, int32_t *out_tokens,
-                           int32_t *amax, void *workspace, size_t workspace_bytes,
-                           void *sample_workspace, size_t sample_workspace_bytes,
-                           hipStream_t stream);
+                           float temperature, const uint64_t *uniforms,
+                           const uint16_t *draft_logits, const uint64_t *accept_uniforms,
+                           const int32_t *dtok, const int32_t *dpar, const int32_t *dn,
+                           int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                           int32_t *out_tokens, int32_t *amax, void *workspace,
+                           size_t workspace_bytes, void *sample_workspace,
+                           size_t sample_workspace_bytes, hipStream_t stream);
 
 /* Bytes of the scratch a draw at T > 0 needs (the weight sums per 16 KB chunk
  * and wave of every row). */
@@ -255,6 +274,12 @@ typedef struct {
     int32_t commit;
     int32_t *draft_pos;      /* [B] in/out */
     int32_t *lag;            /* [B] out    */
+    /* T > 0 with the neural draft's own distribution (switchsd_verify_sample's
+     * draft_logits; NULL = one-hot drafts): a sequence whose neural draft is
+     * chosen is verified by speculative sampling with it, a copy draft keeps
+     * the one-hot rule.  Needs npar == NULL (chains). */
+    const uint16_t *draft_logits;     /* [B, R, V] bf16 bits */
+    const uint64_t *accept_uniforms;  /* [B, R] */
 } switchsd_step_args;
 
 /* One whole step.  Results are identical to calling the four stage entry

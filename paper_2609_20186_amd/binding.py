@@ -71,7 +71,8 @@ class StepArgs(ctypes.Structure):
                 ("amax", _P), ("accept_len", _P), ("accept_node", _P), ("bonus", _P),
                 ("out_tokens", _P), ("temperature", ctypes.c_float), ("uniforms", _P),
                 ("sample_workspace", _P), ("sample_workspace_bytes", ctypes.c_size_t),
-                ("commit", _I), ("draft_pos", _P), ("lag", _P)]
+                ("commit", _I), ("draft_pos", _P), ("lag", _P),
+                ("draft_logits", _P), ("accept_uniforms", _P)]
 
 
 def _load():
@@ -88,7 +89,7 @@ def _load():
                                            S, _P]
     lib.switchsd_tree_mask.argtypes = [_P, _P, _I, _I, _P, _P]
     lib.switchsd_verify_sample.argtypes = [_P, _I, _I, _I, ctypes.c_float, _P, _P, _P, _P, _P,
-                                           _P, _P, _P, _P, _P, S, _P, S, _P]
+                                           _P, _P, _P, _P, _P, _P, _P, S, _P, S, _P]
     lib.switchsd_sample_workspace_bytes.argtypes = [_I, _I, _I]
     lib.switchsd_commit.argtypes = [_P, _P, _I, _I, _P, _I, _P, _P, _P, _P, _P]
     lib.switchsd_copy_labels.argtypes = [_P, _P, _I, _I, _I, _P, _P, S, _P]
@@ -191,12 +192,15 @@ def switchsd_verify_accept(logits, dtok, dpar, dn, accept_len, accept_node, bonu
 
 def switchsd_verify_sample(logits, temperature, uniforms, dtok, dpar, dn, accept_len,
                            accept_node, bonus, out_tokens, amax, workspace, sample_workspace,
-                           stream=None):
-    """uniforms: uint64 (or int64 holding the same bits) [B, R]."""
+                           stream=None, draft_logits=None, accept_uniforms=None):
+    """uniforms, accept_uniforms: uint64 (or int64 holding the same bits) [B, R];
+    draft_logits (bf16 [B, R, V]) verifies chains by speculative sampling with
+    the draft's distribution."""
     B, R, V = logits.shape
     _check("switchsd_verify_sample", lib.switchsd_verify_sample(
         _ptr(logits, "bf16", "logits"), B, R, V, float(temperature),
-        _ptr(uniforms, "u64", "uniforms"), _ptr(dtok, "i32", "dtok"),
+        _ptr(uniforms, "u64", "uniforms"), _ptr(draft_logits, "bf16", "draft_logits", True),
+        _ptr(accept_uniforms, "u64", "accept_uniforms", True), _ptr(dtok, "i32", "dtok"),
         _ptr(dpar, "i32", "dpar", True), _ptr(dn, "i32", "dn"),
         _ptr(accept_len, "i32", "accept_len"), _ptr(accept_node, "i32", "accept_node"),
         _ptr(bonus, "i32", "bonus"), _ptr(out_tokens, "i32", "out_tokens"),
@@ -270,12 +274,15 @@ def alloc_workspace(B, R, Lmax=0, n_cand=0, device="cuda"):
 
 
 def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=None,
-                    sample_workspace=None, draft_pos=None, lag=None):
+                    sample_workspace=None, draft_pos=None, lag=None, draft_logits=None,
+                    accept_uniforms=None):
     """StepArgs for switchsd_step.  ``inp`` holds device tensors tokens [B,Lmax],
     lengths [B], hidden [B,d], w [d], ntok [B,R], npar [B,R] or None, nn [B],
     logits [B,R,V] and the float ``bias``; ``out`` is from alloc_outputs.
     temperature > 0 draws the rows' tokens with ``uniforms`` [B,R] (uint64
-    bits) and ``sample_workspace`` (alloc_sample_workspace).  With ``draft_pos``
+    bits) and ``sample_workspace`` (alloc_sample_workspace); with
+    ``draft_logits`` [B,R,V] and ``accept_uniforms`` [B,R] a chosen neural draft
+    is verified by speculative sampling with its distribution.  With ``draft_pos``
     and ``lag`` [B] the step also commits (decode loop): tokens and lengths are
     then updated in place."""
     tokens, logits, hidden = inp["tokens"], inp["logits"], inp["hidden"]
@@ -306,6 +313,9 @@ def build_step_args(inp, out, cfg, mode=MODE_AUTO, temperature=0.0, uniforms=Non
         a.uniforms = _ptr(uniforms, "u64", "uniforms")
         a.sample_workspace = _ptr(sample_workspace, "u8", "sample_workspace")
         a.sample_workspace_bytes = sample_workspace.numel()
+        a.draft_logits = _ptr(draft_logits, "bf16", "draft_logits", True)
+        a.accept_uniforms = _ptr(accept_uniforms, "u64", "accept_uniforms",
+                                 draft_logits is None)
     return a
 
 

@@ -101,7 +101,8 @@ Workspace carve(void *ws, int32_t B, int32_t R, int32_t Lmax, int32_t W) {
     w.mslot = (int32_t *)(base + 2 * (size_t)B * line);
     w.keys = (unsigned long long *)(base + 3 * (size_t)B * line);
     w.key_stride = key_stride_for(R);
-    w.rtk = (uint32_t *)(base + 3 * (size_t)B * line + (size_t)B * w.key_stride * 8);
+    w.qkeys = w.keys + (size_t)B * w.key_stride;
+    w.rtk = (uint32_t *)(w.qkeys + (size_t)B * w.key_stride);
     w.rtk_stride = rtk_stride_for(R);
     w.cand = (int32_t *)((char *)w.rtk + (size_t)B * w.rtk_stride * 4);
     w.cand_stride = (int32_t)cand_stride_for(Lmax, W);
@@ -169,10 +170,11 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
     if (B < 0 || R < 0 || Lmax < 0 || n_cand < 0)
         return 0;
     // per sequence: three 256-byte lines (two tickets, the n-gram slots), the
-    // row keys, the row tickets of the draw at T > 0 and the candidate lists,
-    // each rounded up to whole lines
+    // row keys of the target's and of the draft's distribution, the row
+    // tickets of the draw at T > 0 and the candidate lists, each rounded up to
+    // whole lines
     const int64_t W = n_cand > SWITCHSD_MAX_CAND ? SWITCHSD_MAX_CAND : n_cand_of(n_cand);
-    return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8 +
+    return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8 * 2 +
                         (size_t)rtk_stride_for(R) * 4 +
                         (size_t)cand_stride_for(Lmax, (int32_t)W) * 4);
 }
@@ -296,14 +298,31 @@ struct SampleArgs {
     const uint64_t *uniforms;
     void *ws;
     size_t bytes;
+    const uint16_t *qlogits;          // the draft's logits (speculative sampling with q) or null
+    const uint64_t *accept_uniforms;  // [B, R] with qlogits
+    const int32_t *spec_copy;         // the step's use_copy (copy drafts stay one-hot) or null
 };
 
 int64_t chunks_per_row(int32_t V) { return ((int64_t)V / 8 + kChunkVecs - 1) / kChunkVecs; }
+
+size_t round_line(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+// The sample workspace: weight sums of the p rows and of the q rows per
+// (chunk, wave), the residual sums of one row per sequence (128-bit per
+// (chunk, wave)) and the test result of every row.
+size_t csum_bytes(int32_t B, int32_t R, int32_t V) {
+    return round_line((size_t)B * R * chunks_per_row(V) * kCsumPerChunk * 8);
+}
+size_t rcsum_bytes(int32_t B, int32_t V) {
+    return round_line((size_t)B * chunks_per_row(V) * kCsumPerChunk * 16);
+}
 
 int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_t R, int32_t V) {
     if (!(sa->temperature > 0.0f) || !isfinite(sa->temperature) || !sa->uniforms)
         return SWITCHSD_EINVAL;
     if (V % 8 != 0 || ((uintptr_t)logits & 15))
+        return SWITCHSD_EINVAL;
+    if (sa->qlogits && (!sa->accept_uniforms || ((uintptr_t)sa->qlogits & 15)))
         return SWITCHSD_EINVAL;
     if (chunks_per_row(V) * (kThreads / 64) > kThreads)
         return SWITCHSD_ESHAPE;
@@ -314,20 +333,54 @@ int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_
 }
 
 // After the row maxima are in the row keys: the weight-sum launch, which also
-// draws each row's token and runs the accept epilogue.  `p` carries the rows,
-// the draft, the outputs and the carved workspace.
+// draws each row's token and runs the accept epilogue.  With the draft's q:
+// first the q row maxima, then the sums of the p and the q rows (the last
+// work-group of a row with a drafted child takes its accept test), then the
+// residual launch, which draws the emitted token where the chain ends and
+// writes the outputs.  `p` carries the rows, the draft, the outputs and the
+// carved workspace.
 int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_t stream) {
     int cus = 0;
     int rc = cu_count(&cus);
     if (rc)
         return rc;
+    const bool q = sa->qlogits != nullptr;
     // long drafts: the sums stream the drafted rows' chunks over a fixed grid
-    const bool stream_sums = p.R > 64 && p.B <= kListMaxB;
+    const bool stream_sums = p.R > 64 && p.B <= kListMaxB && !q;
     p.uniforms = sa->uniforms;
     p.samp_c = (float)(1.4426950408889634 / (double)sa->temperature);
-    p.csum = (unsigned long long *)sa->ws;
     p.cpr = (int32_t)chunks_per_row(p.V);
+    char *sw = (char *)sa->ws;
+    p.csum = (unsigned long long *)sw;
+    p.qcsum = (unsigned long long *)(sw + csum_bytes(p.B, p.R, p.V));
+    p.rcsum = (unsigned long long *)(sw + 2 * csum_bytes(p.B, p.R, p.V));
+    p.rdec = (uint32_t *)(sw + 2 * csum_bytes(p.B, p.R, p.V) + rcsum_bytes(p.B, p.V));
+    p.qlogits = sa->qlogits;
+    p.accept_uniforms = sa->accept_uniforms;
+    p.spec_copy = sa->spec_copy;
     const int64_t rows = (int64_t)p.B * p.R;
+    if (q) {
+        // the q row maxima: the argmax role alone, over the rows with a
+        // drafted child of the sequences verified with q
+        StepParams pq = p;
+        pq.logits = sa->qlogits;
+        pq.ws.keys = p.ws.qkeys;
+        pq.n_front_wg = pq.n_scan_wg = 0;
+        pq.probe_on = pq.scan_probe = 0;
+        pq.epi_front = EPI_NONE;
+        pq.epi_accept = 0;
+        pq.list_mode = 0;
+        pq.speculate = 0;
+        pq.commit = 0;
+        pq.rows_mode = ROWS_Q;
+        if ((rc = set_segments(pq, rows, p.V)))
+            return rc;
+        const int64_t g = rows * pq.segs;
+        if (!grid_ok(g))
+            return SWITCHSD_ESHAPE;
+        if ((rc = launch_step_kernel(pq, g, stream)))
+            return rc;
+    }
     // about eight sum work-groups per CU: the kernel needs few registers, and
     // eight resident work-groups (their LDS fills the CU's 160 KB) hide the
     // load latency behind the weight arithmetic better than four
@@ -340,12 +393,25 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     p.segs = (int32_t)((p.cpr + p.seg_chunks - 1) / p.seg_chunks);
     p.speculate = speculate ? 1 : 0;
     p.list_mode = stream_sums ? 1 : 0;
-    const int64_t grid = stream_sums ? 4 * (int64_t)cus : rows * p.segs;
+    const int64_t grid = stream_sums ? 4 * (int64_t)cus : rows * p.segs * (q ? 2 : 1);
     if (!grid_ok(grid) || !grid_ok(rows))
         return SWITCHSD_ESHAPE;
-    // the last work-group of each drafted row also draws its token, and the
-    // last drafted row of a sequence runs the accept epilogue
-    return launch_sample_sums_kernel(p, grid, stream);
+    // the last work-group of each drafted row also draws its token (or takes
+    // its accept test), and the last drafted row of a sequence runs the accept
+    // epilogue (sequences verified with q: the residual launch does)
+    if ((rc = launch_sample_sums_kernel(p, grid, stream)) || !q)
+        return rc;
+    int64_t rsegs = (8 * (int64_t)cus + p.B - 1) / p.B;
+    if (rsegs > p.cpr)
+        rsegs = p.cpr;
+    if (rsegs < 1)
+        rsegs = 1;
+    p.rseg_chunks = (int32_t)((p.cpr + rsegs - 1) / rsegs);
+    p.rsegs = (int32_t)((p.cpr + p.rseg_chunks - 1) / p.rseg_chunks);
+    const int64_t rgrid = (int64_t)p.B * p.rsegs;
+    if (!grid_ok(rgrid))
+        return SWITCHSD_ESHAPE;
+    return launch_spec_residual_kernel(p, rgrid, stream);
 }
 
 // Verify launch shared by the entry points and the split step.  `speculate`:
@@ -438,13 +504,17 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
 }
 
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
-                           float temperature, const uint64_t *uniforms, const int32_t *dtok,
-                           const int32_t *dpar, const int32_t *dn, int32_t *accept_len,
-                           int32_t *accept_node, int32_t *bonus, int32_t *out_tokens,
-                           int32_t *amax, void *workspace, size_t workspace_bytes,
-                           void *sample_workspace, size_t sample_workspace_bytes,
-                           hipStream_t stream) {
-    const SampleArgs sa = {temperature, uniforms, sample_workspace, sample_workspace_bytes};
+                           float temperature, const uint64_t *uniforms,
+                           const uint16_t *draft_logits, const uint64_t *accept_uniforms,
+                           const int32_t *dtok, const int32_t *dpar, const int32_t *dn,
+                           int32_t *accept_len, int32_t *accept_node, int32_t *bonus,
+                           int32_t *out_tokens, int32_t *amax, void *workspace,
+                           size_t workspace_bytes, void *sample_workspace,
+                           size_t sample_workspace_bytes, hipStream_t stream) {
+    const SampleArgs sa = {temperature,  uniforms,        sample_workspace, sample_workspace_bytes,
+                           draft_logits, accept_uniforms, nullptr};
+    if (draft_logits && dpar)  // speculative sampling with q: chains only
+        return SWITCHSD_EINVAL;
     const bool speculate = dpar == nullptr || R <= 16;
     return verify_launch(logits, B, R, V, dtok, dpar, dn, accept_len, accept_node, bonus,
                          out_tokens, amax, workspace, workspace_bytes, speculate, &sa, nullptr,
@@ -454,8 +524,7 @@ int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t
 size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
     if (B < 0 || R < 0 || V < 0)
         return 0;
-    const size_t n = (size_t)B * R * chunks_per_row(V) * kCsumPerChunk * 8;
-    return (n + kAlign - 1) / kAlign * kAlign;
+    return 2 * csum_bytes(B, R, V) + rcsum_bytes(B, V) + round_line((size_t)B * R * 4);
 }
 
 int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace_bytes,
@@ -485,8 +554,13 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     if ((rc = check_workspace(workspace, workspace_bytes, B, R, a->Lmax, p.W)))
         return rc;
     const bool sampled = a->temperature != 0.0f;
-    const SampleArgs sa = {a->temperature, a->uniforms, a->sample_workspace,
-                           a->sample_workspace_bytes};
+    // speculative sampling with the neural draft's q (chains; copy drafts
+    // stay one-hot)
+    const SampleArgs sa = {a->temperature,   a->uniforms,        a->sample_workspace,
+                           a->sample_workspace_bytes, a->draft_logits, a->accept_uniforms,
+                           a->use_copy};
+    if (a->draft_logits && (!sampled || a->npar))
+        return SWITCHSD_EINVAL;
     if (sampled && (rc = check_sample(&sa, a->logits, B, R, V)))
         return rc;
     p.tokens = a->tokens;

@@ -27,7 +27,13 @@ constexpr int kLineU64 = 32;
 constexpr int kMaxCand = SWITCHSD_MAX_CAND;
 
 enum : int32_t { EPI_NONE = 0, EPI_MATCH = 1, EPI_SELECT = 2 };
-enum : int32_t { ROWS_ALL = 0, ROWS_NEURAL_OR_COPY = 1, ROWS_DRAFT = 2, ROWS_LISTED = 3 };
+enum : int32_t {
+    ROWS_ALL = 0,
+    ROWS_NEURAL_OR_COPY = 1,
+    ROWS_DRAFT = 2,
+    ROWS_LISTED = 3,
+    ROWS_Q = 4  // the draft's rows r < dn - 1 of sequences verified with q
+};
 // Sequences a work-list verify launch handles (its item prefix sums live in
 // four registers per lane).
 constexpr int kListMaxB = 256;
@@ -45,6 +51,8 @@ struct Workspace {
                                // tile's W most recent ends + 1 (0: none); W > 1 and
                                // more than one tile only
     int32_t cand_stride;       // int32 per sequence (whole 256-byte lines)
+    unsigned long long *qkeys; // [B] x key_stride: row maxima of the draft's distribution q
+                               // (between keys and rtk)
 };
 
 struct StepParams {
@@ -104,6 +112,17 @@ struct StepParams {
     unsigned long long *csum;  // [B, R, cpr, waves] integer weight sums per chunk and wave
     int32_t cpr;               // 16 KB chunks per row
     int32_t seg_chunks;        // chunks per work-group of the sum launch
+    // speculative sampling with the draft's own distribution q (chains, T > 0)
+    const uint16_t *qlogits;          // [B, R, V] the draft's logits, or null (one-hot drafts)
+    const uint64_t *accept_uniforms;  // [B, R] uniforms of the accept tests
+    const int32_t *spec_copy;         // [B] use_copy of the step (copy drafts stay one-hot)
+                                      // or null (every sequence uses q)
+    unsigned long long *qcsum;        // [B, R, cpr, waves] integer weight sums of the q rows
+    unsigned long long *rcsum;        // [B, cpr, waves, 2] residual sums of the rejected row
+    uint32_t *rdec;                   // [B, R] test of row r: 1 accepted, 2 rejected
+    int32_t rsegs;                    // residual work-groups per sequence
+    int32_t rseg_chunks;              // 16 KB chunks of the rejected row per residual
+                                      // work-group
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all
 };
@@ -114,6 +133,7 @@ int launch_commit_kernel(const StepParams &p, hipStream_t stream);
 int launch_label_kernels(const StepParams &p, int32_t n, uint8_t *labels, int32_t tsize,
                          void *table, hipStream_t stream);
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
+int launch_spec_residual_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                             uint32_t *mask, hipStream_t stream);
 

@@ -505,11 +505,19 @@ __device__ __forceinline__ uint32_t order_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Sequence b is verified by speculative sampling with its draft's own
+// distribution q (T > 0): q is given and the chosen draft is the neural one.
+__device__ __forceinline__ bool spec_seq(const StepParams &p, int b) {
+    return p.qlogits != nullptr && !(p.spec_copy && ld_i32(&p.spec_copy[b]) != 0);
+}
+
 __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
     if (p.rows_mode == ROWS_ALL || p.rows_mode == ROWS_LISTED)
         return (uint32_t)p.R;
     if (p.rows_mode == ROWS_DRAFT)
         return (uint32_t)clampi(ld_i32(&p.dn[b]), 1, p.R);
+    if (p.rows_mode == ROWS_Q)  // q at the rows that have a drafted child
+        return spec_seq(p, b) ? (uint32_t)(clampi(ld_i32(&p.dn[b]), 1, p.R) - 1) : 0u;
     const int nnb = clampi(p.nn[b], 1, p.R);
     const int cn = 1 + p.W * p.k;  // the longest copy draft
     return (uint32_t)(nnb > cn ? nnb : cn);
@@ -1709,14 +1717,122 @@ __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned lo
     }
 }
 
+// ------------------------------------------------------------- speculative sampling with q
+
+typedef unsigned __int128 u128;
+
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ u128 shfl_u128(u128 v, int src) {
+    const unsigned long long lo = __shfl((unsigned long long)v, src);
+    const unsigned long long hi = __shfl((unsigned long long)(v >> 64), src);
+    return ((u128)hi << 64) | lo;
+}
+__device__ __forceinline__ u128 wave_sum_u128(u128 v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const unsigned long long lo = __shfl_xor((unsigned long long)v, o);
+        const unsigned long long hi = __shfl_xor((unsigned long long)(v >> 64), o);
+        v += ((u128)hi << 64) | lo;
+    }
+    return v;
+}
+__device__ __forceinline__ u128 wave_prefix_u128(u128 v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long lo = __shfl_up((unsigned long long)v, o);
+        const unsigned long long hi = __shfl_up((unsigned long long)(v >> 64), o);
+        if (lane >= o)
+            v += ((u128)hi << 64) | lo;
+    }
+    return v;
+}
+// Upper 128 bits of the 192-bit product a * b.
+__device__ __forceinline__ u128 mulhi_128_64(u128 a, unsigned long long b) {
+    const u128 lo = (u128)(unsigned long long)a * b;
+    const u128 hi = (u128)(unsigned long long)(a >> 64) * b;
+    return hi + (lo >> 64);
+}
+
+// One row's two distributions: the target's p (row maxima in keys, weight
+// sums in csum) and the draft's q (qkeys, qcsum).  A row without a finite
+// maximum has one-hot weights 2^40 at its greedy choice g.
+struct SpecRow {
+    float mp, mq;
+    bool ap, aq;
+    int gp, gq;
+    unsigned long long Zp, Zq;
+};
+
+// Every lane of a wave ends with the row's SpecRow.
+__device__ void spec_row_setup(const StepParams &p, int b, int r, SpecRow &s) {
+    const int lane = threadIdx.x & 63;
+    const unsigned long long kp = ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]);
+    const unsigned long long kq = ld_u64(&p.ws.qkeys[(int64_t)b * p.ws.key_stride + r]);
+    s.mp = s.mq = 0.0f;
+    s.ap = key_max(kp, s.mp);
+    s.aq = key_max(kq, s.mq);
+    s.gp = decode_key(kp);
+    s.gq = decode_key(kq);
+    const int ncs = p.cpr * kWaves;
+    const int64_t off = ((int64_t)b * p.R + r) * ncs;
+    unsigned long long zp = 0, zq = 0;
+    for (int i = lane; i < ncs; i += 64) {
+        zp += __hip_atomic_load(&p.csum[off + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        zq += __hip_atomic_load(&p.qcsum[off + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    zp = wave_sum_u64(zp);
+    zq = wave_sum_u64(zq);
+    s.Zp = s.ap ? zp : 1ull << 40;
+    s.Zq = s.aq ? zq : 1ull << 40;
+}
+
+// Integer weight of element j (value bits h) of a row with maximum m, or of a
+// row without a finite maximum (one-hot 2^40 at g).
+__device__ __forceinline__ unsigned long long elem_weight(float l, bool act, float m, int j, int g,
+                                                          float c) {
+    return act ? (unsigned long long)samp_weight(l, m, c) : (j == g ? 1ull << 40 : 0ull);
+}
+
+// The speculative-sampling test at row r of sequence b (wave 0): the drafted
+// token x = dtok[b, r + 1] is accepted with probability min(1, p(x) / q(x)),
+// i.e. iff u Q_x Zp < 2^64 P_x Zq in exact integers (u the row's accept
+// uniform; a token outside [0, V) has P_x = Q_x = 0 and is rejected).
+__device__ void spec_test(const StepParams &p, int b, int r) {
+    SpecRow sr;
+    spec_row_setup(p, b, r, sr);
+    const int64_t row = (int64_t)b * p.R + r;
+    const int x = ld_i32(&p.dtok[row + 1]);
+    unsigned long long Px = 0, Qx = 0;
+    if (x >= 0 && x < p.V) {
+        Px = elem_weight(lo_f((uint32_t)p.logits[row * p.V + x]), sr.ap, sr.mp, x, sr.gp,
+                         p.samp_c);
+        Qx = elem_weight(lo_f((uint32_t)p.qlogits[row * p.V + x]), sr.aq, sr.mq, x, sr.gq,
+                         p.samp_c);
+    }
+    const unsigned long long u = p.accept_uniforms[row];
+    // u Q_x Zp = (hi, lo) with hi its upper 128 bits; 2^64 P_x Zq = (P_x Zq, 0)
+    const u128 lhs_hi = mulhi_128_64((u128)u * Qx, sr.Zp);
+    const bool acc = lhs_hi < (u128)Px * sr.Zq;
+    if ((threadIdx.x & 63) == 0)
+        st_u32(&p.rdec[row], acc ? 1u : 2u);
+}
+
 // The sum work-groups of a drafted row arrive with the units (16 KB chunks or
-// work-groups) they covered; the last one draws the row's token, then arrives
-// for the sequence, and the last of its dn[b] drafted rows runs the accept
-// epilogue (wave 0).  Every thread of the work-group calls this together; all
-// of them continue afterwards.
+// work-groups) they covered.  The last one either takes the row's accept test
+// (a row with a drafted child in a sequence verified with q) or draws the
+// row's token; then it arrives for the sequence, and the last of its dn[b]
+// drafted rows runs the accept epilogue (wave 0) -- for a sequence verified
+// with q, the residual launch closes it instead.  Every thread of the
+// work-group calls this together; all of them continue afterwards.
 template <bool kCommit>
 __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t units,
-                         uint32_t expected, bool active, float m, Shared &sh) {
+                         uint32_t expected, bool spec, Shared &sh) {
     const int tid = threadIdx.x;
     __builtin_amdgcn_s_waitcnt(0);  // this wave's chunk sums are out
     __syncthreads();
@@ -1733,44 +1849,67 @@ __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t un
         return;
     if (tid == 0)
         st_u32(rt, 0u);
-    if (active)
-        pick_row(p, b, r, m, &p.ws.keys[(int64_t)b * p.ws.key_stride + r], sh);
-    if (tid < 64 && arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)dnb))
-        final_epilogue<kCommit>(p, b, sh);
+    if (spec && r < dnb - 1) {
+        if (tid < 64)
+            spec_test(p, b, r);
+    } else {
+        // the row's key is not written before pick_row's barrier, so every
+        // thread reads the same value and takes the same branch
+        unsigned long long *keyp = &p.ws.keys[(int64_t)b * p.ws.key_stride + r];
+        float m = 0.0f;
+        if (key_max(ld_u64(keyp), m))
+            pick_row(p, b, r, m, keyp, sh);
+    }
+    if (tid < 64 && arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)dnb)) {
+        if (spec)
+            st_u32(&p.ws.tk_all[b * kLineU32], 0u);  // the residual launch closes it
+        else
+            final_epilogue<kCommit>(p, b, sh);
+    }
     __syncthreads();
 }
 
 // Sum launch: work-group (row, segment) adds up the weights of each 16 KB
 // chunk of its segment, per wave (a wave's chunk share is < 2^51, exact in
-// binary64).  Rows at
-// and beyond dn and rows without a finite maximum are skipped.
+// binary64).  Rows at and beyond dn and rows without a finite maximum are
+// skipped.  With the draft's q, a second set of work-groups (after the first
+// in the grid) does the same for the q rows that have a drafted child.
 template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     __shared__ Shared sh;
     // segment-major, as the argmax role of the step kernel
     const int nrows = p.B * p.R;
-    const int s = blockIdx.x / nrows;
-    const int rowi = blockIdx.x - s * nrows;
+    int idx = blockIdx.x;
+    const bool qrow = idx >= nrows * p.segs;
+    if (qrow)
+        idx -= nrows * p.segs;
+    const int s = idx / nrows;
+    const int rowi = idx - s * nrows;
     const int b = rowi / p.R, r = rowi - b * p.R;
     const int nq = p.V >> 3;
     // every work-group of the row covers at least one chunk (segs = chunks
     // per row / chunks per work-group, rounded up)
     const int c0 = s * p.seg_chunks;
     const int c1 = c0 + p.seg_chunks < p.cpr ? c0 + p.seg_chunks : p.cpr;
-    const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + ((int64_t)b * p.R + r) * p.V);
+    const u32x4 *vp = reinterpret_cast<const u32x4 *>((qrow ? p.qlogits : p.logits) +
+                                                      ((int64_t)b * p.R + r) * p.V);
     u32x4 A[kUnroll], Bv[kUnroll];
-    if (p.speculate)
+    const bool early = p.speculate && !qrow;
+    if (early)
         load_chunk_w(A, vp, c0 * kChunkVecs, nq);
     const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
-    if (r >= dnb) {  // not drafted: no part in the draw
+    const bool spec = spec_seq(p, b);
+    if (r >= (qrow ? dnb - 1 : dnb) || (qrow && !spec)) {  // no part in the draw
         __builtin_amdgcn_s_waitcnt(0);
         return;
     }
     float m = 0.0f;
-    const bool active = key_max(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]), m);
-    if (active && !p.speculate)
+    const bool active = key_max(
+        ld_u64(&(qrow ? p.ws.qkeys : p.ws.keys)[(int64_t)b * p.ws.key_stride + r]), m);
+    if (active && !early)
         load_chunk_w(A, vp, c0 * kChunkVecs, nq);
-    unsigned long long *cs = p.csum + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+    unsigned long long *cs =
+        (qrow ? p.qcsum : p.csum) + ((int64_t)b * p.R + r) * p.cpr * kWaves;
     for (int c = c0; active && c < c1; ++c) {
         if (c + 1 < c1)
             load_chunk_w(Bv, vp, (c + 1) * kChunkVecs, nq);
@@ -1779,7 +1918,9 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
         for (int u = 0; u < kUnroll; ++u)
             A[u] = Bv[u];
     }
-    row_done<kCommit>(p, b, r, dnb, 1u, (uint32_t)p.segs, active, m, sh);
+    // a tested row waits for its p and its q work-groups
+    const bool tested = spec && r < dnb - 1;
+    row_done<kCommit>(p, b, r, dnb, 1u, (uint32_t)(tested ? 2 * p.segs : p.segs), spec, sh);
 }
 
 // Sum launch for long drafts (p.list_mode): the chunks of the drafted rows,
@@ -1869,7 +2010,7 @@ k_sample_sums_stream(StepParams p) {
                              p.csum + ((int64_t)b * p.R + r) * cpr * kWaves);
         ++done_r;
         if (c == cpr - 1 || u + 1 == u1) {  // end of this row's piece
-            row_done<kCommit>(p, b, r, dnb, done_r, (uint32_t)cpr, active, m, sh);
+            row_done<kCommit>(p, b, r, dnb, done_r, (uint32_t)cpr, false, sh);
             done_r = 0;
         }
         b = nb;
@@ -1880,6 +2021,249 @@ k_sample_sums_stream(StepParams p) {
 #pragma unroll
         for (int q = 0; q < kUnroll; ++q)
             A[q] = Bv[q];
+    }
+}
+
+// Residual weight max(0, P_j Zq - Q_j Zp) of element j (use_p: the weight
+// P_j itself, for the draw from p when the residual has no mass).
+__device__ __forceinline__ u128 resid_weight(float lp, float lq, int j, const SpecRow &s, float c,
+                                             bool use_p) {
+    const unsigned long long P = elem_weight(lp, s.ap, s.mp, j, s.gp, c);
+    if (use_p)
+        return (u128)P;
+    const unsigned long long Q = elem_weight(lq, s.aq, s.mq, j, s.gq, c);
+    const u128 x = (u128)P * s.Zq, y = (u128)Q * s.Zp;
+    return x > y ? x - y : (u128)0;
+}
+// Residual weight of the 8 elements of vector q (elements 8q .. 8q+7).
+__device__ __forceinline__ u128 resid_vec(const u32x4 &vp, const u32x4 &vq, int q,
+                                          const SpecRow &s, float c, bool use_p) {
+    u128 acc = 0;
+#pragma unroll
+    for (int w4 = 0; w4 < 4; ++w4) {
+        acc += resid_weight(lo_f(vp[w4]), lo_f(vq[w4]), 8 * q + 2 * w4, s, c, use_p);
+        acc += resid_weight(hi_f(vp[w4]), hi_f(vq[w4]), 8 * q + 2 * w4 + 1, s, c, use_p);
+    }
+    return acc;
+}
+
+// The draw from the residual of row a (wave 0): the (chunk, wave) sums give
+// S and the target floor(u S / 2^64); the chunk, the wave's 256 vectors, the
+// block of 64, the vector and the element follow by prefix sums, reading only
+// those 256 vectors of p and q again.  With S = 0 (no residual mass) the draw
+// is from p itself, with its weight sums.  Returns the token in every lane.
+__device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)b * p.R + a;
+    const unsigned long long *rc = p.rcsum + (int64_t)b * p.cpr * kWaves * 2;
+    const unsigned long long *pc = p.csum + row * p.cpr * kWaves;
+    auto entry = [&](int i, bool use_p) -> u128 {
+        if (use_p)
+            return (u128)__hip_atomic_load(&pc[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned long long lo =
+            __hip_atomic_load(&rc[2 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned long long hi =
+            __hip_atomic_load(&rc[2 * i + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return ((u128)hi << 64) | lo;
+    };
+    auto chunk_total = [&](bool use_p) -> u128 {
+        u128 cc = 0;
+        if (lane < p.cpr)
+            for (int e = 0; e < kWaves; ++e)
+                cc += entry(lane * kWaves + e, use_p);
+        return cc;
+    };
+    u128 cc = chunk_total(false);
+    u128 inc = wave_prefix_u128(cc);
+    u128 S = shfl_u128(inc, 63);
+    const bool use_p = S == 0;
+    if (use_p) {
+        if (!sr.ap) {  // p is one-hot at its greedy choice
+            return sr.gp;
+        }
+        cc = chunk_total(true);
+        inc = wave_prefix_u128(cc);
+        S = shfl_u128(inc, 63);
+    }
+    const unsigned long long uni = p.uniforms[row];
+    u128 tg = mulhi_128_64(S, uni);
+    const unsigned long long hit = __ballot(lane < p.cpr && inc > tg);
+    const int cst = __ffsll((long long)hit) - 1;  // exists: target < S
+    tg -= shfl_u128(inc - cc, cst);
+    const u128 ce = lane < kWaves ? entry(cst * kWaves + lane, use_p) : (u128)0;
+    const u128 ie = wave_prefix_u128(ce);
+    const unsigned long long hit2 = __ballot(lane < kWaves && ie > tg);
+    const int est = __ffsll((long long)hit2) - 1;
+    tg -= shfl_u128(ie - ce, est);
+    const int nq = p.V >> 3;
+    const int q0 = cst * kChunkVecs + est * (kUnroll * 64) + lane;
+    const u32x4 *pv = reinterpret_cast<const u32x4 *>(p.logits + row * p.V);
+    const u32x4 *qv = reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V);
+    u32x4 vp[kUnroll], vq[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const bool in = q0 + u * 64 < nq;
+        vp[u] = in ? pv[q0 + u * 64] : u32x4{0u, 0u, 0u, 0u};
+        vq[u] = in ? qv[q0 + u * 64] : u32x4{0u, 0u, 0u, 0u};
+    }
+    u128 vw[kUnroll], bs[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        vw[u] = q0 + u * 64 < nq ? resid_vec(vp[u], vq[u], q0 + u * 64, sr, p.samp_c, use_p)
+                                 : (u128)0;
+        bs[u] = wave_sum_u128(vw[u]);
+    }
+    int us = kUnroll - 1;
+    u128 incl = 0, us_before = 0;
+    bool found = false;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const u128 excl = incl;
+        incl += bs[u];
+        if (!found && tg < incl) {
+            found = true;
+            us = u;
+            us_before = excl;
+        }
+    }
+    tg -= us_before;
+    u128 w = 0;
+    u32x4 xp = vp[0], xq = vq[0];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        if (u == us) {
+            w = vw[u];
+            xp = vp[u];
+            xq = vq[u];
+        }
+    const u128 iv = wave_prefix_u128(w);
+    const unsigned long long hit3 = __ballot(iv > tg);
+    const int lst = __ffsll((long long)hit3) - 1;
+    int y = 0;
+    if (lane == lst) {
+        const int q = q0 + us * 64;
+        u128 run = iv - w;
+        int e = 7;
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t hp = xp[j >> 1], hq = xq[j >> 1];
+            run += resid_weight((j & 1) ? hi_f(hp) : lo_f(hp), (j & 1) ? hi_f(hq) : lo_f(hq),
+                                8 * q + j, sr, p.samp_c, use_p);
+            if (run > tg) {
+                e = j;
+                break;
+            }
+        }
+        y = 8 * q + e;
+    }
+    return __shfl(y, lst);
+}
+
+// Outputs of a chain verified with q that ends at row a (wave 0): the
+// accepted tokens dtok[1..a], then the emitted token at row a, -1 after;
+// amax holds the same per row.  With the decode loop's commit the tokens are
+// appended to the context too.  Clears the sequence's row keys.
+template <bool kCommit>
+__device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus) {
+    const int lane = threadIdx.x & 63;
+    const int64_t base = (int64_t)b * p.R;
+    int cL = 0, cdp = 0;
+    if (kCommit) {
+        cL = clampi(p.clen[b], 0, p.Lmax);
+        cdp = p.draft_pos[b];
+    }
+    for (int i = lane; i < p.R; i += 64) {
+        const int v = i < a ? ld_i32(&p.dtok[base + i + 1]) : (i == a ? bonus : -1);
+        p.out_tokens[base + i] = v;
+        if (p.amax)
+            p.amax[base + i] = v;
+        if (kCommit && i <= a && cL + i < p.Lmax)
+            p.ctok[(int64_t)b * p.Lmax + cL + i] = v;
+        st_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + i], 0ull);
+        st_u64(&p.ws.qkeys[(int64_t)b * p.ws.key_stride + i], 0ull);
+    }
+    if (lane == 0) {
+        p.accept_len[b] = a;
+        p.accept_node[b] = a;
+        p.bonus[b] = bonus;
+        if (kCommit) {  // a neural step: the draft model drafted the accepted tokens
+            const int Lnew = cL + a + 1 < p.Lmax ? cL + a + 1 : p.Lmax;
+            const int pos = clampi(cL + a, 0, Lnew);
+            (void)cdp;
+            p.clen[b] = Lnew;
+            p.draft_pos[b] = pos;
+            p.lag[b] = Lnew - pos;
+        }
+    }
+}
+
+// Residual launch of sequences verified with q: work-group (segment s,
+// sequence b), segment-major.  Every work-group finds the first rejected row
+// a from the tests; if there is one, it adds up the residual weights of its
+// chunks of row a per wave (128-bit).  The last of the sequence's rsegs
+// work-groups draws the emitted token (the residual draw at a, or the bonus
+// drawn from p at the last row when every test passed) and writes the
+// outputs.
+template <bool kCommit>
+__global__ __launch_bounds__(kThreads) void k_spec_residual(StepParams p) {
+    const int s = blockIdx.x / p.B, b = blockIdx.x - s * p.B;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    if (!spec_seq(p, b))
+        return;
+    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    int a = dnb - 1;
+    for (int r0 = 0; r0 < dnb - 1; r0 += 64) {
+        const int r = r0 + lane;
+        const bool rej = r < dnb - 1 &&
+                         __hip_atomic_load(&p.rdec[(int64_t)b * p.R + r], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT) != 1u;
+        const unsigned long long m = __ballot(rej);
+        if (m) {
+            a = r0 + __ffsll((long long)m) - 1;
+            break;
+        }
+    }
+    const bool resid = a < dnb - 1;
+    SpecRow sr;
+    if (resid) {
+        spec_row_setup(p, b, a, sr);
+        const int nq = p.V >> 3;
+        const int64_t row = (int64_t)b * p.R + a;
+        const u32x4 *pv = reinterpret_cast<const u32x4 *>(p.logits + row * p.V);
+        const u32x4 *qv = reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V);
+        const int c0 = s * p.rseg_chunks;
+        const int c1 = c0 + p.rseg_chunks < p.cpr ? c0 + p.rseg_chunks : p.cpr;
+        unsigned long long *rc = p.rcsum + (int64_t)b * p.cpr * kWaves * 2;
+        for (int c = c0; c < c1; ++c) {
+            u32x4 A[kUnroll], Q4[kUnroll];
+            load_chunk_w(A, pv, c * kChunkVecs, nq);
+            load_chunk_w(Q4, qv, c * kChunkVecs, nq);
+            const int q0 = c * kChunkVecs + wave * (kUnroll * 64) + lane;
+            u128 acc = 0;
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                if (q0 + u * 64 < nq)
+                    acc += resid_vec(A[u], Q4[u], q0 + u * 64, sr, p.samp_c, false);
+            acc = wave_sum_u128(acc);
+            if (lane == 0) {
+                const int i = c * kWaves + wave;
+                __hip_atomic_store(&rc[2 * i], (unsigned long long)acc, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&rc[2 * i + 1], (unsigned long long)(acc >> 64),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid >= 64)
+        return;
+    if (arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)p.rsegs)) {
+        if (lane == 0)
+            st_u32(&p.ws.tk_all[b * kLineU32], 0u);
+        const int bonus = resid ? resid_draw(p, b, a, sr)
+                                : decode_key(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride +
+                                                               dnb - 1]));
+        spec_epilogue<kCommit>(p, b, a, bonus);
     }
 }
 
@@ -2223,6 +2607,15 @@ int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t str
         hipLaunchKernelGGL((k_sample_sums<true>), g, dim3(kThreads), 0, stream, p);
     else
         hipLaunchKernelGGL((k_sample_sums<false>), g, dim3(kThreads), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_spec_residual_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
+    const dim3 g((unsigned)grid);
+    if (p.commit)
+        hipLaunchKernelGGL((k_spec_residual<true>), g, dim3(kThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL((k_spec_residual<false>), g, dim3(kThreads), 0, stream, p);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 

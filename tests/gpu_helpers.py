@@ -44,9 +44,13 @@ def oracle_step(d, rows=None):
     npar = None if d["npar"] is None else d["npar"][sl]
     T = d.get("T", 0.0)
     un = d["uniforms"][sl] if T > 0 else None
+    ql = d.get("draft_logits")
+    ua = d.get("accept_uniforms")
     return oracle.step(d["tokens"][sl], d["lengths"][sl], d["hidden"][sl], d["w"], d["bias"],
                        d["ntok"][sl], npar, d["nn"][sl], d["logits"][sl], cfg,
-                       threads=ORACLE_THREADS, temperature=T, uniforms=un)
+                       threads=ORACLE_THREADS, temperature=T, uniforms=un,
+                       draft_logits=None if ql is None else ql[sl],
+                       accept_uniforms=None if ua is None else ua[sl])
 
 
 def to_device(d):
@@ -64,6 +68,11 @@ def to_device(d):
     if d.get("T", 0.0) > 0:
         dev["uniforms"] = torch.from_numpy(
             np.ascontiguousarray(d["uniforms"], dtype=np.uint64).view(np.int64)).cuda()
+    if d.get("draft_logits") is not None:
+        dev["draft_logits"] = torch.from_numpy(
+            np.ascontiguousarray(d["draft_logits"]).view(np.int16)).cuda()
+        dev["accept_uniforms"] = torch.from_numpy(
+            np.ascontiguousarray(d["accept_uniforms"], dtype=np.uint64).view(np.int64)).cuda()
     return dev
 
 
@@ -91,7 +100,9 @@ def gpu_step(dev, d, mode=0, out=None, ws=None):
     ws = ws if ws is not None else sd.alloc_workspace(B, R, dev["tokens"].shape[1], W)
     T = d.get("T", 0.0)
     sws = sd.alloc_sample_workspace(B, R, dev["logits"].shape[2]) if T > 0 else None
-    args = sd.build_step_args(dev, out, sd_cfg(d), mode, T, dev.get("uniforms"), sws)
+    args = sd.build_step_args(dev, out, sd_cfg(d), mode, T, dev.get("uniforms"), sws,
+                              draft_logits=dev.get("draft_logits"),
+                              accept_uniforms=dev.get("accept_uniforms"))
     sd.switchsd_step(args, ws)
     torch.cuda.synchronize()
     res = {k2: v.cpu().numpy() for k2, v in out.items()}
@@ -115,10 +126,17 @@ def gpu_stages(dev, d):
                              o["dn"])
     T = d.get("T", 0.0)
     if T > 0:
-        sd.switchsd_verify_sample(dev["logits"], T, dev["uniforms"], o["dtok"], o["dpar"],
+        # the stage entry point verifies every sequence with q when given (the
+        # step keeps copy drafts one-hot); with q the drafts are chains and
+        # dpar is not passed
+        q = dev.get("draft_logits")
+        sd.switchsd_verify_sample(dev["logits"], T, dev["uniforms"], o["dtok"],
+                                  None if q is not None else o["dpar"],
                                   o["dn"], o["accept_len"], o["accept_node"], o["bonus"],
                                   o["out_tokens"], o["amax"], ws,
-                                  sd.alloc_sample_workspace(B, R, dev["logits"].shape[2]))
+                                  sd.alloc_sample_workspace(B, R, dev["logits"].shape[2]),
+                                  draft_logits=dev.get("draft_logits"),
+                                  accept_uniforms=dev.get("accept_uniforms"))
     else:
         sd.switchsd_verify_accept(dev["logits"], o["dtok"], o["dpar"], o["dn"],
                                   o["accept_len"], o["accept_node"], o["bonus"],

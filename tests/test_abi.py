@@ -62,7 +62,7 @@ def step_args(**kw):
     for f, _ in sd.StepArgs._fields_:
         if f not in ("B", "Lmax", "d", "R", "V", "bias", "cfg", "mode", "temperature",
                      "uniforms", "sample_workspace", "sample_workspace_bytes", "commit",
-                     "draft_pos", "lag"):
+                     "draft_pos", "lag", "draft_logits", "accept_uniforms"):
             setattr(a, f, P)
     a.B, a.Lmax, a.d, a.R, a.V = 2, 16, 8, 8, 100
     a.cfg = sd.make_cfg((3, 2, 1), 1, 7, 0.0)
@@ -164,14 +164,17 @@ def test_sample_entry_point_rejects():
     A16 = (P + 15) & ~15
     SW = WS
     need = sd.sample_workspace_bytes(2, 8, 128)
-    assert need >= 2 * 8 * 1 * 4 * 4 and need % 256 == 0
-    # a 32-bit weight sum per 16 KB chunk, block of 256 vectors (4) and wave (4)
-    assert sd.sample_workspace_bytes(2, 8, 128256) == 2 * 8 * 16 * 4 * 4 * 4
+    assert need % 256 == 0
+    # 64-bit weight sums per 16 KB chunk and wave (4) for the p rows and for the
+    # q rows, 128-bit residual sums for one row per sequence, a test word per row
+    assert sd.sample_workspace_bytes(2, 8, 128256) == 2 * (2 * 8 * 16 * 4 * 8) + \
+        2 * 16 * 4 * 16 + 256
     assert sd.sample_workspace_bytes(-1, 8, 8) == 0
 
-    def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS, wsn=4096):
-        return lib.switchsd_verify_sample(logits, 2, 8, V, T, uni, P, P, P, P, P, P, P, P, ws,
-                                          wsn, sw, swn, None)
+    def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS, wsn=4096, q=None,
+             ua=None, dpar=P):
+        return lib.switchsd_verify_sample(logits, 2, 8, V, T, uni, q, ua, P, dpar, P, P, P, P,
+                                          P, P, ws, wsn, sw, swn, None)
     for T in (0.0, -0.5, float("nan"), float("inf")):
         assert call(T=T) == EINVAL
     assert call(uni=None) == EINVAL
@@ -182,10 +185,19 @@ def test_sample_entry_point_rejects():
     assert call(sw=SW + 4) == EWORKSPACE
     assert call(swn=need - 1) == EWORKSPACE
     assert call(wsn=8) == EWORKSPACE
+    # the draft's distribution: chains only, with its accept uniforms, aligned
+    assert call(q=A16, ua=P, dpar=P) == EINVAL
+    assert call(q=A16, ua=None, dpar=None) == EINVAL
+    assert call(q=A16 + 2, ua=P, dpar=None) == EINVAL
     assert lib.switchsd_verify_sample(P, 0, 8, 128, 0.5, None, None, None, None, None, None,
-                                      None, None, None, None, 0, None, 0, None) == OK
+                                      None, None, None, None, None, None, 0, None, 0,
+                                      None) == OK
     a = step_args(temperature=0.7)                     # sampled step without uniforms
     a.uniforms = None
+    assert call_step(a, nbytes=1 << 15) == EINVAL
+    a = step_args(temperature=0.0, draft_logits=P, accept_uniforms=P)   # q needs T > 0
+    assert call_step(a, nbytes=1 << 15) == EINVAL
+    a = step_args(temperature=0.7, draft_logits=P, accept_uniforms=P)   # q needs chains
     assert call_step(a, nbytes=1 << 15) == EINVAL
 
 
