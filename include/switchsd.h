@@ -70,7 +70,9 @@ typedef enum {
     SWITCHSD_EINVAL = -1,    /* null pointer, bad configuration value        */
     SWITCHSD_ESHAPE = -2,    /* sizes out of range or inconsistent           */
     SWITCHSD_EHIP = -3,      /* a HIP runtime call or kernel launch failed   */
-    SWITCHSD_EWORKSPACE = -4 /* workspace null, misaligned or too small      */
+    SWITCHSD_EWORKSPACE = -4, /* workspace null, misaligned or too small     */
+    SWITCHSD_EDEVICE = -5     /* reported by switchsd_workspace_status: a
+                                 bounded device-side wait gave up           */
 } switchsd_status;
 
 #define SWITCHSD_MAX_NGRAM 8       /* most n-gram lengths in one configuration  */
@@ -329,6 +331,25 @@ size_t switchsd_label_workspace_bytes(int32_t B, int32_t Lmax);
  * take: R for the match stage, Lmax for verification).  0 for a negative
  * argument. */
 size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_cand);
+
+/* Device-side status of the calls that used `workspace` (B sequences),
+ * written to *status (a DEVICE int32) asynchronously on `stream`:
+ * SWITCHSD_OK, or SWITCHSD_EDEVICE when a bounded wait inside a kernel gave
+ * up since the last status call.  The one such wait: in switchsd_step with
+ * contexts longer than 1024 tokens, the last scan work-group of a sequence
+ * waits for the probe's work-group (dispatched before it, so in practice the
+ * wait always ends); if it gives up, that sequence's switch takes the neural
+ * draft and its outputs are not valid.  The call reads and clears the error
+ * words; after SWITCHSD_EDEVICE, zero the workspace again before its next use.
+ *   workspace of at least switchsd_workspace_bytes(B, 0, 0, 0) bytes, the
+ *   same B as the calls; status [1] int32 on the device. */
+int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B,
+                              int32_t *status, hipStream_t stream);
+
+/* Test support only: while `on` is nonzero, switchsd_step's probe work-groups
+ * withhold their flag and the wait above gives up after a few iterations, so
+ * that a test can force the give-up path (every kernel still exits). */
+void switchsd_test_withhold_probe_flag(int32_t on);
 
 /* Static, thread-safe text of a status code. */
 const char *switchsd_status_string(int status);

@@ -19,14 +19,14 @@ MAX_NGRAM = 8
 MAX_CAND = 16
 MODE_AUTO, MODE_FUSED, MODE_SPLIT = 0, 1, 2
 
-STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE"}
+STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE", -5: "EDEVICE"}
 
 EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
            "switchsd_verify_accept", "switchsd_verify_sample", "switchsd_tree_mask",
            "switchsd_commit", "switchsd_step", "switchsd_copy_labels",
            "switchsd_workspace_bytes", "switchsd_sample_workspace_bytes",
-           "switchsd_label_workspace_bytes",
-           "switchsd_status_string")
+           "switchsd_label_workspace_bytes", "switchsd_workspace_status",
+           "switchsd_test_withhold_probe_flag", "switchsd_status_string")
 
 
 class SwitchsdError(RuntimeError):
@@ -99,10 +99,14 @@ def _load():
     lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
     lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
     lib.switchsd_workspace_bytes.restype = S
+    lib.switchsd_workspace_status.argtypes = [_P, S, _I, _P, _P]
+    lib.switchsd_test_withhold_probe_flag.argtypes = [_I]
+    lib.switchsd_test_withhold_probe_flag.restype = None
     lib.switchsd_status_string.argtypes = [ctypes.c_int]
     lib.switchsd_status_string.restype = ctypes.c_char_p
     for name in EXPORTS:
-        getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
+        if name != "switchsd_test_withhold_probe_flag":
+            getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
     return lib
 
 
@@ -231,6 +235,19 @@ def switchsd_copy_labels(tokens, lengths, n, labels, workspace, stream=None):
         _ptr(tokens, "i32", "tokens"), _ptr(lengths, "i32", "lengths"), B, Lmax, int(n),
         _ptr(labels, "u8", "labels"), _ptr(workspace, "u8", "workspace"), workspace.numel(),
         _stream(stream)))
+
+
+def switchsd_workspace_status(workspace, B, status, stream=None):
+    """Writes OK (0) or EDEVICE (-5) to the device int32 ``status`` [1] and
+    clears the workspace's error words of B sequences."""
+    _check("switchsd_workspace_status", lib.switchsd_workspace_status(
+        _ptr(workspace, "u8", "workspace"), workspace.numel(), int(B),
+        _ptr(status, "i32", "status"), _stream(stream)))
+
+
+def withhold_probe_flag_for_tests(on):
+    """Test support: force the step's bounded wait for the probe flag to give up."""
+    lib.switchsd_test_withhold_probe_flag(1 if on else 0)
 
 
 def switchsd_tree_mask(dpar, dn, mask, stream=None):

@@ -7,6 +7,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "switchsd.h"
 #include "switchsd_internal.h"
 
@@ -15,6 +17,11 @@ using namespace switchsd;
 namespace {
 
 constexpr size_t kAlign = 256;
+
+// Test knob (switchsd_test_withhold_probe_flag): the step's probe work-groups
+// never set their flag and the front gives up its wait after a few
+// iterations, so that the give-up path runs with every kernel exiting.
+std::atomic<int> g_withhold_probe_flag{0};
 
 
 bool shape_ok_B(int32_t B) { return B >= 0 && B <= (1 << 24); }
@@ -191,6 +198,9 @@ const char *switchsd_status_string(int status) {
         return "HIP runtime call or kernel launch failed";
     case SWITCHSD_EWORKSPACE:
         return "workspace null, not 256-byte aligned or too small";
+    case SWITCHSD_EDEVICE:
+        return "a bounded device-side wait gave up (results of that call are not valid; "
+               "zero the workspace again)";
     default:
         return "unknown status";
     }
@@ -553,6 +563,8 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     fill_cfg(p, &a->cfg);
     if ((rc = check_workspace(workspace, workspace_bytes, B, R, a->Lmax, p.W)))
         return rc;
+    p.withhold_flag = g_withhold_probe_flag.load() ? 1 : 0;
+    p.spin_cap = p.withhold_flag ? 256 : (1 << 22);
     const bool sampled = a->temperature != 0.0f;
     // speculative sampling with the neural draft's q (chains; copy drafts
     // stay one-hot)
@@ -699,6 +711,20 @@ int switchsd_commit(int32_t *tokens, int32_t *lengths, int32_t B, int32_t Lmax,
     p.lag = lag;
     return launch_commit_kernel(p, stream);
 }
+
+int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B,
+                              int32_t *status, hipStream_t stream) {
+    if (!shape_ok_B(B))
+        return SWITCHSD_ESHAPE;
+    if (!status)
+        return SWITCHSD_EINVAL;
+    if (!workspace || ((uintptr_t)workspace & (kAlign - 1)) ||
+        workspace_bytes < switchsd_workspace_bytes(B, 0, 0, 0))
+        return SWITCHSD_EWORKSPACE;
+    return launch_status_kernel(carve(workspace, B, 0, 0, 0).mslot, B, status, stream);
+}
+
+void switchsd_test_withhold_probe_flag(int32_t on) { g_withhold_probe_flag.store(on ? 1 : 0); }
 
 int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                        uint32_t *mask, hipStream_t stream) {

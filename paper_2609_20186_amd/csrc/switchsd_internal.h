@@ -123,6 +123,10 @@ struct StepParams {
     int32_t rsegs;                    // residual work-groups per sequence
     int32_t rseg_chunks;              // 16 KB chunks of the rejected row per residual
                                       // work-group
+    // bounded waits: spin limit of the front's wait for the probe flag; with
+    // withhold_flag (a test knob) the probe never sets its flag
+    int32_t spin_cap;
+    int32_t withhold_flag;
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all
 };
@@ -134,6 +138,7 @@ int launch_label_kernels(const StepParams &p, int32_t n, uint8_t *labels, int32_
                          void *table, hipStream_t stream);
 int launch_sample_sums_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_spec_residual_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
+int launch_status_kernel(int32_t *mslot, int32_t B, int32_t *out, hipStream_t stream);
 int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                             uint32_t *mask, hipStream_t stream);
 

@@ -469,6 +469,13 @@ __device__ __forceinline__ uint32_t *probe_flag(const StepParams &p, int b) {
     return (uint32_t *)&p.ws.mslot[b * kLineU32 + kLineU32 - 1];
 }
 
+// Device-side error word of sequence b, next to the probe flag: nonzero when
+// a bounded wait of this call gave up (read and cleared by
+// switchsd_workspace_status).
+__device__ __forceinline__ uint32_t *error_word(const StepParams &p, int b) {
+    return (uint32_t *)&p.ws.mslot[b * kLineU32 + kLineU32 - 2];
+}
+
 // Stand-alone probe work-group (the probe entry point, or the step's probe
 // when a sequence has several scan tiles).
 __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
@@ -482,7 +489,7 @@ __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
     __syncthreads();
     if (tid == 0) {
         st_f32(&p.z[b], probe_combine(sh.probe.s, sh.probe.c, p.bias));
-        if (p.epi_front == EPI_SELECT) {  // the step: z is ready for the front
+        if (p.epi_front == EPI_SELECT && !p.withhold_flag) {  // the step: z is ready
             __builtin_amdgcn_s_waitcnt(0);
             st_u32(probe_flag(p, b), 1u);
         }
@@ -1013,14 +1020,25 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
     if (p.epi_front == EPI_SELECT) {
         if (p.probe_on) {
             // the probe's work-group was dispatched before every tile and
-            // depends on nothing, so the flag is set in bounded time (the cap
-            // only guards against a broken launch)
+            // depends on nothing, so the flag is set in bounded time; the cap
+            // only guards against a broken launch.  If it is reached, the
+            // sequence's error word is set and the switch takes the neural
+            // draft (a NaN score never clears the threshold).
             uint32_t *fl = probe_flag(p, b);
-            for (int spin = 0; spin < (1 << 22) && __hip_atomic_load(fl, __ATOMIC_RELAXED,
-                                                                    __HIP_MEMORY_SCOPE_AGENT) == 0u;
-                 ++spin)
-                __builtin_amdgcn_s_sleep(2);
-            zb = ld_f32(&p.z[b]);
+            bool seen = false;
+            for (int spin = 0; spin < p.spin_cap && !seen; ++spin) {
+                seen = __builtin_amdgcn_readfirstlane((int)__hip_atomic_load(
+                           fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) != 0;
+                if (!seen)
+                    __builtin_amdgcn_s_sleep(2);
+            }
+            if (seen) {
+                zb = ld_f32(&p.z[b]);
+            } else {
+                zb = __builtin_nanf("");
+                if (lane == 0)
+                    st_u32(error_word(p, b), 1u);
+            }
             if (lane == 0)
                 st_u32(fl, 0u);
         } else {
@@ -2507,6 +2525,21 @@ __global__ __launch_bounds__(64) void k_commit(StepParams p) {
     }
 }
 
+// Reads and clears the error words of B sequences (one work-group, any B).
+__global__ __launch_bounds__(kThreads) void k_status(int32_t *mslot, int32_t B, int32_t *out) {
+    int err = 0;
+    for (int b = threadIdx.x; b < B; b += kThreads) {
+        uint32_t *w = (uint32_t *)&mslot[(int64_t)b * kLineU32 + kLineU32 - 2];
+        if (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) {
+            err = 1;
+            st_u32(w, 0u);
+        }
+    }
+    err = __syncthreads_or(err);
+    if (threadIdx.x == 0)
+        out[0] = err ? SWITCHSD_EDEVICE : SWITCHSD_OK;
+}
+
 __global__ __launch_bounds__(64) void k_select(StepParams p) {
     __shared__ ChainShared ch;
     const int b = blockIdx.x;
@@ -2616,6 +2649,11 @@ int launch_spec_residual_kernel(const StepParams &p, int64_t grid, hipStream_t s
         hipLaunchKernelGGL((k_spec_residual<true>), g, dim3(kThreads), 0, stream, p);
     else
         hipLaunchKernelGGL((k_spec_residual<false>), g, dim3(kThreads), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
+}
+
+int launch_status_kernel(int32_t *mslot, int32_t B, int32_t *out, hipStream_t stream) {
+    hipLaunchKernelGGL(k_status, dim3(1), dim3(kThreads), 0, stream, mslot, B, out);
     return hipGetLastError() == hipSuccess ? SWITCHSD_OK : SWITCHSD_EHIP;
 }
 

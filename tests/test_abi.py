@@ -13,7 +13,7 @@ from paper_2609_20186_amd import binding as sd
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
                       "switchsd.h")
 
-OK, EINVAL, ESHAPE, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
+OK, EINVAL, ESHAPE, EHIP, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4, -5
 
 
 def declared_functions():
@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings_and_workspace_size():
-    for s in (OK, EINVAL, ESHAPE, EHIP, EWORKSPACE):
+    for s in (OK, EINVAL, ESHAPE, EHIP, EWORKSPACE, EDEVICE):
         assert sd.status_string(s) and sd.status_string(s) != "unknown status"
     assert sd.status_string(17) == "unknown status"
     assert sd.workspace_bytes(32, 8) >= 32 * 8 * 8 + 32 * 8 * 4 + 2 * 32 * 4
@@ -230,3 +230,13 @@ def test_commit_entry_point_rejects():
     assert lib.switchsd_commit(None, None, 0, 16, None, 8, None, None, None, None, None) == OK
     a = step_args(commit=1)                            # loop step without its counters
     assert call_step(a, nbytes=1 << 15) == EINVAL
+
+
+def test_status_entry_point_rejects():
+    lib = sd.lib
+    need = sd.workspace_bytes(3, 0)
+    assert lib.switchsd_workspace_status(WS, need, -1, P, None) == ESHAPE
+    assert lib.switchsd_workspace_status(WS, need, 3, None, None) == EINVAL
+    assert lib.switchsd_workspace_status(None, need, 3, P, None) == EWORKSPACE
+    assert lib.switchsd_workspace_status(WS + 8, need, 3, P, None) == EWORKSPACE
+    assert lib.switchsd_workspace_status(WS, need - 1, 3, P, None) == EWORKSPACE
