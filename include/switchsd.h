@@ -71,14 +71,18 @@ typedef enum {
     SWITCHSD_ESHAPE = -2,    /* sizes out of range or inconsistent           */
     SWITCHSD_EHIP = -3,      /* a HIP runtime call or kernel launch failed   */
     SWITCHSD_EWORKSPACE = -4, /* workspace null, misaligned or too small     */
-    SWITCHSD_EDEVICE = -5     /* reported by switchsd_workspace_status: a
+    SWITCHSD_EDEVICE = -5,    /* reported by switchsd_workspace_status: a
                                  bounded device-side wait gave up           */
+    SWITCHSD_ESCRATCH = -6    /* switchsd_step_noalloc: the call needs more
+                                 than SWITCHSD_NOALLOC_SCRATCH_BYTES         */
 } switchsd_status;
 
 #define SWITCHSD_MAX_NGRAM 8       /* most n-gram lengths in one configuration  */
 #define SWITCHSD_MAX_NGRAM_LEN 64  /* longest n-gram length                     */
 #define SWITCHSD_MAX_R 1024        /* most draft nodes (logits rows) per sequence */
 #define SWITCHSD_MAX_CAND 16       /* most copy candidates W                     */
+/* device scratch of switchsd_step_noalloc, per GPU (32 MiB)                  */
+#define SWITCHSD_NOALLOC_SCRATCH_BYTES (32u << 20)
 
 /* Step configuration.
  *   ngram_lens  lengths searched, strictly descending, each in [1, 64]; the
@@ -289,6 +293,24 @@ typedef struct {
  * MODE_FUSED does the greedy step in one kernel launch. */
 int switchsd_step(const switchsd_step_args *args, void *workspace, size_t workspace_bytes,
                   hipStream_t stream);
+
+/* switchsd_step for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Identical results to switchsd_step; the workspace and the scratch of a draw
+ * at T > 0 (args->sample_workspace is ignored) come from a fixed device array
+ * of SWITCHSD_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends.
+ * Nothing is allocated or freed.  The array's address is looked up at the
+ * first call on each GPU (with that GPU current), and that call also clears
+ * the array with a kernel on `stream`, ordered before its own kernels; every
+ * kernel leaves the workspace part zeroed again.  All calls on one GPU share
+ * the array: calls that overlap in time (different streams, or host threads
+ * without ordering) race and give undefined results.  A call that fails
+ * inside HIP can leave the array dirty for the next one.
+ * Returns SWITCHSD_ESCRATCH (and launches nothing) when
+ * switchsd_workspace_bytes(B, R, Lmax, cfg.n_cand) rounded up to 256 bytes,
+ * plus switchsd_sample_workspace_bytes(B, R, V) at T != 0, exceeds the array;
+ * otherwise the codes of switchsd_step. */
+int switchsd_step_noalloc(const switchsd_step_args *args, hipStream_t stream);
 
 /* Decode-loop commit of a finished step -- Sec. 3.3, KV Cache
  * Synchronization (lazy propagation).  For each sequence, with

@@ -19,13 +19,14 @@ MAX_NGRAM = 8
 MAX_CAND = 16
 MODE_AUTO, MODE_FUSED, MODE_SPLIT = 0, 1, 2
 
-STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE", -5: "EDEVICE"}
+STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EHIP", -4: "EWORKSPACE", -5: "EDEVICE",
+          -6: "ESCRATCH"}
 
 EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draft",
            "switchsd_verify_accept", "switchsd_verify_sample", "switchsd_tree_mask",
            "switchsd_commit", "switchsd_step", "switchsd_copy_labels",
            "switchsd_workspace_bytes", "switchsd_sample_workspace_bytes",
-           "switchsd_label_workspace_bytes", "switchsd_workspace_status",
+           "switchsd_label_workspace_bytes", "switchsd_workspace_status", "switchsd_step_noalloc",
            "switchsd_test_withhold_probe_flag", "switchsd_status_string")
 
 
@@ -97,6 +98,7 @@ def _load():
     lib.switchsd_label_workspace_bytes.restype = S
     lib.switchsd_sample_workspace_bytes.restype = S
     lib.switchsd_step.argtypes = [ctypes.POINTER(StepArgs), _P, S, _P]
+    lib.switchsd_step_noalloc.argtypes = [ctypes.POINTER(StepArgs), _P]
     lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
     lib.switchsd_workspace_bytes.restype = S
     lib.switchsd_workspace_status.argtypes = [_P, S, _I, _P, _P]
@@ -340,3 +342,10 @@ def switchsd_step(args, workspace, stream=None):
     _check("switchsd_step", lib.switchsd_step(ctypes.byref(args), _ptr(workspace, "u8",
                                               "workspace"), workspace.numel(),
                                               _stream(stream)))
+
+
+def switchsd_step_noalloc(args, stream=None):
+    """switchsd_step with the library's own fixed device scratch (no workspace
+    argument; args.sample_workspace is ignored)."""
+    _check("switchsd_step_noalloc", lib.switchsd_step_noalloc(ctypes.byref(args),
+                                                              _stream(stream)))

@@ -22,7 +22,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",
           "-I", INCLUDE, "-I", CSRC]
 # packed fp32 VALU ops stay disabled in every device compile
 DEVICE = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-SOURCES = ["switchsd_kernels.hip", "switchsd_api.cpp"]
+SOURCES = ["switchsd_kernels.hip", "switchsd_noalloc.hip", "switchsd_api.cpp"]
 
 
 def _run(cmd, verbose):

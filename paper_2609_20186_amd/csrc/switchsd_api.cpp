@@ -198,6 +198,9 @@ const char *switchsd_status_string(int status) {
         return "HIP runtime call or kernel launch failed";
     case SWITCHSD_EWORKSPACE:
         return "workspace null, not 256-byte aligned or too small";
+    case SWITCHSD_ESCRATCH:
+        return "the call needs more scratch than switchsd_step_noalloc holds "
+               "(SWITCHSD_NOALLOC_SCRATCH_BYTES)";
     case SWITCHSD_EDEVICE:
         return "a bounded device-side wait gave up (results of that call are not valid; "
                "zero the workspace again)";
@@ -327,7 +330,8 @@ size_t rcsum_bytes(int32_t B, int32_t V) {
     return round_line((size_t)B * chunks_per_row(V) * kCsumPerChunk * 16);
 }
 
-int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_t R, int32_t V) {
+// The arguments of a draw at T > 0 other than its scratch.
+int check_sample_args(const SampleArgs *sa, const uint16_t *logits, int32_t V) {
     if (!(sa->temperature > 0.0f) || !isfinite(sa->temperature) || !sa->uniforms)
         return SWITCHSD_EINVAL;
     if (V % 8 != 0 || ((uintptr_t)logits & 15))
@@ -336,10 +340,25 @@ int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_
         return SWITCHSD_EINVAL;
     if (chunks_per_row(V) * (kThreads / 64) > kThreads)
         return SWITCHSD_ESHAPE;
+    return SWITCHSD_OK;
+}
+
+int check_sample(const SampleArgs *sa, const uint16_t *logits, int32_t B, int32_t R, int32_t V) {
+    const int rc = check_sample_args(sa, logits, V);
+    if (rc)
+        return rc;
     if (!sa->ws || ((uintptr_t)sa->ws & (kAlign - 1)) ||
         sa->bytes < switchsd_sample_workspace_bytes(B, R, V))
         return SWITCHSD_EWORKSPACE;
     return SWITCHSD_OK;
+}
+
+SampleArgs sample_args_of(const switchsd_step_args *a) {
+    // speculative sampling with the neural draft's q (chains; copy drafts
+    // stay one-hot)
+    return SampleArgs{a->temperature,  a->uniforms,        a->sample_workspace,
+                      a->sample_workspace_bytes, a->draft_logits, a->accept_uniforms,
+                      a->use_copy};
 }
 
 // After the row maxima are in the row keys: the weight-sum launch, which also
@@ -499,6 +518,40 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
 
 }  // namespace
 
+namespace switchsd {
+
+// Every check of switchsd_step's arguments except its two workspaces.
+int check_step_args(const switchsd_step_args *a) {
+    if (!a)
+        return SWITCHSD_EINVAL;
+    int rc = check_cfg(&a->cfg);
+    if (rc)
+        return rc;
+    const int32_t B = a->B, R = a->R, V = a->V;
+    if (!shape_ok_B(B) || a->Lmax < 1 || a->d < 0 || R < 1 || R > SWITCHSD_MAX_R || V < 1 ||
+        copy_nodes(&a->cfg) > R)
+        return SWITCHSD_ESHAPE;
+    if (a->mode < SWITCHSD_MODE_AUTO || a->mode > SWITCHSD_MODE_SPLIT)
+        return SWITCHSD_EINVAL;
+    if (B == 0)
+        return SWITCHSD_OK;
+    if (!a->tokens || !a->lengths || (a->d > 0 && (!a->hidden || !a->w)) || !a->ntok ||
+        !a->nn || !a->logits || ((uintptr_t)a->logits & 1) || !a->match_n || !a->match_end ||
+        !a->copy_len || (a->cfg.k > 0 && !a->copy_tokens) || !a->z || !a->use_copy ||
+        !a->dtok || !a->dpar || !a->dn || !a->accept_len || !a->accept_node || !a->bonus ||
+        !a->out_tokens || (a->commit && (!a->draft_pos || !a->lag)))
+        return SWITCHSD_EINVAL;
+    const bool sampled = a->temperature != 0.0f;
+    if (a->draft_logits && (!sampled || a->npar))
+        return SWITCHSD_EINVAL;
+    const SampleArgs sa = sample_args_of(a);
+    if (sampled && (rc = check_sample_args(&sa, a->logits, V)))
+        return rc;
+    return SWITCHSD_OK;
+}
+
+}  // namespace switchsd
+
 extern "C" {
 
 int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
@@ -539,25 +592,10 @@ size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
 
 int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace_bytes,
                   hipStream_t stream) {
-    if (!a)
-        return SWITCHSD_EINVAL;
-    int rc = check_cfg(&a->cfg);
-    if (rc)
+    int rc = check_step_args(a);
+    if (rc || a->B == 0)
         return rc;
     const int32_t B = a->B, R = a->R, V = a->V;
-    if (!shape_ok_B(B) || a->Lmax < 1 || a->d < 0 || R < 1 || R > SWITCHSD_MAX_R || V < 1 ||
-        copy_nodes(&a->cfg) > R)
-        return SWITCHSD_ESHAPE;
-    if (a->mode < SWITCHSD_MODE_AUTO || a->mode > SWITCHSD_MODE_SPLIT)
-        return SWITCHSD_EINVAL;
-    if (B == 0)
-        return SWITCHSD_OK;
-    if (!a->tokens || !a->lengths || (a->d > 0 && (!a->hidden || !a->w)) || !a->ntok ||
-        !a->nn || !a->logits || ((uintptr_t)a->logits & 1) || !a->match_n || !a->match_end ||
-        !a->copy_len || (a->cfg.k > 0 && !a->copy_tokens) || !a->z || !a->use_copy ||
-        !a->dtok || !a->dpar || !a->dn || !a->accept_len || !a->accept_node || !a->bonus ||
-        !a->out_tokens || (a->commit && (!a->draft_pos || !a->lag)))
-        return SWITCHSD_EINVAL;
     StepParams p;
     memset(&p, 0, sizeof p);
     fill_cfg(p, &a->cfg);
@@ -566,13 +604,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     p.withhold_flag = g_withhold_probe_flag.load() ? 1 : 0;
     p.spin_cap = p.withhold_flag ? 256 : (1 << 22);
     const bool sampled = a->temperature != 0.0f;
-    // speculative sampling with the neural draft's q (chains; copy drafts
-    // stay one-hot)
-    const SampleArgs sa = {a->temperature,   a->uniforms,        a->sample_workspace,
-                           a->sample_workspace_bytes, a->draft_logits, a->accept_uniforms,
-                           a->use_copy};
-    if (a->draft_logits && (!sampled || a->npar))
-        return SWITCHSD_EINVAL;
+    const SampleArgs sa = sample_args_of(a);
     if (sampled && (rc = check_sample(&sa, a->logits, B, R, V)))
         return rc;
     p.tokens = a->tokens;

@@ -131,6 +131,10 @@ struct StepParams {
     uint32_t exp_all;    // arrivals per sequence at tk_all
 };
 
+// Every check of switchsd_step's arguments except its two workspaces
+// (switchsd_step and switchsd_step_noalloc run it before anything else).
+int check_step_args(const switchsd_step_args *a);
+
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream);
 int launch_select_kernel(const StepParams &p, hipStream_t stream);
 int launch_commit_kernel(const StepParams &p, hipStream_t stream);

@@ -13,7 +13,7 @@ from paper_2609_20186_amd import binding as sd
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
                       "switchsd.h")
 
-OK, EINVAL, ESHAPE, EHIP, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ESHAPE, EHIP, EWORKSPACE, EDEVICE, ESCRATCH = 0, -1, -2, -3, -4, -5, -6
 
 
 def declared_functions():
@@ -34,7 +34,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings_and_workspace_size():
-    for s in (OK, EINVAL, ESHAPE, EHIP, EWORKSPACE, EDEVICE):
+    for s in (OK, EINVAL, ESHAPE, EHIP, EWORKSPACE, EDEVICE, ESCRATCH):
         assert sd.status_string(s) and sd.status_string(s) != "unknown status"
     assert sd.status_string(17) == "unknown status"
     assert sd.workspace_bytes(32, 8) >= 32 * 8 * 8 + 32 * 8 * 4 + 2 * 32 * 4
@@ -240,3 +240,21 @@ def test_status_entry_point_rejects():
     assert lib.switchsd_workspace_status(None, need, 3, P, None) == EWORKSPACE
     assert lib.switchsd_workspace_status(WS + 8, need, 3, P, None) == EWORKSPACE
     assert lib.switchsd_workspace_status(WS, need - 1, 3, P, None) == EWORKSPACE
+
+
+def test_noalloc_entry_point_rejects():
+    """Bad arguments and requests beyond the fixed scratch are refused on the
+    host, before the first call's clear or any other HIP call."""
+    lib = sd.lib
+    assert lib.switchsd_step_noalloc(None, None) == EINVAL
+    assert lib.switchsd_step_noalloc(ctypes.byref(step_args(B=-1)), None) == ESHAPE
+    assert lib.switchsd_step_noalloc(ctypes.byref(step_args(tokens=None)), None) == EINVAL
+    big = 32 * 2 ** 20 // sd.workspace_bytes(1, 8, 16) + 1
+    assert sd.workspace_bytes(big, 8, 16) > 32 * 2 ** 20
+    assert lib.switchsd_step_noalloc(ctypes.byref(step_args(B=big)), None) == ESCRATCH
+    # the T > 0 scratch counts too
+    a = step_args(B=512, R=64, V=128256, temperature=0.7, uniforms=P,
+                  logits=(P + 15) & ~15)
+    assert sd.workspace_bytes(512, 64, 16) < 32 * 2 ** 20
+    assert sd.sample_workspace_bytes(512, 64, 128256) > 32 * 2 ** 20
+    assert lib.switchsd_step_noalloc(ctypes.byref(a), None) == ESCRATCH
