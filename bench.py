@@ -33,10 +33,12 @@ HBM_PEAK_GBPS = 8000.0
 # VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a wave64 op takes 4
 # cycles on one SIMD) = 39.3 T lane-ops/s; one FMA is one op here
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
-# VALU ops per logit of the draw at T > 0: about 1.5 in the row-maximum pass,
-# 16 for the fixed-point weight (unpack, shift, scale, clamp, rint, reduce,
-# 7 fused multiply-adds, convert, ldexp, convert, accumulate) in the sum pass
-SAMPLE_OPS_PER_LOGIT = 17.5
+# VALU ops per logit of the draw at T > 0: about 1.5 in the row-maximum pass
+# and 19.3 in the sum pass (the compiled chunk loop of k_sample_sums issues 617
+# VALU instructions per 32 logits of a lane: unpack, subtract, scale, clamp,
+# rint, reduce, 6 fused multiply-adds, convert, ldexp, floor, widen to
+# binary64, accumulate, and the wave sums)
+SAMPLE_OPS_PER_LOGIT = 20.8
 METRIC = "speculation-control steps/s + verify-argmax HBM GB/s (% peak), B=32 V=128256"
 PROFILES = os.path.join(ROOT, "profiles")
 ROTATE_BYTES = 512 << 20
@@ -95,10 +97,21 @@ def plant_with_library(wl, d, sd):
     return sel
 
 
+def host_cores():
+    """Cores this process may run on (its affinity mask), and what the host
+    reports in all."""
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count() or 1
+    return max(1, usable), os.cpu_count() or usable
+
+
 def cpu_baseline(wl_name, budget_s):
-    """The oracle as it stands, on this host's cores, over whole steps of the
-    same workload (inputs generated and planted on the CPU), repeated until
-    about `budget_s` seconds of work."""
+    """The oracle as it stands, on this host, over whole steps of the same
+    workload (inputs generated and planted on the CPU): once with one thread
+    per usable core and once with one thread, each repeated for about half of
+    `budget_s` seconds."""
     import oracle
     wl = W.WORKLOADS[wl_name]
     d = W.generate(wl)
@@ -106,86 +119,132 @@ def cpu_baseline(wl_name, budget_s):
     sel = oracle.front(d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"],
                        d["npar"], d["nn"], cfg)
     W.plant_batch(wl, d, sel)
-    threads = max(1, min(16, os.cpu_count() or 1))
     args = (d["tokens"], d["lengths"], d["hidden"], d["w"], d["bias"], d["ntok"], d["npar"],
             d["nn"], d["logits"], cfg)
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle.step(*args, threads=threads)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or n >= 100000:
-            break
-    return {"value": n / el, "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} whole {wl_name} steps (B={wl.B}, all sequences) in {el:.1f} s, "
-                      f"{threads} threads"}
+    usable, reported = host_cores()
+
+    def timed(threads, seconds):
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            oracle.step(*args, threads=threads)
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= seconds or n >= 100000:
+                return n, el
+
+    n, el = timed(usable, budget_s / 2)
+    n1, el1 = timed(1, budget_s / 2)
+    return {"value": n / el, "unit": "steps/s", "cores": usable, "kind": "oracle",
+            "sample": f"{n} whole {wl_name} steps (B={wl.B}, all sequences) in {el:.1f} s on "
+                      f"{usable} threads (the cores of this process's affinity mask; the host "
+                      f"reports {reported})",
+            "single_thread": {"value": n1 / el1, "unit": "steps/s", "cores": 1,
+                              "sample": f"{n1} whole {wl_name} steps in {el1:.1f} s"},
+            "host_cpu_count": reported}
 
 
-def decode_loop(args, wl, d, sets, cfg, sd, torch, T, uni, sws):
-    """K steps with commit captured in one HIP graph, cycling over the input
-    copies (the contexts, lengths and draft-model positions are shared and
-    grow); each replay starts from the initial contexts (restored outside the
-    timed region)."""
-    K = args.loop
-    B, R = wl.B, wl.R
-    Lmax = wl.L + K * R
-    tokens = torch.zeros((B, Lmax), dtype=torch.int32, device="cuda")
-    tokens[:, :wl.L] = sets[0]["tokens"]
-    lengths0 = sets[0]["lengths"].clone()
-    lengths = lengths0.clone()
-    draft_pos = lengths0.clone()
-    lag = torch.zeros(B, dtype=torch.int32, device="cuda")
-    tokens0 = tokens.clone()
-    nset = len(sets)
-    outs = [sd.alloc_outputs(B, R, wl.k, wl.n_cand) for _ in range(nset)]
-    ws = sd.alloc_workspace(B, R, Lmax, wl.n_cand)
-    args_l = []
-    for st, o in zip(sets, outs):
-        inp = dict(st)
-        inp["tokens"], inp["lengths"] = tokens, lengths
-        args_l.append(sd.build_step_args(inp, o, cfg, args.mode, T, uni, sws, draft_pos, lag))
+def draft_distribution(wl, d, sets, T, torch):
+    """Draft logits for --draft-q (the target's plus N(0, 0.5) noise, one
+    device copy per rotation set) with the neural drafts' tokens drawn from
+    softmax(q / T) row by row (written into every set), and the accept
+    uniforms."""
+    rng = np.random.default_rng(20187)
+    lf = (d["logits"].astype(np.uint32) << 16).view(np.float32)
+    q = W.f32_to_bf16_bits((lf + rng.normal(0, 0.5, lf.shape)).astype(np.float32))
+    qf = (q.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    ntok = d["ntok"].copy()
+    for b in range(wl.B):
+        for r in range(wl.R - 1):
+            z = (qf[b, r] - qf[b, r].max()) / T
+            pr = np.exp(z)
+            ntok[b, r + 1] = int(rng.choice(wl.V, p=pr / pr.sum()))
+    nt = torch.from_numpy(ntok).cuda()
+    for st in sets:
+        st["ntok"].copy_(nt)
+    qd = torch.from_numpy(q.view(np.int16)).cuda()
+    qdev = [qd] + [qd.clone() for _ in range(len(sets) - 1)]
+    uacc = torch.from_numpy(rng.integers(0, 2 ** 64, (wl.B, wl.R), dtype=np.uint64)
+                            .view(np.int64)).cuda()
+    return qdev, uacc
 
-    def run_steps():
-        for i in range(K):
-            sd.switchsd_step(args_l[i % nset], ws)
 
-    def reset():
-        tokens.copy_(tokens0)
-        lengths.copy_(lengths0)
-        draft_pos.copy_(lengths0)
-
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        run_steps()
-    torch.cuda.current_stream().wait_stream(side)
-    torch.cuda.synchronize()
-    eager_len = lengths.clone()
-    reset()
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        run_steps()
-    reps = max(3, args.steps // K)
+def event_timings(torch, stream, fn, n, reps):
+    """`reps` runs of fn over n calls, back to back on `stream` between two
+    HIP events each: ms per call of every run (launch gaps included)."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    total = 0.0
-    for rep in range(reps + 1):
-        reset()
+    per = []
+    for _ in range(reps):
         torch.cuda.synchronize()
-        e0.record()
-        graph.replay()
-        e1.record()
+        e0.record(stream)
+        fn(0, n)
+        e1.record(stream)
         torch.cuda.synchronize()
-        if rep > 0:                      # the first replay is a warm-up
-            total += e0.elapsed_time(e1)
-        assert torch.equal(lengths, eager_len), "graph replay disagrees with the eager loop"
-    us = total / reps / K * 1e3
-    grown = (eager_len - lengths0).float().mean().item()
-    return {"steps_per_graph": K, "replays": reps, "us_per_step": round(us, 2),
-            "steps_per_s": round(1e6 / us, 1),
-            "tokens_appended_per_sequence_per_step": round(grown / K, 3),
-            "note": "contexts grow in place; inputs cycle over the rotation copies"}
+        per.append(e0.elapsed_time(e1) / n)
+    return per
+
+
+def read_calibration(torch, stream, sets, nbytes, cus):
+    """The streaming-read calibration kernel over the same rotated logits
+    (each launch reads `nbytes` of the next copy), back to back: a sweep of
+    work-groups per CU and chunks in flight, its best point, and the same
+    read without rotation (one copy, which the 256 MB Infinity Cache can
+    hold between launches)."""
+    import ctypes
+    from paper_2609_20186_amd import build as hb
+    lib = ctypes.CDLL(hb.CALIBRATE_LIB)
+    lib.switchsd_calibrate_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                            ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    out = torch.empty(16 * cus, dtype=torch.int32, device="cuda")
+    sp = stream.cuda_stream
+    ptrs = [st["logits"].data_ptr() for st in sets]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(wg, depth, rotate, n=300, src=None, nb=None):
+        srcs = [src] if src is not None else (ptrs if rotate else ptrs[:1])
+        nb = nbytes if nb is None else nb
+
+        def fn(n_):
+            for i in range(n_):
+                rc = lib.switchsd_calibrate_read(srcs[i % len(srcs)], nb, wg, depth,
+                                                 out.data_ptr(), sp)
+                if rc:
+                    raise RuntimeError(f"switchsd_calibrate_read returned {rc}")
+        fn(20)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        fn(n)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3
+
+    sweep = []
+    for per_cu in (1, 2, 4, 8):
+        for depth in (2, 3, 4):
+            us = timed(per_cu * cus, depth, True)
+            sweep.append({"workgroups": per_cu * cus, "depth": depth, "us": round(us, 2)})
+    best = min(sweep, key=lambda r: r["us"])
+    us2 = next(r["us"] for r in sweep if r["workgroups"] == 2 * cus and r["depth"] == 2)
+    cached = timed(2 * cus, 2, False)
+    # the asymptotic rate: one 1 GiB read per launch (no cache can hold it)
+    big = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+    big_us = min(timed(w, dp, False, 20, big.data_ptr(), 1 << 30)
+                 for w in (4 * cus, 8 * cus) for dp in (2, 3))
+    del big
+    gb = lambda us: round(nbytes / (us * 1e-6) / 1e9, 1)  # noqa: E731
+    return {"bytes": nbytes, "kernel": "read_calibration.hip: 16-byte nontemporal loads, 16 KB "
+                                       "chunks per 256-lane work-group, back to back over the "
+                                       "rotated copies",
+            "best": {**best, "GBps": gb(best["us"]),
+                     "frac": round(gb(best["us"]) / HBM_PEAK_GBPS, 4)},
+            "step_kernel_shape": {"workgroups": 2 * cus, "depth": 2, "us": us2, "GBps": gb(us2)},
+            "one_GiB_read": {"us": round(big_us, 1),
+                             "GBps": round((1 << 30) / (big_us * 1e-6) / 1e9, 1),
+                             "frac": round((1 << 30) / (big_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)},
+            "unrotated_same_shape": {"us": round(cached, 2), "GBps": gb(cached),
+                                     "note": "one copy re-read each launch: the Infinity Cache "
+                                             "serves part of it"},
+            "sweep": sweep}
 
 
 def main():
@@ -206,6 +265,14 @@ def main():
                          "contexts with this window length n (the paper's is 5)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="timed runs of --steps steps each; the line reports their median")
+    ap.add_argument("--draft-q", action="store_true",
+                    help="at T > 0, verify the neural drafts by speculative sampling with a "
+                         "draft distribution q (draft logits = the target's plus N(0, 0.5) "
+                         "noise, drafted tokens drawn from q)")
+    ap.add_argument("--no-calibration", action="store_true",
+                    help="skip the streaming-read calibration of the logits' size")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after timing, run a plain device copy of this many MB five times "
                          "(the reference kernel for scaling HBM counters)")
@@ -242,12 +309,17 @@ def main():
     outs = [sd.alloc_outputs(wl.B, wl.R, wl.k, wl.n_cand) for _ in range(nrot)]
     ws = sd.alloc_workspace(wl.B, wl.R, wl.L, wl.n_cand)
     T = args.temperature
+    qdev = uacc = None
     if T > 0:
         uni = torch.from_numpy(np.random.default_rng(20186).integers(
             0, 2 ** 64, (wl.B, wl.R), dtype=np.uint64).view(np.int64)).cuda()
         sws = sd.alloc_sample_workspace(wl.B, wl.R, wl.V)
-        step_args = [sd.build_step_args(s, o, cfg, args.mode, T, uni, sws)
-                     for s, o in zip(sets, outs)]
+        if args.draft_q:
+            qdev, uacc = draft_distribution(wl, d, sets, T, torch)
+        step_args = [sd.build_step_args(s, o, cfg, args.mode, T, uni, sws,
+                                        draft_logits=None if qdev is None else qdev[i],
+                                        accept_uniforms=uacc)
+                     for i, (s, o) in enumerate(zip(sets, outs))]
     else:
         step_args = [sd.build_step_args(s, o, cfg, args.mode) for s, o in zip(sets, outs)]
     import ctypes
@@ -257,21 +329,18 @@ def main():
     wsp, wsn = ws.data_ptr(), ws.numel()
     refs = [ctypes.byref(a) for a in step_args]
 
-    def run(n):
-        for i in range(n):
+    def run(i0, n):
+        for i in range(i0, i0 + n):
             rc = lib.switchsd_step(refs[i % nrot], wsp, wsn, sptr)
             if rc:
                 raise sd.SwitchsdError("switchsd_step", rc)
 
-    run(args.warmup)
-    torch.cuda.synchronize()
+    run(0, args.warmup)
+    # exactly --steps steps per timed run, --repeats runs; the reported figure
+    # is their median; then each step bracketed by its own events
+    per_step = event_timings(torch, stream, run, args.steps, max(1, args.repeats))
+    ms = float(np.median(per_step))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    run(args.steps)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
 
     # every rotation set that ran must agree with the first (same inputs, same
     # outputs); small workloads have more sets than steps
@@ -293,10 +362,13 @@ def main():
     # verification alone (stage entry point), rows of the chosen draft
     if T > 0:
         vargs = [(st["logits"].data_ptr(), wl.B, wl.R, wl.V, T, uni.data_ptr(),
-                  o["dtok"].data_ptr(), o["dpar"].data_ptr(), o["dn"].data_ptr(),
+                  None if qdev is None else qdev[i].data_ptr(),
+                  None if uacc is None else uacc.data_ptr(),
+                  o["dtok"].data_ptr(), None if qdev is not None else o["dpar"].data_ptr(),
+                  o["dn"].data_ptr(),
                   o["accept_len"].data_ptr(), o["accept_node"].data_ptr(), o["bonus"].data_ptr(),
                   o["out_tokens"].data_ptr(), o["amax"].data_ptr(), wsp, wsn, sws.data_ptr(),
-                  sws.numel(), sptr) for st, o in zip(sets, outs)]
+                  sws.numel(), sptr) for i, (st, o) in enumerate(zip(sets, outs))]
         vfn, vname = lib.switchsd_verify_sample, "switchsd_verify_sample"
     else:
         vargs = [(st["logits"].data_ptr(), wl.B, wl.R, wl.V, o["dtok"].data_ptr(),
@@ -306,20 +378,16 @@ def main():
                  for st, o in zip(sets, outs)]
         vfn, vname = lib.switchsd_verify_accept, "switchsd_verify_accept"
 
-    def run_verify(n):
-        for i in range(n):
+    def run_verify(i0, n):
+        for i in range(i0, i0 + n):
             rc = vfn(*vargs[i % nrot])
             if rc:
                 raise sd.SwitchsdError(vname, rc)
 
     nv = max(200, args.steps // 4)
-    run_verify(20)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    run_verify(nv)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    vms = e0.elapsed_time(e1) / nv
+    run_verify(0, 20)
+    v_per = event_timings(torch, stream, run_verify, nv, max(1, args.repeats))
+    vms = float(np.median(v_per))
     vbytes = int(np.sum(sel["dn"])) * wl.V * 2
     v_gbps = vbytes / (vms * 1e-3) / 1e9
 
@@ -357,24 +425,38 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # the dominant kernel: the fused launch, or the verify launch of a split step;
-    # at T > 0 the verification's two launches together
+    # the dominant kernel: the fused launch, or the verify launch of a split
+    # step; at T > 0 the verification's launches together.  `achieved` divides
+    # the algorithmic bytes (ops) of one launch (call) by its own duration,
+    # each launch bracketed by its own HIP events on the launch stream
+    launch_ms = ms
     if T > 0:
-        dom = {"kernel": "sampled verification (row maxima, then weight sums with the draw: 2 launches)",
+        qrows = 0 if qdev is None else int(np.sum(np.clip(sel["dn"] - 1, 0, None) *
+                                                  (sel["use_copy"] == 0)))
+        ops = (vbytes / 2 + qrows * wl.V) * SAMPLE_OPS_PER_LOGIT
+        dom = {"kernel": "sampled verification (row maxima, then weight sums with the draw"
+                         + (", q maxima and residual draw: 4 launches)" if qdev is not None
+                            else ": 2 launches)"),
                "bound": "alu", "unit": "TOP/s (VALU lane-ops)", "peak": round(VALU_PEAK_TOPS, 1),
-               "gbps": vbytes / 2 * SAMPLE_OPS_PER_LOGIT / (vms * 1e-3) / 1e12,
-               "bytes": int(vbytes / 2 * SAMPLE_OPS_PER_LOGIT),
+               "gbps": ops / (vms * 1e-3) / 1e12, "bytes": int(ops), "ms": vms,
                "traffic_file": f"traffic_sampled_verify_{wl.name}.json"}
     elif mode == sd.MODE_FUSED:
-        dom = {"kernel": "k_switchsd (fused step)", "gbps": step_gbps, "bytes": alg,
+        dom = {"kernel": "k_switchsd (fused step)", "gbps": alg / (launch_ms * 1e-3) / 1e9,
+               "bytes": alg, "ms": launch_ms,
                "traffic_file": f"traffic_fused_step_{wl.name}.json"}
     else:
         # long drafts of up to 256 sequences with 16-byte aligned rows: the
         # streamed verify kernel; otherwise the step kernel's argmax role
         streamed = wl.R > 64 and wl.B <= 256 and wl.V % 8 == 0
         kname = "k_verify_stream" if streamed else "k_switchsd"
-        dom = {"kernel": f"{kname} (verify launch of the split step)", "gbps": v_gbps,
-               "bytes": vbytes, "traffic_file": f"traffic_verify_{wl.name}.json"}
+        dom = {"kernel": f"{kname} (verify launch of the split step)",
+               "gbps": vbytes / (vms * 1e-3) / 1e9, "bytes": vbytes, "ms": vms,
+               "traffic_file": f"traffic_verify_{wl.name}.json"}
+    calib = None
+    if not args.no_calibration and T == 0:
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        nb = int(np.sum(rows_read if mode == sd.MODE_FUSED else sel["dn"])) * wl.V * 2 // 16 * 16
+        calib = read_calibration(torch, stream, sets, nb, cus)
     traffic = None
     tf = os.path.join(PROFILES, dom["traffic_file"])
     if os.path.exists(tf):
@@ -401,14 +483,28 @@ def main():
                      "traffic": traffic, "kernel": dom["kernel"],
                      ("algorithmic_ops_per_call" if T > 0 else "algorithmic_bytes_per_launch"):
                          dom["bytes"]},
+        "timing": {"repeats": len(per_step), "steps_per_repeat": args.steps,
+                   "ms_per_step_median": round(ms, 5),
+                   "ms_per_step_min": round(float(np.min(per_step)), 5),
+                   "ms_per_step_max": round(float(np.max(per_step)), 5),
+                   "note": "value, ms_per_step and roofline.achieved: the median of the "
+                           "repeats, each --steps launches back to back between two HIP "
+                           "events on the launch stream (launch gaps included)"},
         "step_GBps": round(step_gbps, 1),
         ("verify_sampled" if T > 0 else "verify_argmax"):
             {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),
-                          "us_per_call": round(vms * 1e3, 2), "bytes_per_call": vbytes},
+             "us_per_call": round(vms * 1e3, 2),
+             "us_per_call_min": round(float(np.min(v_per)) * 1e3, 2),
+             "us_per_call_max": round(float(np.max(v_per)) * 1e3, 2), "bytes_per_call": vbytes},
         "copy_fraction": round(float(np.mean(sel["use_copy"])), 3),
         "mean_accept_len": round(float(o0["accept_len"].float().mean()), 3),
         "kernel_sha": kernel_sha(),
     }
+    if calib:
+        res["read_calibration"] = calib
+    if qdev is not None:
+        res["config"]["draft_distribution"] = ("q: the target's logits plus N(0, 0.5), drafted "
+                                               "tokens drawn from q (speculative sampling)")
     if loop_res:
         res["decode_loop"] = loop_res
     if label_res:

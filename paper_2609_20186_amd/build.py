@@ -14,6 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libswitchsd.so")
+TIMELINE_LIB = os.path.join(PKG, "libswitchsd_timeline.so")
+CALIBRATE_LIB = os.path.join(PKG, "libswitchsd_calibrate.so")
 BUILD = os.path.join(PKG, "_build")
 
 ARCH = "gfx950"
@@ -37,18 +39,33 @@ def _run(cmd, verbose):
         print(out)
 
 
-def build(verbose=False):
-    os.makedirs(BUILD, exist_ok=True)
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp"
+    _run([HIPCC, "-shared", "--offload-arch=" + ARCH, "-fPIC", "-o", tmp] + objs, verbose)
+    os.replace(tmp, lib)
+
+
+def _compile(sources, subdir, defines, verbose):
+    out = os.path.join(BUILD, subdir)
+    os.makedirs(out, exist_ok=True)
     objs = []
-    for src in SOURCES:
-        obj = os.path.join(BUILD, src + ".o")
+    for src in sources:
+        obj = os.path.join(out, src + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        _run([HIPCC] + COMMON + DEVICE + lang + ["-c", os.path.join(CSRC, src), "-o", obj],
+        _run([HIPCC] + COMMON + defines + DEVICE + lang + ["-c", os.path.join(CSRC, src), "-o", obj],
              verbose)
         objs.append(obj)
-    tmp = LIB + ".tmp"
-    _run([HIPCC, "-shared", "--offload-arch=" + ARCH, "-fPIC", "-o", tmp] + objs, verbose)
-    os.replace(tmp, LIB)
+    return objs
+
+
+def build(verbose=False):
+    """The step's library, then the two measurement builds: the same sources
+    with per-work-group phase stamps (libswitchsd_timeline.so, used only by
+    ``timeline.py``) and the streaming-read calibration kernel
+    (libswitchsd_calibrate.so, used only by ``bench.py``)."""
+    _link(_compile(SOURCES, "product", [], verbose), LIB, verbose)
+    _link(_compile(SOURCES, "timeline", ["-DSWITCHSD_TIMELINE"], verbose), TIMELINE_LIB, verbose)
+    _link(_compile(["read_calibration.hip"], "calibrate", [], verbose), CALIBRATE_LIB, verbose)
     return LIB
 
 

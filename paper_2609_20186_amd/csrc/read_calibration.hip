@@ -1,0 +1,93 @@
+// read_calibration.hip -- the achievable HBM read rate of one launch of a
+// given size on this GPU, with the access pattern of the verify argmax
+// stream: 256-lane work-groups each reading a contiguous share in 16 KB
+// chunks of 16-byte nontemporal loads, the next chunk in flight while the
+// current one is reduced (an integer maximum, so that no load is dead).
+// Measurement support for the benchmark; not part of the step's library.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kThreads = 256, kUnroll = 4, kChunkVecs = kThreads * kUnroll;
+
+__device__ __forceinline__ void load(u32x4 (&v)[kUnroll], const u32x4 *p, int64_t q0, int64_t n) {
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const int64_t q = q0 + u * kThreads + threadIdx.x;
+        v[u] = __builtin_nontemporal_load(p + (q < n ? q : n - 1));
+    }
+}
+
+__device__ __forceinline__ uint32_t vmax(const u32x4 (&v)[kUnroll], uint32_t m) {
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+        m = max(max(max(m, v[u][0]), max(v[u][1], v[u][2])), v[u][3]);
+    return m;
+}
+
+// Work-group g reads chunks [C g / G, C (g + 1) / G) with `kDepth` chunks in
+// flight: the loop is unrolled by kDepth so that every buffer is a fixed set
+// of registers.
+template <int kDepth>
+__global__ __launch_bounds__(kThreads) void k_read(const u32x4 *src, int64_t nvec, uint32_t *out) {
+    const int64_t g = blockIdx.x, G = gridDim.x;
+    const int64_t C = (nvec + kChunkVecs - 1) / kChunkVecs;
+    const int64_t c0 = C * g / G, c1 = C * (g + 1) / G;
+    uint32_t m = 0;
+    u32x4 buf[kDepth][kUnroll];
+#pragma unroll
+    for (int j = 0; j < kDepth - 1; ++j)
+        if (c0 + j < c1)
+            load(buf[j], src, (c0 + j) * kChunkVecs, nvec);
+    for (int64_t c = c0; c < c1; c += kDepth) {
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j) {
+            if (c + j + kDepth - 1 < c1)
+                load(buf[(j + kDepth - 1) % kDepth], src, (c + j + kDepth - 1) * kChunkVecs, nvec);
+            if (c + j < c1)
+                m = vmax(buf[j], m);
+        }
+    }
+    // one word per work-group (the lanes' maximum), so the loads are live
+    __shared__ uint32_t red;
+    if (threadIdx.x == 0)
+        red = 0;
+    __syncthreads();
+    atomicMax(&red, m);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        out[g] = red;
+}
+
+}  // namespace
+
+// Reads `bytes` (a multiple of 16, 16-byte aligned device memory) with
+// `workgroups` work-groups and `depth` (1..4) 16 KB chunks in flight per
+// work-group; out [workgroups] receives one word each.  Returns 0, -1 for bad
+// arguments, -3 for a failed launch.
+extern "C" int switchsd_calibrate_read(const void *src, int64_t bytes, int32_t workgroups,
+                                       int32_t depth, uint32_t *out, hipStream_t stream) {
+    if (!src || !out || bytes < 16 || (bytes & 15) || ((uintptr_t)src & 15) || workgroups < 1 ||
+        depth < 1 || depth > 4)
+        return -1;
+    const dim3 g((unsigned)workgroups), t(kThreads);
+    const u32x4 *s = (const u32x4 *)src;
+    switch (depth) {
+    case 1:
+        hipLaunchKernelGGL(k_read<1>, g, t, 0, stream, s, bytes / 16, out);
+        break;
+    case 2:
+        hipLaunchKernelGGL(k_read<2>, g, t, 0, stream, s, bytes / 16, out);
+        break;
+    case 3:
+        hipLaunchKernelGGL(k_read<3>, g, t, 0, stream, s, bytes / 16, out);
+        break;
+    default:
+        hipLaunchKernelGGL(k_read<4>, g, t, 0, stream, s, bytes / 16, out);
+        break;
+    }
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}

@@ -23,6 +23,12 @@ constexpr size_t kAlign = 256;
 // iterations, so that the give-up path runs with every kernel exiting.
 std::atomic<int> g_withhold_probe_flag{0};
 
+#ifdef SWITCHSD_TIMELINE
+// Timeline build only: the buffer of the next step launches' phase stamps
+// (8 per work-group), set by switchsd_timeline_buffer.
+std::atomic<unsigned long long *> g_timeline{nullptr};
+#endif
+
 
 bool shape_ok_B(int32_t B) { return B >= 0 && B <= (1 << 24); }
 
@@ -603,6 +609,9 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         return rc;
     p.withhold_flag = g_withhold_probe_flag.load() ? 1 : 0;
     p.spin_cap = p.withhold_flag ? 256 : (1 << 22);
+#ifdef SWITCHSD_TIMELINE
+    p.tl = g_timeline.load();
+#endif
     const bool sampled = a->temperature != 0.0f;
     const SampleArgs sa = sample_args_of(a);
     if (sampled && (rc = check_sample(&sa, a->logits, B, R, V)))
@@ -757,6 +766,13 @@ int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B
 }
 
 void switchsd_test_withhold_probe_flag(int32_t on) { g_withhold_probe_flag.store(on ? 1 : 0); }
+
+#ifdef SWITCHSD_TIMELINE
+// Timeline build only (not part of the product library's interface): phase
+// stamps of the following switchsd_step launches go to `buf` (device, 8 u64
+// per work-group of the largest launch); NULL stops recording.
+void switchsd_timeline_buffer(unsigned long long *buf) { g_timeline.store(buf); }
+#endif
 
 int switchsd_tree_mask(const int32_t *dpar, const int32_t *dn, int32_t B, int32_t R,
                        uint32_t *mask, hipStream_t stream) {

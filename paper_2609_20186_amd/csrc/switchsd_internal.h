@@ -127,6 +127,7 @@ struct StepParams {
     // withhold_flag (a test knob) the probe never sets its flag
     int32_t spin_cap;
     int32_t withhold_flag;
+    unsigned long long *tl;  // timeline build only: per work-group phase stamps
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all
 };

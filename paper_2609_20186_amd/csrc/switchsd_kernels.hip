@@ -112,6 +112,31 @@ union Shared {
     PickShared pick;
 };
 
+// Timeline build only (compiled with SWITCHSD_TIMELINE, never in the product
+// library): per work-group stamps of the 100 MHz real-time clock, slot
+// [blk * 8 + i]: 0 start, 1 role done, 2 front done, 3 arrival done,
+// 4 epilogue done (its stores complete), 5 the epilogue's loads returned,
+// 7 = role << 32 | sequence.
+#ifdef SWITCHSD_TIMELINE
+#define TL_MARK(i)                                                                           \
+    do {                                                                                     \
+        if (threadIdx.x == 0 && p.tl)                                                        \
+            p.tl[(int64_t)blockIdx.x * 8 + (i)] = __builtin_amdgcn_s_memrealtime();         \
+    } while (0)
+#define TL_TAG(v)                                                                            \
+    do {                                                                                     \
+        if (threadIdx.x == 0 && p.tl)                                                        \
+            p.tl[(int64_t)blockIdx.x * 8 + 7] = (v);                                         \
+    } while (0)
+#else
+#define TL_MARK(i) \
+    do {           \
+    } while (0)
+#define TL_TAG(v) \
+    do {          \
+    } while (0)
+#endif
+
 // ------------------------------------------------------------- atomics
 
 __device__ __forceinline__ int32_t ld_i32(const int32_t *p) {
@@ -217,8 +242,12 @@ __device__ __forceinline__ double bf16_hi(uint32_t x) {
 }
 
 // This lane's share of w . h for sequence b, as a double-double (s, c),
-// reduced over the wave.  Two groups of 8 elements per lane (4096 elements per
-// work-group) are requested before either is used.
+// reduced over the wave.  kGroups groups of 8 elements per lane (2048 kGroups
+// elements per work-group) are requested before any is used: the stand-alone
+// probe work-group takes 4 (all of d = 8192 in one memory round trip; its
+// loads queue behind the argmax streams at 1-2 us per round trip), scan tile 0
+// 2 (its scan state is live, and more would raise the kernel's registers).
+template <int kGroups>
 __device__ __forceinline__ void probe_partial(const StepParams &p, int b, double &s, double &c) {
     const int tid = threadIdx.x;
     const uint16_t *h = p.hidden + (int64_t)b * p.d;
@@ -229,11 +258,11 @@ __device__ __forceinline__ void probe_partial(const StepParams &p, int b, double
         const u32x4 *hv = reinterpret_cast<const u32x4 *>(h);
         const float4 *wv = reinterpret_cast<const float4 *>(p.w);
         const int ng = p.d >> 3;
-        for (int g0 = 0; g0 < ng; g0 += 2 * kThreads) {
-            u32x4 x[2];
-            float4 w0[2], w1[2];
+        for (int g0 = 0; g0 < ng; g0 += kGroups * kThreads) {
+            u32x4 x[kGroups];
+            float4 w0[kGroups], w1[kGroups];
 #pragma unroll
-            for (int q = 0; q < 2; ++q) {
+            for (int q = 0; q < kGroups; ++q) {
                 int g = g0 + q * kThreads + tid;
                 g = g < ng ? g : ng - 1;
                 x[q] = hv[g];
@@ -241,7 +270,7 @@ __device__ __forceinline__ void probe_partial(const StepParams &p, int b, double
                 w1[q] = wv[2 * g + 1];
             }
 #pragma unroll
-            for (int q = 0; q < 2; ++q) {
+            for (int q = 0; q < kGroups; ++q) {
                 if (g0 + q * kThreads + tid < ng) {
                     dd_add_term(s, c, bf16_lo(x[q][0]) * (double)w0[q].x);
                     dd_add_term(s, c, bf16_hi(x[q][0]) * (double)w0[q].y);
@@ -349,7 +378,7 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
     }
     if (t == 0 && p.scan_probe) {
         double ps, pc;
-        probe_partial(p, b, ps, pc);
+        probe_partial<2>(p, b, ps, pc);
         if (lane == 0) {
             sh.scan.ps[wave] = ps;
             sh.scan.pc[wave] = pc;
@@ -480,7 +509,7 @@ __device__ __forceinline__ uint32_t *error_word(const StepParams &p, int b) {
 // when a sequence has several scan tiles).
 __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
     double s, c;
-    probe_partial(p, b, s, c);
+    probe_partial<4>(p, b, s, c);
     const int tid = threadIdx.x;
     if ((tid & 63) == 0) {
         sh.probe.s[tid >> 6] = s;
@@ -1016,6 +1045,24 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
         s = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
         st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
     }
+    int mn, me, jsel;
+    pick_match(p, s, mn, me, jsel);
+    const int L = sh.scan.L;
+    // one candidate: its tokens are requested before the wait for the probe
+    // (they do not depend on z), from this tile's LDS where they lie in it
+    // (positions [t0 - 64, t0 + T), index = position - t0 + 64)
+    const int t0 = t * kScanTile;
+    int cl1 = 0, ct1 = -1;
+    bool in_tile = false;
+    if (!general_select(p)) {
+        cl1 = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
+        const int lo = t0 - 64 > 0 ? t0 - 64 : 0;
+        const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
+        in_tile = cl1 > 0 && me + 1 >= lo && me + cl1 < hi;
+        if (lane < cl1)
+            ct1 = in_tile ? sh.scan.tile[me + 1 + lane - t0 + 64]
+                          : p.tokens[(int64_t)b * p.Lmax + me + 1 + lane];
+    }
     float zb = 0.0f;
     if (p.epi_front == EPI_SELECT) {
         if (p.probe_on) {
@@ -1045,9 +1092,6 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
             zb = ld_f32(&p.z[b]);
         }
     }
-    int mn, me, jsel;
-    pick_match(p, s, mn, me, jsel);
-    const int L = sh.scan.L;
     if (general_select(p)) {
         // W > 1: the tiles' lists of length jsel, latest tile first: the first
         // W occurrences in that order are the W most recent
@@ -1072,23 +1116,14 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
             }
         }
         const int v = lane < W ? sh.scan.merged[lane] : 0;
-        const int t0 = t * kScanTile;
         front_finish_w(p, b, mn, v, L, zb, pre, sh, t0, t0 - 64 > 0 ? t0 - 64 : 0,
                        t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax);
         if (lane == 0)
             st_u32(&p.ws.tk_front[b * kLineU32], 0u);
         return;
     }
-    const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
-    // this tile's LDS holds positions [t0 - 64, t0 + T) (index = position - t0 + 64)
-    const int t0 = t * kScanTile;
-    const int lo = t0 - 64 > 0 ? t0 - 64 : 0;
-    const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
-    const bool in_tile = cl > 0 && me + 1 >= lo && me + cl < hi;
-    int ct = -1;
-    if (in_tile && lane < cl)
-        ct = sh.scan.tile[me + 1 + lane - t0 + 64];
-    front_finish(p, b, mn, me, L, zb, pre, ct, in_tile);
+    (void)in_tile;
+    front_finish(p, b, mn, me, L, zb, pre, ct1, true);
     if (lane == 0)
         st_u32(&p.ws.tk_front[b * kLineU32], 0u);
 }
@@ -1131,6 +1166,10 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
             par = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
         }
         const int dnb = clampi(dn_raw, 1, p.R);
+#ifdef SWITCHSD_TIMELINE
+        __builtin_amdgcn_s_waitcnt(0);
+#endif
+        TL_MARK(5);
         int a = -1;
         if (i < p.R) {
             if (key)
@@ -2438,6 +2477,7 @@ __global__ __launch_bounds__(kThreads) void k_label_clear(u32x4 *table, int64_t 
 
 template <bool kMulti, bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
+    TL_MARK(0);
     // the argmax role's kept chunks share the union: the role is over (every
     // wave) before an epilogue of this work-group uses LDS
     __shared__ Shared sh;
@@ -2470,11 +2510,14 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
         argmax_role(p, b, rowi - b * p.R, s, sh, sh.am.keep);
         role = 2;
     }
+    TL_MARK(1);
+    TL_TAG(((unsigned long long)role << 32) | (uint32_t)b);
     if (threadIdx.x >= 64)
         return;  // waves 1.. are done; wave 0 arrives and may run an epilogue
     if (role == 0 && p.epi_front != EPI_NONE) {
         if (p.scan_tiles == 1) {
             front_local(p, b, sh, pre);
+            TL_MARK(2);
         } else {
             const int lane = threadIdx.x;
             if (lane < p.n_ngram && sh.scan.red[lane] > 0)
@@ -2490,13 +2533,22 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
                         st_i32(&cb[j * p.W + lane], v);
                 }
             }
-            if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front))
+            if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front)) {
                 front_remote(p, b, t, sh, pre);
+                TL_MARK(2);
+            }
         }
     }
     if (p.epi_accept && role != 1) {
-        if (arrive(&p.ws.tk_all[b * kLineU32], p.exp_all))
+        const bool last = arrive(&p.ws.tk_all[b * kLineU32], p.exp_all);
+        TL_MARK(3);
+        if (last) {
             final_epilogue<kCommit>(p, b, sh);
+#ifdef SWITCHSD_TIMELINE
+            __builtin_amdgcn_s_waitcnt(0);
+#endif
+            TL_MARK(4);
+        }
     }
 }
 
