@@ -333,7 +333,8 @@ size_t csum_bytes(int32_t B, int32_t R, int32_t V) {
     return round_line((size_t)B * R * chunks_per_row(V) * kCsumPerChunk * 8);
 }
 size_t rcsum_bytes(int32_t B, int32_t V) {
-    return round_line((size_t)B * chunks_per_row(V) * kCsumPerChunk * 16);
+    // per block of 64 vectors of one row per sequence: 4 u64
+    return round_line((size_t)B * chunks_per_row(V) * (kChunkVecs / 64) * 32);
 }
 
 // The arguments of a draw at T > 0 other than its scratch.
@@ -390,6 +391,7 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     p.qcsum = (unsigned long long *)(sw + csum_bytes(p.B, p.R, p.V));
     p.rcsum = (unsigned long long *)(sw + 2 * csum_bytes(p.B, p.R, p.V));
     p.rdec = (uint32_t *)(sw + 2 * csum_bytes(p.B, p.R, p.V) + rcsum_bytes(p.B, p.V));
+    p.rz = (unsigned long long *)((char *)p.rdec + round_line((size_t)p.B * p.R * 4));
     p.qlogits = sa->qlogits;
     p.accept_uniforms = sa->accept_uniforms;
     p.spec_copy = sa->spec_copy;
@@ -436,13 +438,10 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     // epilogue (sequences verified with q: the residual launch does)
     if ((rc = launch_sample_sums_kernel(p, grid, stream)) || !q)
         return rc;
-    int64_t rsegs = (8 * (int64_t)cus + p.B - 1) / p.B;
-    if (rsegs > p.cpr)
-        rsegs = p.cpr;
-    if (rsegs < 1)
-        rsegs = 1;
-    p.rseg_chunks = (int32_t)((p.cpr + rsegs - 1) / rsegs);
-    p.rsegs = (int32_t)((p.cpr + p.rseg_chunks - 1) / p.rseg_chunks);
+    // residual: one work-group per 256 vectors (4 KB) of the rejected row,
+    // one vector per lane, covering every block of every chunk (the draw sums
+    // 16 block entries per chunk; blocks past the row's end write zero)
+    p.rsegs = p.cpr * (kChunkVecs / kThreads);
     const int64_t rgrid = (int64_t)p.B * p.rsegs;
     if (!grid_ok(rgrid))
         return SWITCHSD_ESHAPE;
@@ -593,7 +592,8 @@ int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t
 size_t switchsd_sample_workspace_bytes(int32_t B, int32_t R, int32_t V) {
     if (B < 0 || R < 0 || V < 0)
         return 0;
-    return 2 * csum_bytes(B, R, V) + rcsum_bytes(B, V) + round_line((size_t)B * R * 4);
+    return 2 * csum_bytes(B, R, V) + rcsum_bytes(B, V) + round_line((size_t)B * R * 4) +
+           round_line((size_t)B * R * 16);
 }
 
 int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace_bytes,

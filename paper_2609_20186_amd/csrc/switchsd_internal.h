@@ -118,11 +118,11 @@ struct StepParams {
     const int32_t *spec_copy;         // [B] use_copy of the step (copy drafts stay one-hot)
                                       // or null (every sequence uses q)
     unsigned long long *qcsum;        // [B, R, cpr, waves] integer weight sums of the q rows
-    unsigned long long *rcsum;        // [B, cpr, waves, 2] residual sums of the rejected row
+    unsigned long long *rcsum;        // [B, cpr * 16, 4] per block of 64 vectors of the
+                                      // rejected row: residual sum (lo, hi), P sum, unused
     uint32_t *rdec;                   // [B, R] test of row r: 1 accepted, 2 rejected
-    int32_t rsegs;                    // residual work-groups per sequence
-    int32_t rseg_chunks;              // 16 KB chunks of the rejected row per residual
-                                      // work-group
+    unsigned long long *rz;           // [B, R, 2] Zp, Zq of each tested row
+    int32_t rsegs;                    // residual work-groups per sequence (4 KB each)
     // bounded waits: spin limit of the front's wait for the probe flag; with
     // withhold_flag (a test knob) the probe never sets its flag
     int32_t spin_cap;

@@ -1876,8 +1876,13 @@ __device__ void spec_test(const StepParams &p, int b, int r) {
     // u Q_x Zp = (hi, lo) with hi its upper 128 bits; 2^64 P_x Zq = (P_x Zq, 0)
     const u128 lhs_hi = mulhi_128_64((u128)u * Qx, sr.Zp);
     const bool acc = lhs_hi < (u128)Px * sr.Zq;
-    if ((threadIdx.x & 63) == 0)
+    if ((threadIdx.x & 63) == 0) {
+        // the row's sums, for the residual launch should this row end the chain
+        __hip_atomic_store(&p.rz[2 * row], sr.Zp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&p.rz[2 * row + 1], sr.Zq, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
         st_u32(&p.rdec[row], acc ? 1u : 2u);
+    }
 }
 
 // The sum work-groups of a drafted row arrive with the units (16 KB chunks or
@@ -2081,53 +2086,74 @@ k_sample_sums_stream(StepParams p) {
     }
 }
 
-// Residual weight max(0, P_j Zq - Q_j Zp) of element j (use_p: the weight
-// P_j itself, for the draw from p when the residual has no mass).
+// Residual weight max(0, P_j Zq - Q_j Zp) of element j, and P_j.
 __device__ __forceinline__ u128 resid_weight(float lp, float lq, int j, const SpecRow &s, float c,
-                                             bool use_p) {
-    const unsigned long long P = elem_weight(lp, s.ap, s.mp, j, s.gp, c);
-    if (use_p)
-        return (u128)P;
+                                             unsigned long long &P) {
+    P = elem_weight(lp, s.ap, s.mp, j, s.gp, c);
     const unsigned long long Q = elem_weight(lq, s.aq, s.mq, j, s.gq, c);
     const u128 x = (u128)P * s.Zq, y = (u128)Q * s.Zp;
     return x > y ? x - y : (u128)0;
 }
-// Residual weight of the 8 elements of vector q (elements 8q .. 8q+7).
+// Residual weights of the 8 elements of vector q (elements 8q .. 8q+7) and
+// their P sum.
 __device__ __forceinline__ u128 resid_vec(const u32x4 &vp, const u32x4 &vq, int q,
-                                          const SpecRow &s, float c, bool use_p) {
+                                          const SpecRow &s, float c, unsigned long long &psum) {
     u128 acc = 0;
+    psum = 0;
 #pragma unroll
     for (int w4 = 0; w4 < 4; ++w4) {
-        acc += resid_weight(lo_f(vp[w4]), lo_f(vq[w4]), 8 * q + 2 * w4, s, c, use_p);
-        acc += resid_weight(hi_f(vp[w4]), hi_f(vq[w4]), 8 * q + 2 * w4 + 1, s, c, use_p);
+        unsigned long long P0, P1;
+        acc += resid_weight(lo_f(vp[w4]), lo_f(vq[w4]), 8 * q + 2 * w4, s, c, P0);
+        acc += resid_weight(hi_f(vp[w4]), hi_f(vq[w4]), 8 * q + 2 * w4 + 1, s, c, P1);
+        psum += P0 + P1;
     }
     return acc;
 }
 
-// The draw from the residual of row a (wave 0): the (chunk, wave) sums give
-// S and the target floor(u S / 2^64); the chunk, the wave's 256 vectors, the
-// block of 64, the vector and the element follow by prefix sums, reading only
-// those 256 vectors of p and q again.  With S = 0 (no residual mass) the draw
-// is from p itself, with its weight sums.  Returns the token in every lane.
+// The residual launch's entries: per block of 64 vectors of the rejected row
+// (16 blocks per 16 KB chunk, in index order), its residual sum (128-bit) and
+// its P sum.
+constexpr int kResBlocks = kChunkVecs / 64;
+__device__ __forceinline__ unsigned long long *resid_entry(const StepParams &p, int b, int e) {
+    return p.rcsum + ((int64_t)b * p.cpr * kResBlocks + e) * 4;
+}
+__device__ __forceinline__ u128 entry_value(const unsigned long long *en, bool use_p) {
+    const auto ld = [](const unsigned long long *q) {
+        return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    if (use_p)
+        return (u128)ld(&en[2]);
+    return ((u128)ld(&en[1]) << 64) | ld(&en[0]);
+}
+
+// The row's maxima and greedy choices (keys), with the sums Zp and Zq that
+// its accept test stored.
+__device__ void spec_row_load(const StepParams &p, int b, int r, SpecRow &s) {
+    const unsigned long long kp = ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride + r]);
+    const unsigned long long kq = ld_u64(&p.ws.qkeys[(int64_t)b * p.ws.key_stride + r]);
+    const int64_t row = (int64_t)b * p.R + r;
+    s.mp = s.mq = 0.0f;
+    s.ap = key_max(kp, s.mp);
+    s.aq = key_max(kq, s.mq);
+    s.gp = decode_key(kp);
+    s.gq = decode_key(kq);
+    s.Zp = __hip_atomic_load(&p.rz[2 * row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s.Zq = __hip_atomic_load(&p.rz[2 * row + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The draw after a rejection at row a (wave 0): the blocks' residual sums
+// give S and the target floor(u S / 2^64); the chunk (16 blocks), the block,
+// the vector (one per lane, p and q read again) and the element follow by
+// prefix sums.  With S = 0 (no residual mass) the same search runs over the
+// blocks' P sums: the draw from p.  Returns the token in every lane.
 __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) {
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)b * p.R + a;
-    const unsigned long long *rc = p.rcsum + (int64_t)b * p.cpr * kWaves * 2;
-    const unsigned long long *pc = p.csum + row * p.cpr * kWaves;
-    auto entry = [&](int i, bool use_p) -> u128 {
-        if (use_p)
-            return (u128)__hip_atomic_load(&pc[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned long long lo =
-            __hip_atomic_load(&rc[2 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned long long hi =
-            __hip_atomic_load(&rc[2 * i + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return ((u128)hi << 64) | lo;
-    };
     auto chunk_total = [&](bool use_p) -> u128 {
         u128 cc = 0;
         if (lane < p.cpr)
-            for (int e = 0; e < kWaves; ++e)
-                cc += entry(lane * kWaves + e, use_p);
+            for (int e = 0; e < kResBlocks; ++e)
+                cc += entry_value(resid_entry(p, b, lane * kResBlocks + e), use_p);
         return cc;
     };
     u128 cc = chunk_total(false);
@@ -2135,9 +2161,6 @@ __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) 
     u128 S = shfl_u128(inc, 63);
     const bool use_p = S == 0;
     if (use_p) {
-        if (!sr.ap) {  // p is one-hot at its greedy choice
-            return sr.gp;
-        }
         cc = chunk_total(true);
         inc = wave_prefix_u128(cc);
         S = shfl_u128(inc, 63);
@@ -2147,64 +2170,40 @@ __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) 
     const unsigned long long hit = __ballot(lane < p.cpr && inc > tg);
     const int cst = __ffsll((long long)hit) - 1;  // exists: target < S
     tg -= shfl_u128(inc - cc, cst);
-    const u128 ce = lane < kWaves ? entry(cst * kWaves + lane, use_p) : (u128)0;
+    const u128 ce =
+        lane < kResBlocks ? entry_value(resid_entry(p, b, cst * kResBlocks + lane), use_p) : 0;
     const u128 ie = wave_prefix_u128(ce);
-    const unsigned long long hit2 = __ballot(lane < kWaves && ie > tg);
+    const unsigned long long hit2 = __ballot(lane < kResBlocks && ie > tg);
     const int est = __ffsll((long long)hit2) - 1;
     tg -= shfl_u128(ie - ce, est);
+    // the block's 64 vectors, one per lane
     const int nq = p.V >> 3;
-    const int q0 = cst * kChunkVecs + est * (kUnroll * 64) + lane;
+    const int q = (cst * kResBlocks + est) * 64 + lane;
     const u32x4 *pv = reinterpret_cast<const u32x4 *>(p.logits + row * p.V);
     const u32x4 *qv = reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V);
-    u32x4 vp[kUnroll], vq[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        const bool in = q0 + u * 64 < nq;
-        vp[u] = in ? pv[q0 + u * 64] : u32x4{0u, 0u, 0u, 0u};
-        vq[u] = in ? qv[q0 + u * 64] : u32x4{0u, 0u, 0u, 0u};
-    }
-    u128 vw[kUnroll], bs[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        vw[u] = q0 + u * 64 < nq ? resid_vec(vp[u], vq[u], q0 + u * 64, sr, p.samp_c, use_p)
-                                 : (u128)0;
-        bs[u] = wave_sum_u128(vw[u]);
-    }
-    int us = kUnroll - 1;
-    u128 incl = 0, us_before = 0;
-    bool found = false;
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-        const u128 excl = incl;
-        incl += bs[u];
-        if (!found && tg < incl) {
-            found = true;
-            us = u;
-            us_before = excl;
-        }
-    }
-    tg -= us_before;
+    u32x4 xp = u32x4{0u, 0u, 0u, 0u}, xq = u32x4{0u, 0u, 0u, 0u};
     u128 w = 0;
-    u32x4 xp = vp[0], xq = vq[0];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        if (u == us) {
-            w = vw[u];
-            xp = vp[u];
-            xq = vq[u];
-        }
+    if (q < nq) {
+        xp = pv[q];
+        xq = qv[q];
+        unsigned long long ps;
+        w = resid_vec(xp, xq, q, sr, p.samp_c, ps);
+        if (use_p)
+            w = ps;
+    }
     const u128 iv = wave_prefix_u128(w);
     const unsigned long long hit3 = __ballot(iv > tg);
-    const int lst = __ffsll((long long)hit3) - 1;
+    const int lst = __ffsll((long long)hit3) - 1;  // exists: tg < the block's sum
     int y = 0;
     if (lane == lst) {
-        const int q = q0 + us * 64;
         u128 run = iv - w;
         int e = 7;
         for (int j = 0; j < 8; ++j) {
             const uint32_t hp = xp[j >> 1], hq = xq[j >> 1];
-            run += resid_weight((j & 1) ? hi_f(hp) : lo_f(hp), (j & 1) ? hi_f(hq) : lo_f(hq),
-                                8 * q + j, sr, p.samp_c, use_p);
+            unsigned long long P;
+            const u128 r = resid_weight((j & 1) ? hi_f(hp) : lo_f(hp),
+                                        (j & 1) ? hi_f(hq) : lo_f(hq), 8 * q + j, sr, p.samp_c, P);
+            run += use_p ? (u128)P : r;
             if (run > tg) {
                 e = j;
                 break;
@@ -2223,11 +2222,9 @@ template <bool kCommit>
 __device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus) {
     const int lane = threadIdx.x & 63;
     const int64_t base = (int64_t)b * p.R;
-    int cL = 0, cdp = 0;
-    if (kCommit) {
+    int cL = 0;
+    if (kCommit)
         cL = clampi(p.clen[b], 0, p.Lmax);
-        cdp = p.draft_pos[b];
-    }
     for (int i = lane; i < p.R; i += 64) {
         const int v = i < a ? ld_i32(&p.dtok[base + i + 1]) : (i == a ? bonus : -1);
         p.out_tokens[base + i] = v;
@@ -2245,7 +2242,6 @@ __device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus) {
         if (kCommit) {  // a neural step: the draft model drafted the accepted tokens
             const int Lnew = cL + a + 1 < p.Lmax ? cL + a + 1 : p.Lmax;
             const int pos = clampi(cL + a, 0, Lnew);
-            (void)cdp;
             p.clen[b] = Lnew;
             p.draft_pos[b] = pos;
             p.lag[b] = Lnew - pos;
@@ -2253,10 +2249,11 @@ __device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus) {
     }
 }
 
-// Residual launch of sequences verified with q: work-group (segment s,
-// sequence b), segment-major.  Every work-group finds the first rejected row
-// a from the tests; if there is one, it adds up the residual weights of its
-// chunks of row a per wave (128-bit).  The last of the sequence's rsegs
+// Residual launch of sequences verified with q: work-group (unit s, sequence
+// b), unit-major; unit s covers blocks 4 s .. 4 s + 3 of 64 vectors (one per
+// wave, one vector per lane).  Every work-group finds the first rejected row
+// a from the tests; if there is one, each wave adds up its block's residual
+// weights (128-bit) and P weights.  The last of the sequence's rsegs
 // work-groups draws the emitted token (the residual draw at a, or the bonus
 // drawn from p at the last row when every test passed) and writes the
 // outputs.
@@ -2282,32 +2279,29 @@ __global__ __launch_bounds__(kThreads) void k_spec_residual(StepParams p) {
     const bool resid = a < dnb - 1;
     SpecRow sr;
     if (resid) {
-        spec_row_setup(p, b, a, sr);
+        spec_row_load(p, b, a, sr);
         const int nq = p.V >> 3;
         const int64_t row = (int64_t)b * p.R + a;
-        const u32x4 *pv = reinterpret_cast<const u32x4 *>(p.logits + row * p.V);
-        const u32x4 *qv = reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V);
-        const int c0 = s * p.rseg_chunks;
-        const int c1 = c0 + p.rseg_chunks < p.cpr ? c0 + p.rseg_chunks : p.cpr;
-        unsigned long long *rc = p.rcsum + (int64_t)b * p.cpr * kWaves * 2;
-        for (int c = c0; c < c1; ++c) {
-            u32x4 A[kUnroll], Q4[kUnroll];
-            load_chunk_w(A, pv, c * kChunkVecs, nq);
-            load_chunk_w(Q4, qv, c * kChunkVecs, nq);
-            const int q0 = c * kChunkVecs + wave * (kUnroll * 64) + lane;
-            u128 acc = 0;
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                if (q0 + u * 64 < nq)
-                    acc += resid_vec(A[u], Q4[u], q0 + u * 64, sr, p.samp_c, false);
-            acc = wave_sum_u128(acc);
-            if (lane == 0) {
-                const int i = c * kWaves + wave;
-                __hip_atomic_store(&rc[2 * i], (unsigned long long)acc, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&rc[2 * i + 1], (unsigned long long)(acc >> 64),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
+        const int blk = s * kWaves + wave;
+        const int q = blk * 64 + lane;
+        u128 acc = 0;
+        unsigned long long ps = 0;
+        if (q < nq) {
+            const u32x4 vp = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4 *>(p.logits + row * p.V) + q);
+            const u32x4 vq = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V) + q);
+            acc = resid_vec(vp, vq, q, sr, p.samp_c, ps);
+        }
+        acc = wave_sum_u128(acc);
+        ps = wave_sum_u64(ps);
+        if (lane == 0 && blk < p.cpr * kResBlocks) {
+            unsigned long long *en = resid_entry(p, b, blk);
+            __hip_atomic_store(&en[0], (unsigned long long)acc, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&en[1], (unsigned long long)(acc >> 64), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&en[2], ps, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
     __builtin_amdgcn_s_waitcnt(0);

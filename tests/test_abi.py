@@ -166,9 +166,10 @@ def test_sample_entry_point_rejects():
     need = sd.sample_workspace_bytes(2, 8, 128)
     assert need % 256 == 0
     # 64-bit weight sums per 16 KB chunk and wave (4) for the p rows and for the
-    # q rows, 128-bit residual sums for one row per sequence, a test word per row
+    # q rows; per block of 64 vectors of one row per sequence a residual and a
+    # P sum (32 bytes); a test word and the two sums Zp, Zq per row
     assert sd.sample_workspace_bytes(2, 8, 128256) == 2 * (2 * 8 * 16 * 4 * 8) + \
-        2 * 16 * 4 * 16 + 256
+        2 * 16 * 16 * 32 + 256 + 256
     assert sd.sample_workspace_bytes(-1, 8, 8) == 0
 
     def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS, wsn=4096, q=None,
