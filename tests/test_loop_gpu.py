@@ -9,6 +9,7 @@ import oracle
 from gpu_helpers import (ORACLE_THREADS, assert_match, ocfg, planted_workload, say, sd_cfg,
                          to_device, with_temperature)
 from test_parity_gpu import AUTO, FUSED, SPLIT, custom_case
+from test_spec_gpu import with_draft_distribution
 
 pytestmark = pytest.mark.gpu
 
@@ -42,7 +43,9 @@ def oracle_loop(d, steps):
     for s in range(steps):
         res = oracle.step(tokens, lengths, d["hidden"], d["w"], d["bias"], d["ntok"], d["npar"],
                           d["nn"], d["logits"], cfg, threads=ORACLE_THREADS, temperature=T,
-                          uniforms=d["uniforms"] if T > 0 else None)
+                          uniforms=d["uniforms"] if T > 0 else None,
+                          draft_logits=d.get("draft_logits"),
+                          accept_uniforms=d.get("accept_uniforms"))
         lag = oracle.commit(tokens, lengths, draft_pos, res)
         outs.append(res)
     return outs, tokens, lengths, draft_pos, lag
@@ -67,7 +70,8 @@ class GpuLoop:
         self.sws = sd.alloc_sample_workspace(B, R, d["logits"].shape[2]) if T > 0 else None
         self.args = sd.build_step_args(self.dev, self.out, sd_cfg(d), mode, T,
                                        self.dev.get("uniforms"), self.sws, self.draft_pos,
-                                       self.lag)
+                                       self.lag, draft_logits=self.dev.get("draft_logits"),
+                                       accept_uniforms=self.dev.get("accept_uniforms"))
         self.sd = sd
 
     def step(self):
@@ -87,6 +91,10 @@ LOOP_CASES = {
                       theta=-0.2, vocab=20, n_cand=10, plant=True), 0.0),
     "chain_sampled": (dict(seed=83, B=5, Lmax=600, V=512, R=6, k=5, lens=(3, 2, 1), kappa=1,
                            theta=-0.3, vocab=6, plant=True), 0.6),
+    # neural drafts verified with their distribution q: the residual launch
+    # closes the step and commits
+    "chain_sampled_q": (dict(seed=87, B=6, Lmax=600, V=512, R=6, k=5, lens=(3, 2, 1), kappa=1,
+                             theta=-0.3, vocab=6), 0.6),
     "tiles_capacity": (dict(seed=84, B=3, Lmax=4200, V=256, R=9, k=8, lens=(3, 2, 1),
                             kappa=1, theta=-np.inf, vocab=5, ragged=False, plant=True), 0.0),
     # long drafts at T > 0: the streamed weight sums close the step and commit
@@ -106,6 +114,8 @@ def test_loop_parity(case):
     d = widen(custom_case(**kw), extra)
     if T > 0:
         d = with_temperature(d, T, seed=9)
+    if case.endswith("_q"):
+        d = with_draft_distribution(d, T, seed=10)
     steps = 12
     outs, t_exp, l_exp, dp_exp, lag_exp = oracle_loop(d, steps)
     for mode in (AUTO, FUSED, SPLIT):
@@ -147,16 +157,18 @@ def test_commit_entry_point_equals_step_commit():
     np.testing.assert_array_equal(lag.cpu().numpy(), lag_exp)
 
 
-@pytest.mark.parametrize("T", [0.0, 0.6])
-def test_loop_graph_replays(T):
+@pytest.mark.parametrize("T,q", [(0.0, False), (0.6, False), (0.6, True)])
+def test_loop_graph_replays(T, q):
     """Eight loop steps captured in one HIP graph; each replay starts from the
     initial state (restored by eager copies between replays) and must end in
     the eager loop's state."""
     import torch
-    say(f"[loop] graph replays T={T}")
+    say(f"[loop] graph replays T={T} q={q}")
     d = widen(planted_workload("C2"), 8 * 8)
     if T > 0:
         d = with_temperature(d, T, seed=11)
+    if q:
+        d = with_draft_distribution(d, T, seed=12)
     g = GpuLoop(d, AUTO)
     t0, l0, dp0 = (g.dev["tokens"].clone(), g.dev["lengths"].clone(), g.draft_pos.clone())
     for _ in range(8):
