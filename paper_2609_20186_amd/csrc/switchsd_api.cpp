@@ -381,6 +381,7 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     if (rc)
         return rc;
     const bool q = sa->qlogits != nullptr;
+    p.tl = nullptr;  // phase stamps (timeline build) cover the step kernel's grid only
     // long drafts: the sums stream the drafted rows' chunks over a fixed grid
     const bool stream_sums = p.R > 64 && p.B <= kListMaxB && !q;
     p.uniforms = sa->uniforms;
