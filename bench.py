@@ -169,18 +169,46 @@ def draft_distribution(wl, d, sets, T, torch):
     return qdev, uacc
 
 
+_CALIB = None
+
+
+def calibrate_lib():
+    """The measurement library (streaming-read calibration, delay kernel)."""
+    global _CALIB
+    if _CALIB is None:
+        import ctypes
+        from paper_2609_20186_amd import build as hb
+        _CALIB = ctypes.CDLL(hb.CALIBRATE_LIB)
+        _CALIB.switchsd_calibrate_delay.argtypes = [ctypes.c_double, ctypes.c_void_p]
+        _CALIB.switchsd_calibrate_read.argtypes = [ctypes.c_void_p, ctypes.c_int64,
+                                                   ctypes.c_int32, ctypes.c_int32,
+                                                   ctypes.c_void_p, ctypes.c_void_p]
+    return _CALIB
+
+
 def event_timings(torch, stream, fn, n, reps):
     """`reps` runs of fn over n calls, back to back on `stream` between two
-    HIP events each: ms per call of every run (launch gaps included)."""
+    HIP events each: ms per call of every run.  Before each run a delay
+    kernel holds the stream (25 us per call, at least 0.5 ms) while the n
+    calls are queued from the host, so that they run back to back: the timed
+    region holds exactly the n calls and the GPU gaps between them, not the
+    host's launch rate."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    lib = calibrate_lib()
     per = []
+    host = []
     for _ in range(reps):
         torch.cuda.synchronize()
+        if lib.switchsd_calibrate_delay(min(500.0 + 25.0 * n, 2e5), stream.cuda_stream):
+            raise RuntimeError("switchsd_calibrate_delay failed")
         e0.record(stream)
+        t0 = time.perf_counter()
         fn(0, n)
+        host.append((time.perf_counter() - t0) / n * 1e6)
         e1.record(stream)
         torch.cuda.synchronize()
         per.append(e0.elapsed_time(e1) / n)
+    event_timings.host_us = float(np.median(host))
     return per
 
 
@@ -190,11 +218,7 @@ def read_calibration(torch, stream, sets, nbytes, cus):
     work-groups per CU and chunks in flight, its best point, and the same
     read without rotation (one copy, which the 256 MB Infinity Cache can
     hold between launches)."""
-    import ctypes
-    from paper_2609_20186_amd import build as hb
-    lib = ctypes.CDLL(hb.CALIBRATE_LIB)
-    lib.switchsd_calibrate_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
-                                            ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    lib = calibrate_lib()
     out = torch.empty(16 * cus, dtype=torch.int32, device="cuda")
     sp = stream.cuda_stream
     ptrs = [st["logits"].data_ptr() for st in sets]
@@ -212,6 +236,7 @@ def read_calibration(torch, stream, sets, nbytes, cus):
                     raise RuntimeError(f"switchsd_calibrate_read returned {rc}")
         fn(20)
         torch.cuda.synchronize()
+        lib.switchsd_calibrate_delay(min(500.0 + 25.0 * n, 2e5), sp)
         e0.record(stream)
         fn(n)
         e1.record(stream)
@@ -339,6 +364,7 @@ def main():
     # exactly --steps steps per timed run, --repeats runs; the reported figure
     # is their median; then each step bracketed by its own events
     per_step = event_timings(torch, stream, run, args.steps, max(1, args.repeats))
+    host_us = event_timings.host_us
     ms = float(np.median(per_step))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
@@ -487,9 +513,11 @@ def main():
                    "ms_per_step_median": round(ms, 5),
                    "ms_per_step_min": round(float(np.min(per_step)), 5),
                    "ms_per_step_max": round(float(np.max(per_step)), 5),
+                   "host_us_per_launch": round(host_us, 2),
                    "note": "value, ms_per_step and roofline.achieved: the median of the "
-                           "repeats, each --steps launches back to back between two HIP "
-                           "events on the launch stream (launch gaps included)"},
+                           "repeats, each --steps launches between two HIP events on the "
+                           "launch stream, queued behind a delay kernel so that they run "
+                           "back to back (GPU launch gaps included, host launch rate not)"},
         "step_GBps": round(step_gbps, 1),
         ("verify_sampled" if T > 0 else "verify_argmax"):
             {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),

@@ -2,8 +2,10 @@
 // given size on this GPU, with the access pattern of the verify argmax
 // stream: 256-lane work-groups each reading a contiguous share in 16 KB
 // chunks of 16-byte nontemporal loads, the next chunk in flight while the
-// current one is reduced (an integer maximum, so that no load is dead).
-// Measurement support for the benchmark; not part of the step's library.
+// current one is reduced (an integer maximum, so that no load is dead); and a
+// delay kernel that lets the benchmark queue its timed launches before they
+// run.  Measurement support for the benchmark; not part of the step's
+// library.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -62,7 +64,25 @@ __global__ __launch_bounds__(kThreads) void k_read(const u32x4 *src, int64_t nve
         out[g] = red;
 }
 
+// Holds the stream for `ticks` of the 100 MHz real-time clock (bounded: it
+// exits when the time is up).
+__global__ void k_delay(uint64_t ticks) {
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (__builtin_amdgcn_s_memrealtime() - t0 < ticks)
+        __builtin_amdgcn_s_sleep(8);
+}
+
 }  // namespace
+
+// Measurement support: a one-lane kernel that returns after `microseconds`
+// (at most one second), so that launches queued behind it start back to
+// back.  Returns 0, -1 for a bad argument, -3 for a failed launch.
+extern "C" int switchsd_calibrate_delay(double microseconds, hipStream_t stream) {
+    if (!(microseconds >= 0.0) || microseconds > 1e6)
+        return -1;
+    hipLaunchKernelGGL(k_delay, dim3(1), dim3(1), 0, stream, (uint64_t)(microseconds * 100.0));
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 // Reads `bytes` (a multiple of 16, 16-byte aligned device memory) with
 // `workgroups` work-groups and `depth` (1..4) 16 KB chunks in flight per
