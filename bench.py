@@ -183,6 +183,10 @@ def calibrate_lib():
         _CALIB.switchsd_calibrate_read.argtypes = [ctypes.c_void_p, ctypes.c_int64,
                                                    ctypes.c_int32, ctypes.c_int32,
                                                    ctypes.c_void_p, ctypes.c_void_p]
+        _CALIB.switchsd_calibrate_read_dyn.argtypes = [ctypes.c_void_p, ctypes.c_int64,
+                                                       ctypes.c_int32, ctypes.c_int32,
+                                                       ctypes.c_void_p, ctypes.c_void_p,
+                                                       ctypes.c_void_p]
     return _CALIB
 
 
@@ -243,6 +247,31 @@ def read_calibration(torch, stream, sets, nbytes, cus):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n * 1e3
 
+    def timed_dyn(wg, static_pct, n=300):
+        ctr = torch.zeros((n + 20) * 128, dtype=torch.int32, device="cuda")
+
+        def fn(i0, n_):
+            for i in range(i0, i0 + n_):
+                rc = lib.switchsd_calibrate_read_dyn(ptrs[i % len(ptrs)], nbytes, wg, static_pct,
+                                                     ctr.data_ptr() + 512 * i, out.data_ptr(),
+                                                     sp)
+                if rc:
+                    raise RuntimeError(f"switchsd_calibrate_read_dyn returned {rc}")
+        fn(0, 20)
+        torch.cuda.synchronize()
+        lib.switchsd_calibrate_delay(min(500.0 + 25.0 * n, 2e5), sp)
+        e0.record(stream)
+        fn(20, n)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3
+
+    dyn = []
+    for per_cu in (2, 4):
+        for pct in (0, 50, 75, 90):
+            dyn.append({"workgroups": per_cu * cus, "static_percent": pct,
+                        "us": round(timed_dyn(per_cu * cus, pct), 2)})
+
     sweep = []
     for per_cu in (1, 2, 4, 8):
         for depth in (2, 3, 4):
@@ -269,7 +298,8 @@ def read_calibration(torch, stream, sets, nbytes, cus):
             "unrotated_same_shape": {"us": round(cached, 2), "GBps": gb(cached),
                                      "note": "one copy re-read each launch: the Infinity Cache "
                                              "serves part of it"},
-            "sweep": sweep}
+            "sweep": sweep,
+            "claims_sweep": dyn}
 
 
 def main():

@@ -64,6 +64,79 @@ __global__ __launch_bounds__(kThreads) void k_read(const u32x4 *src, int64_t nve
         out[g] = red;
 }
 
+// Static share, then dynamic claims: chunks [0, S) are split evenly over the
+// work-groups (two in flight); chunks [S, C) form 8 pools, one per XCD
+// (work-groups are dispatched to the XCDs in turn, block index mod 8), from
+// which wave 0 claims one chunk at a time with an atomic on the pool's
+// counter, one claim ahead of the chunk being reduced, moving on to the next
+// pool when one runs dry.  ctr: 8 zeroed counters per launch.
+__global__ __launch_bounds__(kThreads) void k_read_dyn(const u32x4 *src, int64_t nvec,
+                                                       int64_t S, uint32_t *ctr, uint32_t *out) {
+    const int64_t g = blockIdx.x, G = gridDim.x;
+    const int64_t C = (nvec + kChunkVecs - 1) / kChunkVecs;
+    const int64_t c0 = S * g / G, c1 = S * (g + 1) / G;
+    uint32_t m = 0;
+    u32x4 A[kUnroll], B[kUnroll];
+    __shared__ int64_t claim[2];
+    const int x0 = (int)(g & 7);
+    int pool = 0;  // pools tried so far (wave 0, lane 0)
+    // claims chunk indices from the pools; -1 when every pool is empty
+    auto next_claim = [&]() -> int64_t {
+        while (pool < 8) {
+            const int x = (x0 + pool) & 7;
+            const int64_t p0 = S + (C - S) * x / 8, p1 = S + (C - S) * (x + 1) / 8;
+            const uint32_t i = atomicAdd(&ctr[x * 16], 1u);
+            if (p0 + (int64_t)i < p1)
+                return p0 + i;
+            ++pool;
+        }
+        return -1;
+    };
+    if (threadIdx.x == 0)
+        claim[0] = next_claim();
+    // the static share, two in flight
+    if (c0 < c1) {
+        load(A, src, c0 * kChunkVecs, nvec);
+        int64_t c = c0;
+        for (; c + 1 < c1; c += 2) {
+            load(B, src, (c + 1) * kChunkVecs, nvec);
+            m = vmax(A, m);
+            load(A, src, (c + 2 < c1 ? c + 2 : c + 1) * kChunkVecs, nvec);
+            m = vmax(B, m);
+        }
+        if (c < c1)
+            m = vmax(A, m);
+    }
+    __syncthreads();
+    int64_t cur = claim[0];
+    int k = 0;
+    if (cur >= 0)
+        load(A, src, cur * kChunkVecs, nvec);
+    while (cur >= 0) {
+        if (threadIdx.x == 0)
+            claim[(k + 1) & 1] = next_claim();
+        __syncthreads();
+        const int64_t nxt = claim[(k + 1) & 1];
+        if (nxt >= 0)
+            load(B, src, nxt * kChunkVecs, nvec);
+        m = vmax(A, m);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            A[u] = B[u];
+        cur = nxt;
+        ++k;
+        __syncthreads();
+    }
+    __shared__ uint32_t red;
+    if (threadIdx.x == 0)
+        red = 0;
+    __syncthreads();
+    atomicMax(&red, m);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        out[g] = red;
+}
+
 // Holds the stream for `ticks` of the 100 MHz real-time clock (bounded: it
 // exits when the time is up).
 __global__ void k_delay(uint64_t ticks) {
@@ -73,6 +146,22 @@ __global__ void k_delay(uint64_t ticks) {
 }
 
 }  // namespace
+
+// The static-plus-claims variant: `static_percent` of the chunks split
+// evenly, the rest claimed from 8 per-XCD pools; ctr: 8 zeroed counters, each
+// on its own 64-byte line (128 uint32), used by this launch only.
+extern "C" int switchsd_calibrate_read_dyn(const void *src, int64_t bytes, int32_t workgroups,
+                                           int32_t static_percent, uint32_t *ctr, uint32_t *out,
+                                           hipStream_t stream) {
+    if (!src || !out || !ctr || bytes < 16 || (bytes & 15) || ((uintptr_t)src & 15) ||
+        workgroups < 1 || static_percent < 0 || static_percent > 100)
+        return -1;
+    const int64_t nvec = bytes / 16;
+    const int64_t C = (nvec + kChunkVecs - 1) / kChunkVecs;
+    hipLaunchKernelGGL(k_read_dyn, dim3((unsigned)workgroups), dim3(kThreads), 0, stream,
+                       (const u32x4 *)src, nvec, C * static_percent / 100, ctr, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 // Measurement support: a one-lane kernel that returns after `microseconds`
 // (at most one second), so that launches queued behind it start back to
