@@ -357,12 +357,19 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
 /* Device-side status of the calls that used `workspace` (B sequences),
  * written to *status (a DEVICE int32) asynchronously on `stream`:
  * SWITCHSD_OK, or SWITCHSD_EDEVICE when a bounded wait inside a kernel gave
- * up since the last status call.  The one such wait: in switchsd_step with
- * contexts longer than 1024 tokens, the last scan work-group of a sequence
- * waits for the probe's work-group (dispatched before it, so in practice the
- * wait always ends); if it gives up, that sequence's switch takes the neural
- * draft and its outputs are not valid.  The call reads and clears the error
- * words; after SWITCHSD_EDEVICE, zero the workspace again before its next use.
+ * up since the last status call.  There are two such waits, both in
+ * switchsd_step, and in practice both always end:
+ *   - with contexts longer than 1024 tokens, the last scan work-group of a
+ *     sequence waits for the probe's work-group (dispatched before it); if it
+ *     gives up, that sequence's switch takes the neural draft;
+ *   - in the fused launch at T = 0 with R <= 64 and B no larger than the
+ *     device's compute-unit count, the work-group that chose a sequence's
+ *     draft waits for the results of that sequence's argmax work-groups
+ *     (which wait for nothing); if it gives up, a segment whose result is
+ *     missing counts as holding no maximum.
+ * After a give-up that sequence's outputs are not valid.  The call reads and
+ * clears the error words; after SWITCHSD_EDEVICE, zero the workspace again
+ * before its next use.
  *   workspace of at least switchsd_workspace_bytes(B, 0, 0, 0) bytes, the
  *   same B as the calls; status [1] int32 on the device. */
 int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B,
@@ -372,6 +379,12 @@ int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B
  * withhold their flag and the wait above gives up after a few iterations, so
  * that a test can force the give-up path (every kernel still exits). */
 void switchsd_test_withhold_probe_flag(int32_t on);
+
+/* Test support only: while `on` is nonzero, the fused switchsd_step's argmax
+ * work-group of sequence 0, row 0, first segment withholds its result and the
+ * second wait above gives up after a few iterations (every kernel still
+ * exits). */
+void switchsd_test_withhold_segment(int32_t on);
 
 /* Static, thread-safe text of a status code. */
 const char *switchsd_status_string(int status);

@@ -27,7 +27,8 @@ EXPORTS = ("switchsd_ngram_match", "switchsd_probe_score", "switchsd_select_draf
            "switchsd_commit", "switchsd_step", "switchsd_copy_labels",
            "switchsd_workspace_bytes", "switchsd_sample_workspace_bytes",
            "switchsd_label_workspace_bytes", "switchsd_workspace_status", "switchsd_step_noalloc",
-           "switchsd_test_withhold_probe_flag", "switchsd_status_string")
+           "switchsd_test_withhold_probe_flag", "switchsd_test_withhold_segment",
+           "switchsd_status_string")
 
 
 class SwitchsdError(RuntimeError):
@@ -102,12 +103,13 @@ def _load():
     lib.switchsd_workspace_bytes.argtypes = [_I, _I, _I, _I]
     lib.switchsd_workspace_bytes.restype = S
     lib.switchsd_workspace_status.argtypes = [_P, S, _I, _P, _P]
-    lib.switchsd_test_withhold_probe_flag.argtypes = [_I]
-    lib.switchsd_test_withhold_probe_flag.restype = None
+    for knob in ("switchsd_test_withhold_probe_flag", "switchsd_test_withhold_segment"):
+        getattr(lib, knob).argtypes = [_I]
+        getattr(lib, knob).restype = None
     lib.switchsd_status_string.argtypes = [ctypes.c_int]
     lib.switchsd_status_string.restype = ctypes.c_char_p
     for name in EXPORTS:
-        if name != "switchsd_test_withhold_probe_flag":
+        if not name.startswith("switchsd_test_"):
             getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
     return lib
 
@@ -250,6 +252,11 @@ def switchsd_workspace_status(workspace, B, status, stream=None):
 def withhold_probe_flag_for_tests(on):
     """Test support: force the step's bounded wait for the probe flag to give up."""
     lib.switchsd_test_withhold_probe_flag(1 if on else 0)
+
+
+def withhold_segment_for_tests(on):
+    """Test support: force the fused step's poll of the segment results to give up."""
+    lib.switchsd_test_withhold_segment(1 if on else 0)
 
 
 def switchsd_tree_mask(dpar, dn, mask, stream=None):

@@ -22,6 +22,10 @@ constexpr size_t kAlign = 256;
 // never set their flag and the front gives up its wait after a few
 // iterations, so that the give-up path runs with every kernel exiting.
 std::atomic<int> g_withhold_probe_flag{0};
+// Test knob (switchsd_test_withhold_segment): in the fused step, sequence 0's
+// row 0 segment 0 never stores its result and the accept epilogue's poll gives
+// up after a few iterations.
+std::atomic<int> g_withhold_segment{0};
 
 #ifdef SWITCHSD_TIMELINE
 // Timeline build only: the buffer of the next step launches' phase stamps
@@ -90,6 +94,23 @@ int64_t label_table_slots(int32_t Lmax) {
     return t;
 }
 
+// Per-segment row maxima of the fused step (R <= 64 only): R * kMaxSegs
+// keys per sequence on whole lines.
+int32_t skey_stride_for(int32_t R) {
+    if (R > 64)
+        return 0;
+    return (int32_t)(((int64_t)R * kMaxSegs + kLineU64 - 1) / kLineU64 * kLineU64);
+}
+
+// Per-tile match slots of a sequence whose context has 2..kMaxPollTiles scan
+// tiles (8 per tile, on whole lines).
+int32_t tslot_stride_for(int32_t Lmax) {
+    const int64_t tiles = Lmax > 0 ? ((int64_t)Lmax + kScanTile - 1) / kScanTile : 0;
+    if (tiles <= 1 || tiles > kMaxPollTiles)
+        return 0;
+    return (int32_t)((tiles * SWITCHSD_MAX_NGRAM + kLineU32 - 1) / kLineU32 * kLineU32);
+}
+
 int32_t rtk_stride_for(int32_t R) {
     return (int32_t)(((int64_t)R + kLineU32 - 1) / kLineU32 * kLineU32);
 }
@@ -117,7 +138,11 @@ Workspace carve(void *ws, int32_t B, int32_t R, int32_t Lmax, int32_t W) {
     w.qkeys = w.keys + (size_t)B * w.key_stride;
     w.rtk = (uint32_t *)(w.qkeys + (size_t)B * w.key_stride);
     w.rtk_stride = rtk_stride_for(R);
-    w.cand = (int32_t *)((char *)w.rtk + (size_t)B * w.rtk_stride * 4);
+    w.skeys = (unsigned long long *)((char *)w.rtk + (size_t)B * w.rtk_stride * 4);
+    w.skey_stride = skey_stride_for(R);
+    w.tslot = (int32_t *)(w.skeys + (size_t)B * w.skey_stride);
+    w.tslot_stride = tslot_stride_for(Lmax);
+    w.cand = w.tslot + (size_t)B * w.tslot_stride;
     w.cand_stride = (int32_t)cand_stride_for(Lmax, W);
     return w;
 }
@@ -144,8 +169,9 @@ int cu_count(int *out) {
 
 // Split each of `rows` logits rows into segments so that the argmax role has
 // about two work-groups per compute unit, each segment at least one 16 KB
-// chunk long.  Sets p.segs and p.seg_elems.
-int set_segments(StepParams &p, int64_t rows, int32_t V) {
+// chunk long and at most seg_cap segments per row.  Sets p.segs and
+// p.seg_elems.
+int set_segments(StepParams &p, int64_t rows, int32_t V, int64_t seg_cap = kMaxSegs) {
     int cus = 0;
     const int rc = cu_count(&cus);
     if (rc)
@@ -155,6 +181,8 @@ int set_segments(StepParams &p, int64_t rows, int32_t V) {
     const int64_t max_segs = nvec / kChunkVecs > 1 ? nvec / kChunkVecs : 1;
     if (segs > max_segs)
         segs = max_segs;
+    if (segs > seg_cap)
+        segs = seg_cap;
     if (segs < 1)
         segs = 1;
     int64_t seg_elems = ((V + segs - 1) / segs + 7) / 8 * 8;
@@ -184,11 +212,13 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
         return 0;
     // per sequence: three 256-byte lines (two tickets, the n-gram slots), the
     // row keys of the target's and of the draft's distribution, the row
-    // tickets of the draw at T > 0 and the candidate lists, each rounded up to
-    // whole lines
+    // tickets of the draw at T > 0, the per-segment row keys of the fused
+    // step, the per-tile match slots and the candidate lists, each rounded up
+    // to whole lines
     const int64_t W = n_cand > SWITCHSD_MAX_CAND ? SWITCHSD_MAX_CAND : n_cand_of(n_cand);
     return (size_t)B * ((size_t)kLineU32 * 4 * 3 + (size_t)key_stride_for(R) * 8 * 2 +
-                        (size_t)rtk_stride_for(R) * 4 +
+                        (size_t)rtk_stride_for(R) * 4 + (size_t)skey_stride_for(R) * 8 +
+                        (size_t)tslot_stride_for(Lmax) * 4 +
                         (size_t)cand_stride_for(Lmax, (int32_t)W) * 4);
 }
 
@@ -609,7 +639,8 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     if ((rc = check_workspace(workspace, workspace_bytes, B, R, a->Lmax, p.W)))
         return rc;
     p.withhold_flag = g_withhold_probe_flag.load() ? 1 : 0;
-    p.spin_cap = p.withhold_flag ? 256 : (1 << 22);
+    p.withhold_seg = g_withhold_segment.load() ? 1 : 0;
+    p.spin_cap = p.withhold_flag || p.withhold_seg ? 256 : (1 << 22);
 #ifdef SWITCHSD_TIMELINE
     p.tl = g_timeline.load();
 #endif
@@ -666,13 +697,22 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     }
     p.epi_front = EPI_SELECT;
     p.exp_front = (uint32_t)p.scan_tiles;
+    // One waiting work-group per sequence (the last scan tile) and at most one
+    // per compute unit; every other work-group of the grid runs to completion
+    // without waiting.
+    int cus = 0;
+    if ((rc = cu_count(&cus)))
+        return rc;
+    p.poll_front = p.W == 1 && p.ws.tslot_stride > 0 && B <= cus ? 1 : 0;
 
     const int64_t cn = copy_nodes(&a->cfg);
     int mode = a->mode;
     if (mode == SWITCHSD_MODE_AUTO)  // short drafts that may use every row: one launch
         mode = cn >= R && R <= 64 ? SWITCHSD_MODE_FUSED : SWITCHSD_MODE_SPLIT;
     if (mode == SWITCHSD_MODE_FUSED) {
-        if ((rc = set_segments(p, (int64_t)B * R, V)))
+        // the accept epilogue polls at most kMaxPollSlots segment results
+        const int64_t cap = kMaxPollSlots / R < kMaxSegs ? kMaxPollSlots / R : kMaxSegs;
+        if ((rc = set_segments(p, (int64_t)B * R, V, cap < 1 ? 1 : cap)))
             return rc;
         const int64_t grid = p.n_front_wg + (int64_t)B * R * p.segs;
         if (!grid_ok(grid))
@@ -680,6 +720,13 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         p.rows_mode = cn >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;
         p.epi_accept = sampled ? 0 : 1;
         p.exp_all = p.exp_front + (uint32_t)(R * p.segs);
+        // The accept epilogue polls the segment slots from the front's
+        // work-group when at most one such waiting work-group per compute
+        // unit exists: every other work-group of the grid runs to completion
+        // without waiting, so the waiting ones cannot hold every slot the
+        // argmax work-groups need.
+        p.poll_accept =
+            !sampled && R <= 64 && (int64_t)R * p.segs <= kMaxPollSlots && B <= cus ? 1 : 0;
         if ((rc = launch_step_kernel(p, grid, stream)) || !sampled)
             return rc;
         return sample_finish(p, &sa, true, stream);
@@ -767,6 +814,8 @@ int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B
 }
 
 void switchsd_test_withhold_probe_flag(int32_t on) { g_withhold_probe_flag.store(on ? 1 : 0); }
+
+void switchsd_test_withhold_segment(int32_t on) { g_withhold_segment.store(on ? 1 : 0); }
 
 #ifdef SWITCHSD_TIMELINE
 // Timeline build only (not part of the product library's interface): phase

@@ -25,6 +25,14 @@ constexpr int kLineU32 = 64;
 constexpr int kLineU64 = 32;
 // Copy candidates per sequence, at most.
 constexpr int kMaxCand = SWITCHSD_MAX_CAND;
+// Argmax segments per logits row, at most (the fused step's per-segment
+// result slots hold R * kMaxSegs keys per sequence).
+constexpr int kMaxSegs = 16;
+// Workspace slots one poll of wave 0 covers, at most (8 per lane).
+constexpr int kMaxPollSlots = 512;
+// Scan tiles per sequence, at most, for which the last tile polls per-tile
+// match slots instead of an arrival (the other tiles' 8 slots each).
+constexpr int kMaxPollTiles = kMaxPollSlots / 8;
 
 enum : int32_t { EPI_NONE = 0, EPI_MATCH = 1, EPI_SELECT = 2 };
 enum : int32_t {
@@ -53,6 +61,15 @@ struct Workspace {
     int32_t cand_stride;       // int32 per sequence (whole 256-byte lines)
     unsigned long long *qkeys; // [B] x key_stride: row maxima of the draft's distribution q
                                // (between keys and rtk)
+    unsigned long long *skeys; // [B] x skey_stride: the fused step's per-segment row maxima,
+                               // segment s of row r at s * R + r (0: not yet written,
+                               // 1: the segment has no candidate); between rtk and cand
+    int32_t skey_stride;       // u64 per sequence (R * kMaxSegs on whole lines; 0 if R > 64)
+    int32_t *tslot;            // [B] x tslot_stride: per scan tile t and n-gram length j at
+                               // t * 8 + j, the tile's most recent end + 2 (1: none, 0: not
+                               // yet written); between skeys and cand
+    int32_t tslot_stride;      // int32 per sequence (tiles * 8 on whole lines; 0 unless
+                               // 1 < tiles <= kMaxPollTiles)
 };
 
 struct StepParams {
@@ -98,6 +115,13 @@ struct StepParams {
     int32_t speculate;   // 1: issue a row's first chunk before reading whether it is needed
     int32_t epi_front;
     int32_t epi_accept;
+    int32_t poll_accept; // 1 (fused step, R <= 64): each argmax work-group stores its result
+                         // in its own slot and the sequence's front work-group, once the
+                         // draft is chosen, polls the slots and runs the accept epilogue
+                         // (no arrivals at tk_all)
+    int32_t poll_front;  // 1 (the step, one candidate, 1 < scan_tiles <= kMaxPollTiles): each
+                         // scan tile stores its match slots in its own line and the last
+                         // tile polls them (no arrivals at tk_front)
     int32_t list_mode;   // 1: verify only, a fixed grid streaming the chunks of the drafted
                          // rows r < dn[b] (segs = chunks per row)
     // decode loop: the accept epilogue appends to the context (read-write)
@@ -123,10 +147,12 @@ struct StepParams {
     uint32_t *rdec;                   // [B, R] test of row r: 1 accepted, 2 rejected
     unsigned long long *rz;           // [B, R, 2] Zp, Zq of each tested row
     int32_t rsegs;                    // residual work-groups per sequence (4 KB each)
-    // bounded waits: spin limit of the front's wait for the probe flag; with
-    // withhold_flag (a test knob) the probe never sets its flag
+    // bounded waits: spin limit of the front's wait for the probe flag and of
+    // its poll of the segment slots; with withhold_flag (a test knob) the
+    // probe never sets its flag
     int32_t spin_cap;
     int32_t withhold_flag;
+    int32_t withhold_seg;  // test knob: sequence 0's row 0 segment 0 never stores its slot
     unsigned long long *tl;  // timeline build only: per work-group phase stamps
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all

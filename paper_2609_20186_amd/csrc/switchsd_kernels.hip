@@ -104,8 +104,12 @@ struct PickShared {  // one row's draw at T > 0
     unsigned long long cw[64 * kWaves];  // the row's weight sums per (chunk, wave)
     int32_t last;                      // this work-group completed the row (row_done)
 };
+struct PollShared {  // the segment results a sequence's accept epilogue polled
+    unsigned long long k[kMaxSegs * 64];
+};
 union Shared {
     ScanShared scan;
+    PollShared poll;
     ArgmaxShared am;
     ProbeShared probe;
     EpiShared epi;
@@ -114,8 +118,10 @@ union Shared {
 
 // Timeline build only (compiled with SWITCHSD_TIMELINE, never in the product
 // library): per work-group stamps of the 100 MHz real-time clock, slot
-// [blk * 8 + i]: 0 start, 1 role done, 2 front done, 3 arrival done,
-// 4 epilogue done (its stores complete), 5 the epilogue's loads returned,
+// [blk * 8 + i]: 0 start, 1 role done, 2 front done, 3 arrival done (with
+// polling: every segment result seen), 4 epilogue done (its stores complete),
+// 5 the epilogue's loads returned (with polling: the accept poll started),
+// 6 poll rounds (accept poll << 32 | tile poll, each + 1),
 // 7 = role << 32 | sequence.
 #ifdef SWITCHSD_TIMELINE
 #define TL_MARK(i)                                                                           \
@@ -128,12 +134,20 @@ union Shared {
         if (threadIdx.x == 0 && p.tl)                                                        \
             p.tl[(int64_t)blockIdx.x * 8 + 7] = (v);                                         \
     } while (0)
+#define TL_ADD(i, v)                                                                         \
+    do {                                                                                     \
+        if (threadIdx.x == 0 && p.tl)                                                        \
+            p.tl[(int64_t)blockIdx.x * 8 + (i)] += (v);                                      \
+    } while (0)
 #else
 #define TL_MARK(i) \
     do {           \
     } while (0)
 #define TL_TAG(v) \
     do {          \
+    } while (0)
+#define TL_ADD(i, v) \
+    do {             \
     } while (0)
 #endif
 
@@ -492,10 +506,12 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
 
 // In the step with several scan tiles per sequence the probe has a
 // work-group of its own, dispatched before every tile (block order), and the
-// last tile waits for this flag before it reads z.  It sits in the last word
-// of the sequence's n-gram slot line (at most 8 n-gram lengths use the line).
-__device__ __forceinline__ uint32_t *probe_flag(const StepParams &p, int b) {
-    return (uint32_t *)&p.ws.mslot[b * kLineU32 + kLineU32 - 1];
+// tile that chooses the draft waits for z here: bit 32 set once z is ready,
+// bits 0..31 its float (one 64-bit word, so that the wait and the value are a
+// single read).  Words 60-61 of the sequence's n-gram slot line (at most 8
+// n-gram lengths use the line).
+__device__ __forceinline__ unsigned long long *probe_zslot(const StepParams &p, int b) {
+    return (unsigned long long *)&p.ws.mslot[b * kLineU32 + kLineU32 - 4];
 }
 
 // Device-side error word of sequence b, next to the probe flag: nonzero when
@@ -517,11 +533,10 @@ __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
     }
     __syncthreads();
     if (tid == 0) {
-        st_f32(&p.z[b], probe_combine(sh.probe.s, sh.probe.c, p.bias));
-        if (p.epi_front == EPI_SELECT && !p.withhold_flag) {  // the step: z is ready
-            __builtin_amdgcn_s_waitcnt(0);
-            st_u32(probe_flag(p, b), 1u);
-        }
+        const float z = probe_combine(sh.probe.s, sh.probe.c, p.bias);
+        st_f32(&p.z[b], z);
+        if (p.epi_front == EPI_SELECT && !p.withhold_flag)  // the step: z for the switch
+            st_u64(probe_zslot(p, b), (1ull << 32) | __float_as_uint(z));
     }
 }
 
@@ -547,6 +562,15 @@ __device__ __forceinline__ bool spec_seq(const StepParams &p, int b) {
     return p.qlogits != nullptr && !(p.spec_copy && ld_i32(&p.spec_copy[b]) != 0);
 }
 
+// Rows a sequence may need in the fused step: every row, or the longer of its
+// neural draft (nnb nodes) and the longest copy draft.
+__device__ __forceinline__ uint32_t rows_of_drafts(const StepParams &p, int nnb) {
+    if (p.rows_mode == ROWS_ALL)
+        return (uint32_t)p.R;
+    const int cn = 1 + p.W * p.k;  // the longest copy draft
+    return (uint32_t)(nnb > cn ? nnb : cn);
+}
+
 __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
     if (p.rows_mode == ROWS_ALL || p.rows_mode == ROWS_LISTED)
         return (uint32_t)p.R;
@@ -554,9 +578,7 @@ __device__ __forceinline__ uint32_t rows_needed(const StepParams &p, int b) {
         return (uint32_t)clampi(ld_i32(&p.dn[b]), 1, p.R);
     if (p.rows_mode == ROWS_Q)  // q at the rows that have a drafted child
         return spec_seq(p, b) ? (uint32_t)(clampi(ld_i32(&p.dn[b]), 1, p.R) - 1) : 0u;
-    const int nnb = clampi(p.nn[b], 1, p.R);
-    const int cn = 1 + p.W * p.k;  // the longest copy draft
-    return (uint32_t)(nnb > cn ? nnb : cn);
+    return rows_of_drafts(p, clampi(p.nn[b], 1, p.R));
 }
 
 // Running argmax of one lane over the 16 KB chunks it reduces, in increasing
@@ -800,9 +822,16 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
                 best = iq;
             }
         }
-        if (best != kNoIdx) {
-            const unsigned long long key =
-                ((unsigned long long)order_key(M) << 32) | (0xFFFFFFFFu - best);
+        const unsigned long long key =
+            best != kNoIdx ? ((unsigned long long)order_key(M) << 32) | (0xFFFFFFFFu - best)
+                           : 0ull;
+        if (p.poll_accept) {
+            // the segment's own slot (1: no candidate); nothing waits for the
+            // store here, the sequence's epilogue polls for it
+            if (!(p.withhold_seg && b == 0 && r == 0 && s == 0))
+                st_u64(&p.ws.skeys[(int64_t)b * p.ws.skey_stride + (int64_t)s * p.R + r],
+                       key ? key : 1ull);
+        } else if (key) {
             atomicMax(&p.ws.keys[(int64_t)b * p.ws.key_stride + r], key);
         }
     }
@@ -810,46 +839,94 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
 
 // ------------------------------------------------------------- epilogues
 
-// Steps 1 and 3 for sequence b in wave 0 once the match (mn, me) is known:
-// copy candidate, switch (Eq. 4 with the kappa gate), chosen draft.  When
-// `have_ct`, ct_in is this lane's copied token (read from LDS by the caller);
-// otherwise it is read from the context here.
-__device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, float zb,
-                             const Prefetch &pre, int ct_in, bool have_ct) {
+// The chosen draft of a sequence as wave 0 of its front holds it (R <= 64):
+// lane i has node i's token and parent (-1 past the draft), every lane the
+// node count, the switch decision and the neural draft's clamped node count
+// (set where the neural draft was read, so that no later use waits for that
+// read again).  With `deferred` the front's outputs are not written yet: the
+// match (mn, me, cl; lane j < k holds copied token ct), the draft, the score z
+// when this work-group computed it (zstore), the clearing of the probe's z
+// word (zclear) and of the tile slots this lane polled (bit q of tclear: slot
+// q * 64 + lane) go out with store_front once the accept epilogue has polled
+// its results, so that its first poll does not also wait for these stores
+// (a wave's loads and stores complete in one count).
+struct DraftRegs {
+    int tok, par, dn, use, nnb;
+    int mn, me, cl, ct;
+    float z;
+    uint32_t tclear;
+    bool deferred, zstore, zclear;
+};
+
+__device__ __forceinline__ unsigned long long *probe_zslot(const StepParams &p, int b);
+
+// Outputs of steps 1 and 3 from dr (wave 0; one candidate, R <= 64, k < 64).
+__device__ void store_front(const StepParams &p, int b, const DraftRegs &dr, bool select) {
     const int lane = threadIdx.x;
-    const int64_t row = (int64_t)b * p.Lmax;
     const int64_t base = (int64_t)b * p.R;
-    const bool select = p.epi_front == EPI_SELECT;
-    const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
     if (lane == 0) {
-        p.match_n[b] = mn;
-        p.match_end[b] = me;
-        p.copy_len[b] = cl;
+        p.match_n[b] = dr.mn;
+        p.match_end[b] = dr.me;
+        p.copy_len[b] = dr.cl;
+        if (dr.zstore)
+            p.z[b] = dr.z;
+        if (dr.zclear)
+            st_u64(probe_zslot(p, b), 0ull);
     }
-    {
-        // lane j holds copied token j (R <= 64, k < 64, one candidate)
-        const int ct = lane < cl ? (have_ct ? ct_in : p.tokens[row + me + 1 + lane]) : -1;
-        if (lane < p.k)
-            p.copy_tokens[(int64_t)b * p.k + lane] = ct;
-        if (select) {
-            const int use = (mn >= p.kappa) && (zb >= p.theta);
-            const int dnb = use ? cl + 1 : pre.nnb;
-            const int ctp = __shfl(ct, lane >= 1 ? lane - 1 : 0);
-            int tok = -1, par = -1;
-            if (lane >= 1 && lane < dnb) {
-                tok = use ? ctp : pre.ntok;
-                par = use ? lane - 1 : pre.npar;
-            }
-            if (lane < p.R) {
-                st_i32(&p.dtok[base + lane], tok);  // read by the accept epilogue of this launch
-                st_i32(&p.dpar[base + lane], par);
-            }
-            if (lane == 0) {
-                st_i32(&p.use_copy[b], use);  // read by the commit of this launch
-                st_i32(&p.dn[b], dnb);
-            }
+    if (dr.tclear) {
+        int32_t *ts = p.ws.tslot + (int64_t)b * p.ws.tslot_stride;
+        for (int q = 0; q < 8; ++q)
+            if ((dr.tclear >> q) & 1u)
+                st_i32(&ts[q * 64 + lane], 0);
+    }
+    if (lane < p.k)
+        p.copy_tokens[(int64_t)b * p.k + lane] = dr.ct;
+    if (select) {
+        if (lane < p.R) {
+            st_i32(&p.dtok[base + lane], dr.tok);  // read by the accept epilogue of this launch
+            st_i32(&p.dpar[base + lane], dr.par);
+        }
+        if (lane == 0) {
+            st_i32(&p.use_copy[b], dr.use);  // read by the commit of this launch
+            st_i32(&p.dn[b], dr.dn);
         }
     }
+}
+
+// Steps 1 and 3 for sequence b in wave 0 once the match (mn, me) is known:
+// copy candidate, switch (Eq. 4 with the kappa gate), chosen draft (also left
+// in dr).  When `have_ct`, ct_in is this lane's copied token (read from LDS
+// by the caller); otherwise it is read from the context here.
+__device__ void front_finish(const StepParams &p, int b, int mn, int me, int L, float zb,
+                             const Prefetch &pre, int ct_in, bool have_ct, DraftRegs &dr) {
+    const int lane = threadIdx.x;
+    const int64_t row = (int64_t)b * p.Lmax;
+    const bool select = p.epi_front == EPI_SELECT;
+    const int cl = mn > 0 ? (p.k < L - 1 - me ? p.k : L - 1 - me) : 0;
+    // lane j holds copied token j (R <= 64, k < 64, one candidate)
+    const int ct = lane < cl ? (have_ct ? ct_in : p.tokens[row + me + 1 + lane]) : -1;
+    dr.mn = mn;
+    dr.me = me;
+    dr.cl = cl;
+    dr.ct = ct;
+    dr.deferred = select && p.poll_accept;
+    if (select) {
+        const int use = (mn >= p.kappa) && (zb >= p.theta);
+        const int dnb = use ? cl + 1 : pre.nnb;
+        const int ctp = __shfl(ct, lane >= 1 ? lane - 1 : 0);
+        int tok = -1, par = -1;
+        if (lane >= 1 && lane < dnb) {
+            tok = use ? ctp : pre.ntok;
+            par = use ? lane - 1 : pre.npar;
+        }
+        dr.tok = tok;
+        dr.par = par;
+        dr.dn = dnb;
+        dr.use = use;
+        dr.nnb = pre.nnb;
+    }
+    if (!dr.deferred)
+        store_front(p, b, dr, select);
 }
 
 // First length (in the configured order) whose slot holds an occurrence:
@@ -916,9 +993,10 @@ __device__ int chain_layout(const StepParams &p, int cl, ChainShared &ch) {
 // Wave 0: writes the chosen draft of sequence b (Eq. 4 with the kappa gate);
 // a copy draft is the chains laid out in ch, token j of candidate c being
 // src(c, j); the neural draft has nnb nodes, node i given by nsrc(i, tok, par).
+// Nodes 0..63 are also left in dr.
 template <typename Src, typename NSrc>
 __device__ void write_chains(const StepParams &p, int b, int use, int total, int nnb,
-                             const ChainShared &ch, Src src, NSrc nsrc) {
+                             const ChainShared &ch, Src src, NSrc nsrc, DraftRegs &dr) {
     const int lane = threadIdx.x;
     const int64_t base = (int64_t)b * p.R;
     const int dnb = use ? total : nnb;
@@ -927,6 +1005,7 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total, int
 #pragma unroll
     for (int q = 0; q < kMaxCand; ++q)
         stq[q] = q < p.W ? ch.st[q] : 0x7FFFFFFF;
+    dr = DraftRegs{-1, -1, dnb, use, nnb, 0, -1, 0, -1, 0.0f, 0u, false, false, false};
     for (int i = lane; i < p.R; i += 64) {
         int tok = -1, par = -1;
         if (i >= 1 && i < dnb) {
@@ -946,6 +1025,10 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total, int
         }
         st_i32(&p.dtok[base + i], tok);  // read by the accept epilogue of the same launch
         st_i32(&p.dpar[base + i], par);
+        if (i == lane) {
+            dr.tok = tok;
+            dr.par = par;
+        }
     }
     if (lane == 0) {
         st_i32(&p.use_copy[b], use);  // read by the commit of this launch
@@ -958,7 +1041,8 @@ __device__ void write_chains(const StepParams &p, int b, int use, int total, int
 // [lo, hi) are read from this work-group's LDS tile (index = position - t0 +
 // 64), the others from memory; the neural draft was staged in LDS.
 __device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L, float zb,
-                               const Prefetch &pre, Shared &sh, int t0, int lo, int hi) {
+                               const Prefetch &pre, Shared &sh, int t0, int lo, int hi,
+                               DraftRegs &dr) {
     const int lane = threadIdx.x;
     const int W = p.W;
     const int64_t row = (int64_t)b * p.Lmax;
@@ -985,7 +1069,8 @@ __device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L,
             v4[q] = -1;
             if (idx < ntk && j < ch.cl[c]) {
                 const int pos = ch.e[c] + 1 + j;
-                v4[q] = (pos >= lo && pos < hi) ? sh.scan.tile[pos - t0 + 64] : p.tokens[row + pos];
+                v4[q] = (pos >= lo && pos < hi) ? sh.scan.tile[pos - t0 + 64]
+                                                : ld_i32(&p.tokens[row + pos]);  // as in front_remote
             }
         }
 #pragma unroll
@@ -1003,48 +1088,52 @@ __device__ void front_finish_w(const StepParams &p, int b, int mn, int v, int L,
                      [&](int i, int &tok, int &par) {
                          tok = sh.scan.nt[i];
                          par = sh.scan.np[i];
-                     });
+                     },
+                     dr);
 }
 
 // A context held by one scan tile: everything the switch needs is already in
 // this work-group (match in LDS, probe partial sums in LDS, the copy
 // candidate in the LDS tile, the neural draft prefetched).  No arrival.
-__device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefetch &pre) {
+__device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefetch &pre,
+                            DraftRegs &dr) {
     const int lane = threadIdx.x;
     const int32_t s = lane < p.n_ngram ? sh.scan.red[lane] : 0;
     int mn, me, jsel;
     pick_match(p, s, mn, me, jsel);
     const int L = sh.scan.L;
     float zb = 0.0f;
+    const bool defer = p.epi_front == EPI_SELECT && p.poll_accept && !general_select(p);
     if (p.scan_probe) {
         float z0 = 0.0f;
         if (lane == 0) {
             z0 = probe_combine(sh.scan.ps, sh.scan.pc, p.bias);
-            p.z[b] = z0;
+            if (!defer)
+                p.z[b] = z0;
         }
         zb = __shfl(z0, 0);
+        dr.z = zb;
+        dr.zstore = defer;
     }
     if (general_select(p)) {
         const int v = mn <= 0 ? 0 : (p.W > 1 ? merge_waves(p, sh, jsel) : (lane == 0 ? me + 1 : 0));
         front_finish_w(p, b, mn, v, L, zb, pre, sh, 0, 0,
-                       p.Lmax < kScanTile ? p.Lmax : kScanTile);
+                       p.Lmax < kScanTile ? p.Lmax : kScanTile, dr);
         return;
     }
     const int pos = me + 1 + lane;  // tile index = position + 64 (tile 0)
     const int ct = (mn > 0 && lane < p.k && pos < L) ? sh.scan.tile[pos + 64] : -1;
-    front_finish(p, b, mn, me, L, zb, pre, ct, true);
+    front_finish(p, b, mn, me, L, zb, pre, ct, true, dr);
 }
 
-// Last arriving scan tile of a longer context: the other tiles' results come
-// from the workspace; the copy candidate from this tile's LDS when it lies
-// there, else from the context.
-__device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, const Prefetch &pre) {
+// The scan tile that chooses the draft of a longer context, once every tile's
+// result is in: s is lane j's n-gram slot value over all tiles (end + 1 of
+// the most recent occurrence of length j, 0 none), zs a first read of the
+// probe's z word (the step).  The copy candidate comes from this tile's LDS
+// when it lies there, else from the context.
+__device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, const Prefetch &pre,
+                             DraftRegs &dr, int32_t s, unsigned long long zs) {
     const int lane = threadIdx.x;
-    int32_t s = 0;
-    if (lane < p.n_ngram) {
-        s = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
-        st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
-    }
     int mn, me, jsel;
     pick_match(p, s, mn, me, jsel);
     const int L = sh.scan.L;
@@ -1059,35 +1148,43 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
         const int lo = t0 - 64 > 0 ? t0 - 64 : 0;
         const int hi = t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax;
         in_tile = cl1 > 0 && me + 1 >= lo && me + cl1 < hi;
+        // (the context read is an atomic one, so that the compiler cannot
+        // merge the two reads into one through a generic pointer: such a
+        // read is counted as both an LDS and a memory access, and every
+        // later wait for it would also wait for all of this wave's stores)
         if (lane < cl1)
             ct1 = in_tile ? sh.scan.tile[me + 1 + lane - t0 + 64]
-                          : p.tokens[(int64_t)b * p.Lmax + me + 1 + lane];
+                          : ld_i32(&p.tokens[(int64_t)b * p.Lmax + me + 1 + lane]);
     }
     float zb = 0.0f;
     if (p.epi_front == EPI_SELECT) {
         if (p.probe_on) {
             // the probe's work-group was dispatched before every tile and
-            // depends on nothing, so the flag is set in bounded time; the cap
-            // only guards against a broken launch.  If it is reached, the
+            // depends on nothing, so z is ready in bounded time; the cap only
+            // guards against a broken launch.  If it is reached, the
             // sequence's error word is set and the switch takes the neural
             // draft (a NaN score never clears the threshold).
-            uint32_t *fl = probe_flag(p, b);
-            bool seen = false;
-            for (int spin = 0; spin < p.spin_cap && !seen; ++spin) {
-                seen = __builtin_amdgcn_readfirstlane((int)__hip_atomic_load(
-                           fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) != 0;
-                if (!seen)
-                    __builtin_amdgcn_s_sleep(2);
+            unsigned long long *zp = probe_zslot(p, b);
+            uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(zs >> 32));
+            uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)zs);
+            for (int spin = 0; hi == 0u && spin < p.spin_cap; ++spin) {
+                __builtin_amdgcn_s_sleep(2);
+                const unsigned long long v = ld_u64(zp);
+                hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+                lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
             }
-            if (seen) {
-                zb = ld_f32(&p.z[b]);
+            if (hi != 0u) {
+                zb = __uint_as_float(lo);
             } else {
                 zb = __builtin_nanf("");
                 if (lane == 0)
                     st_u32(error_word(p, b), 1u);
             }
-            if (lane == 0)
-                st_u32(fl, 0u);
+            // with the accept epilogue polling, the clearing goes out after its
+            // poll (store_front)
+            dr.zclear = p.poll_accept && !general_select(p);
+            if (lane == 0 && !dr.zclear)
+                st_u64(zp, 0ull);
         } else {
             zb = ld_f32(&p.z[b]);
         }
@@ -1117,19 +1214,243 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
         }
         const int v = lane < W ? sh.scan.merged[lane] : 0;
         front_finish_w(p, b, mn, v, L, zb, pre, sh, t0, t0 - 64 > 0 ? t0 - 64 : 0,
-                       t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax);
-        if (lane == 0)
+                       t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax, dr);
+        if (lane == 0 && !p.poll_front)
             st_u32(&p.ws.tk_front[b * kLineU32], 0u);
         return;
     }
     (void)in_tile;
-    front_finish(p, b, mn, me, L, zb, pre, ct1, true);
-    if (lane == 0)
+    front_finish(p, b, mn, me, L, zb, pre, ct1, true, dr);
+    if (lane == 0 && !p.poll_front)
         st_u32(&p.ws.tk_front[b * kLineU32], 0u);
+}
+
+// ------------------------------------------------------------- polling
+
+__device__ __forceinline__ unsigned long long ld_slot(const unsigned long long *p) {
+    return ld_u64(p);
+}
+__device__ __forceinline__ int32_t ld_slot(const int32_t *p) { return ld_i32(p); }
+
+// Wave 0 polls workspace slots base[q * 64 + lane] (q < kQ) for the ones it
+// waits for (bit q of want(), evaluated once the first round of requests is
+// out, so that whatever it waits for overlaps with that round) until each
+// holds a nonzero value, one round of requests at a time, each issued as soon
+// as the previous one returned.  Every request is issued unconditionally
+// (slots past n re-read slot n - 1): one load instruction per q and round,
+// with no branch around it.  (Measured: keeping a second round in flight, or
+// pausing between rounds, gains nothing and the former slows the step.)
+// got[q] gets each slot's first nonzero value, 0 if `cap` rounds pass first
+// (returns false then); rounds is the number of rounds after the first.
+// on_miss() runs once, when the first round did not find every value.
+template <typename T, int kQ, typename Want, typename Miss>
+__device__ bool poll_slots(const T *base, int n, Want want, T (&got)[kQ], int cap, int &rounds,
+                           Miss on_miss) {
+    const int lane = threadIdx.x;
+    T v[kQ];
+    auto issue = [&]() {
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+            const int i = q * 64 + lane;
+            v[q] = ld_slot(base + (i < n ? i : n - 1));
+        }
+    };
+    issue();
+    uint32_t pend = want();
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+        got[q] = 0;
+    for (int spin = 0;; ++spin) {
+        rounds = spin;
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+            const bool hit = ((pend >> q) & 1u) != 0u && v[q] != 0;
+            got[q] = hit ? v[q] : got[q];
+            pend = hit ? pend & ~(1u << q) : pend;
+        }
+        if (__ballot(pend != 0u) == 0ull)
+            return true;
+        if (spin >= cap)
+            return false;
+        issue();
+        if (spin == 0)
+            on_miss();
+    }
+}
+
+// poll_slots over n <= kMaxPollSlots slots with as few requests per lane as n
+// allows; got[q] past them is 0.
+template <typename T, typename Want, typename Miss>
+__device__ bool poll_wave(const T *base, int n, Want want, T (&got)[8], int cap, int &rounds,
+                          Miss on_miss) {
+    if (n > 256)
+        return poll_slots<T, 8>(base, n, want, got, cap, rounds, on_miss);
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+        got[q] = 0;
+    bool ok;
+    if (n <= 64) {
+        T g[1];
+        ok = poll_slots<T, 1>(base, n, want, g, cap, rounds, on_miss);
+        got[0] = g[0];
+    } else {
+        T g[4];
+        ok = poll_slots<T, 4>(base, n, want, g, cap, rounds, on_miss);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            got[q] = g[q];
+    }
+    return ok;
+}
+
+// The last scan tile of sequence b when the tiles hand over through per-tile
+// slots (poll_front): polls the other tiles' slots (tile t's length j at
+// t * 8 + j, read by lane (t * 8 + j) mod 64, so lane j mod 8 always reads
+// length j) until each holds its value, zeroes them again (at once, or with
+// the front's outputs: DraftRegs), and folds them with this tile's own
+// result; lane j < n_ngram gets the slot value of length j over all tiles.  The other tiles wait for nothing, so every slot is
+// written in bounded time; the cap guards a broken launch, and on reaching it
+// the sequence's error word is set and the missing tiles count as holding no
+// occurrence.
+__device__ int32_t poll_tiles(const StepParams &p, int b, const Shared &sh, DraftRegs &dr) {
+    const int lane = threadIdx.x;
+    const int n = (p.scan_tiles - 1) * SWITCHSD_MAX_NGRAM;  // <= kMaxPollSlots
+    int32_t *ts = p.ws.tslot + (int64_t)b * p.ws.tslot_stride;
+    const int j = lane & (SWITCHSD_MAX_NGRAM - 1);
+    auto want = [&]() {  // bit q: slot q * 64 + lane is awaited
+        uint32_t w = 0;
+        for (int q = 0; q * 64 < n; ++q)
+            if (q * 64 + lane < n && j < p.n_ngram)
+                w |= 1u << q;
+        return w;
+    };
+    int32_t got[8];
+    int rounds = 0;
+    if (!poll_wave(ts, n, want, got, p.spin_cap, rounds, [] {}) && lane == 0)
+        st_u32(error_word(p, b), 1u);  // gave up: missing tiles hold no occurrence
+    TL_ADD(6, (unsigned long long)(rounds + 1));
+    int32_t best = 0;
+    uint32_t seen = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+        if (got[q]) {
+            best = got[q] - 1 > best ? got[q] - 1 : best;
+            seen |= 1u << q;
+        }
+    // the slots are zeroed again now, or with the front's outputs after the
+    // accept epilogue's poll (store_front)
+    if (p.poll_accept && !general_select(p))
+        dr.tclear = seen;
+    else
+        for (int q = 0; q < 8; ++q)
+            if ((seen >> q) & 1u)
+                st_i32(&ts[q * 64 + lane], 0);
+#pragma unroll
+    for (int o = SWITCHSD_MAX_NGRAM; o < 64; o <<= 1) {
+        const int32_t y = __shfl_xor(best, o);
+        best = y > best ? y : best;
+    }
+    if (lane < p.n_ngram) {
+        const int32_t own = sh.scan.red[lane];
+        return own > best ? own : best;
+    }
+    return 0;
 }
 
 __device__ __forceinline__ int32_t decode_key(unsigned long long key) {
     return key ? (int32_t)(0xFFFFFFFFu - (uint32_t)key) : 0;
+}
+
+// Accept and bonus of sequence b with R <= 64 nodes (Sec. 3.3, verification;
+// tree drafts App. D), node i in lane i: its row maximum `key` (packed; 0
+// none), its drafted token and parent, and the raw node count dn_raw.  Writes
+// amax, out_tokens, accept_len, accept_node and bonus, and with kCommit the
+// accepted tokens and the bonus into the context at cL; returns the accepted
+// length (uniform over the wave).
+template <bool kCommit>
+__device__ int accept_lanes(const StepParams &p, int b, unsigned long long key, int tok, int par,
+                            int dn_raw, int cL) {
+    const int i = threadIdx.x;
+    const int64_t base = (int64_t)b * p.R;
+    const int64_t crow = (int64_t)b * p.Lmax;
+    // output position j of the accepted path (then the bonus) holds v
+    auto emit = [&](int j, int v) {
+        p.out_tokens[base + j] = v;
+        if (kCommit && cL + j < p.Lmax)
+            p.ctok[crow + cL + j] = v;
+    };
+    const int dnb = clampi(dn_raw, 1, p.R);
+    int a = -1;
+    if (i < p.R) {
+        if (i < dnb)
+            a = decode_key(key);
+        if (p.amax)
+            p.amax[base + i] = a;
+    }
+    const bool valid = i >= 1 && i < dnb && par >= 0 && par < i;
+    const int anc0 = valid ? par : 0;
+    const int apar = __shfl(a, anc0);
+    int ok = i == 0 ? 1 : (valid && tok == apar ? 1 : 0);
+    int best, depth, dep;
+    unsigned long long onpath;
+    // a chain (every node's parent is the node before it): the accepted
+    // nodes are the prefix before the first rejection
+    const bool chain = __ballot(i >= 1 && i < dnb && par != i - 1) == 0ull;
+    if (chain) {
+        const unsigned long long rej = __ballot(i >= 1 && i < dnb && !ok);
+        depth = rej ? __ffsll((long long)rej) - 2 : dnb - 1;
+        best = depth;
+        dep = i;
+        onpath = depth > 0 ? (((~0ull) >> (64 - depth)) << 1) : 0ull;
+    } else {
+        dep = i == 0 ? 0 : 1;
+        int anc = anc0;
+#pragma unroll
+        for (int round = 0; round < 6; ++round) {  // 2^6 >= 64 levels
+            const int ok2 = __shfl(ok, anc), dep2 = __shfl(dep, anc),
+                      anc2 = __shfl(anc, anc);
+            ok &= ok2;
+            dep += dep2;
+            anc = anc2;
+        }
+        const uint32_t key2 =
+            (ok && i < dnb) ? (((uint32_t)dep << 16) | (0xFFFFu - (uint32_t)i)) : 0u;
+        const uint32_t kbest = wave_max_u32(key2);
+        best = (int)(0xFFFFu - (kbest & 0xFFFFu));
+        depth = (int)(kbest >> 16);
+        onpath = 0ull;
+        int cur = best;
+        for (int s2 = 0; s2 < depth; ++s2) {
+            onpath |= 1ull << cur;
+            cur = __shfl(anc0, cur);
+        }
+    }
+    const int bon = __shfl(a, best);
+    if (i < p.R) {
+        if ((onpath >> i) & 1ull)
+            emit(dep - 1, tok);
+        if (i == depth)
+            emit(i, bon);
+        else if (i > depth)
+            p.out_tokens[base + i] = -1;
+    }
+    if (i == 0) {
+        p.accept_len[b] = depth;
+        p.accept_node[b] = best;
+        p.bonus[b] = bon;
+    }
+    return depth;
+}
+
+// Decode loop: the context's new length and the draft model's position after
+// a step that accepted acc tokens (lane 0).
+__device__ __forceinline__ void commit_lengths(const StepParams &p, int b, int cL, int cdp,
+                                               int cuc, int acc) {
+    const int Lnew = cL + acc + 1 < p.Lmax ? cL + acc + 1 : p.Lmax;
+    const int pos = clampi(cuc ? cdp : cL + acc, 0, Lnew);
+    p.clen[b] = Lnew;
+    p.draft_pos[b] = pos;
+    p.lag[b] = Lnew - pos;
 }
 
 // kCommit: the decode loop's commit is compiled in.
@@ -1165,73 +1486,13 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
             tok = ld_i32(&p.dtok[base + i]);
             par = p.dpar ? ld_i32(&p.dpar[base + i]) : i - 1;
         }
-        const int dnb = clampi(dn_raw, 1, p.R);
 #ifdef SWITCHSD_TIMELINE
         __builtin_amdgcn_s_waitcnt(0);
 #endif
         TL_MARK(5);
-        int a = -1;
-        if (i < p.R) {
-            if (key)
-                st_u64(&keys[i], 0ull);
-            if (i < dnb)
-                a = decode_key(key);
-            if (p.amax)
-                p.amax[base + i] = a;
-        }
-        const bool valid = i >= 1 && i < dnb && par >= 0 && par < i;
-        const int anc0 = valid ? par : 0;
-        const int apar = __shfl(a, anc0);
-        int ok = i == 0 ? 1 : (valid && tok == apar ? 1 : 0);
-        int best, depth, dep;
-        unsigned long long onpath;
-        // a chain (every node's parent is the node before it): the accepted
-        // nodes are the prefix before the first rejection
-        const bool chain = __ballot(i >= 1 && i < dnb && par != i - 1) == 0ull;
-        if (chain) {
-            const unsigned long long rej = __ballot(i >= 1 && i < dnb && !ok);
-            depth = rej ? __ffsll((long long)rej) - 2 : dnb - 1;
-            best = depth;
-            dep = i;
-            onpath = depth > 0 ? (((~0ull) >> (64 - depth)) << 1) : 0ull;
-        } else {
-            dep = i == 0 ? 0 : 1;
-            int anc = anc0;
-#pragma unroll
-            for (int round = 0; round < 6; ++round) {  // 2^6 >= 64 levels
-                const int ok2 = __shfl(ok, anc), dep2 = __shfl(dep, anc),
-                          anc2 = __shfl(anc, anc);
-                ok &= ok2;
-                dep += dep2;
-                anc = anc2;
-            }
-            const uint32_t key2 =
-                (ok && i < dnb) ? (((uint32_t)dep << 16) | (0xFFFFu - (uint32_t)i)) : 0u;
-            const uint32_t kbest = wave_max_u32(key2);
-            best = (int)(0xFFFFu - (kbest & 0xFFFFu));
-            depth = (int)(kbest >> 16);
-            onpath = 0ull;
-            int cur = best;
-            for (int s2 = 0; s2 < depth; ++s2) {
-                onpath |= 1ull << cur;
-                cur = __shfl(anc0, cur);
-            }
-        }
-        const int bon = __shfl(a, best);
-        if (i < p.R) {
-            if ((onpath >> i) & 1ull)
-                emit(dep - 1, tok);
-            if (i == depth)
-                emit(i, bon);
-            else if (i > depth)
-                p.out_tokens[base + i] = -1;
-        }
-        if (lane == 0) {
-            p.accept_len[b] = depth;
-            p.accept_node[b] = best;
-            p.bonus[b] = bon;
-        }
-        acc = depth;
+        if (i < p.R && key)
+            st_u64(&keys[i], 0ull);
+        acc = accept_lanes<kCommit>(p, b, key, tok, par, dn_raw, cL);
     } else {
         const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
         // the draft and the row maxima into LDS, 256 nodes at a time with all
@@ -1396,15 +1657,86 @@ __device__ void final_epilogue(const StepParams &p, int b, Shared &sh) {
         }
         acc = depth;
     }
-    if (kCommit && lane == 0) {
-        const int Lnew = cL + acc + 1 < p.Lmax ? cL + acc + 1 : p.Lmax;
-        const int pos = clampi(cuc ? cdp : cL + acc, 0, Lnew);
-        p.clen[b] = Lnew;
-        p.draft_pos[b] = pos;
-        p.lag[b] = Lnew - pos;
-    }
+    if (kCommit && lane == 0)
+        commit_lengths(p, b, cL, cdp, cuc, acc);
     if (lane == 0)
         st_u32(&p.ws.tk_all[b * kLineU32], 0u);
+}
+
+// Row maxima of sequence b in the fused step with per-segment slots (wave 0
+// of the work-group that chose the draft; R <= 64, R * segs <= kMaxPollSlots):
+// lane r gets the maximum over the segments of row r (0: no candidate, or a
+// row that is not verified).  Slot j = s * R + r is read by lane j mod 64;
+// every slot of a needed row is polled until it holds its segment's result
+// (nonzero), then zeroed again.  The argmax work-groups wait for nothing, so the results
+// arrive in bounded time; the cap guards a broken launch, and on reaching it
+// the sequence's error word is set and the missing results count as none.
+template <typename Miss>
+__device__ unsigned long long poll_rows(const StepParams &p, int b, int nnb, Shared &sh,
+                                        Miss on_miss) {
+    const int lane = threadIdx.x;
+    const int R = p.R, n = R * p.segs;  // <= kMaxPollSlots
+    unsigned long long *sk = p.ws.skeys + (int64_t)b * p.ws.skey_stride;
+    unsigned long long *lk = sh.poll.k;
+    TL_MARK(5);
+    int need = 0;
+    uint32_t want = 0;
+    auto wantf = [&]() {  // bit q: slot q * 64 + lane is awaited
+        need = (int)rows_of_drafts(p, nnb);  // as rows_needed, nn[b] already read
+        want = 0;
+        for (int q = 0, r = lane % R; q * 64 < n; ++q, r = (r + 64) % R)
+            if (q * 64 + lane < n && r < need)
+                want |= 1u << q;
+        return want;
+    };
+    unsigned long long got[8];
+    int rounds = 0;
+    if (!poll_wave(sk, n, wantf, got, p.spin_cap, rounds, on_miss) && lane == 0)
+        st_u32(error_word(p, b), 1u);  // gave up: missing segments hold no maximum
+    TL_ADD(6, (unsigned long long)(rounds + 1) << 32);
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+        if ((want >> q) & 1u) {
+            lk[q * 64 + lane] = got[q];
+            if (got[q])
+                st_u64(&sk[q * 64 + lane], 0ull);
+        }
+    __builtin_amdgcn_wave_barrier();
+    unsigned long long key = 0ull;
+    if (lane < need)
+        for (int sg = 0; sg < p.segs; ++sg) {
+            const unsigned long long v = lk[sg * R + lane];
+            key = v > key ? v : key;
+        }
+    return key > 1ull ? key : 0ull;
+}
+
+// The fused step's accept epilogue from the work-group that chose the draft
+// (still in registers, dr): polls the segment results, then accept, bonus and
+// the decode loop's commit as in final_epilogue.
+template <bool kCommit>
+__device__ void poll_epilogue(const StepParams &p, int b, const DraftRegs &dr, Shared &sh) {
+    int cL = 0, cdp = 0;
+    if (kCommit) {
+        cL = clampi(p.clen[b], 0, p.Lmax);
+        cdp = p.draft_pos[b];
+    }
+    // the front's deferred outputs go out once the first poll round has
+    // returned without every result (they then complete while the poll goes
+    // on), else with the accept's outputs
+    bool stored = !dr.deferred;
+    const unsigned long long key = poll_rows(p, b, dr.nnb, sh, [&] {
+        if (!stored) {
+            store_front(p, b, dr, true);
+            stored = true;
+        }
+    });
+    TL_MARK(3);
+    if (!stored)
+        store_front(p, b, dr, true);
+    const int acc = accept_lanes<kCommit>(p, b, key, dr.tok, dr.par, dr.dn, cL);
+    if (kCommit && threadIdx.x == 0)
+        commit_lengths(p, b, cL, cdp, dr.use, acc);
 }
 
 // ------------------------------------------------------------- streamed verify
@@ -2509,30 +2841,73 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     if (threadIdx.x >= 64)
         return;  // waves 1.. are done; wave 0 arrives and may run an epilogue
     if (role == 0 && p.epi_front != EPI_NONE) {
+        // The scan's reads, the prefetched neural draft included, returned
+        // long ago; an explicit wait for them here costs nothing and keeps the
+        // compiler's count of outstanding reads exact through the branches
+        // below (otherwise a use of the prefetched values after them waits for
+        // every store of the front as well).
+        __builtin_amdgcn_s_waitcnt(0);
+        DraftRegs dr = {-1, -1, 1, 0, 1, 0, -1, 0, -1, 0.0f, 0u, false, false, false};
+        bool chose = false;  // this work-group chose sequence b's draft
         if (p.scan_tiles == 1) {
-            front_local(p, b, sh, pre);
+            front_local(p, b, sh, pre, dr);
+            chose = true;
             TL_MARK(2);
         } else {
             const int lane = threadIdx.x;
-            if (lane < p.n_ngram && sh.scan.red[lane] > 0)
-                atomicMax(&p.ws.mslot[b * kLineU32 + lane], sh.scan.red[lane]);
+            const bool zread = p.epi_front == EPI_SELECT && p.probe_on;
             if (t == 0 && p.scan_probe && lane == 0)
                 st_f32(&p.z[b], probe_combine(sh.scan.ps, sh.scan.pc, p.bias));
-            if (kMulti && p.W > 1) {
-                int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride +
-                              (int64_t)t * SWITCHSD_MAX_NGRAM * p.W;
-                for (int j = 0; j < p.n_ngram; ++j) {
-                    const int v = merge_waves(p, sh, j);
-                    if (lane < p.W)
-                        st_i32(&cb[j * p.W + lane], v);
+            if (p.poll_front) {
+                if (t + 1 < p.scan_tiles) {
+                    // this tile's result in its own slots; nothing waits here
+                    if (lane < p.n_ngram)
+                        st_i32(&p.ws.tslot[(int64_t)b * p.ws.tslot_stride +
+                                           t * SWITCHSD_MAX_NGRAM + lane],
+                               sh.scan.red[lane] + 1);
+                } else {
+                    const unsigned long long zs = zread ? ld_u64(probe_zslot(p, b)) : 0ull;
+                    const int32_t sl = poll_tiles(p, b, sh, dr);
+                    front_remote(p, b, t, sh, pre, dr, sl, zs);
+                    chose = true;
+                    TL_MARK(2);
+                }
+            } else {
+                if (lane < p.n_ngram && sh.scan.red[lane] > 0)
+                    atomicMax(&p.ws.mslot[b * kLineU32 + lane], sh.scan.red[lane]);
+                if (kMulti && p.W > 1) {
+                    int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride +
+                                  (int64_t)t * SWITCHSD_MAX_NGRAM * p.W;
+                    for (int j = 0; j < p.n_ngram; ++j) {
+                        const int v = merge_waves(p, sh, j);
+                        if (lane < p.W)
+                            st_i32(&cb[j * p.W + lane], v);
+                    }
+                }
+                if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front)) {
+                    // the tiles' results and the probe's z, requested together
+                    const unsigned long long zs = zread ? ld_u64(probe_zslot(p, b)) : 0ull;
+                    int32_t sl = 0;
+                    if (lane < p.n_ngram) {
+                        sl = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
+                        st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
+                    }
+                    front_remote(p, b, t, sh, pre, dr, sl, zs);
+                    chose = true;
+                    TL_MARK(2);
                 }
             }
-            if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front)) {
-                front_remote(p, b, t, sh, pre);
-                TL_MARK(2);
-            }
+        }
+        if (p.poll_accept && chose) {
+            poll_epilogue<kCommit>(p, b, dr, sh);
+#ifdef SWITCHSD_TIMELINE
+            __builtin_amdgcn_s_waitcnt(0);
+#endif
+            TL_MARK(4);
         }
     }
+    if (p.poll_accept)
+        return;  // an argmax work-group's slot is its only hand-off
     if (p.epi_accept && role != 1) {
         const bool last = arrive(&p.ws.tk_all[b * kLineU32], p.exp_all);
         TL_MARK(3);
@@ -2595,12 +2970,14 @@ __global__ __launch_bounds__(64) void k_select(StepParams p) {
     const int use = (p.match_n_in[b] >= p.kappa) && (p.z_in[b] >= p.theta);
     const int32_t *ct = p.copy_tokens_in + (int64_t)b * p.W * p.k;
     const int64_t base = (int64_t)b * p.R;
+    DraftRegs dr;
     write_chains(p, b, use, total, clampi(p.nn[b], 1, p.R), ch,
                  [&](int c, int j) { return ct[c * p.k + j]; },
                  [&](int i, int &tok, int &par) {
                      tok = p.ntok[base + i];
                      par = p.npar ? p.npar[base + i] : i - 1;
-                 });
+                 },
+                 dr);
 }
 
 // One work-group of 256 (row, word) cells of sequence b's ancestor mask;

@@ -8,7 +8,9 @@ clock at the end of each phase -- over rotated copies of the workload's inputs
 (more than 512 MB between two uses of one copy), and prints, as the median
 over the launches, when each phase ends relative to the first work-group's
 start: the scan tiles, the front (match, probe, switch, draft), the argmax
-row segments, the sequences' last arrivals and the accept epilogues.  The
+row segments, the sequences' last arrivals (or, where the epilogue polls the
+segment results, when it has seen all of them, and how many poll rounds that
+took) and the accept epilogues.  The
 stamps cost a few stores per work-group.
 """
 import argparse
@@ -66,11 +68,24 @@ def analyse(st, B_):
                              if (ar & (seq == b)).any()])
         out["sequence's last arrival (median)"] = _q(last_arr, 0.5)
         out["sequence's last arrival (last)"] = last_arr.max()
-    el = st[:, 5] != 0
+    polled = (st[:, 6] >> 32) != 0     # the accept epilogue polled the segment results
+    el = (st[:, 5] != 0) & ~polled
     if el.any():
         v = us(st[el, 5])
         out["accept epilogue's loads returned (median)"] = _q(v, 0.5)
         out["accept epilogue's loads returned (last)"] = v.max()
+    if polled.any():
+        v = us(st[polled, 5])
+        out["accept poll started (median)"] = _q(v, 0.5)
+        out["accept poll started (last)"] = v.max()
+        rounds = (st[polled, 6] >> 32).astype(np.int64) - 1
+        out["accept poll rounds (median)"] = _q(rounds, 0.5)
+        out["accept poll rounds (max)"] = rounds.max()
+    tiles = (st[:, 6] & 0xFFFFFFFF) != 0
+    if tiles.any():
+        rounds = (st[tiles, 6] & 0xFFFFFFFF).astype(np.int64) - 1
+        out["tile poll rounds (median)"] = _q(rounds, 0.5)
+        out["tile poll rounds (max)"] = rounds.max()
     am = role == 2
     if am.any():
         # work-groups are dispatched to the 8 XCDs in turn (block index mod 8)

@@ -38,13 +38,20 @@ def test_status_strings_and_workspace_size():
         assert sd.status_string(s) and sd.status_string(s) != "unknown status"
     assert sd.status_string(17) == "unknown status"
     assert sd.workspace_bytes(32, 8) >= 32 * 8 * 8 + 32 * 8 * 4 + 2 * 32 * 4
+    # per sequence: 3 lines, two key lines, a ticket line, and for R <= 64 the
+    # fused step's per-segment row keys (R * 16 u64)
+    assert sd.workspace_bytes(1, 8) == 3 * 256 + 2 * 256 + 256 + 8 * 16 * 8
+    assert sd.workspace_bytes(1, 65) == 3 * 256 + 2 * 768 + 512
     assert sd.workspace_bytes(64, 8) >= sd.workspace_bytes(32, 8)
     assert sd.workspace_bytes(-1, 8) == 0
     assert sd.workspace_bytes(2, 8, -1, 0) == 0 and sd.workspace_bytes(2, 8, 16, -1) == 0
     # candidate lists only with several candidates over several scan tiles
     # (1024 positions each)
     assert sd.workspace_bytes(2, 8, 1024, 10) == sd.workspace_bytes(2, 8)
-    assert sd.workspace_bytes(2, 8, 1025, 1) == sd.workspace_bytes(2, 8)
+    # per-tile match slots (8 int32 per tile, whole lines) for 2..64 tiles
+    assert sd.workspace_bytes(2, 8, 1025, 1) == sd.workspace_bytes(2, 8) + 2 * 256
+    assert sd.workspace_bytes(2, 8, 64 * 1024, 1) == sd.workspace_bytes(2, 8) + 2 * 2 * 1024
+    assert sd.workspace_bytes(2, 8, 64 * 1024 + 1, 1) == sd.workspace_bytes(2, 8)
     assert sd.workspace_bytes(2, 8, 1025, 10) > sd.workspace_bytes(2, 8)
     extra = sd.workspace_bytes(2, 8, 3 * 1024, 10) - sd.workspace_bytes(2, 8)
     assert extra >= 2 * 3 * 8 * 10 * 4 and extra % 256 == 0
@@ -172,8 +179,8 @@ def test_sample_entry_point_rejects():
         2 * 16 * 16 * 32 + 256 + 256
     assert sd.sample_workspace_bytes(-1, 8, 8) == 0
 
-    def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS, wsn=4096, q=None,
-             ua=None, dpar=P):
+    def call(logits=A16, V=128, T=0.5, uni=P, sw=SW, swn=4096, ws=WS,
+             wsn=sd.workspace_bytes(2, 8), q=None, ua=None, dpar=P):
         return lib.switchsd_verify_sample(logits, 2, 8, V, T, uni, q, ua, P, dpar, P, P, P, P,
                                           P, P, ws, wsn, sw, swn, None)
     for T in (0.0, -0.5, float("nan"), float("inf")):

@@ -55,3 +55,37 @@ def test_probe_wait_give_up_is_reported(mode):
     torch.cuda.synchronize()
     assert int(st.item()) == 0
     assert int(ws.count_nonzero()) == 0
+
+
+def test_segment_poll_give_up_is_reported():
+    """The fused step's accept epilogue polls the argmax segments' result
+    slots; with sequence 0's first segment of row 0 withheld the poll gives up,
+    the status reports it, every other sequence still matches the oracle, and
+    the workspace is left zeroed once the status call has read the error."""
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    say("[errors] withheld segment result, fused step")
+    d = planted_workload("C2")
+    B, R = d["ntok"].shape
+    dev = to_device(d)
+    ws = sd.alloc_workspace(B, R, d["tokens"].shape[1])
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    exp = oracle_step(d)
+    sd.withhold_segment_for_tests(True)
+    try:
+        got, ws = gpu_step(dev, d, FUSED, ws=ws)
+    finally:
+        sd.withhold_segment_for_tests(False)
+    sd.switchsd_workspace_status(ws, B, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == EDEVICE
+    rest = slice(1, None)
+    assert_match(got, {k: v[rest] for k, v in exp.items()}, rows=rest,
+                 what="other sequences while sequence 0 gave up")
+    assert int(ws.count_nonzero()) == 0
+    got, ws = gpu_step(dev, d, FUSED, ws=ws)
+    assert_match(got, exp, what="after the segment give-up")
+    sd.switchsd_workspace_status(ws, B, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert int(ws.count_nonzero()) == 0
