@@ -171,6 +171,9 @@ __device__ __forceinline__ unsigned long long ld_u64(const unsigned long long *p
 __device__ __forceinline__ void st_u64(unsigned long long *p, unsigned long long v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ uint32_t ld_u32(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ void st_u32(uint32_t *p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -506,12 +509,13 @@ __device__ void scan_role(const StepParams &p, int b, int t, Shared &sh, Prefetc
 
 // In the step with several scan tiles per sequence the probe has a
 // work-group of its own, dispatched before every tile (block order), and the
-// tile that chooses the draft waits for z here: bit 32 set once z is ready,
-// bits 0..31 its float (one 64-bit word, so that the wait and the value are a
-// single read).  Words 60-61 of the sequence's n-gram slot line (at most 8
-// n-gram lengths use the line).
-__device__ __forceinline__ unsigned long long *probe_zslot(const StepParams &p, int b) {
-    return (unsigned long long *)&p.ws.mslot[b * kLineU32 + kLineU32 - 4];
+// tile that chooses the draft waits for this flag before it reads z.  It sits
+// in the last word of the sequence's n-gram slot line (at most 8 n-gram
+// lengths use the line).  (Measured: z and a ready bit in one 64-bit word,
+// read once, made C3 and C4 0.05-0.1 us slower than the flag and a second
+// read.)
+__device__ __forceinline__ uint32_t *probe_flag(const StepParams &p, int b) {
+    return (uint32_t *)&p.ws.mslot[b * kLineU32 + kLineU32 - 1];
 }
 
 // Device-side error word of sequence b, next to the probe flag: nonzero when
@@ -533,10 +537,11 @@ __device__ void probe_role(const StepParams &p, int b, Shared &sh) {
     }
     __syncthreads();
     if (tid == 0) {
-        const float z = probe_combine(sh.probe.s, sh.probe.c, p.bias);
-        st_f32(&p.z[b], z);
-        if (p.epi_front == EPI_SELECT && !p.withhold_flag)  // the step: z for the switch
-            st_u64(probe_zslot(p, b), (1ull << 32) | __float_as_uint(z));
+        st_f32(&p.z[b], probe_combine(sh.probe.s, sh.probe.c, p.bias));
+        if (p.epi_front == EPI_SELECT && !p.withhold_flag) {  // the step: z is ready
+            __builtin_amdgcn_s_waitcnt(0);
+            st_u32(probe_flag(p, b), 1u);
+        }
     }
 }
 
@@ -845,8 +850,8 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
 // (set where the neural draft was read, so that no later use waits for that
 // read again).  With `deferred` the front's outputs are not written yet: the
 // match (mn, me, cl; lane j < k holds copied token ct), the draft, the score z
-// when this work-group computed it (zstore), the clearing of the probe's z
-// word (zclear) and of the tile slots this lane polled (bit q of tclear: slot
+// when this work-group computed it (zstore), the clearing of the probe's flag
+// (zclear) and of the tile slots this lane polled (bit q of tclear: slot
 // q * 64 + lane) go out with store_front once the accept epilogue has polled
 // its results, so that its first poll does not also wait for these stores
 // (a wave's loads and stores complete in one count).
@@ -858,7 +863,7 @@ struct DraftRegs {
     bool deferred, zstore, zclear;
 };
 
-__device__ __forceinline__ unsigned long long *probe_zslot(const StepParams &p, int b);
+__device__ __forceinline__ uint32_t *probe_flag(const StepParams &p, int b);
 
 // Outputs of steps 1 and 3 from dr (wave 0; one candidate, R <= 64, k < 64).
 __device__ void store_front(const StepParams &p, int b, const DraftRegs &dr, bool select) {
@@ -871,7 +876,7 @@ __device__ void store_front(const StepParams &p, int b, const DraftRegs &dr, boo
         if (dr.zstore)
             p.z[b] = dr.z;
         if (dr.zclear)
-            st_u64(probe_zslot(p, b), 0ull);
+            st_u32(probe_flag(p, b), 0u);
     }
     if (dr.tclear) {
         int32_t *ts = p.ws.tslot + (int64_t)b * p.ws.tslot_stride;
@@ -1128,11 +1133,11 @@ __device__ void front_local(const StepParams &p, int b, Shared &sh, const Prefet
 
 // The scan tile that chooses the draft of a longer context, once every tile's
 // result is in: s is lane j's n-gram slot value over all tiles (end + 1 of
-// the most recent occurrence of length j, 0 none), zs a first read of the
-// probe's z word (the step).  The copy candidate comes from this tile's LDS
+// the most recent occurrence of length j, 0 none), fl0 a first read of the
+// probe's flag (the step).  The copy candidate comes from this tile's LDS
 // when it lies there, else from the context.
 __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, const Prefetch &pre,
-                             DraftRegs &dr, int32_t s, unsigned long long zs) {
+                             DraftRegs &dr, int32_t s, uint32_t fl0) {
     const int lane = threadIdx.x;
     int mn, me, jsel;
     pick_match(p, s, mn, me, jsel);
@@ -1160,21 +1165,18 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
     if (p.epi_front == EPI_SELECT) {
         if (p.probe_on) {
             // the probe's work-group was dispatched before every tile and
-            // depends on nothing, so z is ready in bounded time; the cap only
-            // guards against a broken launch.  If it is reached, the
+            // depends on nothing, so the flag is set in bounded time; the cap
+            // only guards against a broken launch.  If it is reached, the
             // sequence's error word is set and the switch takes the neural
             // draft (a NaN score never clears the threshold).
-            unsigned long long *zp = probe_zslot(p, b);
-            uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(zs >> 32));
-            uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)zs);
-            for (int spin = 0; hi == 0u && spin < p.spin_cap; ++spin) {
+            uint32_t *fl = probe_flag(p, b);
+            bool seen = __builtin_amdgcn_readfirstlane((int)fl0) != 0;
+            for (int spin = 0; spin < p.spin_cap && !seen; ++spin) {
                 __builtin_amdgcn_s_sleep(2);
-                const unsigned long long v = ld_u64(zp);
-                hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-                lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+                seen = __builtin_amdgcn_readfirstlane((int)ld_u32(fl)) != 0;
             }
-            if (hi != 0u) {
-                zb = __uint_as_float(lo);
+            if (seen) {
+                zb = ld_f32(&p.z[b]);
             } else {
                 zb = __builtin_nanf("");
                 if (lane == 0)
@@ -1184,7 +1186,7 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
             // poll (store_front)
             dr.zclear = p.poll_accept && !general_select(p);
             if (lane == 0 && !dr.zclear)
-                st_u64(zp, 0ull);
+                st_u32(fl, 0u);
         } else {
             zb = ld_f32(&p.z[b]);
         }
@@ -2855,7 +2857,7 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
             TL_MARK(2);
         } else {
             const int lane = threadIdx.x;
-            const bool zread = p.epi_front == EPI_SELECT && p.probe_on;
+            const bool fread = p.epi_front == EPI_SELECT && p.probe_on;
             if (t == 0 && p.scan_probe && lane == 0)
                 st_f32(&p.z[b], probe_combine(sh.scan.ps, sh.scan.pc, p.bias));
             if (p.poll_front) {
@@ -2866,9 +2868,10 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
                                            t * SWITCHSD_MAX_NGRAM + lane],
                                sh.scan.red[lane] + 1);
                 } else {
-                    const unsigned long long zs = zread ? ld_u64(probe_zslot(p, b)) : 0ull;
+                    // the probe's flag is read once with the tiles' slots
+                    const uint32_t fl0 = fread ? ld_u32(probe_flag(p, b)) : 0u;
                     const int32_t sl = poll_tiles(p, b, sh, dr);
-                    front_remote(p, b, t, sh, pre, dr, sl, zs);
+                    front_remote(p, b, t, sh, pre, dr, sl, fl0);
                     chose = true;
                     TL_MARK(2);
                 }
@@ -2885,14 +2888,14 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
                     }
                 }
                 if (arrive(&p.ws.tk_front[b * kLineU32], p.exp_front)) {
-                    // the tiles' results and the probe's z, requested together
-                    const unsigned long long zs = zread ? ld_u64(probe_zslot(p, b)) : 0ull;
+                    // the tiles' results and the probe's flag, requested together
+                    const uint32_t fl0 = fread ? ld_u32(probe_flag(p, b)) : 0u;
                     int32_t sl = 0;
                     if (lane < p.n_ngram) {
                         sl = ld_i32(&p.ws.mslot[b * kLineU32 + lane]);
                         st_i32(&p.ws.mslot[b * kLineU32 + lane], 0);
                     }
-                    front_remote(p, b, t, sh, pre, dr, sl, zs);
+                    front_remote(p, b, t, sh, pre, dr, sl, fl0);
                     chose = true;
                     TL_MARK(2);
                 }

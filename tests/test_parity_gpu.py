@@ -202,6 +202,10 @@ CASES = {
                                 kappa=1, theta=0.0, vocab=3, tree=True, ties=True),
     "chain_r100_general": dict(seed=12, B=3, Lmax=300, V=3, R=100, k=99, lens=(1,), kappa=1,
                                theta=-np.inf, vocab=2, ties=True, plant=True),
+    # more than 64 scan tiles: the tiles hand over through arrivals (no per-tile
+    # slots), the accept epilogue still polls the segment results
+    "tiles_over_poll_limit": dict(seed=20, B=2, Lmax=66600, V=1000, R=8, k=7, lens=(3, 2, 1),
+                                  kappa=1, theta=0.0, vocab=20, plant=True),
     "long_halo_ngram64": dict(seed=13, B=3, Lmax=8300, V=100, R=3, k=2, lens=(64, 63, 1),
                               kappa=1, theta=0.0, vocab=2, ragged=False, repeat_tail=80),
     # rows with no element above -0 over many chunks (the argmax must compare
@@ -231,11 +235,12 @@ CASES = {
 
 
 def workspace_left_clean(ws, d):
-    """Tickets, slots and row keys are zero again (the candidate lists of long
-    contexts, kept at the end of the workspace, are rewritten before use)."""
+    """Tickets, slots, row keys, segment and tile slots are zero again (the
+    candidate lists of several copy candidates, kept at the end of the
+    workspace, are rewritten before use)."""
     from paper_2609_20186_amd import binding as sd
     B, R = d["ntok"].shape
-    return int(ws[:sd.workspace_bytes(B, R)].count_nonzero()) == 0
+    return int(ws[:sd.workspace_bytes(B, R, d["tokens"].shape[1], 1)].count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("case", sorted(CASES))
