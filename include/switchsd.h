@@ -47,9 +47,9 @@
  *   - Calls that take a workspace (the step and its stages) need
  *     `switchsd_workspace_bytes(B, R, Lmax, cfg.n_cand)` bytes, 256-byte
  *     aligned, zeroed once by the caller at allocation.  Every kernel leaves
- *     its tickets, slots and row keys zeroed again when it completes (the
- *     candidate lists of long contexts are rewritten before every read), so
- *     no per-call clearing is needed.  After a call fails inside HIP, or if the
+ *     the workspace zeroed again when it completes (tickets, slots, row keys,
+ *     candidate lists), so no per-call clearing is needed, and calls of
+ *     different shapes may share one workspace of the largest size.  After a call fails inside HIP, or if the
  *     stream is torn down mid-call, zero it again.  Calls that share one
  *     workspace must be ordered (same stream, or synchronized).
  */
@@ -362,11 +362,13 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
  *   - with contexts longer than 1024 tokens, the last scan work-group of a
  *     sequence waits for the probe's work-group (dispatched before it); if it
  *     gives up, that sequence's switch takes the neural draft;
- *   - in the fused launch at T = 0 with R <= 64 and B no larger than the
- *     device's compute-unit count, the work-group that chose a sequence's
- *     draft waits for the results of that sequence's argmax work-groups
- *     (which wait for nothing); if it gives up, a segment whose result is
- *     missing counts as holding no maximum.
+ *   - at T = 0 with R <= 64 and B no larger than the device's compute-unit
+ *     count, in switchsd_step's fused launch (one candidate) and in the
+ *     verification launch (switchsd_verify_accept, and switchsd_step's split
+ *     mode), the work-group holding a sequence's draft waits for the results
+ *     of that sequence's argmax work-groups (which wait for nothing); if it
+ *     gives up, a segment whose result is missing counts as holding no
+ *     maximum.
  * After a give-up that sequence's outputs are not valid.  The call reads and
  * clears the error words; after SWITCHSD_EDEVICE, zero the workspace again
  * before its next use.

@@ -433,7 +433,8 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
         StepParams pq = p;
         pq.logits = sa->qlogits;
         pq.ws.keys = p.ws.qkeys;
-        pq.n_front_wg = pq.n_scan_wg = 0;
+        pq.n_front_wg = pq.n_scan_wg = pq.n_poll_wg = 0;
+        pq.poll_accept = 0;
         pq.probe_on = pq.scan_probe = 0;
         pq.epi_front = EPI_NONE;
         pq.epi_accept = 0;
@@ -515,9 +516,23 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
         p.list_mode = 1;
         grid = 4 * (int64_t)cus;
     } else {
-        if ((rc = set_segments(p, (int64_t)B * R, V)))
+        // At T = 0 with R <= 64 and B no larger than the CU count, one
+        // work-group per sequence (first in the grid) holds the draft and
+        // polls the segment results (as the fused step's front does); the
+        // other work-groups wait for nothing.
+        int cus = 0;
+        if ((rc = cu_count(&cus)))
             return rc;
-        grid = (int64_t)B * R * p.segs;
+        const bool poll = !sa && R <= 64 && B <= cus;
+        const int64_t cap = poll && kMaxPollSlots / R < kMaxSegs ? kMaxPollSlots / R : kMaxSegs;
+        if ((rc = set_segments(p, (int64_t)B * R, V, cap)))
+            return rc;
+        if (poll) {
+            p.poll_accept = 1;
+            p.n_poll_wg = B;
+            p.spin_cap = 1 << 22;  // the bound of the poll (see switchsd_workspace_status)
+        }
+        grid = p.n_poll_wg + (int64_t)B * R * p.segs;
         if (!grid_ok(grid))
             return SWITCHSD_ESHAPE;
     }
@@ -725,8 +740,10 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         // unit exists: every other work-group of the grid runs to completion
         // without waiting, so the waiting ones cannot hold every slot the
         // argmax work-groups need.
-        p.poll_accept =
-            !sampled && R <= 64 && (int64_t)R * p.segs <= kMaxPollSlots && B <= cus ? 1 : 0;
+        p.poll_accept = !sampled && p.W == 1 && R <= 64 &&
+                                (int64_t)R * p.segs <= kMaxPollSlots && B <= cus
+                            ? 1
+                            : 0;
         if ((rc = launch_step_kernel(p, grid, stream)) || !sampled)
             return rc;
         return sample_finish(p, &sa, true, stream);

@@ -115,10 +115,13 @@ struct StepParams {
     int32_t speculate;   // 1: issue a row's first chunk before reading whether it is needed
     int32_t epi_front;
     int32_t epi_accept;
-    int32_t poll_accept; // 1 (fused step, R <= 64): each argmax work-group stores its result
-                         // in its own slot and the sequence's front work-group, once the
-                         // draft is chosen, polls the slots and runs the accept epilogue
-                         // (no arrivals at tk_all)
+    int32_t poll_accept; // 1 (R <= 64, T = 0): each argmax work-group stores its result in
+                         // its own slot, and the work-group holding the sequence's draft
+                         // (the front's chooser in the fused step, a poller work-group
+                         // in the verify launch) polls the slots and runs the accept
+                         // epilogue (no arrivals at tk_all)
+    int32_t n_poll_wg;   // verify launch with poll_accept: one waiting work-group per
+                         // sequence, first in the grid, runs its accept epilogue
     int32_t poll_front;  // 1 (the step, one candidate, 1 < scan_tiles <= kMaxPollTiles): each
                          // scan tile stores its match slots in its own line and the last
                          // tile polls them (no arrivals at tk_front)

@@ -567,11 +567,14 @@ __device__ __forceinline__ bool spec_seq(const StepParams &p, int b) {
     return p.qlogits != nullptr && !(p.spec_copy && ld_i32(&p.spec_copy[b]) != 0);
 }
 
-// Rows a sequence may need in the fused step: every row, or the longer of its
-// neural draft (nnb nodes) and the longest copy draft.
+// Rows a sequence may need, as rows_needed with the node count already read:
+// every row; the chosen draft's nnb nodes (verify launch); or the longer of
+// the neural draft (nnb nodes) and the longest copy draft (fused step).
 __device__ __forceinline__ uint32_t rows_of_drafts(const StepParams &p, int nnb) {
     if (p.rows_mode == ROWS_ALL)
         return (uint32_t)p.R;
+    if (p.rows_mode == ROWS_DRAFT)
+        return (uint32_t)nnb;
     const int cn = 1 + p.W * p.k;  // the longest copy draft
     return (uint32_t)(nnb > cn ? nnb : cn);
 }
@@ -1214,6 +1217,14 @@ __device__ void front_remote(const StepParams &p, int b, int t, Shared &sh, cons
                 cnt += __popcll(nz);
             }
         }
+        if (W > 1 && p.ws.cand_stride > 0) {
+            // every tile's lists zeroed again: calls sharing a workspace carve
+            // it by their own shapes, so a list left behind could sit under
+            // another call's slots
+            int32_t *cw = p.ws.cand + (int64_t)b * p.ws.cand_stride;
+            for (int q = lane; q < T * SWITCHSD_MAX_NGRAM * W; q += 64)
+                st_i32(&cw[q], 0);
+        }
         const int v = lane < W ? sh.scan.merged[lane] : 0;
         front_finish_w(p, b, mn, v, L, zb, pre, sh, t0, t0 - 64 > 0 ? t0 - 64 : 0,
                        t0 + kScanTile < p.Lmax ? t0 + kScanTile : p.Lmax, dr);
@@ -1739,6 +1750,24 @@ __device__ void poll_epilogue(const StepParams &p, int b, const DraftRegs &dr, S
     const int acc = accept_lanes<kCommit>(p, b, key, dr.tok, dr.par, dr.dn, cL);
     if (kCommit && threadIdx.x == 0)
         commit_lengths(p, b, cL, cdp, dr.use, acc);
+}
+
+// The verify launch's waiting work-group of sequence b (wave 0; R <= 64):
+// the draft, written by an earlier launch, read into registers while the
+// argmax work-groups stream (its accept epilogue then polls their results).
+template <bool kCommit>
+__device__ __forceinline__ void poller_draft(const StepParams &p, int b, DraftRegs &dr) {
+    const int lane = threadIdx.x;
+    const int64_t base = (int64_t)b * p.R;
+    const int dn_raw = p.dn[b];
+    if (lane < p.R) {
+        dr.tok = p.dtok[base + lane];
+        dr.par = p.dpar ? p.dpar[base + lane] : lane - 1;
+    }
+    dr.dn = dn_raw;
+    dr.nnb = clampi(dn_raw, 1, p.R);  // the rows the argmax work-groups verify
+    if (kCommit)
+        dr.use = p.use_copy[b];
 }
 
 // ------------------------------------------------------------- streamed verify
@@ -2901,7 +2930,10 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
                 }
             }
         }
-        if (p.poll_accept && chose) {
+        // (polling is compiled into the one-candidate kernels only: the host
+        // never sets it for several candidates, and the several-candidate
+        // kernels then stay small enough for the accept epilogue to be inlined)
+        if (!kMulti && p.poll_accept && chose) {
             poll_epilogue<kCommit>(p, b, dr, sh);
 #ifdef SWITCHSD_TIMELINE
             __builtin_amdgcn_s_waitcnt(0);
@@ -2909,7 +2941,7 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
             TL_MARK(4);
         }
     }
-    if (p.poll_accept)
+    if (!kMulti && p.poll_accept)
         return;  // an argmax work-group's slot is its only hand-off
     if (p.epi_accept && role != 1) {
         const bool last = arrive(&p.ws.tk_all[b * kLineU32], p.exp_all);
@@ -2922,6 +2954,30 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
             TL_MARK(4);
         }
     }
+}
+
+// The verify launch with polling (T = 0, R <= 64, B no larger than the CU
+// count): block order [one poller per sequence | argmax row segments,
+// segment-major].  A poller holds its sequence's draft and runs the accept
+// epilogue once the segment results are in (poll_epilogue); the argmax
+// work-groups store their results and wait for nothing.
+template <bool kCommit>
+__global__ __launch_bounds__(kThreads) void k_verify_poll(StepParams p) {
+    __shared__ Shared sh;
+    if ((int)blockIdx.x < p.B) {
+        if (threadIdx.x < 64) {
+            DraftRegs dr = {-1, -1, 1, 0, 1, 0, -1, 0, -1, 0.0f, 0u, false, false, false};
+            poller_draft<kCommit>(p, (int)blockIdx.x, dr);
+            poll_epilogue<kCommit>(p, (int)blockIdx.x, dr, sh);
+        }
+        return;
+    }
+    const int idx = (int)blockIdx.x - p.B;
+    const int nrows = p.B * p.R;
+    const int s = idx / nrows;
+    const int rowi = idx - s * nrows;
+    const int b = rowi / p.R;
+    argmax_role(p, b, rowi - b * p.R, s, sh, sh.am.keep);
 }
 
 // The grid is four work-groups per compute unit, all resident at once.
@@ -3034,7 +3090,14 @@ int launch_tree_mask_kernel(const int32_t *dpar, const int32_t *dn, int32_t B, i
 }
 
 int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
-    if (p.list_mode)
+    if (p.n_poll_wg > 0)
+        if (p.commit)
+            hipLaunchKernelGGL((k_verify_poll<true>), dim3((unsigned)grid), dim3(kThreads), 0,
+                               stream, p);
+        else
+            hipLaunchKernelGGL((k_verify_poll<false>), dim3((unsigned)grid), dim3(kThreads), 0,
+                               stream, p);
+    else if (p.list_mode)
         if (p.commit)
             hipLaunchKernelGGL((k_verify_stream<true>), dim3((unsigned)grid), dim3(kThreads), 0,
                                stream, p);
