@@ -302,6 +302,72 @@ def read_calibration(torch, stream, sets, nbytes, cus):
             "claims_sweep": dyn}
 
 
+def decode_loop(args, wl, d, sets, cfg, sd, torch, T, uni, sws):
+    """K steps with commit captured in one HIP graph, cycling over the input
+    copies (the contexts, lengths and draft-model positions are shared and
+    grow); each replay starts from the initial contexts (restored outside the
+    timed region)."""
+    K = args.loop
+    B, R = wl.B, wl.R
+    Lmax = wl.L + K * R
+    tokens = torch.zeros((B, Lmax), dtype=torch.int32, device="cuda")
+    tokens[:, :wl.L] = sets[0]["tokens"]
+    lengths0 = sets[0]["lengths"].clone()
+    lengths = lengths0.clone()
+    draft_pos = lengths0.clone()
+    lag = torch.zeros(B, dtype=torch.int32, device="cuda")
+    tokens0 = tokens.clone()
+    nset = len(sets)
+    outs = [sd.alloc_outputs(B, R, wl.k, wl.n_cand) for _ in range(nset)]
+    ws = sd.alloc_workspace(B, R, Lmax, wl.n_cand)
+    args_l = []
+    for st, o in zip(sets, outs):
+        inp = dict(st)
+        inp["tokens"], inp["lengths"] = tokens, lengths
+        args_l.append(sd.build_step_args(inp, o, cfg, args.mode, T, uni, sws, draft_pos, lag))
+
+    def run_steps():
+        for i in range(K):
+            sd.switchsd_step(args_l[i % nset], ws)
+
+    def reset():
+        tokens.copy_(tokens0)
+        lengths.copy_(lengths0)
+        draft_pos.copy_(lengths0)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run_steps()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    eager_len = lengths.clone()
+    reset()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_steps()
+    reps = max(3, args.steps // K)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    total = 0.0
+    for rep in range(reps + 1):
+        reset()
+        torch.cuda.synchronize()
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if rep > 0:                      # the first replay is a warm-up
+            total += e0.elapsed_time(e1)
+        assert torch.equal(lengths, eager_len), "graph replay disagrees with the eager loop"
+    us = total / reps / K * 1e3
+    grown = (eager_len - lengths0).float().mean().item()
+    return {"steps_per_graph": K, "replays": reps, "us_per_step": round(us, 2),
+            "steps_per_s": round(1e6 / us, 1),
+            "tokens_appended_per_sequence_per_step": round(grown / K, 3),
+            "note": "contexts grow in place; inputs cycle over the rotation copies"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -502,9 +568,12 @@ def main():
                "traffic_file": f"traffic_fused_step_{wl.name}.json"}
     else:
         # long drafts of up to 256 sequences with 16-byte aligned rows: the
-        # streamed verify kernel; otherwise the step kernel's argmax role
+        # streamed verify kernel; short drafts of at most one sequence per CU:
+        # the polling verify kernel; otherwise the step kernel's argmax role
         streamed = wl.R > 64 and wl.B <= 256 and wl.V % 8 == 0
-        kname = "k_verify_stream" if streamed else "k_switchsd"
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        kname = ("k_verify_stream" if streamed else
+                 "k_verify_poll" if wl.R <= 64 and wl.B <= cus else "k_switchsd")
         dom = {"kernel": f"{kname} (verify launch of the split step)",
                "gbps": vbytes / (vms * 1e-3) / 1e9, "bytes": vbytes, "ms": vms,
                "traffic_file": f"traffic_verify_{wl.name}.json"}

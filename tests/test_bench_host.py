@@ -42,3 +42,28 @@ def test_c2_algorithmic_bytes():
     # a split step counts only the drafted rows
     _, part = bench.algorithmic_bytes(wl, np.full(wl.B, 3))
     assert part == 32 * 3 * 128256 * 2
+
+
+def test_every_name_bench_calls_is_defined():
+    """Every bare name bench.py calls is a builtin, an import or a definition
+    of the script (the decode-loop option once called a function that a
+    rewrite had dropped)."""
+    import ast
+    import builtins
+    src = open(os.path.join(ROOT, "bench.py")).read()
+    tree = ast.parse(src)
+    known = set(dir(builtins))
+    for node in ast.walk(tree):
+        if isinstance(node, (ast.FunctionDef, ast.ClassDef)):
+            known.add(node.name)
+            known.update(a.arg for a in node.args.args + node.args.kwonlyargs) \
+                if isinstance(node, ast.FunctionDef) else None
+        elif isinstance(node, (ast.Import, ast.ImportFrom)):
+            known.update((a.asname or a.name).split(".")[0] for a in node.names)
+        elif isinstance(node, ast.Name) and isinstance(node.ctx, ast.Store):
+            known.add(node.id)
+        elif isinstance(node, ast.arg):
+            known.add(node.arg)
+    called = {n.func.id for n in ast.walk(tree)
+              if isinstance(n, ast.Call) and isinstance(n.func, ast.Name)}
+    assert not called - known, sorted(called - known)
