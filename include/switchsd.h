@@ -357,11 +357,18 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
 /* Device-side status of the calls that used `workspace` (B sequences),
  * written to *status (a DEVICE int32) asynchronously on `stream`:
  * SWITCHSD_OK, or SWITCHSD_EDEVICE when a bounded wait inside a kernel gave
- * up since the last status call.  There are two such waits, both in
- * switchsd_step, and in practice both always end:
- *   - with contexts longer than 1024 tokens, the last scan work-group of a
- *     sequence waits for the probe's work-group (dispatched before it); if it
- *     gives up, that sequence's switch takes the neural draft;
+ * up since the last status call.  There are three such waits, and in
+ * practice each always ends, since what it waits for was dispatched before it
+ * or waits for nothing:
+ *   - with contexts longer than 1024 tokens, the scan work-group that finishes
+ *     a sequence's front in switchsd_step waits for the probe's work-group
+ *     (dispatched before it); if it gives up, that sequence's switch takes
+ *     the neural draft;
+ *   - with contexts of 2 to 64 tiles of 1024 tokens, one candidate and B no
+ *     larger than the device's compute-unit count, the last scan tile of a
+ *     sequence waits for the other tiles' match results (the tiles wait for
+ *     nothing); if it gives up, a missing tile counts as holding no
+ *     occurrence;
  *   - at T = 0 with R <= 64 and B no larger than the device's compute-unit
  *     count, in switchsd_step's fused launch (one candidate) and in the
  *     verification launch (switchsd_verify_accept, and switchsd_step's split
@@ -382,10 +389,11 @@ int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B
  * that a test can force the give-up path (every kernel still exits). */
 void switchsd_test_withhold_probe_flag(int32_t on);
 
-/* Test support only: while `on` is nonzero, the fused switchsd_step's argmax
- * work-group of sequence 0, row 0, first segment withholds its result and the
- * second wait above gives up after a few iterations (every kernel still
- * exits). */
+/* Test support only: while `on` is nonzero, in the fused switchsd_step the
+ * argmax work-group of sequence 0, row 0, first segment withholds its result,
+ * and so does sequence 0's first scan tile when a context has 2 to 64 tiles of
+ * 1024 tokens; the polls that wait for them give up after a few iterations
+ * (every kernel still exits). */
 void switchsd_test_withhold_segment(int32_t on);
 
 /* Static, thread-safe text of a status code. */

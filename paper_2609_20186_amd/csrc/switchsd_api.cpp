@@ -23,8 +23,9 @@ constexpr size_t kAlign = 256;
 // iterations, so that the give-up path runs with every kernel exiting.
 std::atomic<int> g_withhold_probe_flag{0};
 // Test knob (switchsd_test_withhold_segment): in the fused step, sequence 0's
-// row 0 segment 0 never stores its result and the accept epilogue's poll gives
-// up after a few iterations.
+// row 0 segment 0 and (with 2..64 scan tiles) its scan tile 0 never store
+// their results, and the accept epilogue's and the last tile's polls give up
+// after a few iterations.
 std::atomic<int> g_withhold_segment{0};
 
 #ifdef SWITCHSD_TIMELINE

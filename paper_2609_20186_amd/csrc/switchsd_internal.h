@@ -155,7 +155,8 @@ struct StepParams {
     // probe never sets its flag
     int32_t spin_cap;
     int32_t withhold_flag;
-    int32_t withhold_seg;  // test knob: sequence 0's row 0 segment 0 never stores its slot
+    int32_t withhold_seg;  // test knob: sequence 0's row 0 segment 0 and its scan tile 0 never
+                           // store their slots
     unsigned long long *tl;  // timeline build only: per work-group phase stamps
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all

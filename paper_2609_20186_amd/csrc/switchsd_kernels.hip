@@ -2892,7 +2892,8 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
             if (p.poll_front) {
                 if (t + 1 < p.scan_tiles) {
                     // this tile's result in its own slots; nothing waits here
-                    if (lane < p.n_ngram)
+                    // (the test knob withholds sequence 0's first tile)
+                    if (lane < p.n_ngram && !(p.withhold_seg && b == 0 && t == 0))
                         st_i32(&p.ws.tslot[(int64_t)b * p.ws.tslot_stride +
                                            t * SWITCHSD_MAX_NGRAM + lane],
                                sh.scan.red[lane] + 1);

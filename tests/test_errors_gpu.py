@@ -59,9 +59,11 @@ def test_probe_wait_give_up_is_reported(mode):
 
 def test_segment_poll_give_up_is_reported():
     """The fused step's accept epilogue polls the argmax segments' result
-    slots; with sequence 0's first segment of row 0 withheld the poll gives up,
-    the status reports it, every other sequence still matches the oracle, and
-    the workspace is left zeroed once the status call has read the error."""
+    slots, and the last of C2's four scan tiles polls the other tiles' match
+    slots; with sequence 0's first segment of row 0 and its first tile
+    withheld both polls give up, the status reports it, every other sequence
+    still matches the oracle, and the workspace is left zeroed once the status
+    call has read the error."""
     import torch
     from paper_2609_20186_amd import binding as sd
     say("[errors] withheld segment result, fused step")
