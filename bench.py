@@ -622,7 +622,11 @@ def main():
             {"GBps": round(v_gbps, 1), "frac": round(v_gbps / HBM_PEAK_GBPS, 4),
              "us_per_call": round(vms * 1e3, 2),
              "us_per_call_min": round(float(np.min(v_per)) * 1e3, 2),
-             "us_per_call_max": round(float(np.max(v_per)) * 1e3, 2), "bytes_per_call": vbytes},
+             "us_per_call_max": round(float(np.max(v_per)) * 1e3, 2), "bytes_per_call": vbytes,
+             # the whole [B, R, V] tensor over the same time: what the call costs
+             # per byte a caller hands over (rows past a draft are never read)
+             "tensor_bytes": wl.B * wl.R * wl.V * 2,
+             "tensor_GBps_effective": round(wl.B * wl.R * wl.V * 2 / (vms * 1e-3) / 1e9, 1)},
         "copy_fraction": round(float(np.mean(sel["use_copy"])), 3),
         "mean_accept_len": round(float(o0["accept_len"].float().mean()), 3),
         "kernel_sha": kernel_sha(),
