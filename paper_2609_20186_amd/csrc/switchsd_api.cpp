@@ -451,10 +451,10 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
         if ((rc = launch_step_kernel(pq, g, stream)))
             return rc;
     }
-    // about eight sum work-groups per CU: the kernel needs few registers, and
-    // eight resident work-groups (their LDS fills the CU's 160 KB) hide the
-    // load latency behind the weight arithmetic better than four
-    int64_t segs = (8 * (int64_t)cus + rows - 1) / rows;
+    // about six sum work-groups per CU, all resident at once (eight fit).
+    // Measured on C2 at T = 0.7 (16 chunks per row): 2, 3, 4, 6, 8 and 16 per
+    // CU gave 42.2, 39.1, 39.6, 38.6, 40.2 and 42.8 us per step.
+    int64_t segs = (6 * (int64_t)cus + rows - 1) / rows;
     if (segs > p.cpr)
         segs = p.cpr;
     if (segs < 1)
