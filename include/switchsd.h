@@ -210,9 +210,11 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
  *   V % 8 == 0 and V <= 524288; sample_workspace of
  *   switchsd_sample_workspace_bytes(B, R, V) bytes, 256-byte aligned, no
  *   initialization needed; other arguments as in switchsd_verify_accept.
- *   Launches: the row maxima, then the weight sums, whose last work-group per
- *   row draws the row's token; with q also the q row maxima (second) and the
- *   residual draw (last). */
+ *   Launches: the row maxima, then the weight sums, in which one work-group per
+ *   row draws the row's token (without q, R <= 64 and B * R no larger than the
+ *   compute-unit count: the row's first, polling the others' sums; else the
+ *   last to arrive); with q also the q row maxima (second) and the residual
+ *   draw (last). */
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
                            float temperature, const uint64_t *uniforms,
                            const uint16_t *draft_logits, const uint64_t *accept_uniforms,
@@ -357,7 +359,7 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
 /* Device-side status of the calls that used `workspace` (B sequences),
  * written to *status (a DEVICE int32) asynchronously on `stream`:
  * SWITCHSD_OK, or SWITCHSD_EDEVICE when a bounded wait inside a kernel gave
- * up since the last status call.  There are three such waits, and in
+ * up since the last status call.  There are four such waits, and in
  * practice each always ends, since what it waits for was dispatched before it
  * or waits for nothing:
  *   - with contexts longer than 1024 tokens, the scan work-group that finishes
@@ -375,7 +377,13 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
  *     mode), the work-group holding a sequence's draft waits for the results
  *     of that sequence's argmax work-groups (which wait for nothing); if it
  *     gives up, a segment whose result is missing counts as holding no
- *     maximum.
+ *     maximum;
+ *   - at T > 0 without draft_logits, with R <= 64 and B * R no larger than
+ *     the compute-unit count, the weight-sum launch's first work-group of
+ *     each row waits for the row's other sum work-groups (which wait for
+ *     nothing), and row 0's then for the other rows' drawn tokens; if it
+ *     gives up, a row whose sums are missing keeps its greedy choice and a
+ *     missing drawn token counts as none.
  * After a give-up that sequence's outputs are not valid.  The call reads and
  * clears the error words; after SWITCHSD_EDEVICE, zero the workspace again
  * before its next use.
@@ -390,10 +398,11 @@ int switchsd_workspace_status(void *workspace, size_t workspace_bytes, int32_t B
 void switchsd_test_withhold_probe_flag(int32_t on);
 
 /* Test support only: while `on` is nonzero, in the fused switchsd_step the
- * argmax work-group of sequence 0, row 0, first segment withholds its result,
- * and so does sequence 0's first scan tile when a context has 2 to 64 tiles of
- * 1024 tokens; the polls that wait for them give up after a few iterations
- * (every kernel still exits). */
+ * argmax work-group of sequence 0, row 0, first segment withholds its result
+ * (at T > 0 with the polled draw: the weight-sum work-group of that segment
+ * withholds its sums), and so does sequence 0's first scan tile when a context
+ * has 2 to 64 tiles of 1024 tokens; the polls that wait for them give up after
+ * a few iterations (every kernel still exits). */
 void switchsd_test_withhold_segment(int32_t on);
 
 /* Static, thread-safe text of a status code. */

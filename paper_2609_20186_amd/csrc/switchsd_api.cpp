@@ -399,6 +399,42 @@ SampleArgs sample_args_of(const switchsd_step_args *a) {
                       a->use_copy};
 }
 
+// The sample workspace's regions and the draw's parameters in p.
+void sample_carve(StepParams &p, const SampleArgs *sa) {
+    p.uniforms = sa->uniforms;
+    p.samp_c = (float)(1.4426950408889634 / (double)sa->temperature);
+    p.cpr = (int32_t)chunks_per_row(p.V);
+    char *sw = (char *)sa->ws;
+    p.csum = (unsigned long long *)sw;
+    p.qcsum = (unsigned long long *)(sw + csum_bytes(p.B, p.R, p.V));
+    p.rcsum = (unsigned long long *)(sw + 2 * csum_bytes(p.B, p.R, p.V));
+    p.rdec = (uint32_t *)(sw + 2 * csum_bytes(p.B, p.R, p.V) + rcsum_bytes(p.B, p.V));
+    p.rz = (unsigned long long *)((char *)p.rdec + round_line((size_t)p.B * p.R * 4));
+    p.qlogits = sa->qlogits;
+    p.accept_uniforms = sa->accept_uniforms;
+    p.spec_copy = sa->spec_copy;
+}
+
+// The polled draw: one-hot drafts (no q) of at most 64 rows, and at most one
+// waiting work-group per compute unit on average (the first segment's of each
+// of the B * R rows, first in the sum launch's grid), so that they cannot hold
+// every slot the other work-groups need; those wait for nothing.
+bool draw_polled(const StepParams &p, const SampleArgs *sa, int cus) {
+    return !sa->qlogits && p.R <= 64 && p.ws.skey_stride > 0 && (int64_t)p.B * p.R <= cus;
+}
+
+// The row maxima launch before a draw: with the polled draw, it also zeroes
+// the sum slots (csum_clear), so the sample workspace needs no initialization.
+int prepare_draw(StepParams &p, const SampleArgs *sa) {
+    int cus = 0;
+    const int rc = cu_count(&cus);
+    if (rc)
+        return rc;
+    sample_carve(p, sa);
+    p.csum_clear = draw_polled(p, sa, cus) ? 1 : 0;
+    return SWITCHSD_OK;
+}
+
 // After the row maxima are in the row keys: the weight-sum launch, which also
 // draws each row's token and runs the accept epilogue.  With the draft's q:
 // first the q row maxima, then the sums of the p and the q rows (the last
@@ -415,18 +451,10 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     p.tl = nullptr;  // phase stamps (timeline build) cover the step kernel's grid only
     // long drafts: the sums stream the drafted rows' chunks over a fixed grid
     const bool stream_sums = p.R > 64 && p.B <= kListMaxB && !q;
-    p.uniforms = sa->uniforms;
-    p.samp_c = (float)(1.4426950408889634 / (double)sa->temperature);
-    p.cpr = (int32_t)chunks_per_row(p.V);
-    char *sw = (char *)sa->ws;
-    p.csum = (unsigned long long *)sw;
-    p.qcsum = (unsigned long long *)(sw + csum_bytes(p.B, p.R, p.V));
-    p.rcsum = (unsigned long long *)(sw + 2 * csum_bytes(p.B, p.R, p.V));
-    p.rdec = (uint32_t *)(sw + 2 * csum_bytes(p.B, p.R, p.V) + rcsum_bytes(p.B, p.V));
-    p.rz = (unsigned long long *)((char *)p.rdec + round_line((size_t)p.B * p.R * 4));
-    p.qlogits = sa->qlogits;
-    p.accept_uniforms = sa->accept_uniforms;
-    p.spec_copy = sa->spec_copy;
+    sample_carve(p, sa);
+    // the polled draw when the maxima launch cleared its slots
+    const bool polled = p.csum_clear && !stream_sums;
+    p.csum_clear = 0;
     const int64_t rows = (int64_t)p.B * p.R;
     if (q) {
         // the q row maxima: the argmax role alone, over the rows with a
@@ -436,6 +464,7 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
         pq.ws.keys = p.ws.qkeys;
         pq.n_front_wg = pq.n_scan_wg = pq.n_poll_wg = 0;
         pq.poll_accept = 0;
+        pq.csum_clear = 0;
         pq.probe_on = pq.scan_probe = 0;
         pq.epi_front = EPI_NONE;
         pq.epi_accept = 0;
@@ -463,12 +492,14 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     p.segs = (int32_t)((p.cpr + p.seg_chunks - 1) / p.seg_chunks);
     p.speculate = speculate ? 1 : 0;
     p.list_mode = stream_sums ? 1 : 0;
+    p.draw_poll = polled ? 1 : 0;
     const int64_t grid = stream_sums ? 4 * (int64_t)cus : rows * p.segs * (q ? 2 : 1);
     if (!grid_ok(grid) || !grid_ok(rows))
         return SWITCHSD_ESHAPE;
-    // the last work-group of each drafted row also draws its token (or takes
-    // its accept test), and the last drafted row of a sequence runs the accept
-    // epilogue (sequences verified with q: the residual launch does)
+    // polled: the first work-group of row r draws its token and row 0's runs
+    // the accept epilogue; else the last work-group of each drafted row draws its token
+    // (or takes its accept test), and the last drafted row of a sequence runs
+    // the accept epilogue (sequences verified with q: the residual launch does)
     if ((rc = launch_sample_sums_kernel(p, grid, stream)) || !q)
         return rc;
     // residual: one work-group per 256 vectors (4 KB) of the rejected row,
@@ -531,7 +562,6 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
         if (poll) {
             p.poll_accept = 1;
             p.n_poll_wg = B;
-            p.spin_cap = 1 << 22;  // the bound of the poll (see switchsd_workspace_status)
         }
         grid = p.n_poll_wg + (int64_t)B * R * p.segs;
         if (!grid_ok(grid))
@@ -563,6 +593,9 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
         p.use_copy = loop->use_copy;
     }
     p.exp_all = (uint32_t)(R * p.segs);
+    p.spin_cap = 1 << 22;  // the bound of each poll (see switchsd_workspace_status)
+    if (sa && (rc = prepare_draw(p, sa)))
+        return rc;
     if ((rc = launch_step_kernel(p, grid, stream)) || !sa)
         return rc;
     return sample_finish(p, sa, speculate, stream);
@@ -745,6 +778,8 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
                                 (int64_t)R * p.segs <= kMaxPollSlots && B <= cus
                             ? 1
                             : 0;
+        if (sampled && (rc = prepare_draw(p, &sa)))
+            return rc;
         if ((rc = launch_step_kernel(p, grid, stream)) || !sampled)
             return rc;
         return sample_finish(p, &sa, true, stream);

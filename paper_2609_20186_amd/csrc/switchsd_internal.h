@@ -139,6 +139,11 @@ struct StepParams {
     unsigned long long *csum;  // [B, R, cpr, waves] integer weight sums per chunk and wave
     int32_t cpr;               // 16 KB chunks per row
     int32_t seg_chunks;        // chunks per work-group of the sum launch
+    int32_t draw_poll;         // 1: the polled draw (no q, R <= 64): sums stored + 1, the
+                               // work-group of each row's first segment draws the row's token
+                               // and row 0's runs the accept epilogue (no arrivals)
+    int32_t csum_clear;        // the row maxima launch before a polled draw: each argmax
+                               // work-group zeroes its share of its row's sum slots
     // speculative sampling with the draft's own distribution q (chains, T > 0)
     const uint16_t *qlogits;          // [B, R, V] the draft's logits, or null (one-hot drafts)
     const uint64_t *accept_uniforms;  // [B, R] uniforms of the accept tests
@@ -155,8 +160,9 @@ struct StepParams {
     // probe never sets its flag
     int32_t spin_cap;
     int32_t withhold_flag;
-    int32_t withhold_seg;  // test knob: sequence 0's row 0 segment 0 and its scan tile 0 never
-                           // store their slots
+    int32_t withhold_seg;  // test knob: sequence 0's row 0 segment 0 (of the argmax, and of the
+                           // weight sums in a polled draw) and its scan tile 0 never store
+                           // their slots
     unsigned long long *tl;  // timeline build only: per work-group phase stamps
     uint32_t exp_front;  // arrivals per sequence at tk_front
     uint32_t exp_all;    // arrivals per sequence at tk_all

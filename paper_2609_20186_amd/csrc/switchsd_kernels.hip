@@ -107,6 +107,13 @@ struct PickShared {  // one row's draw at T > 0
 struct PollShared {  // the segment results a sequence's accept epilogue polled
     unsigned long long k[kMaxSegs * 64];
 };
+struct DrawShared {  // one row's polled draw at T > 0 (draw_poller)
+    unsigned long long cw[64 * kWaves];  // the row's weight sums per (chunk, wave)
+    unsigned long long bs[kWaves];       // block sums of the chosen entry (wave w: block w)
+    unsigned long long tg;               // the target within the entry
+    unsigned long long key;              // the drawn token's key
+    int32_t cst, est, ok;                // the entry (chunk, wave); every sum arrived
+};
 union Shared {
     ScanShared scan;
     PollShared poll;
@@ -114,6 +121,7 @@ union Shared {
     ProbeShared probe;
     EpiShared epi;
     PickShared pick;
+    DrawShared draw;
 };
 
 // Timeline build only (compiled with SWITCHSD_TIMELINE, never in the product
@@ -771,6 +779,14 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
     const uint32_t xi = (uint32_t)(xg - rowoff);
     const bool has_x = xg >= 0;
 
+    if (p.csum_clear) {
+        // this segment's share of the row's weight-sum slots, zeroed for the
+        // pollers of the sum launch that follows (the polled draw at T > 0)
+        const int n = p.cpr * kCsumPerChunk;
+        const int i0 = s * n / p.segs, i1 = (s + 1) * n / p.segs;
+        if (tid < i1 - i0)
+            p.csum[((int64_t)b * p.R + r) * n + i0 + tid] = 0ull;
+    }
     LazyMaxLds st;
     st.d = keep;
     lazy_init(st);
@@ -1995,6 +2011,39 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
+// Inclusive prefix sum of 64-bit integers over the 64 lanes of a wave, in DPP
+// moves (no LDS): row shifts by 1, 2, 4 and 8 within each row of 16 lanes,
+// then lane 15's total into rows 1 and 3 and lane 31's into rows 2 and 3 (as
+// wave_sum_f64, whose lane 63 is the total).  kSteps < 6 stops after the
+// first kSteps (e.g. 3: the prefix of lanes 0..7 of row 0).
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ unsigned long long dpp_shift_u64(unsigned long long v) {
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, kCtrl, kRowMask, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), kCtrl, kRowMask, 0xf,
+                                               false);
+    return ((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+template <int kSteps = 6>
+__device__ __forceinline__ unsigned long long wave_scan_u64(unsigned long long v) {
+    v += dpp_shift_u64<0x111, 0xf>(v);
+    v += dpp_shift_u64<0x112, 0xf>(v);
+    v += dpp_shift_u64<0x114, 0xf>(v);
+    if (kSteps > 3)
+        v += dpp_shift_u64<0x118, 0xf>(v);
+    if (kSteps > 4)
+        v += dpp_shift_u64<0x142, 0xa>(v);
+    if (kSteps > 5)
+        v += dpp_shift_u64<0x143, 0xc>(v);
+    return v;
+}
+// Lane l's value (l uniform over the wave).
+__device__ __forceinline__ unsigned long long readlane_u64(unsigned long long v, int l) {
+    l = __builtin_amdgcn_readfirstlane(l);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
 // floor(u * Z / 2^64), exactly (the upper half of the 128-bit product).
 __device__ __forceinline__ unsigned long long scaled_target(unsigned long long u,
                                                             unsigned long long Z) {
@@ -2016,10 +2065,12 @@ __device__ __forceinline__ void load_chunk_w(u32x4 (&v)[kUnroll], const u32x4 *v
 }
 
 // Weight sums of chunk c (16 KB) of a row, one per wave (its contiguous 256
-// vectors), stored at cs[c * kWaves + wave]; the entries of a row in index
+// vectors), stored at cs[c * kWaves + wave] (plus `mark`: 1 where a poller
+// tells a written sum from an empty slot); the entries of a row in index
 // order are chunk by chunk, wave by wave.
 __device__ __forceinline__ void store_block_sums(const u32x4 (&A)[kUnroll], int c, int nq, float m,
-                                                 float samp_c, unsigned long long *cs) {
+                                                 float samp_c, unsigned long long *cs,
+                                                 unsigned long long mark) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int q0 = c * kChunkVecs + wave * (kUnroll * 64) + lane;
     double w = 0.0;
@@ -2028,19 +2079,8 @@ __device__ __forceinline__ void store_block_sums(const u32x4 (&A)[kUnroll], int 
         w += q0 + u * 64 < nq ? vec_weight(A[u], m, samp_c) : 0.0;
     w = wave_sum_f64(w);
     if (lane == 0)
-        __hip_atomic_store(&cs[c * kWaves + wave], (unsigned long long)w, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Inclusive prefix over the 64 lanes of a wave.
-__device__ __forceinline__ unsigned long long wave_prefix_u64(unsigned long long v) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const unsigned long long y = __shfl_up(v, o);
-        if ((int)(threadIdx.x & 63) >= o)
-            v += y;
-    }
-    return v;
+        __hip_atomic_store(&cs[c * kWaves + wave], (unsigned long long)w + mark,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // The draw of row r of sequence b (its maximum m), by wave 0: the (chunk,
@@ -2068,7 +2108,7 @@ __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned lo
         for (int e = 0; e < kWaves; ++e)
             cc += sh.pick.cw[lane * kWaves + e];
     }
-    const unsigned long long inc = wave_prefix_u64(cc);
+    const unsigned long long inc = wave_scan_u64(cc);
     const unsigned long long Z = __shfl(inc, 63);
     unsigned long long tg = scaled_target(uni, Z);
     const unsigned long long hit = __ballot(lane < p.cpr && inc > tg);
@@ -2076,7 +2116,7 @@ __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned lo
     tg -= __shfl(inc - cc, cst);
     // the wave entry of that chunk holding the target (lanes 0..kWaves-1)
     const unsigned long long ce = lane < kWaves ? sh.pick.cw[cst * kWaves + lane] : 0ull;
-    const unsigned long long ie = wave_prefix_u64(ce);
+    const unsigned long long ie = wave_scan_u64<3>(ce);
     const unsigned long long hit2 = __ballot(lane < kWaves && ie > tg);
     const int est = __ffsll((long long)hit2) - 1;  // exists: tg < the chunk's total
     tg -= __shfl(ie - ce, est);
@@ -2117,7 +2157,7 @@ __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned lo
             w = vw[u];
             x = v[u];
         }
-    const unsigned long long iv = wave_prefix_u64(w);
+    const unsigned long long iv = wave_scan_u64(w);
     const unsigned long long hit3 = __ballot(iv > tg);
     const int lst = __ffsll((long long)hit3) - 1;  // exists: tg < the block's total
     if (lane == lst) {
@@ -2294,11 +2334,215 @@ __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t un
     __syncthreads();
 }
 
+// The polled draw (T > 0, no q, R <= 64): the work-group of row r's first
+// segment of the sum launch, once its own sums are stored.  Wave 0 polls the
+// row's (chunk, wave) weight sums (each stored + 1, so that 0 is an empty
+// slot; the maxima launch zeroed them), then the work-group draws the row's
+// token as pick_row does, one vector of the chosen entry per thread.  The
+// row's key (the drawn token, or the row maximum's key where nothing is drawn)
+// goes to the row's result slot; row 0's work-group keeps its own and, in wave
+// 0, polls the other drafted rows' results and runs the accept epilogue.  The
+// work-groups of the other segments wait for nothing, and the pollers are the
+// first of the grid (segment-major), so every awaited store is made in bounded
+// time; the caps guard a broken launch (the error word is set, a row whose
+// sums are missing keeps its greedy choice, a missing result counts as none).
+// k0 is the row maximum's key as this work-group read it; the key is cleared
+// once every work-group of the row has read it (its sums are in).
+template <bool kCommit>
+__device__ void draw_poller(const StepParams &p, int b, int r, int dn_raw, unsigned long long k0,
+                            Shared &sh) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int64_t base = (int64_t)b * p.R;
+    unsigned long long *keyp = &p.ws.keys[(int64_t)b * p.ws.key_stride + r];
+    unsigned long long *res = p.ws.skeys + (int64_t)b * p.ws.skey_stride;
+    const int dnb = clampi(dn_raw, 1, p.R);
+    // row 0's draft and lengths, and the row's uniform, requested before the poll
+    int tok = -1, par = -1, cL = 0, cdp = 0, cuc = 0;
+    unsigned long long uni = 0ull;
+    if (wave == 0) {
+        if (r == 0) {
+            if (lane < p.R) {
+                tok = p.dtok[base + lane];
+                par = p.dpar ? p.dpar[base + lane] : lane - 1;
+            }
+            if (kCommit) {
+                cL = clampi(p.clen[b], 0, p.Lmax);
+                cdp = p.draft_pos[b];
+                cuc = p.use_copy[b];
+            }
+        }
+        if (r < dnb)
+            uni = p.uniforms[base + r];
+    }
+    if (r >= dnb) {  // not drawn (no sum work-group of the row reads its key)
+        if (tid == 0 && k0)
+            st_u64(keyp, 0ull);
+        return;
+    }
+    unsigned long long key = k0 ? k0 : 1ull;  // the result where nothing is drawn
+    float m = 0.0f;
+    if (!key_max(k0, m)) {
+        // one-hot: the other work-groups of the row skip it too (they read the
+        // same key, or zero once it is cleared)
+        if (tid == 0 && k0)
+            st_u64(keyp, 0ull);
+    } else {
+        if (wave == 0) {
+            const int n = p.cpr * kCsumPerChunk;  // <= 256
+            const unsigned long long *cs = p.csum + (base + r) * n;
+            auto want = [&]() {
+                uint32_t w = 0;
+                for (int q = 0; q * 64 < n; ++q)
+                    if (q * 64 + lane < n)
+                        w |= 1u << q;
+                return w;
+            };
+            unsigned long long got[8];
+            int rounds = 0;
+            const bool ok = poll_wave(cs, n, want, got, p.spin_cap, rounds, [] {});
+            if (lane == 0) {
+                if (!ok)
+                    st_u32(error_word(p, b), 1u);
+                sh.draw.ok = ok ? 1 : 0;
+            }
+            if (ok) {
+                // the (chunk, wave) entry holding the target and the target
+                // within it (the entry exists, the target being below the
+                // total; the clamps only keep every index in range)
+                unsigned long long tg;
+                int ent;
+                if (n <= 64) {
+                    // one entry per lane, in index order
+                    const unsigned long long x = lane < n ? got[0] - 1ull : 0ull;
+                    const unsigned long long inc = wave_scan_u64(x);
+                    tg = scaled_target(uni, readlane_u64(inc, 63));
+                    ent = __ffsll((long long)__ballot(lane < n && inc > tg)) - 1;
+                    ent = ent < 0 ? 0 : ent;
+                    tg -= readlane_u64(inc - x, ent);
+                } else {
+                    // chunk totals, then the waves of the chunk holding the target
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (q * 64 + lane < n)
+                            sh.draw.cw[q * 64 + lane] = got[q] - 1ull;
+                    unsigned long long cc = 0;
+                    if (lane < p.cpr) {
+#pragma unroll
+                        for (int e = 0; e < kWaves; ++e)
+                            cc += sh.draw.cw[lane * kWaves + e];
+                    }
+                    const unsigned long long inc = wave_scan_u64(cc);
+                    tg = scaled_target(uni, readlane_u64(inc, 63));
+                    int cst = __ffsll((long long)__ballot(lane < p.cpr && inc > tg)) - 1;
+                    cst = cst < 0 ? 0 : cst;
+                    tg -= readlane_u64(inc - cc, cst);
+                    const unsigned long long ce =
+                        lane < kWaves ? sh.draw.cw[cst * kWaves + lane] : 0ull;
+                    const unsigned long long ie = wave_scan_u64<3>(ce);
+                    int est = __ffsll((long long)__ballot(lane < kWaves && ie > tg)) - 1;
+                    est = est < 0 ? 0 : est;
+                    tg -= readlane_u64(ie - ce, est);
+                    ent = cst * kWaves + est;
+                }
+                if (lane == 0) {
+                    sh.draw.cst = ent / kWaves;
+                    sh.draw.est = ent - ent / kWaves * kWaves;
+                    sh.draw.tg = tg;
+                }
+            }
+        }
+        __syncthreads();
+        // every wave has read the row maximum, and every other work-group of
+        // the row has (its sums are in): it is cleared
+        if (tid == 0)
+            st_u64(keyp, 0ull);
+        if (sh.draw.ok) {
+            // the entry's 256 vectors, vector 64 u + l (block u) in thread 64 u + l;
+            // each wave scans its block's weights
+            const int cst = sh.draw.cst, est = sh.draw.est;
+            const int nq = p.V >> 3;
+            const int q0 = cst * kChunkVecs + est * (kUnroll * 64);
+            const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + (base + r) * p.V);
+            const u32x4 v = q0 + tid < nq ? vp[q0 + tid] : u32x4{0u, 0u, 0u, 0u};
+            const unsigned long long w =
+                q0 + tid < nq ? (unsigned long long)vec_weight(v, m, p.samp_c) : 0ull;
+            const unsigned long long iv = wave_scan_u64(w);
+            if (lane == 63)
+                sh.draw.bs[wave] = iv;
+            __syncthreads();
+            // the block holding the target (the same in every wave), then in its
+            // wave the vector and the element
+            unsigned long long tg = sh.draw.tg, incl = 0;
+            int us = kWaves - 1;
+            for (int u = 0; u < kWaves; ++u) {
+                const unsigned long long bu = sh.draw.bs[u];
+                if (tg < incl + bu) {
+                    us = u;
+                    break;
+                }
+                incl += bu;
+            }
+            if (wave == us) {
+                tg -= incl;
+                int lst = __ffsll((long long)__ballot(iv > tg)) - 1;
+                lst = lst < 0 ? 0 : lst;
+                tg -= readlane_u64(iv - w, lst);
+                // the vector's 8 weights in lanes 0..7, their inclusive prefix
+                const int ls = __builtin_amdgcn_readfirstlane(lst);
+                const uint32_t x0 = (uint32_t)__builtin_amdgcn_readlane((int)v[0], ls);
+                const uint32_t x1 = (uint32_t)__builtin_amdgcn_readlane((int)v[1], ls);
+                const uint32_t x2 = (uint32_t)__builtin_amdgcn_readlane((int)v[2], ls);
+                const uint32_t x3 = (uint32_t)__builtin_amdgcn_readlane((int)v[3], ls);
+                const int wj = (lane >> 1) & 3;
+                const uint32_t xj = wj == 0 ? x0 : (wj == 1 ? x1 : (wj == 2 ? x2 : x3));
+                unsigned long long ew = 0ull;
+                if (lane < 8)
+                    ew = (unsigned long long)samp_weight((lane & 1) ? hi_f(xj) : lo_f(xj), m,
+                                                         p.samp_c);
+                ew = wave_scan_u64<3>(ew);
+                int e = __ffsll((long long)__ballot(lane < 8 && ew > tg)) - 1;
+                e = e < 0 ? 7 : e;
+                const uint32_t y = (uint32_t)(q0 + us * 64 + lst) * 8u + (uint32_t)e;
+                if (lane == 0)
+                    sh.draw.key = (1ull << 32) | (unsigned long long)(0xFFFFFFFFu - y);
+            }
+            __syncthreads();
+            key = sh.draw.key;
+        }
+    }
+    if (wave != 0)
+        return;
+    if (r > 0) {
+        if (lane == 0)
+            st_u64(&res[r], key);
+        return;
+    }
+    // row 0: the other drafted rows' results, then accept, bonus and commit
+    unsigned long long kl = lane == 0 ? key : 0ull;
+    if (dnb > 1) {
+        auto want = [&]() { return lane >= 1 && lane < dnb ? 1u : 0u; };
+        unsigned long long got[8];
+        int rounds = 0;
+        if (!poll_wave(res, dnb, want, got, p.spin_cap, rounds, [] {}) && lane == 0)
+            st_u32(error_word(p, b), 1u);
+        if (lane >= 1 && lane < dnb) {
+            kl = got[0];
+            if (got[0])
+                st_u64(&res[lane], 0ull);
+        }
+    }
+    const int acc = accept_lanes<kCommit>(p, b, kl > 1ull ? kl : 0ull, tok, par, dn_raw, cL);
+    if (kCommit && lane == 0)
+        commit_lengths(p, b, cL, cdp, cuc, acc);
+}
+
 // Sum launch: work-group (row, segment) adds up the weights of each 16 KB
 // chunk of its segment, per wave (a wave's chunk share is < 2^51, exact in
 // binary64).  Rows at and beyond dn and rows without a finite maximum are
 // skipped.  With the draft's q, a second set of work-groups (after the first
-// in the grid) does the same for the q rows that have a drafted child.
+// in the grid) does the same for the q rows that have a drafted child.  With
+// the polled draw, the work-group of each row's first segment then draws the
+// row's token (draw_poller); else the last one to arrive does (row_done).
 template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     __shared__ Shared sh;
@@ -2322,26 +2566,39 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     const bool early = p.speculate && !qrow;
     if (early)
         load_chunk_w(A, vp, c0 * kChunkVecs, nq);
-    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    const int dn_raw = ld_i32(&p.dn[b]);
+    const int dnb = clampi(dn_raw, 1, p.R);
     const bool spec = spec_seq(p, b);
-    if (r >= (qrow ? dnb - 1 : dnb) || (qrow && !spec)) {  // no part in the draw
-        __builtin_amdgcn_s_waitcnt(0);
-        return;
-    }
+    const bool skip = r >= (qrow ? dnb - 1 : dnb) || (qrow && !spec);  // no part in the draw
+    const unsigned long long *keyp =
+        &(qrow ? p.ws.qkeys : p.ws.keys)[(int64_t)b * p.ws.key_stride + r];
+    // (the polled draw's first work-group of a skipped row still clears its key)
+    const unsigned long long k0 = !skip || (p.draw_poll && s == 0) ? ld_u64(keyp) : 0ull;
     float m = 0.0f;
-    const bool active = key_max(
-        ld_u64(&(qrow ? p.ws.qkeys : p.ws.keys)[(int64_t)b * p.ws.key_stride + r]), m);
+    bool active = !skip && key_max(k0, m);
+    if (p.withhold_seg && p.draw_poll && b == 0 && r == 0 && s == 0)
+        active = false;  // test knob: this work-group's sums are never stored
     if (active && !early)
         load_chunk_w(A, vp, c0 * kChunkVecs, nq);
     unsigned long long *cs =
         (qrow ? p.qcsum : p.csum) + ((int64_t)b * p.R + r) * p.cpr * kWaves;
+    const unsigned long long mark = p.draw_poll ? 1ull : 0ull;
     for (int c = c0; active && c < c1; ++c) {
         if (c + 1 < c1)
             load_chunk_w(Bv, vp, (c + 1) * kChunkVecs, nq);
-        store_block_sums(A, c, nq, m, p.samp_c, cs);
+        store_block_sums(A, c, nq, m, p.samp_c, cs, mark);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
             A[u] = Bv[u];
+    }
+    if (p.draw_poll) {
+        if (s == 0)
+            draw_poller<kCommit>(p, b, r, dn_raw, k0, sh);
+        return;
+    }
+    if (skip) {
+        __builtin_amdgcn_s_waitcnt(0);
+        return;
     }
     // a tested row waits for its p and its q work-groups
     const bool tested = spec && r < dnb - 1;
@@ -2432,7 +2689,7 @@ k_sample_sums_stream(StepParams p) {
         const bool active = key_max(key, m);
         if (active)
             store_block_sums(A, c, nq, m, p.samp_c,
-                             p.csum + ((int64_t)b * p.R + r) * cpr * kWaves);
+                             p.csum + ((int64_t)b * p.R + r) * cpr * kWaves, 0ull);
         ++done_r;
         if (c == cpr - 1 || u + 1 == u1) {  // end of this row's piece
             row_done<kCommit>(p, b, r, dnb, done_r, (uint32_t)cpr, false, sh);

@@ -91,7 +91,7 @@ def sd_cfg(d):
     return sd.make_cfg(c["lens"], c["kappa"], c["k"], c["theta"], c.get("n_cand", 1))
 
 
-def gpu_step(dev, d, mode=0, out=None, ws=None):
+def gpu_step(dev, d, mode=0, out=None, ws=None, sws=None):
     import torch
     from paper_2609_20186_amd import binding as sd
     B, R = dev["ntok"].shape
@@ -99,7 +99,8 @@ def gpu_step(dev, d, mode=0, out=None, ws=None):
     out = out or sd.alloc_outputs(B, R, k, W)
     ws = ws if ws is not None else sd.alloc_workspace(B, R, dev["tokens"].shape[1], W)
     T = d.get("T", 0.0)
-    sws = sd.alloc_sample_workspace(B, R, dev["logits"].shape[2]) if T > 0 else None
+    if T > 0 and sws is None:
+        sws = sd.alloc_sample_workspace(B, R, dev["logits"].shape[2])
     args = sd.build_step_args(dev, out, sd_cfg(d), mode, T, dev.get("uniforms"), sws,
                               draft_logits=dev.get("draft_logits"),
                               accept_uniforms=dev.get("accept_uniforms"))

@@ -7,7 +7,8 @@ again, the next step matches the oracle."""
 import numpy as np
 import pytest
 
-from gpu_helpers import assert_match, gpu_step, oracle_step, planted_workload, say, to_device
+from gpu_helpers import (assert_match, gpu_step, oracle_step, planted_workload, say, to_device,
+                         with_temperature)
 from test_parity_gpu import FUSED, SPLIT
 
 pytestmark = pytest.mark.gpu
@@ -51,6 +52,41 @@ def test_probe_wait_give_up_is_reported(mode):
     ws.zero_()
     got, ws = gpu_step(dev, d, mode, ws=ws)
     assert_match(got, oracle_step(d), what=f"after give-up, mode {mode}")
+    sd.switchsd_workspace_status(ws, B, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert int(ws.count_nonzero()) == 0
+
+
+def test_draw_poll_give_up_is_reported():
+    """At T > 0 the row pollers of the draw wait for the rows' weight sums;
+    with sequence 0's first sum work-group of row 0 withheld (and its first
+    scan tile, whose poll gives up as well) the status reports it, every other
+    sequence still matches the oracle, the workspace is left zeroed once the
+    status call has read the error, and the next step matches again."""
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    say("[errors] withheld weight sums, fused step at T = 0.7")
+    d = with_temperature(planted_workload("C2"), 0.7, seed=107)
+    B, R = d["ntok"].shape
+    dev = to_device(d)
+    ws = sd.alloc_workspace(B, R, d["tokens"].shape[1])
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    exp = oracle_step(d)
+    sd.withhold_segment_for_tests(True)
+    try:
+        got, ws = gpu_step(dev, d, FUSED, ws=ws)
+    finally:
+        sd.withhold_segment_for_tests(False)
+    sd.switchsd_workspace_status(ws, B, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == EDEVICE
+    rest = slice(1, None)
+    assert_match(got, {k: v[rest] for k, v in exp.items()}, rows=rest,
+                 what="other sequences while sequence 0's draw gave up")
+    assert int(ws.count_nonzero()) == 0
+    got, ws = gpu_step(dev, d, FUSED, ws=ws)
+    assert_match(got, exp, what="after the draw give-up")
     sd.switchsd_workspace_status(ws, B, st)
     torch.cuda.synchronize()
     assert int(st.item()) == 0

@@ -53,6 +53,9 @@ SAMPLE_CASES = {
                  vocab=3, ties=True),
     "tree30": dict(seed=62, B=9, Lmax=2000, V=304, R=30, k=7, lens=(3, 2, 1), kappa=1,
                    theta=0.0, vocab=3, tree=True, plant=True),
+    # few enough rows (B * R <= the CU count) for the polled draw
+    "tree30_polled": dict(seed=71, B=8, Lmax=1500, V=304, R=30, k=7, lens=(3, 2, 1), kappa=1,
+                          theta=0.0, vocab=3, tree=True, plant=True),
     "tree100": dict(seed=63, B=4, Lmax=500, V=40, R=100, k=10, lens=(2, 1), kappa=1, theta=0.0,
                     vocab=2, tree=True, ties=True),
     "w10_d20": dict(seed=64, B=6, Lmax=3000, V=3000, R=204, k=20, lens=(3, 2, 1), kappa=1,
@@ -67,6 +70,26 @@ SAMPLE_CASES = {
     "tree70_wide_batch": dict(seed=69, B=260, Lmax=96, V=64, R=70, k=5, lens=(2, 1), kappa=1,
                               theta=0.0, vocab=3, tree=True, ties=True),
 }
+
+
+def test_sampled_dirty_sample_workspace():
+    """The sample workspace needs no initialization: filled with 0xFF bytes
+    before each call (the polled draw's sum slots included, which the row
+    maxima launch clears), C2 at T = 0.7 still matches the oracle in every
+    launch mode."""
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    say("[sample] C2 T=0.7, sample workspace of 0xFF bytes")
+    d = with_temperature(planted_workload("C2"), 0.7, seed=106)
+    exp = oracle_step(d)
+    dev = to_device(d)
+    B, R = d["ntok"].shape
+    sws = sd.alloc_sample_workspace(B, R, d["logits"].shape[2])
+    for mode in (AUTO, FUSED, SPLIT):
+        sws.fill_(255)
+        got, ws = gpu_step(dev, d, mode, sws=sws)
+        assert_match(got, exp, what=f"C2 T=0.7 dirty sample workspace, mode {mode}")
+        assert workspace_left_clean(ws, d)
 
 
 @pytest.mark.parametrize("T", [1e-4, 0.5, 3.0, 1e6])
