@@ -56,6 +56,12 @@ SAMPLE_CASES = {
     # few enough rows (B * R <= the CU count) for the polled draw
     "tree30_polled": dict(seed=71, B=8, Lmax=1500, V=304, R=30, k=7, lens=(3, 2, 1), kappa=1,
                           theta=0.0, vocab=3, tree=True, plant=True),
+    # polled draws over more than 64 (chunk, wave) entries per row (the
+    # two-level search), up to the largest vocabulary
+    "wide_vocab_polled": dict(seed=72, B=3, Lmax=300, V=200000, R=4, k=3, lens=(2, 1), kappa=1,
+                              theta=0.0, vocab=10, plant=True),
+    "max_vocab_polled": dict(seed=73, B=2, Lmax=200, V=524288, R=3, k=2, lens=(2, 1), kappa=1,
+                             theta=-np.inf, vocab=10, plant=True),
     "tree100": dict(seed=63, B=4, Lmax=500, V=40, R=100, k=10, lens=(2, 1), kappa=1, theta=0.0,
                     vocab=2, tree=True, ties=True),
     "w10_d20": dict(seed=64, B=6, Lmax=3000, V=3000, R=204, k=20, lens=(3, 2, 1), kappa=1,
