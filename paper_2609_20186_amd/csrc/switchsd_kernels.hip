@@ -1860,14 +1860,6 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
     LazyMaxLds st;
     st.d = keep;
     lazy_init(st);
-    int done_b = 0;  // units of sequence b streamed here
-    // sequences whose last arrival was this work-group's: their accept
-    // epilogues run after the stream (inline they held this work-group's
-    // remaining chunks back by the epilogue's round trips under full load)
-    unsigned long long pend[Q];
-#pragma unroll
-    for (int q = 0; q < Q; ++q)
-        pend[q] = 0ull;
     for (int u = u0; u < u1; ++u) {
         // the next unit
         int nb = b, nr = r, nc = c + 1, ndn = dnb;
@@ -1890,7 +1882,6 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
         if (u + 1 < u1)
             load_chunk(Bv, row_vecs(nb, nr), nc * kChunkVecs, nq);
         lazy_chunk(A, c * kChunkVecs, nq, st);
-        ++done_b;
         const bool last_unit = u + 1 == u1;
         if (c == cpr - 1 || last_unit) {  // end of this row's piece
             float runM;
@@ -1902,18 +1893,6 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
             }
             lazy_init(st);
         }
-        if ((nb != b || last_unit) && p.epi_accept) {  // end of this sequence's piece
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-            if (tid < 64 && arrive_n(&p.ws.tk_all[b * kLineU32], (uint32_t)done_b,
-                                     (uint32_t)(dnb * cpr))) {
-#pragma unroll
-                for (int q = 0; q < Q; ++q)
-                    if (q == (b >> 6))
-                        pend[q] |= 1ull << (b & 63);
-            }
-            done_b = 0;
-        }
         b = nb;
         r = nr;
         c = nc;
@@ -1922,12 +1901,38 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
         for (int q = 0; q < kUnroll; ++q)
             A[q] = Bv[q];
     }
-    if (tid < 64) {
+    if (!p.epi_accept)
+        return;
+    // The arrivals, once the whole stream is done: one per sequence this
+    // work-group streamed a piece of, lane b mod 64 arriving for sequence b
+    // with the piece's unit count, all in one round trip.  (Arriving at each
+    // sequence's end inside the stream waited there for the chunk in flight
+    // and the atomic's round trip.)  The sequences whose last arrival this
+    // was then run their accept epilogues.
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's row-key atomics are done
+    __syncthreads();
+    if (tid >= 64)
+        return;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    unsigned long long pend[Q];
 #pragma unroll
-        for (int q = 0; q < Q; ++q)
-            for (unsigned long long m = pend[q]; m != 0ull; m &= m - 1ull)
-                final_epilogue<kCommit>(p, 64 * q + __ffsll((long long)m) - 1, sh);
+    for (int q = 0; q < Q; ++q) {
+        const int bq = lane + 64 * q;
+        const int e = first[q] + dnq[q] * cpr;
+        const int n = (u1 < e ? u1 : e) - (u0 > first[q] ? u0 : first[q]);
+        bool last = false;
+        if (bq < p.B && n > 0) {
+            const uint32_t old = __hip_atomic_fetch_add(&p.ws.tk_all[bq * kLineU32], (uint32_t)n,
+                                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            last = old + (uint32_t)n == (uint32_t)(dnq[q] * cpr);
+        }
+        pend[q] = __ballot(last);
     }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        for (unsigned long long m = pend[q]; m != 0ull; m &= m - 1ull)
+            final_epilogue<kCommit>(p, 64 * q + __ffsll((long long)m) - 1, sh);
 }
 
 // ------------------------------------------------------------- draws at T > 0
