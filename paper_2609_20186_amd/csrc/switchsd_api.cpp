@@ -752,7 +752,7 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
     int cus = 0;
     if ((rc = cu_count(&cus)))
         return rc;
-    p.poll_front = p.W == 1 && p.ws.tslot_stride > 0 && B <= cus ? 1 : 0;
+    p.poll_front = p.ws.tslot_stride > 0 && B <= cus ? 1 : 0;
 
     const int64_t cn = copy_nodes(&a->cfg);
     int mode = a->mode;

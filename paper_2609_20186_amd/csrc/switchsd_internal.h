@@ -122,9 +122,10 @@ struct StepParams {
                          // epilogue (no arrivals at tk_all)
     int32_t n_poll_wg;   // verify launch with poll_accept: one waiting work-group per
                          // sequence, first in the grid, runs its accept epilogue
-    int32_t poll_front;  // 1 (the step, one candidate, 1 < scan_tiles <= kMaxPollTiles): each
-                         // scan tile stores its match slots in its own line and the last
-                         // tile polls them (no arrivals at tk_front)
+    int32_t poll_front;  // 1 (the step, 1 < scan_tiles <= kMaxPollTiles): each scan tile
+                         // stores its match slots in its own line (with several candidates
+                         // after its completed candidate lists) and the last tile polls
+                         // them (no arrivals at tk_front)
     int32_t list_mode;   // 1: verify only, a fixed grid streaming the chunks of the drafted
                          // rows r < dn[b] (segs = chunks per row)
     // decode loop: the accept epilogue appends to the context (read-write)

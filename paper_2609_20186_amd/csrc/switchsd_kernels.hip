@@ -3164,6 +3164,19 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
             if (t == 0 && p.scan_probe && lane == 0)
                 st_f32(&p.z[b], probe_combine(sh.scan.ps, sh.scan.pc, p.bias));
             if (p.poll_front) {
+                if (kMulti && p.W > 1) {
+                    // every tile's W most recent ends per length go to its lists
+                    // first (the chooser reads them once the slots are in); a
+                    // tile's slot store follows the completed list stores
+                    int32_t *cb = p.ws.cand + (int64_t)b * p.ws.cand_stride +
+                                  (int64_t)t * SWITCHSD_MAX_NGRAM * p.W;
+                    for (int j = 0; j < p.n_ngram; ++j) {
+                        const int v = merge_waves(p, sh, j);
+                        if (lane < p.W)
+                            st_i32(&cb[j * p.W + lane], v);
+                    }
+                    __builtin_amdgcn_s_waitcnt(0);
+                }
                 if (t + 1 < p.scan_tiles) {
                     // this tile's result in its own slots; nothing waits here
                     // (the test knob withholds sequence 0's first tile)
