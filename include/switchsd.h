@@ -366,11 +366,10 @@ size_t switchsd_workspace_bytes(int32_t B, int32_t R, int32_t Lmax, int32_t n_ca
  *     a sequence's front in switchsd_step waits for the probe's work-group
  *     (dispatched before it); if it gives up, that sequence's switch takes
  *     the neural draft;
- *   - with contexts of 2 to 64 tiles of 1024 tokens, one candidate and B no
- *     larger than the device's compute-unit count, the last scan tile of a
- *     sequence waits for the other tiles' match results (the tiles wait for
- *     nothing); if it gives up, a missing tile counts as holding no
- *     occurrence;
+ *   - with contexts of 2 to 64 tiles of 1024 tokens and B no larger than
+ *     the device's compute-unit count, the last scan tile of a sequence
+ *     waits for the other tiles' match results (the tiles wait for nothing);
+ *     if it gives up, a missing tile counts as holding no occurrence;
  *   - at T = 0 with R <= 64 and B no larger than the device's compute-unit
  *     count, in switchsd_step's fused launch (one candidate) and in the
  *     verification launch (switchsd_verify_accept, and switchsd_step's split
