@@ -2186,36 +2186,38 @@ __device__ void pick_row(const StepParams &p, int b, int r, float m, unsigned lo
 
 typedef unsigned __int128 u128;
 
+// The wave's total of 64-bit integers (every lane).
 __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1)
-        v += __shfl_xor(v, o);
+    return readlane_u64(wave_scan_u64(v), 63);
+}
+// Lane l's 128-bit value (l uniform over the wave).
+__device__ __forceinline__ u128 readlane_u128(u128 v, int l) {
+    return ((u128)readlane_u64((unsigned long long)(v >> 64), l) << 64) |
+           readlane_u64((unsigned long long)v, l);
+}
+// Inclusive prefix sum of 128-bit integers over the lanes, in DPP moves as
+// wave_scan_u64 (kSteps < 6: the first kSteps shifts only).
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ u128 dpp_shift_u128(u128 v) {
+    return ((u128)dpp_shift_u64<kCtrl, kRowMask>((unsigned long long)(v >> 64)) << 64) |
+           dpp_shift_u64<kCtrl, kRowMask>((unsigned long long)v);
+}
+template <int kSteps = 6>
+__device__ __forceinline__ u128 wave_scan_u128(u128 v) {
+    v += dpp_shift_u128<0x111, 0xf>(v);
+    v += dpp_shift_u128<0x112, 0xf>(v);
+    v += dpp_shift_u128<0x114, 0xf>(v);
+    if (kSteps > 3)
+        v += dpp_shift_u128<0x118, 0xf>(v);
+    if (kSteps > 4)
+        v += dpp_shift_u128<0x142, 0xa>(v);
+    if (kSteps > 5)
+        v += dpp_shift_u128<0x143, 0xc>(v);
     return v;
 }
-__device__ __forceinline__ u128 shfl_u128(u128 v, int src) {
-    const unsigned long long lo = __shfl((unsigned long long)v, src);
-    const unsigned long long hi = __shfl((unsigned long long)(v >> 64), src);
-    return ((u128)hi << 64) | lo;
-}
+// The wave's total of 128-bit integers (every lane).
 __device__ __forceinline__ u128 wave_sum_u128(u128 v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const unsigned long long lo = __shfl_xor((unsigned long long)v, o);
-        const unsigned long long hi = __shfl_xor((unsigned long long)(v >> 64), o);
-        v += ((u128)hi << 64) | lo;
-    }
-    return v;
-}
-__device__ __forceinline__ u128 wave_prefix_u128(u128 v) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const unsigned long long lo = __shfl_up((unsigned long long)v, o);
-        const unsigned long long hi = __shfl_up((unsigned long long)(v >> 64), o);
-        if (lane >= o)
-            v += ((u128)hi << 64) | lo;
-    }
-    return v;
+    return readlane_u128(wave_scan_u128(v), 63);
 }
 // Upper 128 bits of the 192-bit product a * b.
 __device__ __forceinline__ u128 mulhi_128_64(u128 a, unsigned long long b) {
@@ -2774,6 +2776,7 @@ __device__ void spec_row_load(const StepParams &p, int b, int r, SpecRow &s) {
 __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) {
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)b * p.R + a;
+    const unsigned long long uni = p.uniforms[row];  // requested with the entries
     auto chunk_total = [&](bool use_p) -> u128 {
         u128 cc = 0;
         if (lane < p.cpr)
@@ -2782,25 +2785,26 @@ __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) 
         return cc;
     };
     u128 cc = chunk_total(false);
-    u128 inc = wave_prefix_u128(cc);
-    u128 S = shfl_u128(inc, 63);
+    u128 inc = wave_scan_u128(cc);
+    u128 S = readlane_u128(inc, 63);
     const bool use_p = S == 0;
     if (use_p) {
         cc = chunk_total(true);
-        inc = wave_prefix_u128(cc);
-        S = shfl_u128(inc, 63);
+        inc = wave_scan_u128(cc);
+        S = readlane_u128(inc, 63);
     }
-    const unsigned long long uni = p.uniforms[row];
+    // (the chunk, the block and the vector exist, the target being below the
+    // total; the clamps only keep every index in range)
     u128 tg = mulhi_128_64(S, uni);
-    const unsigned long long hit = __ballot(lane < p.cpr && inc > tg);
-    const int cst = __ffsll((long long)hit) - 1;  // exists: target < S
-    tg -= shfl_u128(inc - cc, cst);
+    int cst = __ffsll((long long)__ballot(lane < p.cpr && inc > tg)) - 1;
+    cst = cst < 0 ? 0 : cst;
+    tg -= readlane_u128(inc - cc, cst);
     const u128 ce =
         lane < kResBlocks ? entry_value(resid_entry(p, b, cst * kResBlocks + lane), use_p) : 0;
-    const u128 ie = wave_prefix_u128(ce);
-    const unsigned long long hit2 = __ballot(lane < kResBlocks && ie > tg);
-    const int est = __ffsll((long long)hit2) - 1;
-    tg -= shfl_u128(ie - ce, est);
+    const u128 ie = wave_scan_u128<4>(ce);  // lanes 0..15
+    int est = __ffsll((long long)__ballot(lane < kResBlocks && ie > tg)) - 1;
+    est = est < 0 ? 0 : est;
+    tg -= readlane_u128(ie - ce, est);
     // the block's 64 vectors, one per lane
     const int nq = p.V >> 3;
     const int q = (cst * kResBlocks + est) * 64 + lane;
@@ -2816,42 +2820,45 @@ __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) 
         if (use_p)
             w = ps;
     }
-    const u128 iv = wave_prefix_u128(w);
-    const unsigned long long hit3 = __ballot(iv > tg);
-    const int lst = __ffsll((long long)hit3) - 1;  // exists: tg < the block's sum
-    int y = 0;
-    if (lane == lst) {
-        u128 run = iv - w;
-        int e = 7;
-        for (int j = 0; j < 8; ++j) {
-            const uint32_t hp = xp[j >> 1], hq = xq[j >> 1];
-            unsigned long long P;
-            const u128 r = resid_weight((j & 1) ? hi_f(hp) : lo_f(hp),
-                                        (j & 1) ? hi_f(hq) : lo_f(hq), 8 * q + j, sr, p.samp_c, P);
-            run += use_p ? (u128)P : r;
-            if (run > tg) {
-                e = j;
-                break;
-            }
-        }
-        y = 8 * q + e;
+    const u128 iv = wave_scan_u128(w);
+    int lst = __ffsll((long long)__ballot(iv > tg)) - 1;
+    lst = lst < 0 ? 0 : lst;
+    tg -= readlane_u128(iv - w, lst);
+    // that vector's 8 weights in lanes 0..7, their inclusive prefix
+    const int ls = __builtin_amdgcn_readfirstlane(lst);
+    const int wj = (lane >> 1) & 3;
+    uint32_t hp = 0, hq = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t xpk = (uint32_t)__builtin_amdgcn_readlane((int)xp[k], ls);
+        const uint32_t xqk = (uint32_t)__builtin_amdgcn_readlane((int)xq[k], ls);
+        hp = wj == k ? xpk : hp;
+        hq = wj == k ? xqk : hq;
     }
-    return __shfl(y, lst);
+    const int qs = (cst * kResBlocks + est) * 64 + ls;
+    u128 ew = 0;
+    if (lane < 8) {
+        unsigned long long P;
+        const u128 r = resid_weight((lane & 1) ? hi_f(hp) : lo_f(hp),
+                                    (lane & 1) ? hi_f(hq) : lo_f(hq), 8 * qs + lane, sr, p.samp_c,
+                                    P);
+        ew = use_p ? (u128)P : r;
+    }
+    ew = wave_scan_u128<3>(ew);
+    int e = __ffsll((long long)__ballot(lane < 8 && ew > tg)) - 1;
+    e = e < 0 ? 7 : e;
+    return 8 * qs + e;
 }
-
-// Outputs of a chain verified with q that ends at row a (wave 0): the
-// accepted tokens dtok[1..a], then the emitted token at row a, -1 after;
-// amax holds the same per row.  With the decode loop's commit the tokens are
-// appended to the context too.  Clears the sequence's row keys.
+// Outputs of a sequence verified with q: accepted prefix a, then the emitted
+// token (bonus).  dt: lane i's drafted token i + 1 (i < 64), read before the
+// draw; cL: the context length (decode loop).
 template <bool kCommit>
-__device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus) {
+__device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus, int dt, int cL) {
     const int lane = threadIdx.x & 63;
     const int64_t base = (int64_t)b * p.R;
-    int cL = 0;
-    if (kCommit)
-        cL = clampi(p.clen[b], 0, p.Lmax);
     for (int i = lane; i < p.R; i += 64) {
-        const int v = i < a ? ld_i32(&p.dtok[base + i + 1]) : (i == a ? bonus : -1);
+        const int v =
+            i < a ? (i < 64 ? dt : ld_i32(&p.dtok[base + i + 1])) : (i == a ? bonus : -1);
         p.out_tokens[base + i] = v;
         if (p.amax)
             p.amax[base + i] = v;
@@ -2936,10 +2943,13 @@ __global__ __launch_bounds__(kThreads) void k_spec_residual(StepParams p) {
     if (arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)p.rsegs)) {
         if (lane == 0)
             st_u32(&p.ws.tk_all[b * kLineU32], 0u);
+        // the epilogue's reads, requested before the draw's
+        const int dt = lane + 1 < p.R ? ld_i32(&p.dtok[(int64_t)b * p.R + lane + 1]) : -1;
+        const int cL = kCommit ? clampi(p.clen[b], 0, p.Lmax) : 0;
         const int bonus = resid ? resid_draw(p, b, a, sr)
                                 : decode_key(ld_u64(&p.ws.keys[(int64_t)b * p.ws.key_stride +
                                                                dnb - 1]));
-        spec_epilogue<kCommit>(p, b, a, bonus);
+        spec_epilogue<kCommit>(p, b, a, bonus, dt, cL);
     }
 }
 
