@@ -502,10 +502,11 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     // the accept epilogue (sequences verified with q: the residual launch does)
     if ((rc = launch_sample_sums_kernel(p, grid, stream)) || !q)
         return rc;
-    // residual: one work-group per 256 vectors (4 KB) of the rejected row,
-    // one vector per lane, covering every block of every chunk (the draw sums
-    // 16 block entries per chunk; blocks past the row's end write zero)
-    p.rsegs = p.cpr * (kChunkVecs / kThreads);
+    // residual: one work-group per 512 vectors (8 KB) of the rejected row,
+    // two blocks of 64 vectors per wave, covering every block of every chunk
+    // (the draw sums 16 block entries per chunk; blocks past the row's end
+    // write zero)
+    p.rsegs = p.cpr * (kChunkVecs / kThreads) / 2;
     const int64_t rgrid = (int64_t)p.B * p.rsegs;
     if (!grid_ok(rgrid))
         return SWITCHSD_ESHAPE;

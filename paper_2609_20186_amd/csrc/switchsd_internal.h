@@ -155,7 +155,7 @@ struct StepParams {
                                       // rejected row: residual sum (lo, hi), P sum, unused
     uint32_t *rdec;                   // [B, R] test of row r: 1 accepted, 2 rejected
     unsigned long long *rz;           // [B, R, 2] Zp, Zq of each tested row
-    int32_t rsegs;                    // residual work-groups per sequence (4 KB each)
+    int32_t rsegs;                    // residual work-groups per sequence (8 KB each)
     // bounded waits: spin limit of the front's wait for the probe flag and of
     // its poll of the segment slots; with withhold_flag (a test knob) the
     // probe never sets its flag
