@@ -456,7 +456,7 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
     const bool polled = p.csum_clear && !stream_sums;
     p.csum_clear = 0;
     const int64_t rows = (int64_t)p.B * p.R;
-    if (q) {
+    if (q && !p.qmax) {
         // the q row maxima: the argmax role alone, over the rows with a
         // drafted child of the sequences verified with q
         StepParams pq = p;
@@ -465,6 +465,7 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
         pq.n_front_wg = pq.n_scan_wg = pq.n_poll_wg = 0;
         pq.poll_accept = 0;
         pq.csum_clear = 0;
+        pq.qmax = 0;
         pq.probe_on = pq.scan_probe = 0;
         pq.epi_front = EPI_NONE;
         pq.epi_accept = 0;
@@ -480,10 +481,12 @@ int sample_finish(StepParams p, const SampleArgs *sa, bool speculate, hipStream_
         if ((rc = launch_step_kernel(pq, g, stream)))
             return rc;
     }
-    // about six sum work-groups per CU, all resident at once (eight fit).
-    // Measured on C2 at T = 0.7 (16 chunks per row): 2, 3, 4, 6, 8 and 16 per
-    // CU gave 42.2, 39.1, 39.6, 38.6, 40.2 and 42.8 us per step.
-    int64_t segs = (6 * (int64_t)cus + rows - 1) / rows;
+    // about six sum work-groups per CU, as many as stay resident (with q,
+    // three for the p rows and three for the q rows).  Measured on C2 at
+    // T = 0.7 (16 chunks per row): 2, 3, 4, 6, 8 and 16 per CU gave 42.2,
+    // 39.1, 39.6, 38.6, 40.2 and 42.8 us per step; with q, six per CU per
+    // tensor (two batches) 80.2 us against 77.4 us for three.
+    int64_t segs = ((q ? 3 : 6) * (int64_t)cus + rows - 1) / rows;
     if (segs > p.cpr)
         segs = p.cpr;
     if (segs < 1)
@@ -564,7 +567,9 @@ int verify_launch(const uint16_t *logits, int32_t B, int32_t R, int32_t V, const
             p.poll_accept = 1;
             p.n_poll_wg = B;
         }
-        grid = p.n_poll_wg + (int64_t)B * R * p.segs;
+        // with the draft's q the same launch also takes the q row maxima
+        p.qmax = sa && sa->qlogits && p.W == 1 ? 1 : 0;
+        grid = p.n_poll_wg + (int64_t)B * R * p.segs * (1 + p.qmax);
         if (!grid_ok(grid))
             return SWITCHSD_ESHAPE;
     }
@@ -764,7 +769,10 @@ int switchsd_step(const switchsd_step_args *a, void *workspace, size_t workspace
         const int64_t cap = kMaxPollSlots / R < kMaxSegs ? kMaxPollSlots / R : kMaxSegs;
         if ((rc = set_segments(p, (int64_t)B * R, V, cap < 1 ? 1 : cap)))
             return rc;
-        const int64_t grid = p.n_front_wg + (int64_t)B * R * p.segs;
+        // with the draft's q the same launch also takes the q row maxima
+        // (before the draft is chosen: the neural draft's rows)
+        p.qmax = sampled && sa.qlogits && p.W == 1 ? 1 : 0;
+        const int64_t grid = p.n_front_wg + (int64_t)B * R * p.segs * (1 + p.qmax);
         if (!grid_ok(grid))
             return SWITCHSD_ESHAPE;
         p.rows_mode = cn >= R ? ROWS_ALL : ROWS_NEURAL_OR_COPY;

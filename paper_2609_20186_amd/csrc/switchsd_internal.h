@@ -145,6 +145,9 @@ struct StepParams {
                                // and row 0's runs the accept epilogue (no arrivals)
     int32_t csum_clear;        // the row maxima launch before a polled draw: each argmax
                                // work-group zeroes its share of its row's sum slots
+    int32_t qmax;              // 1: the row maxima launch also takes the draft's q rows, its
+                               // last B * R * segs work-groups (q keys); else a launch of
+                               // their own follows
     // speculative sampling with the draft's own distribution q (chains, T > 0)
     const uint16_t *qlogits;          // [B, R, V] the draft's logits, or null (one-hot drafts)
     const uint64_t *accept_uniforms;  // [B, R] uniforms of the accept tests

@@ -751,8 +751,22 @@ __device__ __forceinline__ void load_chunk(u32x4 (&v)[kUnroll], const u32x4 *vp,
 }
 
 // Segment s of row r of sequence b.
-__device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh, u32x4 *keep) {
+// qpart: a segment of the draft's logits (row maxima of q, into the q keys)
+// in a row maxima launch that takes the q rows too.
+__device__ __forceinline__ uint32_t q_rows(const StepParams &p, int b) {
+    // with the front in the same launch the draft is not chosen yet: the rows
+    // of the neural draft that have a drafted child (a copy draft's q is
+    // one-hot and needs none); else the rows with a drafted child of the
+    // sequences verified with q
+    if (p.epi_front == EPI_SELECT)
+        return (uint32_t)(clampi(p.nn[b], 1, p.R) - 1);
+    return spec_seq(p, b) ? (uint32_t)(clampi(ld_i32(&p.dn[b]), 1, p.R) - 1) : 0u;
+}
+
+__device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh, u32x4 *keep,
+                            bool qpart = false) {
     const int tid = threadIdx.x;
+    const uint16_t *lg = qpart ? p.qlogits : p.logits;
     const int64_t rowoff = ((int64_t)b * p.R + r) * p.V;
     const int64_t e0 = (int64_t)s * p.seg_elems;
     const int64_t e1 = e0 + p.seg_elems < p.V ? e0 + p.seg_elems : (int64_t)p.V;
@@ -760,13 +774,13 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
     // aligned interior [a0, a1) is read with 16-byte loads, the head [g0, a0)
     // and the tail [a1, g1) (at most 7 elements each) one element per lane.
     const int64_t g0 = rowoff + e0, g1 = rowoff + e1;
-    const int64_t mis = (int64_t)((((uintptr_t)p.logits) >> 1) + (uint64_t)g0) & 7;
+    const int64_t mis = (int64_t)((((uintptr_t)lg) >> 1) + (uint64_t)g0) & 7;
     int64_t a0 = g0 + ((8 - mis) & 7);
     if (a0 > g1)
         a0 = g1;
     const int64_t a1 = a0 + ((g1 - a0) & ~(int64_t)7);
     const int nq = (int)((a1 - a0) >> 3);
-    const u32x4 *vp = reinterpret_cast<const u32x4 *>(p.logits + a0);
+    const u32x4 *vp = reinterpret_cast<const u32x4 *>(lg + a0);
     const uint32_t ebase = (uint32_t)(a0 - rowoff);
 
     const int nhead = (int)(a0 - g0), ntail = (int)(g1 - a1);
@@ -775,11 +789,11 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
         xg = g0 + tid;
     else if (tid < nhead + ntail)
         xg = a1 + (tid - nhead);
-    const float xv = xg >= 0 ? lo_f((uint32_t)p.logits[xg]) : -__builtin_inff();
+    const float xv = xg >= 0 ? lo_f((uint32_t)lg[xg]) : -__builtin_inff();
     const uint32_t xi = (uint32_t)(xg - rowoff);
     const bool has_x = xg >= 0;
 
-    if (p.csum_clear) {
+    if (p.csum_clear && !qpart) {
         // this segment's share of the row's weight-sum slots, zeroed for the
         // pollers of the sum launch that follows (the polled draw at T > 0)
         const int n = p.cpr * kCsumPerChunk;
@@ -797,7 +811,7 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
     const bool spec = p.speculate && nch > 0;
     if (spec)
         load_chunk(A, vp, 0, nq);
-    if ((uint32_t)r >= rows_needed(p, b)) {
+    if ((uint32_t)r >= (qpart ? q_rows(p, b) : rows_needed(p, b))) {
         __builtin_amdgcn_s_waitcnt(0);
         return;
     }
@@ -849,7 +863,10 @@ __device__ void argmax_role(const StepParams &p, int b, int r, int s, Shared &sh
         const unsigned long long key =
             best != kNoIdx ? ((unsigned long long)order_key(M) << 32) | (0xFFFFFFFFu - best)
                            : 0ull;
-        if (p.poll_accept) {
+        if (qpart) {
+            if (key)
+                atomicMax(&p.ws.qkeys[(int64_t)b * p.ws.key_stride + r], key);
+        } else if (p.poll_accept) {
             // the segment's own slot (1: no candidate); nothing waits for the
             // store here, the sequence's epilogue polls for it
             if (!(p.withhold_seg && b == 0 && r == 0 && s == 0))
@@ -2333,10 +2350,16 @@ __device__ void row_done(const StepParams &p, int b, int r, int dnb, uint32_t un
             pick_row(p, b, r, m, keyp, sh);
     }
     if (tid < 64 && arrive(&p.ws.tk_all[b * kLineU32], (uint32_t)dnb)) {
-        if (spec)
+        if (spec) {
             st_u32(&p.ws.tk_all[b * kLineU32], 0u);  // the residual launch closes it
-        else
+        } else {
             final_epilogue<kCommit>(p, b, sh);
+            // q row maxima taken before the draft was chosen (the maxima
+            // launch's q part) are not used by a copy draft: cleared here
+            if (p.qlogits)
+                for (int i = tid; i < p.R; i += 64)
+                    st_u64(&p.ws.qkeys[(int64_t)b * p.ws.key_stride + i], 0ull);
+        }
     }
     __syncthreads();
 }
@@ -3127,7 +3150,10 @@ __device__ __forceinline__ int xcd_row(int blk, int rowi0, int nrows) {
     return (nrows & 7) == 0 ? (blk & 7) * (nrows >> 3) + (rowi0 >> 3) : rowi0;
 }
 
-template <bool kMulti, bool kCommit>
+// kQ: the row maxima launch before a draw at T > 0 that also takes the
+// draft's q rows (qmax; compiled apart, so that the other launches keep their
+// code).
+template <bool kMulti, bool kCommit, bool kQ = false>
 __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
     TL_MARK(0);
     // the argmax role's kept chunks share the union: the role is over (every
@@ -3154,12 +3180,15 @@ __global__ __launch_bounds__(kThreads) void k_switchsd(StepParams p) {
         // dispatch stream more slowly (they share their CUs with ones issued
         // earlier), and a sequence waits for its slowest segment; so every
         // sequence gets segments from the whole dispatch order.
-        const int idx = blk - p.n_front_wg;
+        // (with qmax, the same again over the draft's logits after them)
+        const int idx0 = blk - p.n_front_wg;
         const int nrows = p.B * p.R;
+        const bool qpart = kQ && idx0 >= nrows * p.segs;
+        const int idx = qpart ? idx0 - nrows * p.segs : idx0;
         const int s = idx / nrows;
         const int rowi = xcd_row(blk, idx - s * nrows, nrows);
         b = rowi / p.R;
-        argmax_role(p, b, rowi - b * p.R, s, sh, sh.am.keep);
+        argmax_role(p, b, rowi - b * p.R, s, sh, sh.am.keep, qpart);
         role = 2;
     }
     TL_MARK(1);
@@ -3419,6 +3448,12 @@ int launch_step_kernel(const StepParams &p, int64_t grid, hipStream_t stream) {
     else if (p.W > 1)
         hipLaunchKernelGGL((k_switchsd<true, false>), dim3((unsigned)grid), dim3(kThreads), 0,
                            stream, p);
+    else if (p.qmax && p.commit)
+        hipLaunchKernelGGL((k_switchsd<false, true, true>), dim3((unsigned)grid), dim3(kThreads),
+                           0, stream, p);
+    else if (p.qmax)
+        hipLaunchKernelGGL((k_switchsd<false, false, true>), dim3((unsigned)grid),
+                           dim3(kThreads), 0, stream, p);
     else if (p.commit)
         hipLaunchKernelGGL((k_switchsd<false, true>), dim3((unsigned)grid), dim3(kThreads), 0,
                            stream, p);
