@@ -552,13 +552,24 @@ def main():
     # the algorithmic bytes (ops) of one launch (call) by its own duration,
     # each launch bracketed by its own HIP events on the launch stream
     launch_ms = ms
+    # the row maxima launch also takes the q rows unless it streams long
+    # drafts (and, in the step, unless there are several copy candidates)
+    listed = wl.R > 64 and wl.B <= 256 and wl.V % 8 == 0
+    q_merged_verify = qdev is not None and not listed
+    q_merged = (qdev is not None and max(1, wl.n_cand) == 1 and
+                not (mode == sd.MODE_SPLIT and listed))
     if T > 0:
         qrows = 0 if qdev is None else int(np.sum(np.clip(sel["dn"] - 1, 0, None) *
                                                   (sel["use_copy"] == 0)))
         ops = (vbytes / 2 + qrows * wl.V) * SAMPLE_OPS_PER_LOGIT
-        dom = {"kernel": "sampled verification (row maxima, then weight sums with the draw"
-                         + (", q maxima and residual draw: 4 launches)" if qdev is not None
-                            else ": 2 launches)"),
+        dom = {"kernel": ("sampled verification (row maxima of p and q, then weight sums with "
+                          "the accept tests, then the residual draw: 3 launches)"
+                          if q_merged_verify else
+                          "sampled verification (row maxima, q row maxima, weight sums with the "
+                          "accept tests, residual draw: 4 launches)"
+                          if qdev is not None else
+                          "sampled verification (row maxima, then weight sums with the draw: "
+                          "2 launches)"),
                "bound": "alu", "unit": "TOP/s (VALU lane-ops)", "peak": round(VALU_PEAK_TOPS, 1),
                "gbps": ops / (vms * 1e-3) / 1e12, "bytes": int(ops), "ms": vms,
                "traffic_file": f"traffic_sampled_verify_{wl.name}.json"}
@@ -600,7 +611,13 @@ def main():
                                f" kappa={wl.kappa}" + (f" T={T}" if T > 0 else ""),
                    "global_batch": wl.B, "seq_len": wl.L, "parallelism": "none (1 GPU)",
                    "launch": {1: "fused, 1 kernel", 2: "split, 2 kernels"}[mode] +
-                             (" + 1 kernel for the weight sums and the draw at T > 0" if T > 0 else ""),
+                             ("" if T <= 0 else
+                              " + 1 kernel for the weight sums and the draw at T > 0"
+                              if qdev is None else
+                              (" (with the q row maxima)" if q_merged else
+                               " + 1 kernel for the q row maxima") +
+                              " + 2 kernels for the weight sums with the accept tests and the"
+                              " residual draw"),
                    "rotation_sets": nrot},
         "roofline": {"bound": dom.get("bound", "hbm"), "achieved": round(dom["gbps"], 1),
                      "peak": dom.get("peak", HBM_PEAK_GBPS), "unit": dom.get("unit", "GB/s"),
