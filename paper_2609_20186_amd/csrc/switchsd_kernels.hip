@@ -23,23 +23,30 @@
 //           looks up the lowest index holding it once, at the end, before
 //           one wave reduction.
 //           The segment result is packed as (order key << 32 | ~index) and
-//           atomicMax-ed into the row's slot.  (Sec. 2 / App. A: greedy
-//           verification, T = 0.)
+//           stored in the segment's own slot (or atomicMax-ed into the row's
+//           key).  (Sec. 2 / App. A: greedy verification, T = 0.)
 //
-// Two last-arriver epilogues close a sequence without a second launch:
-//   front   when its scan tiles and probe are done: pick the match, gather the
+// Two epilogues close a sequence without a second launch:
+//   front   once its scan tiles and probe are done: pick the match, gather the
 //           copy candidates, apply the switch (Sec. 3.3, Eq. 4) and write the
 //           chosen draft (W candidates: W chains behind the anchor);
-//   final   when every work-group of the sequence is done: decode the row
-//           argmaxes and run the accept walk (Sec. 3.3, Parallel Verification):
-//           a ballot for chains and pointer jumping over trees, in registers
-//           (one node per lane) up to 64 nodes and in LDS beyond.
-// With the decode loop's commit the final epilogue also appends the accepted
-// tokens and the bonus to the context.  Each epilogue resets the workspace
-// slots it consumed, leaving them zeroed for the next call.
+//   accept  once every row maximum is in: decode the row argmaxes and run the
+//           accept walk (Sec. 3.3, Parallel Verification): a ballot for chains
+//           and pointer jumping over trees, in registers (one node per lane)
+//           up to 64 nodes and in LDS beyond.
+// Where few enough work-groups wait (one per sequence, B no larger than the
+// CU count), the hand-offs are polled: the last scan tile polls the other
+// tiles' slots and runs the front, then, holding the draft, polls the argmax
+// segments' slots and runs the accept epilogue; every other work-group stores
+// its result and ends.  Otherwise the last work-group to arrive at a ticket
+// runs the epilogue.  With the decode loop's commit the accept epilogue also
+// appends the accepted tokens and the bonus to the context.  Each epilogue
+// resets the workspace slots it consumed, leaving them zeroed for the next
+// call.
 //
-// Further kernels: k_verify_stream (verification of long drafts over a fixed
-// grid), k_sample_sums / k_sample_sums_stream (verification at
+// Further kernels: k_verify_poll (the greedy verify launch with polling),
+// k_verify_stream (verification of long drafts over a fixed grid),
+// k_sample_sums / k_sample_sums_stream and k_spec_residual (verification at
 // sampling temperature T > 0), k_select and k_commit (stage entry points),
 // k_tree_mask (the verification mask), k_label_insert / k_label_write /
 // k_label_clear (copy-mode labels for probe training).
