@@ -2926,15 +2926,25 @@ template <bool kCommit>
 __global__ __launch_bounds__(kThreads) void k_spec_residual(StepParams p) {
     const int s = blockIdx.x / p.B, b = blockIdx.x - s * p.B;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    if (!spec_seq(p, b))
+    // whether the sequence was verified with q, its draft length and the
+    // first 64 rows' tests, requested together
+    const int copy = p.spec_copy ? ld_i32(&p.spec_copy[b]) : 0;
+    const int dn_raw = ld_i32(&p.dn[b]);
+    const uint32_t dec0 = lane < p.R ? __hip_atomic_load(&p.rdec[(int64_t)b * p.R + lane],
+                                                         __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)
+                                     : 1u;
+    if (!p.qlogits || copy != 0)  // not verified with q (spec_seq)
         return;
-    const int dnb = clampi(ld_i32(&p.dn[b]), 1, p.R);
+    const int dnb = clampi(dn_raw, 1, p.R);
     int a = dnb - 1;
     for (int r0 = 0; r0 < dnb - 1; r0 += 64) {
         const int r = r0 + lane;
         const bool rej = r < dnb - 1 &&
-                         __hip_atomic_load(&p.rdec[(int64_t)b * p.R + r], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT) != 1u;
+                         (r0 == 0 ? dec0
+                                  : __hip_atomic_load(&p.rdec[(int64_t)b * p.R + r],
+                                                      __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)) != 1u;
         const unsigned long long m = __ballot(rej);
         if (m) {
             a = r0 + __ffsll((long long)m) - 1;
