@@ -58,6 +58,41 @@ def test_probe_wait_give_up_is_reported(mode):
     assert int(ws.count_nonzero()) == 0
 
 
+def test_tile_poll_give_up_several_candidates():
+    """With W = 10 copy candidates the scan tiles store their candidate lists
+    before their slots; with sequence 0's first tile withheld the last tile's
+    poll gives up, the status reports it, every other sequence still matches
+    the oracle, the workspace is left zeroed once the status call has read the
+    error, and the next step matches again."""
+    import torch
+    from paper_2609_20186_amd import binding as sd
+    say("[errors] withheld scan tile, W = 10, split step")
+    d = planted_workload("C2W10", batch=range(8))
+    B, R = d["ntok"].shape
+    dev = to_device(d)
+    ws = sd.alloc_workspace(B, R, d["tokens"].shape[1], d["cfg"]["n_cand"])
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    exp = oracle_step(d)
+    sd.withhold_segment_for_tests(True)
+    try:
+        got, ws = gpu_step(dev, d, SPLIT, ws=ws)
+    finally:
+        sd.withhold_segment_for_tests(False)
+    sd.switchsd_workspace_status(ws, B, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == EDEVICE
+    rest = slice(1, None)
+    assert_match(got, {k: v[rest] for k, v in exp.items()}, rows=rest,
+                 what="other sequences while sequence 0's tile poll gave up")
+    assert int(ws.count_nonzero()) == 0
+    got, ws = gpu_step(dev, d, SPLIT, ws=ws)
+    assert_match(got, exp, what="after the tile give-up")
+    sd.switchsd_workspace_status(ws, B, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert int(ws.count_nonzero()) == 0
+
+
 def test_draw_poll_give_up_is_reported():
     """At T > 0 the row pollers of the draw wait for the rows' weight sums;
     with sequence 0's first sum work-group of row 0 withheld (and its first
