@@ -213,8 +213,9 @@ int switchsd_verify_accept(const uint16_t *logits, int32_t B, int32_t R, int32_t
  *   Launches: the row maxima, then the weight sums, in which one work-group per
  *   row draws the row's token (without q, R <= 64 and B * R no larger than the
  *   compute-unit count: the row's first, polling the others' sums; else the
- *   last to arrive); with q also the q row maxima (second) and the residual
- *   draw (last). */
+ *   last to arrive); with q the first launch also takes the q row maxima (a
+ *   launch of their own for streamed long drafts), the weight sums take the
+ *   accept tests, and the residual draw comes last. */
 int switchsd_verify_sample(const uint16_t *logits, int32_t B, int32_t R, int32_t V,
                            float temperature, const uint64_t *uniforms,
                            const uint16_t *draft_logits, const uint64_t *accept_uniforms,
