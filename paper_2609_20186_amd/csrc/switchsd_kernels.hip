@@ -2799,45 +2799,91 @@ __device__ void spec_row_load(const StepParams &p, int b, int r, SpecRow &s) {
 }
 
 // The draw after a rejection at row a (wave 0): the blocks' residual sums
-// give S and the target floor(u S / 2^64); the chunk (16 blocks), the block,
-// the vector (one per lane, p and q read again) and the element follow by
-// prefix sums.  With S = 0 (no residual mass) the same search runs over the
+// give S and the target floor(u S / 2^64); the block (read in one round trip,
+// four per lane, up to 256 blocks; beyond that the chunk of 16 blocks first,
+// then its block), the vector (one per lane, p and q read again) and the
+// element follow by prefix sums.  With S = 0 (no residual mass) the same search runs over the
 // blocks' P sums: the draw from p.  Returns the token in every lane.
 __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) {
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)b * p.R + a;
     const unsigned long long uni = p.uniforms[row];  // requested with the entries
-    auto chunk_total = [&](bool use_p) -> u128 {
-        u128 cc = 0;
-        if (lane < p.cpr)
-            for (int e = 0; e < kResBlocks; ++e)
-                cc += entry_value(resid_entry(p, b, lane * kResBlocks + e), use_p);
-        return cc;
-    };
-    u128 cc = chunk_total(false);
-    u128 inc = wave_scan_u128(cc);
-    u128 S = readlane_u128(inc, 63);
-    const bool use_p = S == 0;
-    if (use_p) {
-        cc = chunk_total(true);
-        inc = wave_scan_u128(cc);
-        S = readlane_u128(inc, 63);
-    }
+    const int nb = p.cpr * kResBlocks;                // the row's blocks of 64 vectors
     // (the chunk, the block and the vector exist, the target being below the
     // total; the clamps only keep every index in range)
-    u128 tg = mulhi_128_64(S, uni);
-    int cst = __ffsll((long long)__ballot(lane < p.cpr && inc > tg)) - 1;
-    cst = cst < 0 ? 0 : cst;
-    tg -= readlane_u128(inc - cc, cst);
-    const u128 ce =
-        lane < kResBlocks ? entry_value(resid_entry(p, b, cst * kResBlocks + lane), use_p) : 0;
-    const u128 ie = wave_scan_u128<4>(ce);  // lanes 0..15
-    int est = __ffsll((long long)__ballot(lane < kResBlocks && ie > tg)) - 1;
-    est = est < 0 ? 0 : est;
-    tg -= readlane_u128(ie - ce, est);
+    u128 tg;
+    int blk;  // the block holding the target
+    bool use_p;
+    if (nb <= 4 * 64) {
+        // every block's sum in one round trip, blocks 4 l .. 4 l + 3 in lane l
+        auto load4 = [&](bool from_p, u128 (&e4)[4]) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int e = 4 * lane + k;
+                e4[k] = e < nb ? entry_value(resid_entry(p, b, e), from_p) : (u128)0;
+            }
+        };
+        u128 e4[4];
+        load4(false, e4);
+        u128 ls = e4[0] + e4[1] + e4[2] + e4[3];
+        u128 inc = wave_scan_u128(ls);
+        u128 S = readlane_u128(inc, 63);
+        use_p = S == 0;
+        if (use_p) {
+            load4(true, e4);
+            ls = e4[0] + e4[1] + e4[2] + e4[3];
+            inc = wave_scan_u128(ls);
+            S = readlane_u128(inc, 63);
+        }
+        tg = mulhi_128_64(S, uni);
+        int l = __ffsll((long long)__ballot(inc > tg)) - 1;
+        l = l < 0 ? 0 : l;
+        tg -= readlane_u128(inc - ls, l);
+        // lane l's four blocks, in order
+        int k = 3;
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            const u128 v = readlane_u128(e4[j], l);
+            if (k == 3 && tg < v)
+                k = j;
+            else if (k == 3)
+                tg -= v;
+        }
+        blk = 4 * l + k;
+    } else {
+        // chunk totals (16 blocks each), then the blocks of the chunk holding
+        // the target: two round trips
+        auto chunk_total = [&](bool from_p) -> u128 {
+            u128 cc = 0;
+            if (lane < p.cpr)
+                for (int e = 0; e < kResBlocks; ++e)
+                    cc += entry_value(resid_entry(p, b, lane * kResBlocks + e), from_p);
+            return cc;
+        };
+        u128 cc = chunk_total(false);
+        u128 inc = wave_scan_u128(cc);
+        u128 S = readlane_u128(inc, 63);
+        use_p = S == 0;
+        if (use_p) {
+            cc = chunk_total(true);
+            inc = wave_scan_u128(cc);
+            S = readlane_u128(inc, 63);
+        }
+        tg = mulhi_128_64(S, uni);
+        int cst = __ffsll((long long)__ballot(lane < p.cpr && inc > tg)) - 1;
+        cst = cst < 0 ? 0 : cst;
+        tg -= readlane_u128(inc - cc, cst);
+        const u128 ce =
+            lane < kResBlocks ? entry_value(resid_entry(p, b, cst * kResBlocks + lane), use_p) : 0;
+        const u128 ie = wave_scan_u128<4>(ce);  // lanes 0..15
+        int est = __ffsll((long long)__ballot(lane < kResBlocks && ie > tg)) - 1;
+        est = est < 0 ? 0 : est;
+        tg -= readlane_u128(ie - ce, est);
+        blk = cst * kResBlocks + est;
+    }
     // the block's 64 vectors, one per lane
     const int nq = p.V >> 3;
-    const int q = (cst * kResBlocks + est) * 64 + lane;
+    const int q = blk * 64 + lane;
     const u32x4 *pv = reinterpret_cast<const u32x4 *>(p.logits + row * p.V);
     const u32x4 *qv = reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V);
     u32x4 xp = u32x4{0u, 0u, 0u, 0u}, xq = u32x4{0u, 0u, 0u, 0u};
@@ -2865,7 +2911,7 @@ __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) 
         hp = wj == k ? xpk : hp;
         hq = wj == k ? xqk : hq;
     }
-    const int qs = (cst * kResBlocks + est) * 64 + ls;
+    const int qs = blk * 64 + ls;
     u128 ew = 0;
     if (lane < 8) {
         unsigned long long P;

@@ -116,6 +116,10 @@ SPEC_CASES = {
                        theta=np.inf, vocab=30),
     "wide_batch": dict(seed=84, B=300, Lmax=64, V=256, R=4, k=3, lens=(1,), kappa=1,
                        theta=np.inf, vocab=50),
+    # more than 256 blocks of 64 vectors per row: the residual draw finds the
+    # chunk first, then the block
+    "wide_vocab": dict(seed=88, B=3, Lmax=80, V=200000, R=4, k=3, lens=(2, 1), kappa=1,
+                       theta=np.inf, vocab=8),
 }
 
 
