@@ -2751,20 +2751,52 @@ __device__ __forceinline__ u128 resid_weight(float lp, float lq, int j, const Sp
     const u128 x = (u128)P * s.Zq, y = (u128)Q * s.Zp;
     return x > y ? x - y : (u128)0;
 }
-// Residual weights of the 8 elements of vector q (elements 8q .. 8q+7) and
-// their P sum.
-__device__ __forceinline__ u128 resid_vec(const u32x4 &vp, const u32x4 &vq, int q,
-                                          const SpecRow &s, float c, unsigned long long &psum) {
-    u128 acc = 0;
-    psum = 0;
+// As elem_weight, as a float (an integer below 2^41, exact).
+__device__ __forceinline__ float elem_weight_f(float l, bool act, float m, int j, int g, float c) {
+    return act ? samp_weight(l, m, c) : (j == g ? 0x1p40f : 0.0f);
+}
+
+// The residual weights of the 8 elements of vector q (elements 8q .. 8q+7),
+// as sums: over the elements where P Zq > Q Zp, the sums of P (pp) and of Q
+// (qp) -- a block's residual sum is then Zq pp - Zp qp, the same integer as
+// the sum of its elements' residual weights -- and the sum of every P (ps).
+// The products are compared in binary64 (each within 2^-52 of its exact
+// value), and in exact 128-bit integers where they lie within 2^-40 of each
+// other.  Every sum is an integer below 2^44, exact in binary64.
+__device__ __forceinline__ void resid_vec(const u32x4 &vp, const u32x4 &vq, int q,
+                                          const SpecRow &s, float c, double zp, double zq,
+                                          double &pp, double &qp, double &ps) {
+    constexpr double kTie = 1.0 + 0x1p-40;
+    auto weights = [&](int e, double &P, double &Q) {
+        const uint32_t wp = vp[e >> 1], wq = vq[e >> 1];
+        const int j = 8 * q + e;
+        P = elem_weight_f((e & 1) ? hi_f(wp) : lo_f(wp), s.ap, s.mp, j, s.gp, c);
+        Q = elem_weight_f((e & 1) ? hi_f(wq) : lo_f(wq), s.aq, s.mq, j, s.gq, c);
+    };
+    uint32_t tie = 0;  // elements whose products lie within the rounding
 #pragma unroll
-    for (int w4 = 0; w4 < 4; ++w4) {
-        unsigned long long P0, P1;
-        acc += resid_weight(lo_f(vp[w4]), lo_f(vq[w4]), 8 * q + 2 * w4, s, c, P0);
-        acc += resid_weight(hi_f(vp[w4]), hi_f(vq[w4]), 8 * q + 2 * w4 + 1, s, c, P1);
-        psum += P0 + P1;
+    for (int e = 0; e < 8; ++e) {
+        double P, Q;
+        weights(e, P, Q);
+        const double x = P * zq, y = Q * zp;
+        const bool pos = x > y * kTie;
+        tie |= (!pos && P != 0.0 && !(y > x * kTie)) ? 1u << e : 0u;
+        pp += pos ? P : 0.0;
+        qp += pos ? Q : 0.0;
+        ps += P;
     }
-    return acc;
+    if (__any(tie != 0u)) {  // rare (q = p, for one): those elements exactly
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            double P, Q;
+            weights(e, P, Q);
+            if (((tie >> e) & 1u) &&
+                (u128)(unsigned long long)P * s.Zq > (u128)(unsigned long long)Q * s.Zp) {
+                pp += P;
+                qp += Q;
+            }
+        }
+    }
 }
 
 // The residual launch's entries: per block of 64 vectors of the rejected row
@@ -2891,10 +2923,10 @@ __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) 
     if (q < nq) {
         xp = pv[q];
         xq = qv[q];
-        unsigned long long ps;
-        w = resid_vec(xp, xq, q, sr, p.samp_c, ps);
-        if (use_p)
-            w = ps;
+        double pp = 0.0, qp = 0.0, ps = 0.0;
+        resid_vec(xp, xq, q, sr, p.samp_c, (double)sr.Zp, (double)sr.Zq, pp, qp, ps);
+        w = use_p ? (u128)(unsigned long long)ps
+                  : (u128)(unsigned long long)pp * sr.Zq - (u128)(unsigned long long)qp * sr.Zp;
     }
     const u128 iv = wave_scan_u128(w);
     int lst = __ffsll((long long)__ballot(iv > tg)) - 1;
@@ -2961,7 +2993,8 @@ __device__ void spec_epilogue(const StepParams &p, int b, int a, int bonus, int 
 // b), unit-major; unit s covers blocks 8 s .. 8 s + 7 of 64 vectors (two per
 // wave, one vector per lane each, both requested together).  Every
 // work-group finds the first rejected row a from the tests; if there is one,
-// each wave adds up its blocks' residual weights (128-bit) and P weights.
+// each wave adds up its blocks' residual weights (128-bit, through resid_vec's
+// sums) and P weights.
 // (Two blocks per wave keep the grid within the resident work-groups, 1024
 // for C2: one block per wave ran the 2048 work-groups in two batches, C2 at
 // T = 0.7 with q 81.9 us per step against 80.0.)  The last of the sequence's rsegs
@@ -3013,16 +3046,19 @@ __global__ __launch_bounds__(kThreads) void k_spec_residual(StepParams p) {
             vq[h] = __builtin_nontemporal_load(
                 reinterpret_cast<const u32x4 *>(p.qlogits + row * p.V) + qc);
         }
+        const double zp = (double)sr.Zp, zq = (double)sr.Zq;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int blk = (s * kWaves + wave) * 2 + h;
             const int q = blk * 64 + lane;
-            u128 acc = 0;
-            unsigned long long ps = 0;
+            double pp = 0.0, qp = 0.0, psd = 0.0;
             if (q < nq)
-                acc = resid_vec(vp[h], vq[h], q, sr, p.samp_c, ps);
-            acc = wave_sum_u128(acc);
-            ps = wave_sum_u64(ps);
+                resid_vec(vp[h], vq[h], q, sr, p.samp_c, zp, zq, pp, qp, psd);
+            // (the block's sums are below 2^50: exact in binary64)
+            const unsigned long long PP = (unsigned long long)wave_sum_f64(pp);
+            const unsigned long long QP = (unsigned long long)wave_sum_f64(qp);
+            const unsigned long long ps = (unsigned long long)wave_sum_f64(psd);
+            const u128 acc = (u128)PP * sr.Zq - (u128)QP * sr.Zp;
             if (lane == 0 && blk < p.cpr * kResBlocks) {
                 unsigned long long *en = resid_entry(p, b, blk);
                 __hip_atomic_store(&en[0], (unsigned long long)acc, __ATOMIC_RELAXED,

@@ -132,6 +132,37 @@ def test_spec_edge_case_parity(case, T):
     check_all_modes(d, f"{case} T={T}")
 
 
+def test_spec_residual_of_near_identical_distributions():
+    """q equal to p except one far-tail element of row 0, one bf16 step lower
+    in q: Zq is a few units below Zp, so at every other element the products
+    P Zq and Q Zp lie within 2^-40 of each other (the residual launch compares
+    them exactly) and its residual weight is 0.  With the accept uniform at
+    its maximum, row 0's drafted token (another element) is rejected, and the
+    residual draw must emit that tail element."""
+    say("[spec] residual of near-identical distributions")
+    T = 0.7
+    B, R, V = 4, 4, 4096
+    d = with_temperature(custom_case(seed=89, B=B, Lmax=50, V=V, R=R, k=3, lens=(1,),
+                                     kappa=1, theta=np.inf, vocab=5), T, seed=90)
+    d["nn"] = np.full(B, R, np.int32)
+    lg = d["logits"].copy()
+    ql = lg.copy()
+    tails = []
+    for b in range(B):
+        x = int(d["ntok"][b, 1])
+        j = (x + 1 + 97 * b) % V
+        lg[b, 0, j] = 0xC140                         # -12.0: a small nonzero weight
+        ql[b, 0, j] = 0xC141                         # -12.0625: one step lower in q
+        tails.append(j)
+    d["logits"] = lg
+    d["draft_logits"] = ql
+    d["accept_uniforms"] = np.full((B, R), 2 ** 64 - 1, np.uint64)
+    exp = check_all_modes(d, "near-identical q")
+    for b in range(B):
+        assert exp["accept_len"][b] == 0
+        assert exp["bonus"][b] == tails[b]
+
+
 def test_spec_identical_distributions_accept_everything():
     """q = p: every valid drafted token is accepted (p(x)/q(x) = 1), and a
     drafted token outside the vocabulary is rejected with an empty residual,
