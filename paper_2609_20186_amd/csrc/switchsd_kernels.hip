@@ -2834,8 +2834,9 @@ __device__ void spec_row_load(const StepParams &p, int b, int r, SpecRow &s) {
 // give S and the target floor(u S / 2^64); the block (read in one round trip,
 // four per lane, up to 256 blocks; beyond that the chunk of 16 blocks first,
 // then its block), the vector (one per lane, p and q read again) and the
-// element follow by prefix sums.  With S = 0 (no residual mass) the same search runs over the
-// blocks' P sums: the draw from p.  Returns the token in every lane.
+// element follow by prefix sums.  With S = 0 (no residual mass) the same
+// search runs over the blocks' P sums: the draw from p.  Returns the token in
+// every lane.
 __device__ int resid_draw(const StepParams &p, int b, int a, const SpecRow &sr) {
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)b * p.R + a;
