@@ -120,6 +120,10 @@ SPEC_CASES = {
     # chunk first, then the block
     "wide_vocab": dict(seed=88, B=3, Lmax=80, V=200000, R=4, k=3, lens=(2, 1), kappa=1,
                        theta=np.inf, vocab=8),
+    # three copy candidates (the q row maxima in a launch of their own), copy
+    # and neural drafts mixed
+    "multi_candidate": dict(seed=91, B=6, Lmax=400, V=2048, R=12, k=3, lens=(2, 1), kappa=1,
+                            theta=0.0, vocab=4, n_cand=3),
 }
 
 
