@@ -2603,14 +2603,18 @@ __global__ __launch_bounds__(kThreads) void k_sample_sums(StepParams p) {
     const bool early = p.speculate && !qrow;
     if (early)
         load_chunk_w(A, vp, c0 * kChunkVecs, nq);
+    // the draft length and the row maximum requested together (a load the
+    // next one waits for would add a round trip); the key is read whether or
+    // not the row takes part
+    const unsigned long long *keyp =
+        &(qrow ? p.ws.qkeys : p.ws.keys)[(int64_t)b * p.ws.key_stride + r];
     const int dn_raw = ld_i32(&p.dn[b]);
+    const unsigned long long k_raw = ld_u64(keyp);
     const int dnb = clampi(dn_raw, 1, p.R);
     const bool spec = spec_seq(p, b);
     const bool skip = r >= (qrow ? dnb - 1 : dnb) || (qrow && !spec);  // no part in the draw
-    const unsigned long long *keyp =
-        &(qrow ? p.ws.qkeys : p.ws.keys)[(int64_t)b * p.ws.key_stride + r];
     // (the polled draw's first work-group of a skipped row still clears its key)
-    const unsigned long long k0 = !skip || (p.draw_poll && s == 0) ? ld_u64(keyp) : 0ull;
+    const unsigned long long k0 = !skip || (p.draw_poll && s == 0) ? k_raw : 0ull;
     float m = 0.0f;
     bool active = !skip && key_max(k0, m);
     if (p.withhold_seg && p.draw_poll && b == 0 && r == 0 && s == 0)
@@ -3007,13 +3011,17 @@ __global__ __launch_bounds__(kThreads) void k_spec_residual(StepParams p) {
     const int s = blockIdx.x / p.B, b = blockIdx.x - s * p.B;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     // whether the sequence was verified with q, its draft length and the
-    // first 64 rows' tests, requested together
-    const int copy = p.spec_copy ? ld_i32(&p.spec_copy[b]) : 0;
+    // first 64 rows' tests, requested together: unconditional loads (a load
+    // under a branch, or into a register a later address reuses, would be
+    // waited for before the next is issued)
+    const int32_t *cp = p.spec_copy ? &p.spec_copy[b] : &p.dn[b];
+    const int copy_raw = ld_i32(cp);
     const int dn_raw = ld_i32(&p.dn[b]);
-    const uint32_t dec0 = lane < p.R ? __hip_atomic_load(&p.rdec[(int64_t)b * p.R + lane],
-                                                         __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT)
-                                     : 1u;
+    const uint32_t dec_raw = __hip_atomic_load(
+        &p.rdec[(int64_t)b * p.R + (lane < p.R ? lane : p.R - 1)], __ATOMIC_RELAXED,
+        __HIP_MEMORY_SCOPE_AGENT);
+    const int copy = p.spec_copy ? copy_raw : 0;
+    const uint32_t dec0 = lane < p.R ? dec_raw : 1u;
     if (!p.qlogits || copy != 0)  // not verified with q (spec_seq)
         return;
     const int dnb = clampi(dn_raw, 1, p.R);
