@@ -1840,11 +1840,16 @@ __device__ void verify_stream(const StepParams &p, Shared &sh, u32x4 *keep) {
     // first unit of sequence b = lane + 64 q (exclusive prefix) and its dn
     int first[Q], dnq[Q];
     int carry = 0;
+    // (every load issued before any is used: the addresses are clamped rather
+    // than the loads made conditional, which would wait for each in turn)
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
         const int b = lane + 64 * q;
-        dnq[q] = b < p.B ? clampi(ld_i32(&p.dn[b]), 1, p.R) : 0;
+        dnq[q] = ld_i32(&p.dn[b < p.B ? b : p.B - 1]);
     }
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        dnq[q] = lane + 64 * q < p.B ? clampi(dnq[q], 1, p.R) : 0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
         const int cnt = dnq[q] * cpr;
@@ -2660,11 +2665,16 @@ k_sample_sums_stream(StepParams p) {
     const int cpr = p.cpr;
     int first[Q], dnq[Q];
     int carry = 0;
+    // (every load issued before any is used: the addresses are clamped rather
+    // than the loads made conditional, which would wait for each in turn)
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
         const int b = lane + 64 * q;
-        dnq[q] = b < p.B ? clampi(ld_i32(&p.dn[b]), 1, p.R) : 0;
+        dnq[q] = ld_i32(&p.dn[b < p.B ? b : p.B - 1]);
     }
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+        dnq[q] = lane + 64 * q < p.B ? clampi(dnq[q], 1, p.R) : 0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
         const int cnt = dnq[q] * cpr;
